@@ -1,0 +1,351 @@
+"""Seeded synthetic inputs for the IntentKV retention path.
+
+This module draws what a serving stack would hand to the retention step: post-RoPE
+keys and values in a paged pool, per-session slot maps, QueryMemory rows, query-span
+rows, a decode query and residual-head weights. Every tensor comes from its own
+counter-keyed Philox stream ``(seed, tensor id, chunk)``, so any chunk can be
+regenerated alone.
+
+It holds none of the method's arithmetic (no scoring, selection, eviction or
+attention). Both the HIP path and the oracle consume the exact bytes produced here;
+nothing else is shared between them.
+
+Layout conventions (the C-ABI's):
+  * pools ``[L][num_slots][Hkv][D]``, bf16 bit patterns (uint16) or float32;
+  * slot 0 is the dead slot; live slots are handed out in pages of ``page`` slots
+    from a seeded shuffle of the free pages;
+  * QueryMemory ``[L][Hkv*R][D]`` float32 per session, concatenated;
+  * query-span rows ``[L][Hkv*R][n_span][D]`` in the pool dtype, concatenated;
+  * decode queries ``[B][L][Hq][D]`` in the pool dtype.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field
+
+import numpy as np
+
+BF16, F32 = 0, 1
+DEAD_SLOT = 0
+# Rotary base of the public Qwen3 / Qwen2.5 configs. Both sides consume the
+# rotated bytes, so the value only shapes the inputs.
+ROPE_BASE = 1.0e6
+
+# Philox key tensor ids.
+T_K, T_V, T_M, T_QDEC, T_QSPAN, T_RESID, T_PAGES, T_HEAVY, T_DEAD, T_SHUF = range(10)
+
+
+def stream(seed: int, tensor: int, chunk: int = 0) -> np.random.Generator:
+    """Independent Philox stream keyed by (seed, tensor id, chunk)."""
+    key = np.array([seed & 0xFFFFFFFFFFFFFFFF, ((tensor & 0xFFFF) << 48) | (chunk & 0xFFFFFFFFFFFF)],
+                   dtype=np.uint64)
+    return np.random.Generator(np.random.Philox(key=key))
+
+
+# ----------------------------------------------------------------------------- bf16
+
+def f64_to_bf16(x) -> np.ndarray:
+    """Round float64 values to bfloat16 (round-to-nearest-even), returned as uint16 bits.
+
+    Rounds the float64 significand directly to 8 bits, so there is no double
+    rounding through float32.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    u = x.view(np.uint64)
+    lsb = (u >> np.uint64(45)) & np.uint64(1)
+    r = ((u + np.uint64((1 << 44) - 1) + lsb) >> np.uint64(45)) << np.uint64(45)
+    f32 = r.view(np.float64).astype(np.float32)  # exact: at most 8 significant bits
+    return (f32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_to_f32(b) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns (uint16) to float32."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def to_dtype(x64: np.ndarray, kv_dtype: int) -> np.ndarray:
+    """Round float64 data to the storage dtype (bf16 bits or float32, both RNE)."""
+    return f64_to_bf16(x64) if kv_dtype == BF16 else x64.astype(np.float32)
+
+
+def widen(a: np.ndarray) -> np.ndarray:
+    """Storage array (bf16 bits or float32) to float64, exactly."""
+    if a.dtype == np.uint16:
+        return bf16_to_f32(a).astype(np.float64)
+    return np.asarray(a, dtype=np.float64)
+
+
+# ----------------------------------------------------------------------------- RoPE
+
+def rope_cos_sin(positions, D: int, base: float = ROPE_BASE):
+    inv = base ** (-np.arange(0, D, 2, dtype=np.float64) / D)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def rope_neox(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """Rotate-half (Neox) RoPE of float64 rows ``x[n, ..., D]`` at the n positions."""
+    h = x.shape[-1] // 2
+    shape = (cos.shape[0],) + (1,) * (x.ndim - 2) + (h,)
+    c, s = cos.reshape(shape), sin.reshape(shape)
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+# ----------------------------------------------------------------------------- specs
+
+@dataclass
+class Shape:
+    L: int
+    Hq: int
+    Hkv: int
+    D: int
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+
+@dataclass
+class SessionSpec:
+    """One request: N positions, budget C, forced prefix [0,pi) and span [qs,qe)."""
+    N: int
+    C: int
+    pi: int
+    qs: int
+    qe: int
+    R: int
+    radix_prefix: int = 0
+    qpos: np.ndarray | None = None       # query positions for the cross-attention (default: span)
+    dead_frac: float = 0.0               # fraction of non-forced positions already redirected
+    heavy_frac: float = 0.0              # fraction of non-forced positions with K scaled
+    heavy_scale: float = 4.0
+
+    def query_positions(self) -> np.ndarray:
+        if self.qpos is not None:
+            return np.asarray(self.qpos, dtype=np.int32)
+        return np.arange(self.qs, self.qe, dtype=np.int32)
+
+
+@dataclass
+class Batch:
+    shape: Shape
+    kv_dtype: int
+    sessions: list
+    num_slots: int
+    k_pool: np.ndarray            # [L][num_slots][Hkv][D]
+    v_pool: np.ndarray
+    slot_maps: np.ndarray         # int32 [sum N]
+    slot_off: np.ndarray          # int64 [B]
+    M: np.ndarray                 # float32 flat
+    mem_off: np.ndarray           # int64 [B]
+    q_span: np.ndarray            # pool dtype, flat
+    qspan_off: np.ndarray         # int64 [B]
+    qpos: np.ndarray              # int32 flat
+    qpos_off: np.ndarray          # int64 [B]
+    q_dec: np.ndarray             # [B][L][Hq][D] pool dtype
+    heavy: list = field(default_factory=list)   # per session: positions with scaled K
+
+    def S(self, b: int) -> np.ndarray:
+        o = int(self.slot_off[b])
+        return self.slot_maps[o:o + self.sessions[b].N]
+
+    def M_of(self, b: int) -> np.ndarray:
+        s, sh = self.sessions[b], self.shape
+        o = int(self.mem_off[b])
+        return self.M[o:o + sh.L * sh.Hkv * s.R * sh.D].reshape(sh.L, sh.Hkv * s.R, sh.D)
+
+    def q_span_of(self, b: int) -> np.ndarray:
+        s, sh = self.sessions[b], self.shape
+        n = s.qe - s.qs
+        o = int(self.qspan_off[b])
+        return self.q_span[o:o + sh.L * sh.Hkv * s.R * n * sh.D].reshape(sh.L, sh.Hkv * s.R, n, sh.D)
+
+    def qpos_of(self, b: int) -> np.ndarray:
+        o = int(self.qpos_off[b])
+        return self.qpos[o:o + len(self.sessions[b].query_positions())]
+
+
+def _workers() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
+               layout: str = "paged", page: int = 16, spare_pages: int = 0) -> Batch:
+    """Draw a batch of sessions sharing one paged pool.
+
+    ``layout``: ``"identity"`` (single session, S[j] = j + 1), ``"shuffled"``
+    (single session, S a seeded permutation of 1..N) or ``"paged"`` (pages of
+    ``page`` slots handed out from a seeded shuffle of all pages).
+    """
+    L, Hkv, D = shape.L, shape.Hkv, shape.D
+    B = len(sessions)
+    Ns = [s.N for s in sessions]
+
+    # --- physical slots ------------------------------------------------------
+    alloc = []
+    if layout in ("identity", "shuffled"):
+        assert B == 1
+        n = Ns[0]
+        num_slots = 1 + n
+        if layout == "identity":
+            alloc.append(np.arange(1, n + 1, dtype=np.int64))
+        else:
+            alloc.append(1 + stream(seed, T_SHUF).permutation(n).astype(np.int64))
+    else:
+        pages_per = [(n + page - 1) // page for n in Ns]
+        total_pages = sum(pages_per) + spare_pages
+        order = stream(seed, T_PAGES).permutation(total_pages).astype(np.int64)
+        num_slots = 1 + total_pages * page
+        p0 = 0
+        for n, pp in zip(Ns, pages_per):
+            pages = order[p0:p0 + pp]
+            p0 += pp
+            j = np.arange(n, dtype=np.int64)
+            alloc.append(1 + pages[j // page] * page + (j % page))
+
+    # --- slot maps with already-dead positions ---------------------------------
+    slot_off = np.zeros(B, dtype=np.int64)
+    slot_maps = np.zeros(sum(Ns), dtype=np.int32)
+    heavy = []
+    o = 0
+    for b, s in enumerate(sessions):
+        slot_off[b] = o
+        S = alloc[b].astype(np.int32).copy()
+        j = np.arange(s.N)
+        forced = (j < s.pi) | ((j >= s.qs) & (j < s.qe))
+        free_pos = np.nonzero(~forced)[0]
+        if s.dead_frac > 0:
+            nd = int(round(s.dead_frac * len(free_pos)))
+            dead = stream(seed, T_DEAD, b).choice(free_pos, size=nd, replace=False)
+            S[dead] = DEAD_SLOT
+        if s.heavy_frac > 0:
+            nh = min(len(free_pos), int(round(s.heavy_frac * s.N)))
+            heavy.append(np.sort(stream(seed, T_HEAVY, b).choice(free_pos, size=nh, replace=False)))
+        else:
+            heavy.append(np.zeros(0, dtype=np.int64))
+        slot_maps[o:o + s.N] = S
+        o += s.N
+
+    # --- pools -------------------------------------------------------------------
+    st = np.uint16 if kv_dtype == BF16 else np.float32
+    k_pool = np.zeros((L, num_slots, Hkv, D), dtype=st)
+    v_pool = np.zeros((L, num_slots, Hkv, D), dtype=st)
+    rope = [rope_cos_sin(np.arange(s.N), D) for s in sessions]
+
+    def fill(job):
+        b, l = job
+        s = sessions[b]
+        k = stream(seed, T_K, (b << 16) | l).standard_normal((s.N, Hkv, D), dtype=np.float32)
+        k = rope_neox(k.astype(np.float64), *rope[b])
+        if len(heavy[b]):
+            k[heavy[b]] *= s.heavy_scale
+        k_pool[l, alloc[b]] = to_dtype(k, kv_dtype)
+        del k
+        v = stream(seed, T_V, (b << 16) | l).standard_normal((s.N, Hkv, D), dtype=np.float32)
+        v_pool[l, alloc[b]] = to_dtype(v.astype(np.float64), kv_dtype)
+
+    jobs = [(b, l) for b in range(B) for l in range(L)]
+    with ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(fill, jobs))
+
+    # --- QueryMemory, span rows, query positions, decode queries ----------------------
+    mem_off = np.zeros(B, dtype=np.int64)
+    qspan_off = np.zeros(B, dtype=np.int64)
+    qpos_off = np.zeros(B, dtype=np.int64)
+    Ms, spans, qps = [], [], []
+    om = osp = oq = 0
+    for b, s in enumerate(sessions):
+        mem_off[b], qspan_off[b], qpos_off[b] = om, osp, oq
+        m = stream(seed, T_M, b).standard_normal((L, Hkv * s.R, D), dtype=np.float32)
+        Ms.append(m.ravel())
+        om += m.size
+        n = s.qe - s.qs
+        q = stream(seed, T_QSPAN, b).standard_normal((n, L, Hkv * s.R, D), dtype=np.float32)
+        cs = rope_cos_sin(np.arange(s.qs, s.qe), D)
+        q = rope_neox(q.astype(np.float64), *cs).transpose(1, 2, 0, 3)
+        spans.append(to_dtype(np.ascontiguousarray(q), kv_dtype).ravel())
+        osp += spans[-1].size
+        qp = s.query_positions()
+        qps.append(qp)
+        oq += len(qp)
+    q_dec = np.zeros((B, L, shape.Hq, D), dtype=st)
+    for b, s in enumerate(sessions):
+        q = stream(seed, T_QDEC, b).standard_normal((1, L, shape.Hq, D), dtype=np.float32)
+        q = rope_neox(q.astype(np.float64), *rope_cos_sin(np.array([s.N]), D))
+        q_dec[b] = to_dtype(q[0], kv_dtype)
+
+    return Batch(shape=shape, kv_dtype=kv_dtype, sessions=sessions, num_slots=num_slots,
+                 k_pool=k_pool, v_pool=v_pool, slot_maps=slot_maps, slot_off=slot_off,
+                 M=np.concatenate(Ms) if Ms else np.zeros(0, np.float32), mem_off=mem_off,
+                 q_span=np.concatenate(spans), qspan_off=qspan_off,
+                 qpos=np.concatenate(qps).astype(np.int32), qpos_off=qpos_off,
+                 q_dec=q_dec, heavy=heavy)
+
+
+# ----------------------------------------------------------------------------- residual weights
+
+def residual_sizes(D: int, h_c: int = 128, hidden: int = 256):
+    """Packed parameter blocks of the residual head, in packing order (name, count)."""
+    f = 3 * D + 1
+    return [("W_Q", h_c * f), ("b_Q", h_c), ("W_K", h_c * D), ("b_K", h_c),
+            ("W_V", h_c * D), ("b_V", h_c), ("W_1", hidden * (f + h_c)), ("b_1", hidden),
+            ("w_2", hidden), ("b_2", 1), ("alpha", 1)]
+
+
+def residual_blob(D: int, seed: int, variant: str = "random", alpha: float = 1.0,
+                  std: float = 0.02) -> np.ndarray:
+    """Residual-head parameters as one float32 blob.
+
+    ``random``: every weight and bias ~ N(0, std^2), alpha as given.
+    ``zero``: as ``random`` but the output projection (w_2, b_2) is zero, which is
+    the head's initial state.
+    """
+    sizes = residual_sizes(D)
+    total = sum(n for _, n in sizes)
+    blob = stream(seed, T_RESID).standard_normal(total, dtype=np.float32) * np.float32(std)
+    o = 0
+    for name, n in sizes:
+        if name in ("w_2", "b_2") and variant == "zero":
+            blob[o:o + n] = 0
+        if name == "alpha":
+            blob[o] = alpha
+        o += n
+    return blob
+
+
+# ----------------------------------------------------------------------------- named workloads
+
+def tiny_shape() -> Shape:
+    return Shape(L=1, Hq=8, Hkv=2, D=64)
+
+
+def qwen3_8b_shape() -> Shape:
+    return Shape(L=36, Hq=32, Hkv=8, D=128)
+
+
+def qwen25_14b_shape() -> Shape:
+    return Shape(L=48, Hq=40, Hkv=8, D=128)
+
+
+def tiny_single_layer(R: int = 16, layout: str = "identity", seed: int = 1, dead_frac: float = 0.0) -> Batch:
+    """Single layer, 8 query / 2 KV heads, D=64, fp32 K/V, N=2048, budget 512, span = last 32."""
+    N = 2048
+    s = SessionSpec(N=N, C=512, pi=0, qs=N - 32, qe=N, R=R, dead_frac=dead_frac)
+    return make_batch(tiny_shape(), [s], seed=seed, kv_dtype=F32, layout=layout)
+
+
+def qwen3_8b_32k(R: int = 64, seed: int = 2) -> Batch:
+    """Qwen3-8B shape, bf16 K/V, history 32768, budget 8192, span = last 64 positions."""
+    N = 32768
+    s = SessionSpec(N=N, C=8192, pi=0, qs=N - 64, qe=N, R=R)
+    return make_batch(qwen3_8b_shape(), [s], seed=seed, kv_dtype=BF16, layout="paged")
+
+
+def qwen25_14b_92k_heavy(R: int = 64, seed: int = 3) -> Batch:
+    """Qwen2.5-14B shape, history 92,300 pruned to 8192; 5% of non-forced keys scaled x4."""
+    N = 92300
+    s = SessionSpec(N=N, C=8192, pi=0, qs=N - 64, qe=N, R=R, heavy_frac=0.05, heavy_scale=4.0)
+    return make_batch(qwen25_14b_shape(), [s], seed=seed, kv_dtype=BF16, layout="paged")
