@@ -1,0 +1,207 @@
+"""Benchmark of the IntentKV retention step on one MI355X.
+
+One step = the whole hot path over one batch resident in HBM:
+    qm_update -> score_history (rule + residual) -> select_budget -> redirect_slots
+    -> decode_attend_slotmap,
+preceded by a device copy that restores the slot map and the QueryMemory so that
+every step sees the same input.
+
+Default workload: Qwen3-8B shape (36 layers, 32 query / 8 KV heads, D = 128), bf16
+K/V, history 32,768 positions, budget 8192, 64 memory rows per KV head, residual
+head on. Prints one JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_VECTOR_PEAK_TFLOPS = 157.3
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def workload(name: str, R: int):
+    import synth
+    if name == "qwen3_8b_32k":
+        return synth.qwen3_8b_32k(R=R), "qwen3_8b_shape_hist32768_budget8192"
+    if name == "qwen25_14b_92k":
+        return synth.qwen25_14b_92k_heavy(R=R), "qwen2.5_14b_shape_hist92300_budget8192_heavy_tail"
+    if name == "tiny":
+        return synth.tiny_single_layer(R=R), "tiny_single_layer_hist2048_budget512"
+    raise SystemExit(f"unknown workload {name}")
+
+
+def cpu_baseline(batch, blob, flags, layers: int):
+    """The float64 oracle on a bounded sample: the per-layer work (rule score and key
+    mean) on `layers` of the L layers for every candidate, scaled by L / layers, plus
+    the residual MLP and the selection over every candidate, done once."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    s = batch.sessions[0]
+    sh = batch.shape
+    S = batch.S(0)
+    sets = oracle.sets(S, s.pi, s.qs, s.qe, s.C, 0)
+    idx = np.nonzero(sets["cand"])[0]
+    Ls = min(layers, sh.L)
+    kp = batch.k_pool[:Ls]
+    M = batch.M_of(0)[:Ls]
+    t0 = time.perf_counter()
+    rule = oracle.rule_scores(kp, S, sets["cand"], M, sh.Hkv, s.R)
+    kb = oracle.kbar(kp, S, idx)
+    kq = oracle.kbar(kp, S, batch.qpos_of(0))
+    t_layers = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    sc = rule.copy()
+    sc[idx] = oracle.residual_scores(rule[idx], kb, oracle.mbar(M), kq, blob, sh.D,
+                                     xattn=not (flags & 2))
+    oracle.select_budget(sc, sets)
+    t_once = time.perf_counter() - t0
+    t_score_select = t_layers * sh.L / Ls + t_once
+    t0 = time.perf_counter()
+    live = S[np.nonzero(sets["live"])[0][: s.C]]
+    oracle.decode(batch.q_dec[0][:Ls], batch.k_pool[:Ls], batch.v_pool[:Ls], live)
+    t_dec = (time.perf_counter() - t0) * sh.L / Ls
+    return {"value": len(idx) / t_score_select, "unit": "history tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"float64 oracle: rule score + key mean on {Ls} of {sh.L} layers for all {len(idx)} "
+                      f"candidates (scaled x{sh.L / Ls:g}), residual MLP + selection once; "
+                      f"{t_layers + t_once:.1f} s measured",
+            "decode_ms_estimate": 1e3 * t_dec, "host_cpus": os.cpu_count()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen3_8b_32k")
+    ap.add_argument("--R", type=int, default=64)
+    ap.add_argument("--no-residual", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=4)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path is single-GPU by design.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_2606_09916_amd import ikv
+    from paper_2606_09916_amd.step import RetentionStep
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    log(f"generating workload {args.workload} R={args.R}")
+    batch, wname = workload(args.workload, args.R)
+    sh = batch.shape
+    s = batch.sessions[0]
+    flags = 0 if args.no_residual else ikv.IKV_RESIDUAL
+    blob = synth.residual_blob(sh.D, seed=22)
+    log("uploading")
+    st = RetentionStep(batch, dev, residual=blob, flags=flags)
+    st.init_dead_slot()
+    torch.cuda.synchronize()
+
+    n_phase = 6
+    names = ["reset", "qm_update", "score", "select", "redirect", "decode"]
+
+    def one_step(evs):
+        evs[0].record()
+        st.reset()
+        evs[1].record()
+        st.qm_update()
+        evs[2].record()
+        st.score()
+        evs[3].record()
+        st.select()
+        evs[4].record()
+        st.redirect()
+        evs[5].record()
+        st.decode()
+        evs[6].record()
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_phase + 1)]
+        one_step(evs)
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    all_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_phase + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(all_evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    phase_ms = np.zeros(n_phase)
+    for evs in all_evs:
+        for i in range(n_phase):
+            phase_ms[i] += evs[i].elapsed_time(evs[i + 1])
+    phase_ms /= args.steps
+    step_ms = float(sum(all_evs[k][0].elapsed_time(all_evs[k][-1]) for k in range(args.steps)) / args.steps)
+
+    n_live = int(st.host("n_live")[0])
+    n_keep = int(st.host("n_keep")[0])
+    import oracle
+    sets = oracle.sets(batch.S(0), s.pi, s.qs, s.qe, s.C, 0)
+    nA = int(sets["cand"].sum())
+    t_ss = (phase_ms[2] + phase_ms[3]) / 1e3
+    tokens_per_s = nA / t_ss
+
+    # algorithmic bytes / flops (per step)
+    kv_row = sh.Hkv * sh.D * 2 * sh.L                          # one position's K over all layers, bf16
+    score_bytes = nA * (kv_row + 4 + 4) + sh.L * sh.Hkv * s.R * sh.D * 4 + (blob.size * 4 if flags else 0)
+    score_flops = 2 * (2.0 * sh.L * sh.Hkv * s.R * sh.D) * nA
+    decode_bytes = n_live * (2 * kv_row + 4)
+    score_gbs = score_bytes / (phase_ms[2] / 1e3) / 1e9
+    decode_gbs = decode_bytes / (phase_ms[5] / 1e3) / 1e9
+    score_tflops = score_flops / (phase_ms[2] / 1e3) / 1e12
+    # The scorer's two logit passes run on the fp32 vector ALUs: that bounds it.
+    roofline = {"bound": "alu", "kernel": "score_history (all its kernels)",
+                "achieved": round(score_tflops, 2), "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(score_tflops / FP32_VECTOR_PEAK_TFLOPS, 4), "traffic": None,
+                "hbm_achieved_gbs": round(score_gbs, 1), "hbm_frac": round(score_gbs / HBM_PEAK_GBS, 4)}
+    out = {
+        "metric": "history tokens scored+selected/s and slot-map decode attn HBM GB/s, 32k hist/8k budget",
+        "value": round(tokens_per_s, 1), "unit": "history tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wname, "L": sh.L, "Hq": sh.Hq, "Hkv": sh.Hkv, "D": sh.D, "N": s.N, "C": s.C,
+                   "R": s.R, "kv_storage": "bf16" if batch.kv_dtype == synth.BF16 else "f32",
+                   "residual": bool(flags), "memory_update": True, "candidates": nA, "n_keep": n_keep,
+                   "n_live": n_live},
+        "decode_attn_gbs": round(decode_gbs, 1), "decode_hbm_frac": round(decode_gbs / HBM_PEAK_GBS, 4),
+        "phase_ms": {n: round(float(v), 4) for n, v in zip(names, phase_ms)},
+        "wall_s_timed": round(wall, 3),
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline (oracle, {args.cpu_layers} layers)")
+        out["cpu_baseline"] = cpu_baseline(batch, blob, flags, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,234 @@
+/*
+ * ikv.h -- C ABI of the IntentKV per-step retention path on MI355X (gfx950).
+ *
+ * One retention step of a request (Sec. 3 of the paper; Appendix H, compression
+ * event) is five calls, in order:
+ *
+ *   ikv_qm_update            QueryMemory recurrence, Eq. 2
+ *   ikv_score_history        rule score, Eq. 3, plus the residual head, Eqs. 4-6
+ *   ikv_select_budget        budgeted top-k of Eq. 1
+ *   ikv_redirect_slots       slot-map eviction, Eq. 7, with the alias-aware free of Sec. 3.4
+ *   ikv_decode_attend_slotmap  GQA decode attention over the live slots only
+ *
+ * plus ikv_init_dead_slot, run once per pool (the sentinel of Sec. 3.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every pointer named *_dev, every pool, map, score, mask and list is DEVICE
+ *    memory; ikv_pool / ikv_session structs passed as `pool` / `sess` are HOST
+ *    memory. Sessions are passed twice: `sess` (host copy, validated and used
+ *    for launch geometry) and `sess_dev` (a byte-identical device copy read by
+ *    the kernels). The caller owns every buffer; the library keeps no pointer
+ *    after a call returns and allocates nothing.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Validation runs
+ *    synchronously on the host; all device work is enqueued on `stream` and the
+ *    call returns without synchronising.
+ *  - Calls are batched over B >= 1 sessions that share one pool. Per-position
+ *    arrays (slot maps, scores, keep masks, live and freed lists) of all sessions
+ *    are concatenated; session b's part starts at sess[b].slot_off.
+ *  - Calls that need scratch take a caller-provided `workspace` of at least
+ *    ikv_workspace_bytes(...) bytes (256-byte aligned). Its contents on entry do
+ *    not matter.
+ *  - Results are deterministic: no result-bearing reduction uses floating-point
+ *    atomics, so two runs on the same inputs give identical bytes.
+ *  - Return value: IKV_OK, or a negative ikv_status; ikv_last_error() then gives
+ *    a message (thread-local, valid until the next call on the same thread).
+ *    On an error return nothing has been enqueued, except for IKV_EHIP, which
+ *    reports a failed launch.
+ *  - Slot ids in slot maps and live lists must lie in [0, num_slots); the
+ *    kernels do not check them.
+ */
+#ifndef IKV_H
+#define IKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ikv_status;
+#define IKV_OK            0
+#define IKV_EINVAL       -1   /* null pointer, bad flag, negative size               */
+#define IKV_ESHAPE       -2   /* inconsistent dimensions or ranges                   */
+#define IKV_EWORKSPACE   -3   /* workspace missing, too small or misaligned          */
+#define IKV_EUNSUPPORTED -4   /* valid but not implemented (e.g. D not in {64,128})  */
+#define IKV_EHIP         -5   /* a HIP runtime call or kernel launch failed          */
+
+/* K/V storage types of the pool. */
+#define IKV_BF16 0
+#define IKV_F32  1
+
+/* ikv_score_history flags. */
+#define IKV_RESIDUAL  1u   /* add alpha * MLP(phi ++ c), Eq. 4 (needs `residual`)           */
+#define IKV_NO_XATTN  2u   /* the "- x-attn" ablation: c_j = 0 in Eq. 4 (Sec. 3.3)          */
+
+/* ikv_workspace_bytes call ids. */
+#define IKV_CALL_SCORE    1
+#define IKV_CALL_SELECT   2
+#define IKV_CALL_REDIRECT 3
+#define IKV_CALL_DECODE   4
+
+/*
+ * The paged KV pool (Sec. 3.1: post-RoPE K, V in R^{L x Hkv x N x D}, stored by
+ * physical slot as in a paged serving stack).
+ *   k_pool, v_pool: device, [L][num_slots][Hkv][D] of kv_dtype, row-major.
+ *   dead_slot: the sentinel slot s_dead (Sec. 3.4); never freed.
+ *   Hq must be a multiple of Hkv (query head h reads KV head h / (Hq/Hkv)).
+ *   Supported: D in {64, 128}; Hq / Hkv <= 8.
+ */
+typedef struct ikv_pool {
+  int32_t L, Hq, Hkv, D;
+  int64_t num_slots;
+  int32_t dead_slot;
+  int32_t kv_dtype;
+  void *k_pool;
+  void *v_pool;
+} ikv_pool;
+
+/*
+ * One request r (Sec. 3.1 problem formulation; Appendix H).
+ *   slot_off   first entry of this session in every per-position array
+ *   mem_off    QueryMemory M_t at M + mem_off: [L][Hkv*R][D] float32. Row
+ *              h*R + r of layer l pairs with KV head h (R rows per KV head; the
+ *              paper's one row per query head is R = Hq/Hkv).
+ *   qspan_off  query-span rows at q_span + qspan_off: [L][Hkv*R][qe-qs][D] in
+ *              the pool's kv_dtype (ikv_qm_update only)
+ *   qpos_off   cross-attention query positions at qpos + qpos_off: nq int32
+ *              positions in [0, N) (Eq. 6; dead ones are skipped)
+ *   N          positions of the request, dead ones included
+ *   pi         protected prefix [0, pi); qs, qe the actionable span [qs, qe);
+ *              F = ([0,pi) u [qs,qe)) restricted to live positions (Eq. 1)
+ *   C          retention budget, F included: C* = max(0, C - |F|)
+ *   radix_prefix  positions below it are never freed (Sec. 3.4, condition (a))
+ *   R          memory rows per KV head, 1 <= R <= 256
+ *   nq         number of cross-attention query positions, 0 <= nq <= 256
+ */
+typedef struct ikv_session {
+  int64_t slot_off;
+  int64_t mem_off;
+  int64_t qspan_off;
+  int64_t qpos_off;
+  int32_t N;
+  int32_t pi, qs, qe;
+  int32_t C;
+  int32_t radix_prefix;
+  int32_t R;
+  int32_t nq;
+} ikv_session;
+
+/*
+ * Sentinel dead slot (Sec. 3.4, sentinel paragraph): K[l][dead_slot][h][:] = -1e4
+ * (stored as bf16 -9984, the nearest bf16 value, or exactly in float32) and
+ * V[l][dead_slot][h][:] = 0 on every layer and head. Run once per pool.
+ */
+ikv_status ikv_init_dead_slot(const ikv_pool *pool, void *stream);
+
+/*
+ * QueryMemory update, Eq. 2 with Sec. 3.2: for every session, layer and memory
+ * row, Enc = mean of the qe-qs span rows; M <- exp(-lambda) * M + Enc; then the
+ * row is divided by max(||row||_2, 1e-12). lambda = INFINITY drops the history
+ * (the "query" scorer mode and the "- memory" ablation). In place on M.
+ *   q_span: device, per session [L][Hkv*R][qe-qs][D] of the pool's kv_dtype.
+ * Sessions with qe == qs leave M unchanged apart from the decay and projection.
+ */
+ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess,
+                         const ikv_session *sess_dev, int32_t B, float *M,
+                         const void *q_span, float lambda, void *stream);
+
+/*
+ * Score every candidate position, Eq. 3 (and Eq. 4 with IKV_RESIDUAL).
+ *   Candidates A = live positions (slot != dead_slot) outside F.
+ *   rule_j = sum over layers l, KV heads h and the R memory rows r of head h of
+ *            softmax_{i in A}(M[l][h*R+r] . K[l][S[i]][h] / sqrt(D)) at i = j.
+ *   With IKV_RESIDUAL: s_j = rule_j + clip(alpha, -5, 5) * MLP(phi_j ++ c_j) with
+ *     phi_j = [kbar_j, mbar, kbar_j * mbar, rule_j] (Eq. 5; kbar_j the mean of the
+ *     key rows over layers and KV heads, mbar the mean of all memory rows),
+ *     c_j the 4-head cross-attention of Eq. 6 over kbar at the live query
+ *     positions (c_j = 0 with IKV_NO_XATTN or when none is live) and
+ *     MLP = w_2 . GELU(W_1 x + b_1) + b_2 (exact erf GELU).
+ *   residual: device float32 blob, row-major [out][in] blocks in this order:
+ *     W_Q[128][3D+1] b_Q[128] W_K[128][D] b_K[128] W_V[128][D] b_V[128]
+ *     W_1[256][3D+1+128] b_1[256] w_2[256] b_2[1] alpha[1]
+ *     (214,274 floats at D = 128; 124,162 at D = 64). Ignored without IKV_RESIDUAL.
+ *   scores: device float32, per session [N]: s_j on A, -INFINITY elsewhere.
+ *   Sessions with N <= C are skipped (Appendix H): all their scores are -INFINITY.
+ *   slot_maps, M, qpos: read only.
+ */
+ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
+                             const ikv_session *sess_dev, int32_t B,
+                             const int32_t *slot_maps, const float *M,
+                             const int32_t *qpos, const float *residual,
+                             uint32_t flags, float *scores, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/*
+ * Budgeted selection, Eq. 1 (Appendix H: K = F u topk(A, max(0, C - |F|))).
+ *   Candidates are ranked by score descending, ties by lower position; NaN counts
+ *   as -INFINITY and -0.0 as +0.0.
+ *   keep: device uint8 per session [N]: 1 on F and on the min(C*, |A|) best
+ *         candidates, 0 elsewhere (the persisted valid mask of Appendix H).
+ *   n_keep: device int32 [B], |F| + min(C*, |A|).
+ *   tau:    device float32 [B], score of the last candidate taken (+INFINITY if
+ *           none is taken).
+ *   Sessions with N <= C keep every live position (n_keep = live count,
+ *   tau = -INFINITY).
+ */
+ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev,
+                             int32_t B, const int32_t *slot_maps, int32_t dead_slot,
+                             const float *scores, uint8_t *keep, int32_t *n_keep,
+                             float *tau, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/*
+ * Slot-map eviction, Eq. 7, and the prefix-safe free of Sec. 3.4 / Appendix H.
+ *   For every live position j with keep[j] == 0: slot_maps[j] <- dead_slot. Kept
+ *   positions keep their slot; K/V rows are never touched.
+ *   The old slot u of such a j is freed iff j >= radix_prefix, u != dead_slot and
+ *   u is not the slot of any kept position of the same session.
+ *   freed:  device int32 per session [N] (first n_freed used): the freed slots in
+ *           ascending slot order, each once.
+ *   live:   device int32 per session [N] (first n_live used): the slots of the
+ *           positions still live afterwards, in position order.
+ *   n_freed, n_live: device int32 [B].
+ *   num_slots: the pool's slot count (sizes the slot sets in the workspace).
+ */
+ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_dev,
+                              int32_t B, int64_t num_slots, int32_t *slot_maps,
+                              int32_t dead_slot, const uint8_t *keep, int32_t *freed,
+                              int32_t *n_freed, int32_t *live, int32_t *n_live,
+                              void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * GQA decode attention over live slots (Sec. 3.4; Appendix C.2: the attention
+ * backend strips the sentinel and reads only kept entries).
+ *   For session b, layer l, query head h (KV head g = h / (Hq/Hkv)):
+ *   out[b][l][h] = softmax_k(q[b][l][h] . K[l][u_k][g] / sqrt(D)) . V[l][u_k][g]
+ *   over u_k = live[slot_off + k], k < n_live[b]. n_live[b] == 0 gives zeros.
+ *   q, out: device [B][L][Hq][D] of the pool's kv_dtype (out rounded to nearest
+ *   even). live, n_live: device, as written by ikv_redirect_slots;
+ *   n_live[b] must not exceed sess[b].N.
+ */
+ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess,
+                                     const ikv_session *sess_dev, int32_t B,
+                                     const void *q, const int32_t *live,
+                                     const int32_t *n_live, void *out, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
+/*
+ * Workspace size of one call (IKV_CALL_*) for these sessions, in bytes (0 when
+ * the call needs none). `pool` may be NULL for SELECT; REDIRECT reads only
+ * pool->num_slots. `flags` matter for SCORE only and are the score call's flags.
+ */
+ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, int32_t B,
+                               int32_t call, uint32_t flags, size_t *bytes);
+
+/* Message of the last error on this thread ("" if none). */
+const char *ikv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IKV_H */

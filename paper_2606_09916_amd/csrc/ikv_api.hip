@@ -1,0 +1,246 @@
+// Host side of the C ABI declared in include/ikv.h: argument validation, workspace
+// sizing and kernel launches. Nothing here allocates device memory.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "ikv_internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+ikv_status fail(ikv_status code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+ikv_status ok() {
+  g_err.clear();
+  return IKV_OK;
+}
+
+ikv_status hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return ok();
+  return fail(IKV_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+ikv_status check_pool(const ikv_pool *p) {
+  if (!p) return fail(IKV_EINVAL, "pool is NULL");
+  if (p->L < 1 || p->Hq < 1 || p->Hkv < 1) return fail(IKV_ESHAPE, "pool: L, Hq, Hkv must be >= 1");
+  if (p->Hq % p->Hkv) return fail(IKV_ESHAPE, "pool: Hq (%d) is not a multiple of Hkv (%d)", p->Hq, p->Hkv);
+  if (p->Hq / p->Hkv > 8) return fail(IKV_EUNSUPPORTED, "pool: Hq/Hkv = %d > 8", p->Hq / p->Hkv);
+  if (p->D != 64 && p->D != 128) return fail(IKV_EUNSUPPORTED, "pool: D = %d (supported: 64, 128)", p->D);
+  if (p->num_slots < 1 || p->num_slots > INT32_MAX) return fail(IKV_ESHAPE, "pool: num_slots out of range");
+  if (p->dead_slot < 0 || p->dead_slot >= p->num_slots) return fail(IKV_ESHAPE, "pool: dead_slot out of range");
+  if (p->kv_dtype != IKV_BF16 && p->kv_dtype != IKV_F32) return fail(IKV_EINVAL, "pool: unknown kv_dtype");
+  if (!p->k_pool || !p->v_pool) return fail(IKV_EINVAL, "pool: k_pool / v_pool is NULL");
+  return IKV_OK;
+}
+
+ikv_status check_sessions(const ikv_session *s, const ikv_session *sd, int32_t B) {
+  if (B < 0) return fail(IKV_EINVAL, "B < 0");
+  if (B > 0 && (!s || !sd)) return fail(IKV_EINVAL, "sess / sess_dev is NULL");
+  for (int b = 0; b < B; ++b) {
+    const ikv_session &x = s[b];
+    if (x.N < 0) return fail(IKV_ESHAPE, "session %d: N < 0", b);
+    if (x.pi < 0 || x.pi > x.N) return fail(IKV_ESHAPE, "session %d: pi outside [0, N]", b);
+    if (x.qs < 0 || x.qs > x.qe || x.qe > x.N) return fail(IKV_ESHAPE, "session %d: need 0 <= qs <= qe <= N", b);
+    if (x.C < 0) return fail(IKV_ESHAPE, "session %d: C < 0", b);
+    if (x.radix_prefix < 0) return fail(IKV_ESHAPE, "session %d: radix_prefix < 0", b);
+    if (x.R < 1 || x.R > ikv::MAX_R) return fail(IKV_ESHAPE, "session %d: R = %d outside [1, %d]", b, x.R, ikv::MAX_R);
+    if (x.nq < 0 || x.nq > ikv::MAX_NQ) return fail(IKV_ESHAPE, "session %d: nq outside [0, %d]", b, ikv::MAX_NQ);
+    if (x.slot_off < 0 || x.mem_off < 0 || x.qspan_off < 0 || x.qpos_off < 0)
+      return fail(IKV_ESHAPE, "session %d: negative offset", b);
+  }
+  return IKV_OK;
+}
+
+ikv_status check_ws(void *ws, size_t have, size_t need) {
+  if (need == 0) return IKV_OK;
+  if (!ws) return fail(IKV_EWORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (have < need) return fail(IKV_EWORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(IKV_EWORKSPACE, "workspace is not 256-byte aligned");
+  return IKV_OK;
+}
+
+int max_n(const ikv_session *s, int B) {
+  int m = 0;
+  for (int b = 0; b < B; ++b) m = s[b].N > m ? s[b].N : m;
+  return m;
+}
+
+size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flags) {
+  const bool resid = (flags & IKV_RESIDUAL) != 0;
+  const int units = p->L * p->Hkv;
+  int64_t f = ikv::score_offset(s, B, p->L, units, p->D, resid);
+  if (resid) f += ikv::score_shared_floats(p->D);
+  return size_t(f) * sizeof(float);
+}
+
+size_t redirect_bytes(int64_t num_slots, int B) {
+  return size_t(B) * 2 * size_t(ikv::bitset_words(num_slots)) * sizeof(uint32_t);
+}
+
+size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
+  const int splits = ikv::decode_splits(max_n(s, B));
+  return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ikv_last_error(void) { return g_err.c_str(); }
+
+ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, int32_t B, int32_t call,
+                               uint32_t flags, size_t *bytes) {
+  if (!bytes) return fail(IKV_EINVAL, "bytes is NULL");
+  *bytes = 0;
+  if (B < 0) return fail(IKV_EINVAL, "B < 0");
+  if (B > 0 && !sess) return fail(IKV_EINVAL, "sess is NULL");
+  ikv_status r;
+  switch (call) {
+    case IKV_CALL_SCORE:
+      if ((r = check_pool(pool))) return r;
+      if ((r = check_sessions(sess, sess, B))) return r;
+      *bytes = score_bytes(pool, sess, B, flags);
+      return ok();
+    case IKV_CALL_SELECT:
+      return ok();
+    case IKV_CALL_REDIRECT:
+      if (!pool) return fail(IKV_EINVAL, "pool is NULL");
+      if (pool->num_slots < 1) return fail(IKV_ESHAPE, "num_slots < 1");
+      *bytes = redirect_bytes(pool->num_slots, B);
+      return ok();
+    case IKV_CALL_DECODE:
+      if ((r = check_pool(pool))) return r;
+      if ((r = check_sessions(sess, sess, B))) return r;
+      *bytes = decode_bytes(pool, sess, B);
+      return ok();
+    default:
+      return fail(IKV_EINVAL, "unknown call id %d", call);
+  }
+}
+
+ikv_status ikv_init_dead_slot(const ikv_pool *pool, void *stream) {
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  return hip_status(ikv::launch_init_dead_slot(*pool, (hipStream_t)stream), "ikv_init_dead_slot");
+}
+
+ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                         float *M, const void *q_span, float lambda, void *stream) {
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  if ((r = check_sessions(sess, sess_dev, B))) return r;
+  if (B == 0) return ok();
+  if (!M || !q_span) return fail(IKV_EINVAL, "M / q_span is NULL");
+  if (!(lambda >= 0.0f)) return fail(IKV_EINVAL, "lambda must be >= 0 (got %g)", double(lambda));
+  int max_rows = 0;
+  for (int b = 0; b < B; ++b) {
+    const int rows = pool->L * pool->Hkv * sess[b].R;
+    max_rows = rows > max_rows ? rows : max_rows;
+  }
+  const float decay = isinf(lambda) ? 0.0f : float(exp(-double(lambda)));
+  return hip_status(ikv::launch_qm_update(*pool, sess_dev, B, max_rows, M, q_span, decay, (hipStream_t)stream),
+                    "ikv_qm_update");
+}
+
+ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                             const int32_t *slot_maps, const float *M, const int32_t *qpos, const float *residual,
+                             uint32_t flags, float *scores, void *workspace, size_t workspace_bytes,
+                             void *stream) {
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  if ((r = check_sessions(sess, sess_dev, B))) return r;
+  if (flags & ~(IKV_RESIDUAL | IKV_NO_XATTN)) return fail(IKV_EINVAL, "unknown flag bits 0x%x", flags);
+  if (B == 0) return ok();
+  if (!slot_maps || !M || !scores) return fail(IKV_EINVAL, "slot_maps / M / scores is NULL");
+  const bool resid = (flags & IKV_RESIDUAL) != 0;
+  if (resid && !residual) return fail(IKV_EINVAL, "IKV_RESIDUAL set but residual is NULL");
+  int maxR = 0, maxNq = 0, anyq = 0;
+  for (int b = 0; b < B; ++b) {
+    maxR = sess[b].R > maxR ? sess[b].R : maxR;
+    maxNq = sess[b].nq > maxNq ? sess[b].nq : maxNq;
+    anyq |= sess[b].nq > 0;
+  }
+  if (resid && anyq && !qpos) return fail(IKV_EINVAL, "qpos is NULL but a session has nq > 0");
+  const size_t need = score_bytes(pool, sess, B, flags);
+  if ((r = check_ws(workspace, workspace_bytes, need))) return r;
+  ikv::ScoreArgs a;
+  a.pool = *pool;
+  a.sess_host = sess;
+  a.sess_dev = sess_dev;
+  a.B = B;
+  a.slot_maps = slot_maps;
+  a.M = M;
+  a.qpos = qpos;
+  a.residual = residual;
+  a.flags = flags;
+  a.scores = scores;
+  a.ws = static_cast<float *>(workspace);
+  a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid);
+  a.maxN = max_n(sess, B);
+  a.maxR = maxR;
+  a.maxNq = maxNq;
+  if (a.maxN == 0) return ok();
+  return hip_status(ikv::launch_score(a, (hipStream_t)stream), "ikv_score_history");
+}
+
+ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                             const int32_t *slot_maps, int32_t dead_slot, const float *scores, uint8_t *keep,
+                             int32_t *n_keep, float *tau, void *workspace, size_t workspace_bytes, void *stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  ikv_status r = check_sessions(sess, sess_dev, B);
+  if (r) return r;
+  if (B == 0) return ok();
+  if (!slot_maps || !scores || !keep || !n_keep || !tau)
+    return fail(IKV_EINVAL, "slot_maps / scores / keep / n_keep / tau is NULL");
+  if (dead_slot < 0) return fail(IKV_ESHAPE, "dead_slot < 0");
+  return hip_status(ikv::launch_select(sess_dev, B, max_n(sess, B), slot_maps, dead_slot, scores, keep, n_keep, tau,
+                                       (hipStream_t)stream),
+                    "ikv_select_budget");
+}
+
+ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_dev, int32_t B, int64_t num_slots,
+                              int32_t *slot_maps, int32_t dead_slot, const uint8_t *keep, int32_t *freed,
+                              int32_t *n_freed, int32_t *live, int32_t *n_live, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+  ikv_status r = check_sessions(sess, sess_dev, B);
+  if (r) return r;
+  if (B == 0) return ok();
+  if (num_slots < 1 || num_slots > INT32_MAX) return fail(IKV_ESHAPE, "num_slots out of range");
+  if (dead_slot < 0 || dead_slot >= num_slots) return fail(IKV_ESHAPE, "dead_slot out of range");
+  if (!slot_maps || !keep || !freed || !n_freed || !live || !n_live)
+    return fail(IKV_EINVAL, "slot_maps / keep / freed / n_freed / live / n_live is NULL");
+  if ((r = check_ws(workspace, workspace_bytes, redirect_bytes(num_slots, B)))) return r;
+  return hip_status(ikv::launch_redirect(sess_dev, B, num_slots, slot_maps, dead_slot, keep, freed, n_freed, live,
+                                         n_live, static_cast<uint32_t *>(workspace), (hipStream_t)stream),
+                    "ikv_redirect_slots");
+}
+
+ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev,
+                                     int32_t B, const void *q, const int32_t *live, const int32_t *n_live, void *out,
+                                     void *workspace, size_t workspace_bytes, void *stream) {
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  if ((r = check_sessions(sess, sess_dev, B))) return r;
+  if (B == 0) return ok();
+  if (!q || !live || !n_live || !out) return fail(IKV_EINVAL, "q / live / n_live / out is NULL");
+  if ((r = check_ws(workspace, workspace_bytes, decode_bytes(pool, sess, B)))) return r;
+  const int splits = ikv::decode_splits(max_n(sess, B));
+  return hip_status(ikv::launch_decode(*pool, sess_dev, B, splits, q, live, n_live, out,
+                                       static_cast<float *>(workspace), (hipStream_t)stream),
+                    "ikv_decode_attend_slotmap");
+}
+
+}  // extern "C"

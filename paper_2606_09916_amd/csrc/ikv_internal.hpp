@@ -1,0 +1,158 @@
+// Internal declarations of the IntentKV HIP library: storage helpers, workspace
+// layout (evaluated identically on host and device) and kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ikv.h"
+
+namespace ikv {
+
+constexpr int WAVE = 64;
+
+// ---------------------------------------------------------------- tiles
+constexpr int SCORE_TILE = 256;     // positions per workgroup in the score passes
+constexpr int SCORE_ROWS = 64;      // memory rows per chunk held in LDS
+constexpr int RES_TILE = 16;        // candidates per workgroup in the residual head
+constexpr int DEC_BLOCK = 64;       // live slots per wave per block in decode
+constexpr int HC = 128;             // cross-attention width d_c
+constexpr int HC_HEADS = 4;         // cross-attention heads H_c
+constexpr int HIDDEN = 256;         // residual MLP hidden width
+constexpr int MAX_NQ = 256;         // cross-attention query positions per session
+constexpr int MAX_R = 256;          // memory rows per KV head
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int64_t(63); }   // floats -> 256 B
+
+// Score workspace, per session b (floats, each block 256-byte aligned):
+//   part  [units][R][tiles][2]  per-tile (max, sum exp) of every memory row
+//   lse   [units][R][2]         (max, 1/Z) of every memory row
+//   rulep [L][N]                per-layer partial rule scores
+//   kbar  [N][D]                mean key row (residual only)
+//   kq    [nq][D]               kbar at the live query positions (residual only)
+//   kp/vp [nq][HC]              W_K kq + b_K, W_V kq + b_V (residual only)
+//   misc  [MBAR_PARTS][D] + [D] + 64   partial and final mbar, live query count (residual only)
+// followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN].
+constexpr int MBAR_PARTS = 64;
+
+struct ScoreSizes {
+  int64_t part, lse, rulep, kbar, kq, kp, vp, misc;
+  __host__ __device__ int64_t total() const { return part + lse + rulep + kbar + kq + kp + vp + misc; }
+};
+
+__host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid) {
+  ScoreSizes z;
+  int64_t tiles = cdiv(s.N, SCORE_TILE);
+  z.part = align64f(int64_t(units) * s.R * tiles * 2);
+  z.lse = align64f(int64_t(units) * s.R * 2);
+  z.rulep = align64f(int64_t(L) * s.N);
+  z.kbar = resid ? align64f(int64_t(s.N) * D) : 0;
+  z.kq = resid ? align64f(int64_t(s.nq) * D) : 0;
+  z.kp = resid ? align64f(int64_t(s.nq) * HC) : 0;
+  z.vp = z.kp;
+  z.misc = resid ? align64f(int64_t(MBAR_PARTS + 1) * D + 64) : 0;
+  return z;
+}
+
+// Offset (floats) of session b's score block: the sum of the blocks before it.
+__host__ __device__ inline int64_t score_offset(const ikv_session *sess, int b, int L, int units, int D,
+                                                bool resid) {
+  int64_t o = 0;
+  for (int i = 0; i < b; ++i) o += score_sizes(sess[i], L, units, D, resid).total();
+  return o;
+}
+
+__host__ __device__ inline int64_t score_shared_floats(int D) {
+  return align64f(int64_t(3 * D + 1) * HC) + align64f(int64_t(3 * D + 1 + HC) * HIDDEN);
+}
+
+// Redirect workspace: two slot bitsets (kept slots, freed slots) per session.
+__host__ __device__ inline int64_t bitset_words(int64_t num_slots) { return align64f(cdiv(num_slots, 32)); }
+
+// Decode workspace: per (session, layer, query head, split) the partial (m, l, o[D]).
+__host__ __device__ inline int64_t decode_part_floats(int D) { return D + 2; }
+
+// ---------------------------------------------------------------- storage
+__device__ __forceinline__ float bf16_bits_to_float(uint16_t u) { return __uint_as_float(uint32_t(u) << 16); }
+
+__device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);   // NaN stays NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+
+template <typename T> struct Store;
+template <> struct Store<uint16_t> {
+  static __device__ __forceinline__ float ld(const uint16_t *p) { return bf16_bits_to_float(*p); }
+  static __device__ __forceinline__ uint16_t from(float f) { return float_to_bf16_bits(f); }
+};
+template <> struct Store<float> {
+  static __device__ __forceinline__ float ld(const float *p) { return *p; }
+  static __device__ __forceinline__ float from(float f) { return f; }
+};
+
+// 8 consecutive elements -> float
+__device__ __forceinline__ void load8(const uint16_t *p, float *o) {
+  uint4 v = *reinterpret_cast<const uint4 *>(p);
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = __uint_as_float(w[i] << 16);
+    o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float *p, float *o) {
+  float4 a = *reinterpret_cast<const float4 *>(p);
+  float4 b = *reinterpret_cast<const float4 *>(p + 4);
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+
+// ---------------------------------------------------------------- wave reductions
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+  return v;
+}
+
+// ---------------------------------------------------------------- launchers
+struct ScoreArgs {
+  ikv_pool pool;
+  const ikv_session *sess_host;
+  const ikv_session *sess_dev;
+  int B;
+  const int32_t *slot_maps;
+  const float *M;
+  const int32_t *qpos;
+  const float *residual;
+  uint32_t flags;
+  float *scores;
+  float *ws;           // session blocks, then the shared block
+  float *ws_shared;
+  int maxN, maxR, maxNq;
+};
+
+hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);
+hipError_t launch_qm_update(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_rows,
+                            float *M, const void *q_span, float decay, hipStream_t st);
+hipError_t launch_score(const ScoreArgs &a, hipStream_t st);
+hipError_t launch_select(const ikv_session *sess_dev, int B, int maxN, const int32_t *slot_maps,
+                         int32_t dead, const float *scores, uint8_t *keep, int32_t *n_keep,
+                         float *tau, hipStream_t st);
+hipError_t launch_redirect(const ikv_session *sess_dev, int B, int64_t num_slots, int32_t *slot_maps,
+                           int32_t dead, const uint8_t *keep, int32_t *freed, int32_t *n_freed,
+                           int32_t *live, int32_t *n_live, uint32_t *ws, hipStream_t st);
+hipError_t launch_decode(const ikv_pool &pool, const ikv_session *sess_dev, int B, int splits,
+                         const void *q, const int32_t *live, const int32_t *n_live, void *out,
+                         float *ws, hipStream_t st);
+
+int decode_splits(int maxN);
+
+}  // namespace ikv

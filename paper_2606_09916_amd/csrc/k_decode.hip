@@ -1,0 +1,232 @@
+// GQA decode attention over the live slots of each session (the kept entries read
+// through the slot map with the sentinel stripped, Sec. 3.4 and Appendix C.2).
+//
+// k_decode_split: one workgroup per (session, layer, KV head, split of the live
+// list). Each wavefront takes blocks of 64 live slots: lane k computes the logits
+// of slot k for the G query heads sharing the KV head, the block's weights are
+// folded into a running (max, sum, output) per head, and the value rows are read
+// with lanes along the head dimension. The partial state of every split goes to
+// the workspace; k_decode_combine merges the splits per (session, layer, head).
+#include <math.h>
+
+#include "ikv_internal.hpp"
+
+namespace ikv {
+
+int decode_splits(int maxN) {
+  const int64_t s = cdiv(maxN, 1024);
+  return int(s < 1 ? 1 : (s > 64 ? 64 : s));
+}
+
+// CPL consecutive value channels of one lane (CPL = D / 64).
+template <typename T, int CPL> struct Chan;
+template <> struct Chan<uint16_t, 2> {
+  static __device__ __forceinline__ void ld(const uint16_t *p, float (&v)[2]) {
+    const uint32_t w = *reinterpret_cast<const uint32_t *>(p);
+    v[0] = __uint_as_float(w << 16);
+    v[1] = __uint_as_float(w & 0xffff0000u);
+  }
+};
+template <> struct Chan<float, 2> {
+  static __device__ __forceinline__ void ld(const float *p, float (&v)[2]) {
+    const float2 x = *reinterpret_cast<const float2 *>(p);
+    v[0] = x.x;
+    v[1] = x.y;
+  }
+};
+template <typename T> struct Chan<T, 1> {
+  static __device__ __forceinline__ void ld(const T *p, float (&v)[1]) { v[0] = Store<T>::ld(p); }
+};
+
+template <typename T, int D, int G>
+__global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpool, const T *__restrict__ vpool,
+                                                      int64_t num_slots, int L, int Hkv,
+                                                      const ikv_session *__restrict__ sess, const T *__restrict__ q,
+                                                      const int32_t *__restrict__ live,
+                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws) {
+  constexpr int CPL = D / 64;          // value channels per lane
+  __shared__ float qs[G][D];
+  __shared__ float pw[4][G][DEC_BLOCK];
+  __shared__ int sl[4][DEC_BLOCK];
+  __shared__ float red[4][G][2];
+  __shared__ float ored[4][G][D];
+
+  const int b = blockIdx.z;
+  const ikv_session s = sess[b];
+  const int Hq = Hkv * G;
+  const int u = blockIdx.y, l = u / Hkv, g = u - l * Hkv;
+  const int split = blockIdx.x, nsplit = gridDim.x;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int n = n_live[b];
+  n = n < 0 ? 0 : (n > s.N ? s.N : n);
+  const int chunk = int(cdiv(n, nsplit));
+  const int k0 = split * chunk, k1 = min(n, k0 + chunk);
+  const float scale = 1.0f / sqrtf(float(D));
+  for (int e = t; e < G * D; e += 256) {
+    const int h = e / D, d = e - h * D;
+    qs[h][d] = Store<T>::ld(q + ((int64_t(b) * L + l) * Hq + g * G + h) * D + d) * scale;
+  }
+  __syncthreads();
+  const int32_t *lv = live + s.slot_off;
+  float m[G], lsum[G], o[G][CPL];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m[h] = -INFINITY;
+    lsum[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) o[h][i] = 0.f;
+  }
+  const int64_t row_stride = int64_t(Hkv) * D;
+  const T *kbase = kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
+  const T *vbase = vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
+  for (int base = k0 + w * DEC_BLOCK; base < k1; base += 4 * DEC_BLOCK) {
+    const int kk = base + lane;
+    const bool valid = kk < k1;
+    const int slot = valid ? lv[kk] : 0;
+    float x[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) x[h] = 0.f;
+    if (valid) {
+      const T *kr = kbase + int64_t(slot) * row_stride;
+#pragma unroll 4
+      for (int d = 0; d < D; d += 8) {
+        float kv[8];
+        load8(kr + d, kv);
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float4 q0 = *reinterpret_cast<const float4 *>(&qs[h][d]);
+          const float4 q1 = *reinterpret_cast<const float4 *>(&qs[h][d + 4]);
+          x[h] = fmaf(kv[0], q0.x, x[h]);
+          x[h] = fmaf(kv[1], q0.y, x[h]);
+          x[h] = fmaf(kv[2], q0.z, x[h]);
+          x[h] = fmaf(kv[3], q0.w, x[h]);
+          x[h] = fmaf(kv[4], q1.x, x[h]);
+          x[h] = fmaf(kv[5], q1.y, x[h]);
+          x[h] = fmaf(kv[6], q1.z, x[h]);
+          x[h] = fmaf(kv[7], q1.w, x[h]);
+        }
+      }
+    }
+    sl[w][lane] = slot;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float xv = valid ? x[h] : -INFINITY;
+      const float mn = fmaxf(m[h], wave_max(xv));
+      const float corr = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mn);
+      const float p = valid ? __expf(xv - mn) : 0.f;
+      lsum[h] = lsum[h] * corr + wave_sum(p);
+      m[h] = mn;
+      pw[w][h][lane] = p;
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) o[h][i] *= corr;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int nb = min(DEC_BLOCK, k1 - base);
+    for (int i = 0; i < nb; ++i) {
+      const T *vr = vbase + int64_t(sl[w][i]) * row_stride;
+      float v[CPL];
+      Chan<T, CPL>::ld(vr + lane * CPL, v);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float p = pw[w][h][i];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) o[h][c] = fmaf(p, v[c], o[h][c]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  }
+  // merge the four wavefronts
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      red[w][h][0] = m[h];
+      red[w][h][1] = lsum[h];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float mm = -INFINITY;
+    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
+    const float f = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mm);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) ored[w][h][lane * CPL + c] = o[h][c] * f;
+  }
+  __syncthreads();
+  for (int e = t; e < G * (D + 2); e += 256) {
+    const int h = e / (D + 2), d = e - h * (D + 2);
+    float mm = -INFINITY;
+    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
+    float val;
+    if (d == 0) {
+      val = mm;
+    } else if (d == 1) {
+      val = 0.f;
+      for (int k = 0; k < 4; ++k)
+        if (red[k][h][0] != -INFINITY) val += red[k][h][1] * __expf(red[k][h][0] - mm);
+    } else {
+      val = (ored[0][h][d - 2] + ored[1][h][d - 2]) + (ored[2][h][d - 2] + ored[3][h][d - 2]);
+    }
+    const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
+    ws[(row * nsplit + split) * (D + 2) + d] = val;
+  }
+}
+
+template <typename T, int D>
+__global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ ws, int nsplit, int L, int Hq,
+                                                      T *__restrict__ out) {
+  const int64_t row = int64_t(blockIdx.y) * L * Hq + blockIdx.x;
+  const float *p = ws + row * nsplit * (D + 2);
+  const int d = threadIdx.x;
+  float mm = -INFINITY;
+  for (int k = 0; k < nsplit; ++k) mm = fmaxf(mm, p[k * (D + 2)]);
+  float lsum = 0.f, acc = 0.f;
+  if (mm != -INFINITY) {
+    for (int k = 0; k < nsplit; ++k) {
+      const float mk = p[k * (D + 2)];
+      if (mk == -INFINITY) continue;
+      const float f = expf(mk - mm);
+      lsum = fmaf(p[k * (D + 2) + 1], f, lsum);
+      acc = fmaf(p[k * (D + 2) + 2 + d], f, acc);
+    }
+  }
+  out[row * D + d] = Store<T>::from(lsum > 0.f ? acc / lsum : 0.f);
+}
+
+template <typename T, int D, int G>
+static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
+                                  const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
+  k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
+      (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws);
+  k_decode_combine<T, D><<<dim3(p.L * p.Hq, B), D, 0, st>>>(ws, splits, p.L, p.Hq, (T *)out);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t launch_decode_d(const ikv_pool &p, const ikv_session *sd, int B, int splits, const void *q,
+                                  const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
+  switch (p.Hq / p.Hkv) {
+    case 1: return launch_decode_g<T, D, 1>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 2: return launch_decode_g<T, D, 2>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 3: return launch_decode_g<T, D, 3>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 4: return launch_decode_g<T, D, 4>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 5: return launch_decode_g<T, D, 5>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 6: return launch_decode_g<T, D, 6>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    case 7: return launch_decode_g<T, D, 7>(p, sd, B, splits, q, live, n_live, out, ws, st);
+    default: return launch_decode_g<T, D, 8>(p, sd, B, splits, q, live, n_live, out, ws, st);
+  }
+}
+
+hipError_t launch_decode(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
+                         const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
+  const bool bf = p.kv_dtype == IKV_BF16;
+  if (p.D == 128)
+    return bf ? launch_decode_d<uint16_t, 128>(p, sess_dev, B, splits, q, live, n_live, out, ws, st)
+              : launch_decode_d<float, 128>(p, sess_dev, B, splits, q, live, n_live, out, ws, st);
+  return bf ? launch_decode_d<uint16_t, 64>(p, sess_dev, B, splits, q, live, n_live, out, ws, st)
+            : launch_decode_d<float, 64>(p, sess_dev, B, splits, q, live, n_live, out, ws, st);
+}
+
+}  // namespace ikv

@@ -1,0 +1,194 @@
+"""Python binding of libikv.so (include/ikv.h): argument marshalling only.
+
+Every function here hands raw device pointers of torch tensors to the C ABI and
+raises IkvError on a non-zero status. All arithmetic runs in the HIP kernels; if
+the library is not built, loading it raises instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import c_float, c_int32, c_int64, c_size_t, c_uint32, c_void_p
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libikv.so")
+
+IKV_BF16, IKV_F32 = 0, 1
+IKV_RESIDUAL, IKV_NO_XATTN = 1, 2
+CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE = 1, 2, 3, 4
+STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE", -4: "IKV_EUNSUPPORTED",
+          -5: "IKV_EHIP"}
+
+# Every symbol include/ikv.h declares.
+SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget",
+           "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error")
+
+
+class IkvError(RuntimeError):
+    def __init__(self, status: int, func: str, msg: str):
+        super().__init__(f"{func}: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Pool(ctypes.Structure):
+    _fields_ = [("L", c_int32), ("Hq", c_int32), ("Hkv", c_int32), ("D", c_int32),
+                ("num_slots", c_int64), ("dead_slot", c_int32), ("kv_dtype", c_int32),
+                ("k_pool", c_void_p), ("v_pool", c_void_p)]
+
+
+class Session(ctypes.Structure):
+    _fields_ = [("slot_off", c_int64), ("mem_off", c_int64), ("qspan_off", c_int64), ("qpos_off", c_int64),
+                ("N", c_int32), ("pi", c_int32), ("qs", c_int32), ("qe", c_int32), ("C", c_int32),
+                ("radix_prefix", c_int32), ("R", c_int32), ("nq", c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libikv.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_09916_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, S = ctypes.POINTER(Pool), ctypes.POINTER(Session)
+        sig = {
+            "ikv_init_dead_slot": [P, c_void_p],
+            "ikv_qm_update": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_float, c_void_p],
+            "ikv_score_history": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_uint32,
+                                  c_void_p, c_void_p, c_size_t, c_void_p],
+            "ikv_select_budget": [S, c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                  c_void_p, c_size_t, c_void_p],
+            "ikv_redirect_slots": [S, c_void_p, c_int32, c_int64, c_void_p, c_int32, c_void_p, c_void_p, c_void_p,
+                                   c_void_p, c_void_p, c_void_p, c_size_t, c_void_p],
+            "ikv_decode_attend_slotmap": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                          c_void_p, c_size_t, c_void_p],
+            "ikv_workspace_bytes": [P, S, c_int32, c_int32, c_uint32, ctypes.POINTER(c_size_t)],
+        }
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = c_int32
+        L.ikv_last_error.argtypes = []
+        L.ikv_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int, func: str) -> None:
+    if status != 0:
+        raise IkvError(status, func, lib().ikv_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+# ----------------------------------------------------------------------------- descriptors
+
+def make_pool(k_pool, v_pool, L, Hq, Hkv, D, num_slots, dead_slot=0) -> Pool:
+    """Pool descriptor over two device tensors [L][num_slots][Hkv][D] (bfloat16 or float32)."""
+    import torch
+    dt = {torch.bfloat16: IKV_BF16, torch.float32: IKV_F32}[k_pool.dtype]
+    return Pool(L, Hq, Hkv, D, num_slots, dead_slot, dt, k_pool.data_ptr(), v_pool.data_ptr())
+
+
+class Sessions:
+    """Host array of session descriptors plus its device copy (same bytes)."""
+
+    def __init__(self, rows, device):
+        import torch
+        self.B = len(rows)
+        self.host = (Session * max(1, self.B))()
+        for i, r in enumerate(rows):
+            for k, v in r.items():
+                setattr(self.host[i], k, int(v))
+        raw = bytes(memoryview(self.host).cast("B"))[: self.B * ctypes.sizeof(Session)]
+        self.dev = torch.frombuffer(bytearray(raw or b"\0"), dtype=torch.uint8).to(device)
+
+    @property
+    def host_ptr(self):
+        return ctypes.cast(self.host, ctypes.POINTER(Session))
+
+    @property
+    def dev_ptr(self) -> int:
+        return self.dev.data_ptr()
+
+    def __getitem__(self, i) -> Session:
+        return self.host[i]
+
+
+class Workspace:
+    """Reusable device scratch, grown on demand and kept 256-byte aligned."""
+
+    def __init__(self, device):
+        self.device = device
+        self.buf = None
+        self.nbytes = 0
+
+    def get(self, nbytes: int):
+        import torch
+        if nbytes == 0:
+            return None, 0
+        if self.buf is None or self.nbytes < nbytes:
+            self.buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+            self.nbytes = nbytes
+        p = self.buf.data_ptr()
+        return (p + 255) & ~255, nbytes
+
+
+def workspace_bytes(pool: Pool | None, sess: Sessions, call: int, flags: int = 0) -> int:
+    n = c_size_t(0)
+    _check(lib().ikv_workspace_bytes(ctypes.byref(pool) if pool is not None else None, sess.host_ptr, sess.B,
+                                     call, flags, ctypes.byref(n)), "ikv_workspace_bytes")
+    return n.value
+
+
+# ----------------------------------------------------------------------------- calls
+
+def init_dead_slot(pool: Pool, stream=None) -> None:
+    _check(lib().ikv_init_dead_slot(ctypes.byref(pool), _stream(stream)), "ikv_init_dead_slot")
+
+
+def qm_update(pool: Pool, sess: Sessions, M, q_span, lam: float = 0.5, stream=None) -> None:
+    _check(lib().ikv_qm_update(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(M), _ptr(q_span),
+                               float(lam), _stream(stream)), "ikv_qm_update")
+
+
+def score_history(pool: Pool, sess: Sessions, slot_maps, M, scores, ws: Workspace, qpos=None, residual=None,
+                  flags: int = 0, stream=None) -> None:
+    wp, wn = ws.get(workspace_bytes(pool, sess, CALL_SCORE, flags))
+    _check(lib().ikv_score_history(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps),
+                                   _ptr(M), _ptr(qpos), _ptr(residual), flags, _ptr(scores), wp, wn,
+                                   _stream(stream)), "ikv_score_history")
+
+
+def select_budget(sess: Sessions, slot_maps, dead_slot: int, scores, keep, n_keep, tau, stream=None) -> None:
+    _check(lib().ikv_select_budget(sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps), dead_slot, _ptr(scores),
+                                   _ptr(keep), _ptr(n_keep), _ptr(tau), None, 0, _stream(stream)),
+           "ikv_select_budget")
+
+
+def redirect_slots(sess: Sessions, num_slots: int, slot_maps, dead_slot: int, keep, freed, n_freed, live, n_live,
+                   ws: Workspace, stream=None) -> None:
+    pool = Pool()
+    pool.num_slots = num_slots
+    wp, wn = ws.get(workspace_bytes(pool, sess, CALL_REDIRECT))
+    _check(lib().ikv_redirect_slots(sess.host_ptr, sess.dev_ptr, sess.B, num_slots, _ptr(slot_maps), dead_slot,
+                                    _ptr(keep), _ptr(freed), _ptr(n_freed), _ptr(live), _ptr(n_live), wp, wn,
+                                    _stream(stream)), "ikv_redirect_slots")
+
+
+def decode_attend_slotmap(pool: Pool, sess: Sessions, q, live, n_live, out, ws: Workspace, stream=None) -> None:
+    wp, wn = ws.get(workspace_bytes(pool, sess, CALL_DECODE))
+    _check(lib().ikv_decode_attend_slotmap(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(q),
+                                           _ptr(live), _ptr(n_live), _ptr(out), wp, wn, _stream(stream)),
+           "ikv_decode_attend_slotmap")
+

@@ -349,3 +349,41 @@ def qwen25_14b_92k_heavy(R: int = 64, seed: int = 3) -> Batch:
     N = 92300
     s = SessionSpec(N=N, C=8192, pi=0, qs=N - 64, qe=N, R=R, heavy_frac=0.05, heavy_scale=4.0)
     return make_batch(qwen25_14b_shape(), [s], seed=seed, kv_dtype=BF16, layout="paged")
+
+
+# ----------------------------------------------------------------------------- isolated-call inputs
+
+def score_vector(n: int, seed: int, ties: bool = True) -> np.ndarray:
+    """float32 scores for selection tests: many exact ties, NaN, -0.0, +0.0 and infinities."""
+    g = stream(seed, T_MISC_SCORES)
+    if ties:
+        s = g.integers(-20, 20, n).astype(np.float32) * np.float32(0.125)
+    else:
+        s = g.standard_normal(n).astype(np.float32)
+    k = max(1, n // 50)
+    idx = g.choice(n, size=min(n, 5 * k), replace=False)
+    s[idx[:k]] = np.nan
+    s[idx[k:2 * k]] = -0.0
+    s[idx[2 * k:3 * k]] = 0.0
+    s[idx[3 * k:4 * k]] = -np.inf
+    s[idx[4 * k:5 * k]] = np.float32(1e30)
+    return s
+
+
+def keep_mask(S: np.ndarray, seed: int, frac: float = 0.3, dead: int = DEAD_SLOT) -> np.ndarray:
+    """uint8 keep mask over live positions (about `frac` of them), for isolated redirect tests."""
+    g = stream(seed, T_MISC_KEEP)
+    return ((g.random(len(S)) < frac) & (S != dead)).astype(np.uint8)
+
+
+def alias_slots(S: np.ndarray, seed: int, pairs: int) -> np.ndarray:
+    """Copy of S where `pairs` live positions reuse the slot of another live position."""
+    g = stream(seed, T_MISC_ALIAS)
+    S = S.copy()
+    live = np.nonzero(S != DEAD_SLOT)[0]
+    pick = g.choice(live, size=2 * pairs, replace=False)
+    S[pick[:pairs]] = S[pick[pairs:]]
+    return S
+
+
+T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS = 20, 21, 22

@@ -1,0 +1,60 @@
+"""Comparison rules between the HIP path and the float64 oracle.
+
+* scores: |s_gpu - s_o| <= 1e-3 |s_o| + 1e-6 max|s_o| on candidates, -inf elsewhere;
+* kept sets: identical except at positions whose oracle score lies within
+  1e-5 |tau_o| of the oracle threshold tau_o; the kept counts are identical;
+* attention outputs: |o_gpu - o_o| <= 2e-3 plus half a bf16 ulp of o_o for bf16
+  outputs (the output is rounded to bf16), 2e-3 for float32 outputs.
+"""
+import math
+
+import numpy as np
+
+SCORE_RTOL = 1e-3
+SCORE_FLOOR = 1e-6
+BAND = 1e-5
+ATTN_ATOL = 2e-3
+
+
+def check_scores(s_gpu, s_o, cand):
+    s_gpu = np.asarray(s_gpu, np.float64)
+    assert np.all(np.isneginf(s_gpu[~cand])), "non-candidates must score -inf"
+    if not cand.any():
+        return 0.0
+    a, o = s_gpu[cand], s_o[cand]
+    tol = SCORE_RTOL * np.abs(o) + SCORE_FLOOR * np.abs(o).max()
+    err = np.abs(a - o)
+    bad = np.nonzero(err > tol)[0]
+    assert len(bad) == 0, f"{len(bad)} scores out of tolerance, worst {err.max():.3e}"
+    return float((err / np.maximum(np.abs(o), 1e-300)).max())
+
+
+def band_positions(s_o, tau_o, cand):
+    if not math.isfinite(tau_o):
+        return np.zeros_like(cand)
+    return cand & (np.abs(s_o - tau_o) <= BAND * abs(tau_o))
+
+
+def check_keep(keep_gpu, n_keep_gpu, keep_o, n_keep_o, s_o, tau_o, cand):
+    keep_gpu = np.asarray(keep_gpu).astype(bool)
+    assert n_keep_gpu == n_keep_o, f"kept count {n_keep_gpu} != {n_keep_o}"
+    assert int(keep_gpu.sum()) == n_keep_o
+    band = band_positions(s_o, tau_o, cand)
+    diff = keep_gpu != keep_o
+    outside = diff & ~band
+    assert not outside.any(), f"{int(outside.sum())} kept-set differences outside the band"
+    return int(diff.sum())
+
+
+def bf16_half_ulp(x):
+    ax = np.abs(np.asarray(x, np.float64))
+    e = np.floor(np.log2(np.where(ax > 0, ax, 1.0)))
+    return np.where(ax > 0, np.exp2(e - 8), 0.0)
+
+
+def check_attention(o_gpu, o_o, bf16: bool):
+    o_gpu = np.asarray(o_gpu, np.float64)
+    tol = ATTN_ATOL + (bf16_half_ulp(o_o) if bf16 else 0.0)
+    err = np.abs(o_gpu - o_o)
+    assert np.all(err <= tol), f"attention error {err.max():.3e} above tolerance"
+    return float(err.max())

@@ -1,0 +1,360 @@
+"""HIP path vs the float64 oracle, call by call and end to end, through the C ABI.
+
+Inputs come from the seeded generator; expected values come from the oracle only.
+Where several results are correct (kept-set members whose score lies within the
+selection band of the threshold), the unique parts are compared and the rest is
+checked for validity.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2606_09916_amd import ikv
+from paper_2606_09916_amd.step import RetentionStep
+from parity import band_positions, check_attention, check_keep, check_scores
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def sess_sets(batch, b, S=None):
+    s = batch.sessions[b]
+    S = batch.S(b) if S is None else S
+    return oracle.sets(S, s.pi, s.qs, s.qe, s.C, synth.DEAD_SLOT)
+
+
+def seg(arr, batch, b):
+    o = int(batch.slot_off[b])
+    return arr[o:o + batch.sessions[b].N]
+
+
+def oracle_scores(batch, b, blob=None, flags=0, M=None, S=None):
+    s = batch.sessions[b]
+    S = batch.S(b) if S is None else S
+    M = batch.M_of(b) if M is None else M
+    st = sess_sets(batch, b, S)
+    return oracle.scores(batch.k_pool, S, st, M, batch.shape.Hkv, s.R, blob, flags,
+                         batch.qpos_of(b), synth.DEAD_SLOT), st
+
+
+def tiny_bf16(R=16, seed=11):
+    N = 2048
+    s = synth.SessionSpec(N=N, C=512, pi=0, qs=N - 32, qe=N, R=R)
+    return synth.make_batch(synth.tiny_shape(), [s], seed=seed, kv_dtype=synth.BF16, layout="paged")
+
+
+# ============================================================================ sentinel
+
+@pytest.mark.parametrize("kind", ["f32", "bf16"])
+def test_init_dead_slot(dev, kind):
+    batch = synth.tiny_single_layer() if kind == "f32" else tiny_bf16()
+    st = RetentionStep(batch, dev)
+    st.init_dead_slot()
+    k, v = st.host("k_pool"), st.host("v_pool")
+    kw = synth.widen(k[:, 0])
+    assert np.all(kw == (-1.0e4 if kind == "f32" else -9984.0))
+    assert np.all(synth.widen(v[:, 0]) == 0)
+    assert np.array_equal(k[:, 1:], batch.k_pool[:, 1:]) and np.array_equal(v[:, 1:], batch.v_pool[:, 1:])
+
+
+# ============================================================================ Eq. 2
+
+@pytest.mark.parametrize("kind,lam", [("f32", 0.5), ("bf16", 0.5), ("f32", math.inf)])
+def test_qm_update(dev, kind, lam):
+    batch = synth.tiny_single_layer() if kind == "f32" else tiny_bf16()
+    st = RetentionStep(batch, dev)
+    st.qm_update(lam)
+    got = st.host("M").reshape(batch.M_of(0).shape)
+    want = oracle.qm_update(batch.M_of(0), batch.q_span_of(0), lam)
+    np.testing.assert_allclose(got, want, rtol=0, atol=2e-6)
+    st.qm_update(lam)                                  # a second turn on the updated memory
+    want2 = oracle.qm_update(want, batch.q_span_of(0), lam)
+    np.testing.assert_allclose(st.host("M").reshape(want.shape), want2, rtol=0, atol=4e-6)
+
+
+# ============================================================================ Eq. 3
+
+@pytest.mark.parametrize("layout,R,dead_frac", [("identity", 16, 0.0), ("shuffled", 16, 0.2), ("identity", 4, 0.0),
+                                                ("shuffled", 7, 0.5)])
+def test_rule_scores_tiny(dev, layout, R, dead_frac):
+    batch = synth.tiny_single_layer(R=R, layout=layout, dead_frac=dead_frac)
+    st = RetentionStep(batch, dev)
+    st.init_dead_slot()
+    st.score(flags=0)
+    want, sets = oracle_scores(batch, 0)
+    rel = check_scores(st.host("scores"), want, sets["cand"])
+    assert rel < 1e-5, rel
+    assert math.isclose(float(st.host("scores")[sets["cand"]].astype(np.float64).sum()), 2 * R, rel_tol=1e-5)
+
+
+def test_rule_scores_bf16_tiny(dev):
+    batch = tiny_bf16(R=32)
+    st = RetentionStep(batch, dev)
+    st.score(flags=0)
+    want, sets = oracle_scores(batch, 0)
+    assert check_scores(st.host("scores"), want, sets["cand"]) < 1e-5
+
+
+# ============================================================================ Eqs. 4-6
+
+@pytest.mark.parametrize("variant,flags", [("random", ikv.IKV_RESIDUAL), ("random", ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN),
+                                           ("alpha7", ikv.IKV_RESIDUAL)])
+def test_residual_scores_tiny(dev, variant, flags):
+    batch = synth.tiny_single_layer(R=16, layout="shuffled")
+    blob = synth.residual_blob(64, seed=5, variant="random", alpha=7.0 if variant == "alpha7" else 1.0)
+    st = RetentionStep(batch, dev, residual=blob, flags=flags)
+    st.score()
+    want, sets = oracle_scores(batch, 0, blob, flags)
+    rel = check_scores(st.host("scores"), want, sets["cand"])
+    assert rel < 1e-4, rel
+
+
+def test_zero_initialised_head_is_bitwise_the_rule(dev):
+    batch = synth.tiny_single_layer(R=16)
+    blob = synth.residual_blob(64, seed=6, variant="zero")
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.score()
+    with_head = st.host("scores").copy()
+    st.score(flags=0)
+    assert np.array_equal(with_head, st.host("scores"))
+    blob0 = synth.residual_blob(64, seed=6, variant="random", alpha=0.0)
+    st0 = RetentionStep(batch, dev, residual=blob0, flags=ikv.IKV_RESIDUAL)
+    st0.score()
+    assert np.array_equal(st0.host("scores"), with_head)
+
+
+def test_residual_without_live_query_positions(dev):
+    batch = synth.tiny_single_layer(R=8)
+    s = batch.sessions[0]
+    s.qpos = np.array([10, 20, 30], dtype=np.int32)
+    batch.qpos = s.qpos.copy()
+    batch.slot_maps[[10, 20, 30]] = synth.DEAD_SLOT
+    blob = synth.residual_blob(64, seed=7)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.score()
+    want, sets = oracle_scores(batch, 0, blob, ikv.IKV_RESIDUAL)
+    check_scores(st.host("scores"), want, sets["cand"])
+    st.score(flags=ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN)
+    want2, _ = oracle_scores(batch, 0, blob, ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN)
+    np.testing.assert_array_equal(want, want2)
+    check_scores(st.host("scores"), want2, sets["cand"])
+
+
+# ============================================================================ Eq. 1
+
+@pytest.mark.parametrize("C,pi", [(512, 0), (300, 40), (60, 50), (10, 40), (2000, 0), (2048, 0), (5000, 0)])
+def test_select_isolated_exact(dev, C, pi):
+    torch = _torch()
+    batch = synth.tiny_single_layer(R=4, layout="shuffled", dead_frac=0.1)
+    s = batch.sessions[0]
+    s.C, s.pi = C, pi
+    st = RetentionStep(batch, dev)
+    sc = synth.score_vector(s.N, seed=C + pi)
+    st.scores.copy_(torch.from_numpy(sc).to(dev))
+    st.select()
+    sets = sess_sets(batch, 0)
+    keep_o, n_o, tau_o = oracle.select_budget(sc.astype(np.float64), sets)
+    assert np.array_equal(st.host("keep").astype(bool), keep_o)
+    assert int(st.host("n_keep")[0]) == n_o
+    tau = float(st.host("tau")[0])
+    assert tau == tau_o or (math.isnan(tau) and math.isnan(tau_o))
+
+
+def test_select_on_scores_tiny(dev):
+    batch = synth.tiny_single_layer(R=16, layout="shuffled", dead_frac=0.1)
+    blob = synth.residual_blob(64, seed=8)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.score()
+    st.select()
+    want, sets = oracle_scores(batch, 0, blob, ikv.IKV_RESIDUAL)
+    keep_o, n_o, tau_o = oracle.select_budget(want, sets)
+    check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
+    assert math.isclose(float(st.host("tau")[0]), tau_o, rel_tol=1e-5)
+
+
+# ============================================================================ Eq. 7
+
+@pytest.mark.parametrize("radix,aliases", [(0, 0), (100, 0), (300, 40)])
+def test_redirect_isolated_exact(dev, radix, aliases):
+    torch = _torch()
+    batch = synth.tiny_single_layer(R=4, layout="shuffled", dead_frac=0.15)
+    s = batch.sessions[0]
+    s.radix_prefix = radix
+    S = batch.S(0)
+    if aliases:
+        S = synth.alias_slots(S, seed=radix, pairs=aliases)
+        batch.slot_maps[:] = S
+    keep = synth.keep_mask(S, seed=radix + 1)
+    st = RetentionStep(batch, dev)
+    st.keep.copy_(torch.from_numpy(keep).to(dev))
+    k_before = st.host("k_pool").copy()
+    st.redirect()
+    S_o, freed_o, live_o = oracle.redirect(S, keep.astype(bool), synth.DEAD_SLOT, radix)
+    assert np.array_equal(st.host("S"), S_o)
+    nf, nl = int(st.host("n_freed")[0]), int(st.host("n_live")[0])
+    assert np.array_equal(st.host("freed")[:nf], freed_o)
+    assert np.array_equal(st.host("live")[:nl], live_o)
+    assert np.array_equal(st.host("k_pool"), k_before)          # no K/V row moves
+
+
+# ============================================================================ decode
+
+@pytest.mark.parametrize("kind,frac", [("f32", 0.25), ("bf16", 0.25), ("f32", 0.0005), ("bf16", 1.0)])
+def test_decode_isolated(dev, kind, frac):
+    torch = _torch()
+    batch = synth.tiny_single_layer() if kind == "f32" else tiny_bf16()
+    S = batch.S(0)
+    keep = synth.keep_mask(S, seed=3, frac=frac)
+    live = S[keep.astype(bool)].astype(np.int32)
+    st = RetentionStep(batch, dev)
+    st.live[:len(live)].copy_(torch.from_numpy(live).to(dev))
+    st.n_live.fill_(len(live))
+    st.decode()
+    want = oracle.decode(batch.q_dec[0], batch.k_pool, batch.v_pool, live)
+    got = synth.widen(st.host("out")[0])
+    check_attention(got, want, bf16=(kind == "bf16"))
+
+
+def test_decode_empty_live_list(dev):
+    batch = synth.tiny_single_layer()
+    st = RetentionStep(batch, dev)
+    st.n_live.fill_(0)
+    st.decode()
+    assert np.all(st.host("out") == 0)
+
+
+# ============================================================================ whole step
+
+def _compare_step(st, batch, b, blob, flags, update_memory):
+    s = batch.sessions[b]
+    M = oracle.qm_update(batch.M_of(b), batch.q_span_of(b)) if update_memory else batch.M_of(b)
+    if update_memory:
+        np.testing.assert_allclose(seg_M(st, batch, b), M, atol=4e-6, rtol=0)
+    want, sets = oracle_scores(batch, b, blob, flags, M=M)
+    check_scores(seg(st.host("scores"), batch, b), want, sets["cand"])
+    keep_o, n_o, tau_o = oracle.select_budget(want, sets)
+    nk = int(st.host("n_keep")[b])
+    keep_g = seg(st.host("keep"), batch, b).astype(bool)
+    ndiff = check_keep(keep_g, nk, keep_o, n_o, want, tau_o, sets["cand"])
+    S_o, freed_o, live_o = oracle.redirect(batch.S(b), keep_o, synth.DEAD_SLOT, s.radix_prefix)
+    S_g = seg(st.host("S"), batch, b)
+    band = band_positions(want, tau_o, sets["cand"])
+    assert np.array_equal(S_g[~band], S_o[~band])
+    assert np.all((S_g[band] == batch.S(b)[band]) | (S_g[band] == synth.DEAD_SLOT))
+    nl, nf = int(st.host("n_live")[b]), int(st.host("n_freed")[b])
+    live_g = seg(st.host("live"), batch, b)[:nl]
+    assert np.array_equal(live_g, S_g[S_g != synth.DEAD_SLOT])
+    freed_g = seg(st.host("freed"), batch, b)[:nf]
+    band_slots = set(batch.S(b)[band].tolist())
+    assert set(freed_g.tolist()) ^ set(freed_o.tolist()) <= band_slots
+    if ndiff == 0:
+        assert np.array_equal(live_g, live_o) and np.array_equal(freed_g, freed_o)
+        o = synth.widen(st.host("out")[b])
+        check_attention(o, oracle.decode(batch.q_dec[b], batch.k_pool, batch.v_pool, live_o),
+                        bf16=batch.kv_dtype == synth.BF16)
+    return ndiff
+
+
+def seg_M(st, batch, b):
+    s, sh = batch.sessions[b], batch.shape
+    o = int(batch.mem_off[b])
+    return st.host("M")[o:o + sh.L * sh.Hkv * s.R * sh.D].reshape(sh.L, sh.Hkv * s.R, sh.D)
+
+
+@pytest.mark.parametrize("update_memory", [False, True])
+def test_step_end_to_end_tiny(dev, update_memory):
+    batch = synth.tiny_single_layer(R=16, layout="shuffled", dead_frac=0.05)
+    blob = synth.residual_blob(64, seed=9)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    st.step(update_memory=update_memory)
+    _compare_step(st, batch, 0, blob, ikv.IKV_RESIDUAL, update_memory)
+
+
+def test_step_batched_ragged(dev):
+    """Three sessions of different length, budget, memory rows and forced sets in one
+    pool, plus an empty one and one that the N <= C gate skips."""
+    shape = synth.Shape(L=2, Hq=8, Hkv=2, D=64)
+    sessions = [synth.SessionSpec(N=1000, C=300, pi=16, qs=960, qe=1000, R=4, radix_prefix=16, dead_frac=0.1),
+                synth.SessionSpec(N=2500, C=700, pi=0, qs=2440, qe=2500, R=16),
+                synth.SessionSpec(N=0, C=10, pi=0, qs=0, qe=0, R=3),
+                synth.SessionSpec(N=300, C=400, pi=8, qs=280, qe=300, R=7, dead_frac=0.2),
+                synth.SessionSpec(N=777, C=100, pi=50, qs=700, qe=777, R=5)]
+    batch = synth.make_batch(shape, sessions, seed=21, kv_dtype=synth.BF16, layout="paged", spare_pages=7)
+    blob = synth.residual_blob(64, seed=10)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    st.step(update_memory=True)
+    for b in range(len(sessions)):
+        if sessions[b].N == 0:
+            assert int(st.host("n_keep")[b]) == 0 and int(st.host("n_live")[b]) == 0
+            continue
+        _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, True)
+    # the gated session: nothing scored, nothing dropped
+    b = 3
+    assert np.all(np.isneginf(seg(st.host("scores"), batch, b)))
+    assert np.array_equal(seg(st.host("S"), batch, b), batch.S(b))
+    assert float(st.host("tau")[b]) == -math.inf and int(st.host("n_freed")[b]) == 0
+
+
+def test_step_forced_set_exceeds_budget(dev):
+    batch = synth.tiny_single_layer(R=4)
+    s = batch.sessions[0]
+    s.pi = 600                          # |F| = 600 + 32 > C = 512: C* = 0
+    st = RetentionStep(batch, dev)
+    st.step(update_memory=False)
+    sets = sess_sets(batch, 0)
+    assert np.array_equal(st.host("keep").astype(bool), sets["forced"])
+    assert float(st.host("tau")[0]) == math.inf and int(st.host("n_keep")[0]) == int(sets["forced"].sum())
+
+
+def test_step_no_candidates(dev):
+    batch = synth.tiny_single_layer(R=4, dead_frac=1.0)
+    st = RetentionStep(batch, dev)
+    st.step(update_memory=False)
+    sets = sess_sets(batch, 0)
+    assert not sets["cand"].any()
+    assert np.all(np.isneginf(st.host("scores")))
+    assert np.array_equal(st.host("keep").astype(bool), sets["forced"])
+
+
+def test_step_is_deterministic_and_layout_invariant(dev):
+    blob = synth.residual_blob(64, seed=12)
+    outs = []
+    for layout in ("identity", "shuffled", "shuffled"):
+        batch = synth.tiny_single_layer(R=16, layout=layout)
+        st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+        st.step(update_memory=True)
+        outs.append((st.host("scores").copy(), st.host("keep").copy(), st.host("out").copy(), st.host("M").copy()))
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+    for a, b in zip(outs[1], outs[2]):
+        assert np.array_equal(a, b)
+
+
+# ============================================================================ full size
+
+@pytest.fixture(scope="module")
+def qwen3_8b(dev):
+    batch = synth.qwen3_8b_32k(R=64)
+    blob = synth.residual_blob(128, seed=22)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    return batch, blob, st
+
+
+def test_qwen3_8b_32k_step_full(qwen3_8b):
+    """Full Qwen3-8B-shaped step (36 layers, 8 KV heads, 32,768 positions, budget 8192,
+    64 memory rows per KV head, residual head on) against the full oracle."""
+    batch, blob, st = qwen3_8b
+    st.reset()
+    st.step(update_memory=False)
+    ndiff = _compare_step(st, batch, 0, blob, ikv.IKV_RESIDUAL, False)
+    print(f"kept-set differences inside the band: {ndiff}")
