@@ -26,7 +26,8 @@ def check_scores(s_gpu, s_o, cand):
     err = np.abs(a - o)
     bad = np.nonzero(err > tol)[0]
     assert len(bad) == 0, f"{len(bad)} scores out of tolerance, worst {err.max():.3e}"
-    return float((err / np.maximum(np.abs(o), 1e-300)).max())
+    # error relative to the score, with scores near zero measured against 1e-3 of the largest
+    return float((err / np.maximum(np.abs(o), 1e-3 * np.abs(o).max())).max())
 
 
 def band_positions(s_o, tau_o, cand):
