@@ -77,10 +77,18 @@ int max_n(const ikv_session *s, int B) {
   return m;
 }
 
+// The MFMA score passes need D = 128 and every session's R a multiple of 16.
+bool use_mfma(const ikv_pool *p, const ikv_session *s, int B) {
+  if (p->D != 128 || p->kv_dtype != IKV_BF16) return false;
+  for (int b = 0; b < B; ++b)
+    if (s[b].R % 16) return false;
+  return true;
+}
+
 size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flags) {
   const bool resid = (flags & IKV_RESIDUAL) != 0;
   const int units = p->L * p->Hkv;
-  int64_t f = ikv::score_offset(s, B, p->L, units, p->D, resid);
+  int64_t f = ikv::score_offset(s, B, p->L, units, p->D, resid, use_mfma(p, s, B));
   if (resid) f += ikv::score_shared_floats(p->D);
   return size_t(f) * sizeof(float);
 }
@@ -187,7 +195,8 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.flags = flags;
   a.scores = scores;
   a.ws = static_cast<float *>(workspace);
-  a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid);
+  a.mfma = use_mfma(pool, sess, B);
+  a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.maxR = maxR;
   a.maxNq = maxNq;

@@ -25,28 +25,41 @@ constexpr int MAX_R = 256;          // memory rows per KV head
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int64_t(63); }   // floats -> 256 B
 
-// Score workspace, per session b (floats, each block 256-byte aligned):
-//   part  [units][R][tiles][2]  per-tile (max, sum exp) of every memory row
-//   lse   [units][R][2]         (max, 1/Z) of every memory row
-//   rulep [L][N]                per-layer partial rule scores
-//   kbar  [N][D]                mean key row (residual only)
-//   kq    [nq][D]               kbar at the live query positions (residual only)
-//   kp/vp [nq][HC]              W_K kq + b_K, W_V kq + b_V (residual only)
-//   misc  [MBAR_PARTS][D] + [D] + 64   partial and final mbar, live query count (residual only)
+// Score workspace, per session b (floats, each block 256-byte aligned). Two
+// layouts: the MFMA path (D = 128, R a multiple of 16) and the VALU path.
+//   msplit [units][R][256 bf16]   memory rows pre-split into bf16 hi + lo (MFMA only)
+//   part   per-tile (max, sum exp) of every memory row:
+//            MFMA [tiles of 128][units][R][2], VALU [units][R][tiles of 256][2]
+//   lse    [units][R][2]          (max, 1/Z) of every memory row
+//   rulep  [L][N]                 per-layer partial rule scores (VALU only)
+//   kbar   [N][D]                 mean key row (residual only)
+//   kq     [nq][D]                kbar at the live query positions (residual only)
+//   kp/vp  [nq][HC]               W_K kq + b_K, W_V kq + b_V (residual only)
+//   misc   [MBAR_PARTS][D] + [D] + 64   partial and final mbar, live query count (residual only)
 // followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN].
 constexpr int MBAR_PARTS = 64;
+constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
 
 struct ScoreSizes {
-  int64_t part, lse, rulep, kbar, kq, kp, vp, misc;
-  __host__ __device__ int64_t total() const { return part + lse + rulep + kbar + kq + kp + vp + misc; }
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc;
+  __host__ __device__ int64_t total() const { return msplit + part + lse + rulep + kbar + kq + kp + vp + misc; }
+  __host__ __device__ int64_t off_part() const { return msplit; }
+  __host__ __device__ int64_t off_lse() const { return msplit + part; }
+  __host__ __device__ int64_t off_rulep() const { return msplit + part + lse; }
+  __host__ __device__ int64_t off_kbar() const { return msplit + part + lse + rulep; }
+  __host__ __device__ int64_t off_kq() const { return off_kbar() + kbar; }
+  __host__ __device__ int64_t off_kp() const { return off_kq() + kq; }
+  __host__ __device__ int64_t off_vp() const { return off_kp() + kp; }
+  __host__ __device__ int64_t off_misc() const { return off_vp() + vp; }
 };
 
-__host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid) {
+__host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid,
+                                                  bool mfma) {
   ScoreSizes z;
-  int64_t tiles = cdiv(s.N, SCORE_TILE);
-  z.part = align64f(int64_t(units) * s.R * tiles * 2);
+  z.msplit = mfma ? align64f(int64_t(units) * s.R * 128) : 0;
+  z.part = mfma ? align64f(cdiv(s.N, MFMA_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
   z.lse = align64f(int64_t(units) * s.R * 2);
-  z.rulep = align64f(int64_t(L) * s.N);
+  z.rulep = mfma ? 0 : align64f(int64_t(L) * s.N);
   z.kbar = resid ? align64f(int64_t(s.N) * D) : 0;
   z.kq = resid ? align64f(int64_t(s.nq) * D) : 0;
   z.kp = resid ? align64f(int64_t(s.nq) * HC) : 0;
@@ -57,9 +70,9 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
 
 // Offset (floats) of session b's score block: the sum of the blocks before it.
 __host__ __device__ inline int64_t score_offset(const ikv_session *sess, int b, int L, int units, int D,
-                                                bool resid) {
+                                                bool resid, bool mfma) {
   int64_t o = 0;
-  for (int i = 0; i < b; ++i) o += score_sizes(sess[i], L, units, D, resid).total();
+  for (int i = 0; i < b; ++i) o += score_sizes(sess[i], L, units, D, resid, mfma).total();
   return o;
 }
 
@@ -137,6 +150,7 @@ struct ScoreArgs {
   float *ws;           // session blocks, then the shared block
   float *ws_shared;
   int maxN, maxR, maxNq;
+  bool mfma;           // MFMA score passes (D = 128 and every R a multiple of 16)
 };
 
 hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);

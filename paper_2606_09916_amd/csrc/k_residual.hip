@@ -54,7 +54,7 @@ __global__ void k_res_transpose(const float *__restrict__ blob, float *__restric
 // Partial column sums of the memory rows: part p sums rows [p*rows/P, (p+1)*rows/P).
 template <int D>
 __global__ void __launch_bounds__(256) k_mbar_part(const ikv_session *__restrict__ sess, const float *__restrict__ M,
-                                                   float *__restrict__ ws, int L, int Hkv) {
+                                                   float *__restrict__ ws, int L, int Hkv, bool mfma) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
@@ -72,9 +72,8 @@ __global__ void __launch_bounds__(256) k_mbar_part(const ikv_session *__restrict
   if (g == 0) {
     float t = 0.f;
     for (int k = 0; k < NG; ++k) t += red[k][d];
-    const ScoreSizes z = score_sizes(s, L, units, D, true);
-    float *misc = ws + score_offset(sess, b, L, units, D, true) + z.part + z.lse + z.rulep + z.kbar + z.kq + z.kp +
-                  z.vp;
+    const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
+    float *misc = ws + score_offset(sess, b, L, units, D, true, mfma) + z.off_misc();
     misc[int64_t(p) * D + d] = t;
   }
 }
@@ -85,19 +84,19 @@ __global__ void __launch_bounds__(256) k_res_prep(const ikv_session *__restrict_
                                                   const int32_t *__restrict__ slot_maps,
                                                   const int32_t *__restrict__ qpos, int dead,
                                                   const float *__restrict__ blob, float *__restrict__ ws, int L,
-                                                  int Hkv) {
+                                                  int Hkv, bool mfma) {
   const int b = blockIdx.x;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   const int units = L * Hkv;
   const ResLayout lay(D);
-  const ScoreSizes z = score_sizes(s, L, units, D, true);
-  float *base = ws + score_offset(sess, b, L, units, D, true);
-  const float *kbar = base + z.part + z.lse + z.rulep;
-  float *kq = base + z.part + z.lse + z.rulep + z.kbar;
-  float *kp = kq + z.kq;
-  float *vp = kp + z.kp;
-  float *misc = vp + z.vp;
+  const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
+  float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
+  const float *kbar = base + z.off_kbar();
+  float *kq = base + z.off_kq();
+  float *kp = base + z.off_kp();
+  float *vp = base + z.off_vp();
+  float *misc = base + z.off_misc();
   float *mbar = misc + int64_t(MBAR_PARTS) * D;
   __shared__ int live_pos[MAX_NQ];
   __shared__ int nlive;
@@ -145,7 +144,7 @@ __global__ void __launch_bounds__(256) k_residual(const ikv_session *__restrict_
                                                   const int32_t *__restrict__ slot_maps, int dead,
                                                   float *__restrict__ scores, const float *__restrict__ ws,
                                                   const float *__restrict__ shared, const float *__restrict__ blob,
-                                                  int L, int Hkv, bool xattn) {
+                                                  int L, int Hkv, bool xattn, bool mfma) {
   constexpr int F = 3 * D + 1;
   constexpr int X = F + HC;
   constexpr int TK = 32;       // candidates per workgroup
@@ -164,12 +163,12 @@ __global__ void __launch_bounds__(256) k_residual(const ikv_session *__restrict_
   if (j0 >= s.N) return;
   const int units = L * Hkv;
   const ResLayout lay(D);
-  const ScoreSizes z = score_sizes(s, L, units, D, true);
-  const float *base = ws + score_offset(sess, b, L, units, D, true);
-  const float *kbar = base + z.part + z.lse + z.rulep;
-  const float *kp = base + z.part + z.lse + z.rulep + z.kbar + z.kq;
-  const float *vp = kp + z.kp;
-  const float *mbar = vp + z.vp + int64_t(MBAR_PARTS) * D;
+  const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
+  const float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
+  const float *kbar = base + z.off_kbar();
+  const float *kp = base + z.off_kp();
+  const float *vp = base + z.off_vp();
+  const float *mbar = base + z.off_misc() + int64_t(MBAR_PARTS) * D;
   const int nql = reinterpret_cast<const int *>(mbar)[D];
   const float *wqT = shared;
   const float *w1T = shared + align64f(int64_t(F) * HC);
@@ -313,11 +312,12 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   const int64_t F = 3 * D + 1;
   const int64_t n = F * HC + (F + HC) * HIDDEN;
   k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
-  k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv);
-  k_res_prep<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.residual, a.ws, p.L, p.Hkv);
+  k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);
+  k_res_prep<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.residual, a.ws, p.L, p.Hkv,
+                                     a.mfma);
   k_residual<D><<<dim3(unsigned(cdiv(a.maxN, 32)), a.B), 256, 0, st>>>(
       a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
-      (a.flags & IKV_NO_XATTN) == 0);
+      (a.flags & IKV_NO_XATTN) == 0, a.mfma);
   return hipGetLastError();
 }
 

@@ -76,7 +76,7 @@ __global__ void __launch_bounds__(256) k_score_stats(const T *__restrict__ kpool
   }
   const float scale = 1.0f / sqrtf(float(D));
   const int64_t tiles = cdiv(s.N, SCORE_TILE);
-  float *part = ws + score_offset(sess, b, L, units, D, resid);
+  float *part = ws + score_offset(sess, b, L, units, D, resid, false);
   const float *Mu = M + s.mem_off + int64_t(u) * s.R * D;
 
   for (int r0 = 0; r0 < s.R; r0 += RC) {
@@ -126,17 +126,17 @@ __global__ void __launch_bounds__(256) k_score_lse(const ikv_session *__restrict
   if (s.N <= s.C) return;
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= units * s.R) return;
-  float *base = ws + score_offset(sess, b, L, units, D, resid);
-  const ScoreSizes z = score_sizes(s, L, units, D, resid);
+  float *base = ws + score_offset(sess, b, L, units, D, resid, false);
+  const ScoreSizes z = score_sizes(s, L, units, D, resid, false);
   const int64_t tiles = cdiv(s.N, SCORE_TILE);
-  const float *p = base + int64_t(i) * tiles * 2;
+  const float *p = base + z.off_part() + int64_t(i) * tiles * 2;
   float m = -INFINITY;
   for (int64_t k = 0; k < tiles; ++k) m = fmaxf(m, p[2 * k]);
   double zs = 0.0;
   if (m != -INFINITY)
     for (int64_t k = 0; k < tiles; ++k)
       if (p[2 * k] != -INFINITY) zs += double(p[2 * k + 1]) * double(expf(p[2 * k] - m));
-  float *lse = base + z.part;
+  float *lse = base + z.off_lse();
   lse[2 * i] = m;
   lse[2 * i + 1] = zs > 0.0 ? float(1.0 / zs) : 0.f;
 }
@@ -167,10 +167,10 @@ __global__ void __launch_bounds__(256) k_score_rule(const T *__restrict__ kpool,
     cand = slot != dead && !is_forced(s, j);
   }
   const float scale = 1.0f / sqrtf(float(D));
-  float *base = ws + score_offset(sess, b, L, units, D, resid);
-  const ScoreSizes z = score_sizes(s, L, units, D, resid);
-  const float *lse = base + z.part;
-  float *rulep = base + z.part + z.lse;
+  float *base = ws + score_offset(sess, b, L, units, D, resid, false);
+  const ScoreSizes z = score_sizes(s, L, units, D, resid, false);
+  const float *lse = base + z.off_lse();
+  float *rulep = base + z.off_rulep();
   double acc = 0.0;
   float kr[D];
   for (int h = 0; h < Hkv; ++h) {
@@ -224,9 +224,9 @@ __global__ void __launch_bounds__(256) k_score_finish(const ikv_session *__restr
     out[j] = -INFINITY;
     return;
   }
-  const float *base = ws + score_offset(sess, b, L, units, D, resid);
-  const ScoreSizes z = score_sizes(s, L, units, D, resid);
-  const float *rulep = base + z.part + z.lse;
+  const float *base = ws + score_offset(sess, b, L, units, D, resid, false);
+  const ScoreSizes z = score_sizes(s, L, units, D, resid, false);
+  const float *rulep = base + z.off_rulep();
   double acc = 0.0;
   for (int l = 0; l < L; ++l) acc += double(rulep[int64_t(l) * s.N + j]);
   out[j] = float(acc);
@@ -247,9 +247,9 @@ __global__ void __launch_bounds__(256) k_kbar(const T *__restrict__ kpool, int64
   if (j >= s.N) return;
   const int d = (t % TPT) * 2;
   const int units = L * Hkv;
-  float *base = ws + score_offset(sess, b, L, units, D, true);
-  const ScoreSizes z = score_sizes(s, L, units, D, true);
-  float *kbar = base + z.part + z.lse + z.rulep;
+  float *base = ws + score_offset(sess, b, L, units, D, true, false);
+  const ScoreSizes z = score_sizes(s, L, units, D, true, false);
+  float *kbar = base + z.off_kbar();
   const int slot = slot_maps[s.slot_off + j];
   float a0 = 0.f, a1 = 0.f;
   if (slot != dead) {
@@ -293,7 +293,10 @@ static hipError_t launch_score_t(const ScoreArgs &a, hipStream_t st) {
   return launch_residual(a, st);
 }
 
+hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st);
+
 hipError_t launch_score(const ScoreArgs &a, hipStream_t st) {
+  if (a.mfma) return launch_score_mfma(a, st);
   const bool bf = a.pool.kv_dtype == IKV_BF16;
   if (a.pool.D == 128) return bf ? launch_score_t<uint16_t, 128>(a, st) : launch_score_t<float, 128>(a, st);
   return bf ? launch_score_t<uint16_t, 64>(a, st) : launch_score_t<float, 64>(a, st);

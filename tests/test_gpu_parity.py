@@ -102,6 +102,53 @@ def test_rule_scores_bf16_tiny(dev):
     assert check_scores(st.host("scores"), want, sets["cand"]) < 1e-5
 
 
+def small_d128(R=64, N=1000, seed=31, dead_frac=0.1, C=300, L=2, Hkv=2, G=4):
+    s = synth.SessionSpec(N=N, C=min(C, N // 3), pi=4, qs=N - 16, qe=N, R=R, dead_frac=dead_frac)
+    return synth.make_batch(synth.Shape(L=L, Hq=Hkv * G, Hkv=Hkv, D=128), [s], seed=seed, kv_dtype=synth.BF16,
+                            layout="paged")
+
+
+@pytest.mark.parametrize("R,N", [(16, 1000), (48, 777), (64, 1000), (80, 333), (128, 1280), (64, 129)])
+def test_rule_scores_d128_matrix_cores(dev, R, N):
+    """Head dimension 128, bf16 pool, R a multiple of 16: the MFMA score passes."""
+    batch = small_d128(R=R, N=N, seed=R + N)
+    st = RetentionStep(batch, dev)
+    st.init_dead_slot()
+    st.score(flags=0)
+    want, sets = oracle_scores(batch, 0)
+    rel = check_scores(st.host("scores"), want, sets["cand"])
+    assert rel < 1e-5, rel
+    st.select()
+    keep_o, n_o, tau_o = oracle.select_budget(want, sets)
+    check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
+
+
+@pytest.mark.parametrize("R", [16, 64])
+def test_residual_scores_d128_matrix_cores(dev, R):
+    batch = small_d128(R=R, N=1500, seed=40 + R, dead_frac=0.05)
+    blob = synth.residual_blob(128, seed=R)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.score()
+    want, sets = oracle_scores(batch, 0, blob, ikv.IKV_RESIDUAL)
+    rel = check_scores(st.host("scores"), want, sets["cand"])
+    print(f"max scale-aware relative score error {rel:.2e}")
+
+
+def test_step_batched_d128_matrix_cores(dev):
+    shape = synth.Shape(L=3, Hq=10, Hkv=2, D=128)
+    sessions = [synth.SessionSpec(N=900, C=200, pi=8, qs=880, qe=900, R=16, dead_frac=0.1),
+                synth.SessionSpec(N=2000, C=500, pi=0, qs=1950, qe=2000, R=48),
+                synth.SessionSpec(N=150, C=400, pi=0, qs=140, qe=150, R=32),
+                synth.SessionSpec(N=1300, C=100, pi=16, qs=1240, qe=1300, R=64, radix_prefix=16)]
+    batch = synth.make_batch(shape, sessions, seed=41, kv_dtype=synth.BF16, layout="paged", spare_pages=3)
+    blob = synth.residual_blob(128, seed=42)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    st.step(update_memory=True)
+    for b in range(len(sessions)):
+        _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, True)
+
+
 # ============================================================================ Eqs. 4-6
 
 @pytest.mark.parametrize("variant,flags", [("random", ikv.IKV_RESIDUAL), ("random", ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN),
