@@ -8,10 +8,12 @@
 // (M' = hi + lo to 2^-18 relative), so two MFMAs per fragment give float32-grade
 // logits. log2(e)/sqrt(D) is folded into M', so the softmax uses native exp2.
 //
-// One workgroup owns 128 positions and walks every unit: the unit's keys are
-// staged in LDS with 256-byte coalesced row loads (the next unit's rows are
-// fetched into registers while the current one computes), and wave w takes the
-// 16-row slices w, w+4, ... of the memory.
+// One workgroup owns 128 positions and walks every unit. The unit's key rows
+// stream into a 4-stage LDS ring by direct global->LDS loads (three units in
+// flight while one computes); every 16 lanes load one 256-byte row, and the
+// row's 16-byte chunks are XOR-swizzled by position so that the MFMA fragment
+// reads hit distinct banks. Wave w takes the 16-row slices w, w+4, ... of the
+// memory; its first slice's fragments are prefetched one unit ahead.
 //   pass A: per (tile, unit, row) the max and sum of exp2 over the tile's candidates;
 //   lse:    per (unit, row) the tiles combine into (max, 1/Z);
 //   pass B: p = exp2(x - max) / Z summed over every unit and row, per position, in
@@ -33,8 +35,9 @@ constexpr float LOG2E = 1.4426950408889634f;
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// M' = M * log2(e) / sqrt(D) split into bf16 hi and lo. Per (unit, row): four groups
-// of 32 channels, each stored as [hi 32 | lo 32].
+// M' = M * log2(e) / sqrt(D) split into bf16 hi and lo. Per (unit, row), 256 bf16
+// in fragment order [g 0..3][k-step 0..3][hi 8 | lo 8], where (k-step, g) holds
+// channels (4 k-step + g) * 8 .. + 8: lane group g of an MFMA reads 128 contiguous bytes.
 __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ sess, const float *__restrict__ M,
                                                 float *__restrict__ ws, int L, int Hkv, bool resid) {
   const int b = blockIdx.y;
@@ -46,24 +49,40 @@ __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ 
   const int64_t row = i >> 2;
   const int g = int(i & 3);
   const float scale = LOG2E / sqrtf(float(MD));
-  const float *src = M + s.mem_off + row * MD + g * 32;
   uint16_t *dst = reinterpret_cast<uint16_t *>(ws + score_offset(sess, b, L, units, MD, resid, true)) + row * 256 +
                   g * 64;
-  for (int e = 0; e < 32; ++e) {
-    const float v = src[e] * scale;
-    const uint16_t hi = float_to_bf16_bits(v);
-    dst[e] = hi;
-    dst[32 + e] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+  for (int ks = 0; ks < 4; ++ks) {
+    const float *src = M + s.mem_off + row * MD + (4 * ks + g) * 8;
+    for (int e = 0; e < 8; ++e) {
+      const float v = src[e] * scale;
+      const uint16_t hi = float_to_bf16_bits(v);
+      dst[ks * 16 + e] = hi;
+      dst[ks * 16 + 8 + e] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+    }
   }
+}
+
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr int RING = 4;                          // LDS stages of key rows
+constexpr int STAGE = MFMA_TILE * MD;            // bf16 per stage (32 KB)
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16 * lane.
+// Issued from asm so that the compiler does not serialise LDS reads behind every
+// outstanding load; the waits on these loads are placed by hand.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(g)
+               : "memory", "m0");
 }
 
 template <bool PASS_B, bool KBAR>
 __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__ kpool, int64_t num_slots, int L,
-                                                       int Hkv, int dead, const ikv_session *__restrict__ sess,
-                                                       const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-                                                       float *__restrict__ scores, bool resid) {
-  __shared__ __align__(16) uint16_t kt[2][MFMA_TILE * KROW];
-  __shared__ int slot_s[MFMA_TILE];
+                                                    int Hkv, int dead, const ikv_session *__restrict__ sess,
+                                                    const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+                                                    float *__restrict__ scores, bool resid) {
+  __shared__ __align__(1024) uint16_t kt[RING * STAGE];
   __shared__ int cand_s[MFMA_TILE];
   __shared__ float red[4][MFMA_TILE];
 
@@ -84,32 +103,43 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
 
   if (t < MFMA_TILE) {
     const int j = j0 + t;
-    int slot = -1, c = 0;
+    int c = 0;
     if (j < s.N) {
-      slot = slot_maps[s.slot_off + j];
+      const int slot = slot_maps[s.slot_off + j];
       c = slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
     }
-    slot_s[t] = slot;
     cand_s[t] = c;
   }
-  __syncthreads();
 
-  // key-row loader: 16 threads per 256-byte row, rows lr + 16 i
-  const int lc = t & 15, lr = t >> 4;
+  // DMA mapping: wave w, instruction k loads positions (8w + k)*4 + lane/16, 16-byte
+  // slot lane%16 of the row, which holds chunk (lane%16) ^ (position%16).
+  const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(kt));
   const int64_t slot_stride = int64_t(Hkv) * MD;
-  uint4 pre[8];
-  auto fetch = [&](int u) {
+  const uint16_t *src[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int tok = (8 * w + k) * 4 + (lane >> 4);
+    const int j = j0 + tok;
+    const int slot = j < s.N ? slot_maps[s.slot_off + j] : dead;     // past the end: any valid row
+    const int chunk = (lane & 15) ^ (tok & 15);
+    src[k] = kpool + int64_t(slot) * slot_stride + chunk * 8;
+  }
+  auto issue = [&](int u) {
     const int l = u / Hkv, h = u - l * Hkv;
-    const uint16_t *bl = kpool + int64_t(l) * num_slots * slot_stride + int64_t(h) * MD + lc * 8;
+    const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
+    const uint32_t st = lds0 + uint32_t((u % RING) * STAGE * 2);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int sl = slot_s[lr + 16 * i];
-      pre[i] = sl >= 0 ? *reinterpret_cast<const uint4 *>(bl + int64_t(sl) * slot_stride) : make_uint4(0, 0, 0, 0);
-    }
+    for (int k = 0; k < 8; ++k)
+      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * w + k) * 4) * MD * 2)));
   };
-  auto stash = [&](int buf) {
+  auto mload = [&](int u, bf16x8 (&mh)[4], bf16x8 (&ml)[4], int sl) {
+    if (u >= units || sl >= nsl) return;
+    const uint16_t *mp = msplit + (int64_t(u) * R + sl * 16 + (lane & 15)) * 256 + (lane >> 4) * 64;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4 *>(&kt[buf][(lr + 16 * i) * KROW + lc * 8]) = pre[i];
+    for (int ks = 0; ks < 4; ++ks) {
+      mh[ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16);
+      ml[ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16 + 8);
+    }
   };
 
   float racc[8][4];
@@ -121,65 +151,56 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
 #pragma unroll
   for (int i = 0; i < 64; ++i) kb[i] = 0.f;
 
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int u = 0; u < units; ++u) {
-    const int buf = u & 1;
-    if (u + 1 < units) fetch(u + 1);
-    const uint16_t *kl = kt[buf];
+  auto compute = [&](int u, const uint16_t *kl, const bf16x8 (&mh0)[4], const bf16x8 (&ml0)[4]) {
     for (int sl = w; sl < nsl; sl += 4) {
       const int row = sl * 16 + (lane & 15);
-      const uint16_t *mp = msplit + (int64_t(u) * R + row) * 256 + (lane >> 4) * 64;
       bf16x8 mh[4], ml[4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        mh[ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 8);
-        ml[ks] = *reinterpret_cast<const bf16x8 *>(mp + 32 + ks * 8);
-      }
-      float mrow = 0.f, iz = 0.f;
-      if (PASS_B) {
-        mrow = lse[(int64_t(u) * R + row) * 2];
-        iz = lse[(int64_t(u) * R + row) * 2 + 1];
-      }
-      float m = -INFINITY, zs = 0.f;
-#pragma unroll
-      for (int blk = 0; blk < MFMA_TILE / 16; ++blk) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        const uint16_t *kr = kl + (blk * 16 + (lane & 15)) * KROW + (lane >> 4) * 32;
+      if (sl == w) {
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kr + ks * 8);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, mh[ks], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ml[ks], acc, 0, 0, 0);
+          mh[ks] = mh0[ks];
+          ml[ks] = ml0[ks];
         }
-        // acc[i]: position blk*16 + 4*(lane >> 4) + i, memory row `row`
-        const int tb = blk * 16 + 4 * (lane >> 4);
-        if (!PASS_B) {
-          const float x0 = cand_s[tb] ? acc[0] : -INFINITY;
-          const float x1 = cand_s[tb + 1] ? acc[1] : -INFINITY;
-          const float x2 = cand_s[tb + 2] ? acc[2] : -INFINITY;
-          const float x3 = cand_s[tb + 3] ? acc[3] : -INFINITY;
-          const float bm = fmaxf(fmaxf(x0, x1), fmaxf(x2, x3));
-          if (bm > m) {
-            zs *= exp2f(m - bm);
-            m = bm;
-          }
-          if (m != -INFINITY) zs += (exp2f(x0 - m) + exp2f(x1 - m)) + (exp2f(x2 - m) + exp2f(x3 - m));
-        } else {
+      } else {
+        mload(u, mh, ml, sl);
+      }
+      f32x4 acc[MFMA_TILE / 16];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (cand_s[tb + i]) racc[blk][i] += exp2f(acc[i] - mrow) * iz;
+      for (int blk = 0; blk < MFMA_TILE / 16; ++blk) {
+        acc[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int tok = blk * 16 + (lane & 15);
+        const uint16_t *kr = kl + tok * MD;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const int chunk = 4 * ks + (lane >> 4);
+          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kr + ((chunk ^ (tok & 15)) * 8));
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, mh[ks], acc[blk], 0, 0, 0);
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ml[ks], acc[blk], 0, 0, 0);
         }
       }
+      // acc[blk][i]: position blk*16 + 4*(lane >> 4) + i, memory row `row`
       if (!PASS_B) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (!cand_s[blk * 16 + 4 * (lane >> 4) + i]) acc[blk][i] = -INFINITY;
+            m = fmaxf(m, acc[blk][i]);
+          }
+        const float mb = (m == -INFINITY) ? 0.f : m;
+        float zs = 0.f;
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) zs += ex2(acc[blk][i] - mb);
 #pragma unroll
         for (int o = 16; o < 64; o <<= 1) {
           const float m2 = __shfl_xor(m, o, WAVE);
           const float z2 = __shfl_xor(zs, o, WAVE);
           const float mm = fmaxf(m, m2);
-          const float a = (m == -INFINITY) ? 0.f : zs * exp2f(m - mm);
-          const float c = (m2 == -INFINITY) ? 0.f : z2 * exp2f(m2 - mm);
+          const float a = (m == -INFINITY) ? 0.f : zs * ex2(m - mm);
+          const float c = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
           m = mm;
           zs = a + c;
         }
@@ -188,13 +209,25 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
           p[0] = m;
           p[1] = zs;
         }
+      } else {
+        const float mrow = lse[(int64_t(u) * R + row) * 2];
+        const float iz = lse[(int64_t(u) * R + row) * 2 + 1];
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float p = ex2(acc[blk][i] - mrow) * iz;
+            racc[blk][i] += cand_s[blk * 16 + 4 * (lane >> 4) + i] ? p : 0.f;
+          }
       }
     }
     if (KBAR) {
-      const uint16_t *kr = kl + (32 * w + (lane & 31)) * KROW + (lane >> 5) * 64;
+      const int tok = 32 * w + (lane & 31);
+      const uint16_t *kr = kl + tok * MD;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(kr + 8 * i);
+        const int chunk = (lane >> 5) * 8 + i;
+        const uint4 v = *reinterpret_cast<const uint4 *>(kr + ((chunk ^ (tok & 15)) * 8));
         kb[8 * i + 0] += bf_lo(v.x);
         kb[8 * i + 1] += bf_hi(v.x);
         kb[8 * i + 2] += bf_lo(v.y);
@@ -205,9 +238,36 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
         kb[8 * i + 7] += bf_hi(v.w);
       }
     }
-    if (u + 1 < units) stash(buf ^ 1);
+  };
+
+  // Unit u waits until its own 8 loads have landed: at most the loads of the later
+  // units already issued (8 each) may still be in flight. Other vector-memory ops
+  // issued in between only make the wait longer, never too short.
+  auto wait_unit = [&](int u) {
+    const int later = min(RING - 2, units - 1 - u);
+    if (later >= 2) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    else if (later == 1) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  };
+
+  bf16x8 mh0[4], ml0[4], mh1[4], ml1[4];
+  for (int u = 0; u < RING - 1 && u < units; ++u) issue(u);
+  mload(0, mh0, ml0, w);
+  mload(1, mh1, ml1, w);
+  for (int u = 0; u < units; u += 2) {
+    wait_unit(u);
     __syncthreads();
+    if (u + RING - 1 < units) issue(u + RING - 1);
+    compute(u, kt + (u % RING) * STAGE, mh0, ml0);
+    mload(u + 2, mh0, ml0, w);
+    if (u + 1 >= units) break;
+    wait_unit(u + 1);
+    __syncthreads();
+    if (u + RING < units) issue(u + RING);
+    compute(u + 1, kt + ((u + 1) % RING) * STAGE, mh1, ml1);
+    mload(u + 3, mh1, ml1, w);
   }
+  __syncthreads();
 
   if (PASS_B) {
 #pragma unroll
@@ -243,6 +303,7 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
 }
 
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
+// Four threads share a row and split its tiles; they combine with two shuffles.
 __global__ void __launch_bounds__(256) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
                                                   int Hkv, bool resid) {
   const int b = blockIdx.y;
@@ -250,23 +311,31 @@ __global__ void __launch_bounds__(256) k_lse_mfma(const ikv_session *__restrict_
   if (s.N <= s.C) return;
   const int units = L * Hkv;
   const int64_t rows = int64_t(units) * s.R;
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= rows) return;
+  const int64_t i = int64_t(blockIdx.x) * 64 + (threadIdx.x >> 2);
+  const int q = threadIdx.x & 3;
+  const bool on = i < rows;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const float *part = base + z.off_part();
   const int64_t tiles = cdiv(s.N, MFMA_TILE);
   float m = -INFINITY;
-  for (int64_t k = 0; k < tiles; ++k) m = fmaxf(m, part[(k * rows + i) * 2]);
+  if (on)
+    for (int64_t k = q; k < tiles; k += 4) m = fmaxf(m, part[(k * rows + i) * 2]);
+  m = fmaxf(m, __shfl_xor(m, 1, WAVE));
+  m = fmaxf(m, __shfl_xor(m, 2, WAVE));
   double zs = 0.0;
-  if (m != -INFINITY)
-    for (int64_t k = 0; k < tiles; ++k) {
+  if (on && m != -INFINITY)
+    for (int64_t k = q; k < tiles; k += 4) {
       const float mk = part[(k * rows + i) * 2];
       if (mk != -INFINITY) zs += double(part[(k * rows + i) * 2 + 1]) * double(exp2f(mk - m));
     }
-  float *lse = base + z.off_lse();
-  lse[2 * i] = m;
-  lse[2 * i + 1] = zs > 0.0 ? float(1.0 / zs) : 0.f;
+  zs += __shfl_xor(zs, 1, WAVE);
+  zs += __shfl_xor(zs, 2, WAVE);
+  if (on && q == 0) {
+    float *lse = base + z.off_lse();
+    lse[2 * i] = m;
+    lse[2 * i + 1] = zs > 0.0 ? float(1.0 / zs) : 0.f;
+  }
 }
 
 // The gate: sessions with N <= C get -inf everywhere (the passes skip them).
@@ -289,7 +358,7 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
                                                                                         p.Hkv, resid);
   k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                a.slot_maps, a.ws, a.scores, resid);
-  k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
+  k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
                                                                                       resid);
   if (resid)
     k_score_mfma<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
