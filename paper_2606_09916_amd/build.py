@@ -21,8 +21,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libikv.so")
 ARCH = "gfx950"
 
-SOURCES = ["ikv_api.hip", "k_memory.hip", "k_score.hip", "k_score_mfma.hip", "k_residual.hip", "k_select.hip",
-           "k_decode.hip"]
+SOURCES = ["ikv_api.hip", "k_memory.hip", "k_score.hip", "k_score_mfma.hip", "k_residual.hip",
+           "k_residual_mfma.hip", "k_select.hip", "k_decode.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",

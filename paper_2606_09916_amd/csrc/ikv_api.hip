@@ -196,6 +196,7 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.scores = scores;
   a.ws = static_cast<float *>(workspace);
   a.mfma = use_mfma(pool, sess, B);
+  a.mfma_resid = a.mfma && resid && maxNq <= 64;
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.maxR = maxR;

@@ -36,13 +36,19 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 //   kq     [nq][D]                kbar at the live query positions (residual only)
 //   kp/vp  [nq][HC]               W_K kq + b_K, W_V kq + b_V (residual only)
 //   misc   [MBAR_PARTS][D] + [D] + 64   partial and final mbar, live query count (residual only)
-// followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN].
+//   fold   folded first-layer weights [HC+HIDDEN][D] as bf16 hi + lo, then the
+//          constant terms q0 [HC], h0 [HIDDEN] (residual on the MFMA path only)
+//   qlist  [nq] live query positions (residual only)
+// followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN], and on the
+// MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC].
 constexpr int MBAR_PARTS = 64;
 constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
 
 struct ScoreSizes {
-  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc;
-  __host__ __device__ int64_t total() const { return msplit + part + lse + rulep + kbar + kq + kp + vp + misc; }
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist;
+  __host__ __device__ int64_t total() const {
+    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist;
+  }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
   __host__ __device__ int64_t off_rulep() const { return msplit + part + lse; }
@@ -51,7 +57,12 @@ struct ScoreSizes {
   __host__ __device__ int64_t off_kp() const { return off_kq() + kq; }
   __host__ __device__ int64_t off_vp() const { return off_kp() + kp; }
   __host__ __device__ int64_t off_misc() const { return off_vp() + vp; }
+  __host__ __device__ int64_t off_fold() const { return off_misc() + misc; }
+  __host__ __device__ int64_t off_qlist() const { return off_fold() + fold; }
 };
+
+// Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0).
+__host__ __device__ inline int64_t fold_floats(int D) { return int64_t(HC + HIDDEN) * D + HC + HIDDEN; }
 
 __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid,
                                                   bool mfma) {
@@ -65,6 +76,8 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   z.kp = resid ? align64f(int64_t(s.nq) * HC) : 0;
   z.vp = z.kp;
   z.misc = resid ? align64f(int64_t(MBAR_PARTS + 1) * D + 64) : 0;
+  z.fold = resid && mfma ? align64f(fold_floats(D)) : 0;
+  z.qlist = resid ? align64f(s.nq) : 0;
   return z;
 }
 
@@ -77,7 +90,8 @@ __host__ __device__ inline int64_t score_offset(const ikv_session *sess, int b, 
 }
 
 __host__ __device__ inline int64_t score_shared_floats(int D) {
-  return align64f(int64_t(3 * D + 1) * HC) + align64f(int64_t(3 * D + 1 + HC) * HIDDEN);
+  return align64f(int64_t(3 * D + 1) * HC) + align64f(int64_t(3 * D + 1 + HC) * HIDDEN) +
+         align64f(int64_t(HIDDEN) * HC);
 }
 
 // Redirect workspace: two slot bitsets (kept slots, freed slots) per session.
@@ -151,6 +165,7 @@ struct ScoreArgs {
   float *ws_shared;
   int maxN, maxR, maxNq;
   bool mfma;           // MFMA score passes (D = 128 and every R a multiple of 16)
+  bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
 };
 
 hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);

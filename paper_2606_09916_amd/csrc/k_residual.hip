@@ -33,14 +33,16 @@ struct ResLayout {
 
 int64_t residual_floats(int D) { return ResLayout(D).total; }
 
-// W_Q^T [F][HC] and W_1^T [F+HC][HIDDEN] so that consecutive threads read consecutive outputs.
+// W_Q^T [F][HC] and W_1^T [F+HC][HIDDEN] so that consecutive threads read consecutive
+// outputs, and the cross-attention columns of W_1 as bf16 hi [HIDDEN][HC] then lo.
 __global__ void k_res_transpose(const float *__restrict__ blob, float *__restrict__ shared, int D) {
   const ResLayout lay(D);
   const int64_t F = 3 * D + 1;
-  const int64_t nq = F * HC, n1 = (F + HC) * HIDDEN;
+  const int64_t nq = F * HC, n1 = (F + HC) * HIDDEN, nc = int64_t(HIDDEN) * HC;
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   float *wqT = shared;
   float *w1T = shared + align64f(F * HC);
+  uint16_t *w1c = reinterpret_cast<uint16_t *>(w1T + align64f((F + HC) * HIDDEN));
   if (i < nq) {
     const int64_t in = i / HC, o = i - in * HC;
     wqT[i] = blob[lay.WQ + o * F + in];
@@ -48,6 +50,13 @@ __global__ void k_res_transpose(const float *__restrict__ blob, float *__restric
     const int64_t k = i - nq;
     const int64_t in = k / HIDDEN, o = k - in * HIDDEN;
     w1T[k] = blob[lay.W1 + o * (F + HC) + in];
+  } else if (i < nq + n1 + nc) {
+    const int64_t k = i - nq - n1;
+    const int64_t o = k / HC, c = k - o * HC;
+    const float v = blob[lay.W1 + o * (F + HC) + F + c];
+    const uint16_t hi = float_to_bf16_bits(v);
+    w1c[k] = hi;
+    w1c[nc + k] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
   }
 }
 
@@ -78,28 +87,21 @@ __global__ void __launch_bounds__(256) k_mbar_part(const ikv_session *__restrict
   }
 }
 
-// Per session: mbar, the live query rows kq and their projections K', V'.
+// Per session: mbar (from the partial sums) and the list of live query positions.
 template <int D>
-__global__ void __launch_bounds__(256) k_res_prep(const ikv_session *__restrict__ sess,
-                                                  const int32_t *__restrict__ slot_maps,
-                                                  const int32_t *__restrict__ qpos, int dead,
-                                                  const float *__restrict__ blob, float *__restrict__ ws, int L,
-                                                  int Hkv, bool mfma) {
+__global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict__ sess,
+                                                   const int32_t *__restrict__ slot_maps,
+                                                   const int32_t *__restrict__ qpos, int dead, float *__restrict__ ws,
+                                                   int L, int Hkv, bool mfma) {
   const int b = blockIdx.x;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   const int units = L * Hkv;
-  const ResLayout lay(D);
   const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
   float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
-  const float *kbar = base + z.off_kbar();
-  float *kq = base + z.off_kq();
-  float *kp = base + z.off_kp();
-  float *vp = base + z.off_vp();
   float *misc = base + z.off_misc();
   float *mbar = misc + int64_t(MBAR_PARTS) * D;
-  __shared__ int live_pos[MAX_NQ];
-  __shared__ int nlive;
+  int *qlist = reinterpret_cast<int *>(base + z.off_qlist());
   const int t = threadIdx.x;
   if (t < D) {
     float a = 0.f;
@@ -112,28 +114,89 @@ __global__ void __launch_bounds__(256) k_res_prep(const ikv_session *__restrict_
     const int32_t *qp = qpos + s.qpos_off;
     for (int i = 0; i < s.nq; ++i) {
       const int j = qp[i];
-      if (j >= 0 && j < s.N && S[j] != dead) live_pos[n++] = j;
+      if (j >= 0 && j < s.N && S[j] != dead) qlist[n++] = j;
     }
-    nlive = n;
     reinterpret_cast<int *>(mbar)[D] = n;
   }
-  __syncthreads();
-  const int n = nlive;
-  for (int e = t; e < n * D; e += 256) {
-    const int i = e / D, d = e - i * D;
-    kq[e] = kbar[int64_t(live_pos[i]) * D + d];
+}
+
+// K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup.
+template <int D>
+__global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
+                                                float *__restrict__ ws, int L, int Hkv, bool mfma) {
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int units = L * Hkv;
+  const ResLayout lay(D);
+  const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
+  float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
+  const float *kbar = base + z.off_kbar();
+  float *kp = base + z.off_kp();
+  float *vp = base + z.off_vp();
+  const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
+  const int *qlist = reinterpret_cast<const int *>(base + z.off_qlist());
+  const int i0 = blockIdx.x * 4;
+  if (i0 >= n) return;
+  __shared__ float kq[4][D];
+  const int t = threadIdx.x;
+  for (int e = t; e < 4 * D; e += 256) {
+    const int r = e / D, d = e - r * D;
+    kq[r][d] = (i0 + r < n) ? kbar[int64_t(qlist[i0 + r]) * D + d] : 0.f;
   }
   __syncthreads();
-  // K' (threads 0..127) and V' (threads 128..255)
   const int o = t & (HC - 1);
   const bool isv = t >= HC;
   const float *W = blob + (isv ? lay.WV : lay.WK) + int64_t(o) * D;
   const float bias = blob[(isv ? lay.bV : lay.bK) + o];
+  float a[4] = {bias, bias, bias, bias};
+  for (int d = 0; d < D; ++d) {
+    const float wv = W[d];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) a[r] = fmaf(wv, kq[r][d], a[r]);
+  }
   float *dst = isv ? vp : kp;
-  for (int i = 0; i < n; ++i) {
-    float a = bias;
-    for (int d = 0; d < D; ++d) a = fmaf(W[d], kq[int64_t(i) * D + d], a);
-    dst[int64_t(i) * HC + o] = a;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    if (i0 + r < n) dst[int64_t(i0 + r) * HC + o] = a[r];
+}
+
+// Folded first layer of one session (exact in real arithmetic):
+//   W_Q phi + b_Q  = (W_Q^k + W_Q^km diag(mbar)) kbar + (W_Q^m mbar + b_Q) + w_Q^r rule
+//   W_1 [phi; c] + b_1 = (W_1^k + W_1^km diag(mbar)) kbar + (W_1^m mbar + b_1) + w_1^r rule + W_1^c c
+// Rows 0..HC-1 of the folded matrix are the W_Q part, rows HC.. the W_1 part; stored
+// as bf16 hi [HC+HIDDEN][D] then lo, then q0 [HC] and h0 [HIDDEN] in float32.
+template <int D>
+__global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
+                                                  float *__restrict__ ws, int L, int Hkv) {
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int units = L * Hkv;
+  const ResLayout lay(D);
+  const int64_t F = 3 * D + 1;
+  const ScoreSizes z = score_sizes(s, L, units, D, true, true);
+  float *base = ws + score_offset(sess, b, L, units, D, true, true);
+  const float *mbar = base + z.off_misc() + int64_t(MBAR_PARTS) * D;
+  float *fold = base + z.off_fold();
+  uint16_t *hi = reinterpret_cast<uint16_t *>(fold);
+  uint16_t *lo = hi + int64_t(HC + HIDDEN) * D;
+  float *q0 = fold + int64_t(HC + HIDDEN) * D;
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t nw = int64_t(HC + HIDDEN) * D;
+  if (i < nw) {
+    const int64_t o = i / D, d = i - o * D;
+    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
+    const float v = fmaf(row[2 * D + d], mbar[d], row[d]);
+    const uint16_t h = float_to_bf16_bits(v);
+    hi[i] = h;
+    lo[i] = float_to_bf16_bits(v - bf16_bits_to_float(h));
+  } else if (i < nw + HC + HIDDEN) {
+    const int64_t o = i - nw;
+    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
+    float a = o < HC ? blob[lay.bQ + o] : blob[lay.b1 + (o - HC)];
+    for (int d = 0; d < D; ++d) a = fmaf(row[D + d], mbar[d], a);
+    q0[o] = a;
   }
 }
 
@@ -306,15 +369,26 @@ __global__ void __launch_bounds__(256) k_residual(const ikv_session *__restrict_
   }
 }
 
+hipError_t launch_residual_mfma(const ScoreArgs &a, hipStream_t st);
+
 template <int D>
 static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   const int64_t F = 3 * D + 1;
-  const int64_t n = F * HC + (F + HC) * HIDDEN;
+  const int64_t n = F * HC + (F + HC) * HIDDEN + int64_t(HIDDEN) * HC;
   k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
   k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);
-  k_res_prep<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.residual, a.ws, p.L, p.Hkv,
-                                     a.mfma);
+  k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma);
+  if (a.maxNq > 0)
+    k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
+                                                                         a.mfma);
+  if (a.mfma_resid) {
+    k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + HC + HIDDEN, 256)), a.B), 256, 0, st>>>(
+        a.sess_dev, a.residual, a.ws, p.L, p.Hkv);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_residual_mfma(a, st);
+  }
   k_residual<D><<<dim3(unsigned(cdiv(a.maxN, 32)), a.B), 256, 0, st>>>(
       a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
       (a.flags & IKV_NO_XATTN) == 0, a.mfma);

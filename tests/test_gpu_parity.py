@@ -123,15 +123,35 @@ def test_rule_scores_d128_matrix_cores(dev, R, N):
     check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
 
 
-@pytest.mark.parametrize("R", [16, 64])
-def test_residual_scores_d128_matrix_cores(dev, R):
+@pytest.mark.parametrize("R,flags,nq", [(16, ikv.IKV_RESIDUAL, 16), (64, ikv.IKV_RESIDUAL, 16),
+                                        (64, ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN, 16),
+                                        (32, ikv.IKV_RESIDUAL, 64), (48, ikv.IKV_RESIDUAL, 100)])
+def test_residual_scores_d128_matrix_cores(dev, R, flags, nq):
+    """Residual head at D = 128: on the matrix cores up to 64 live query positions,
+    on the vector units beyond."""
     batch = small_d128(R=R, N=1500, seed=40 + R, dead_frac=0.05)
+    s = batch.sessions[0]
+    s.qpos = np.arange(s.N - nq, s.N, dtype=np.int32)
+    batch.qpos = s.qpos.copy()
     blob = synth.residual_blob(128, seed=R)
-    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st = RetentionStep(batch, dev, residual=blob, flags=flags)
     st.score()
-    want, sets = oracle_scores(batch, 0, blob, ikv.IKV_RESIDUAL)
+    want, sets = oracle_scores(batch, 0, blob, flags)
     rel = check_scores(st.host("scores"), want, sets["cand"])
     print(f"max scale-aware relative score error {rel:.2e}")
+    keep_o, n_o, tau_o = oracle.select_budget(want, sets)
+    st.select()
+    check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
+
+
+def test_zero_initialised_head_is_bitwise_the_rule_d128(dev):
+    batch = small_d128(R=64, N=1200, seed=77)
+    st = RetentionStep(batch, dev, residual=synth.residual_blob(128, seed=3, variant="zero"),
+                       flags=ikv.IKV_RESIDUAL)
+    st.score()
+    with_head = st.host("scores").copy()
+    st.score(flags=0)
+    assert np.array_equal(with_head, st.host("scores"))
 
 
 def test_step_batched_d128_matrix_cores(dev):
