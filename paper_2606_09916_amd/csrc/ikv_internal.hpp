@@ -30,7 +30,8 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 //   msplit [units][R][256 bf16]   memory rows pre-split into bf16 hi + lo (MFMA only)
 //   part   per-tile (max, sum exp) of every memory row:
 //            MFMA [tiles of 128][units][R][2], VALU [units][R][tiles of 256][2]
-//   lse    [units][R][2]          (max, 1/Z) of every memory row
+//   lse    [units][R][2]          (max, 1/Z) of every memory row, then (MFMA only)
+//          [units][R]             -(max + log2 Z), the seed of the second pass
 //   rulep  [L][N]                 per-layer partial rule scores (VALU only)
 //   kbar   [N][D]                 mean key row (residual only)
 //   kq     [nq][D]                kbar at the live query positions (residual only)
@@ -46,12 +47,15 @@ constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score
 
 struct ScoreSizes {
   int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist;
+  int64_t lse_pairs;   // units * R * 2: the (max, 1/Z) pairs at the start of lse
   __host__ __device__ int64_t total() const {
     return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist;
   }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
   __host__ __device__ int64_t off_rulep() const { return msplit + part + lse; }
+  // -(max + log2 Z) per row, after the (max, 1/Z) pairs (MFMA layout only)
+  __host__ __device__ int64_t off_nl2() const { return off_lse() + lse_pairs; }
   __host__ __device__ int64_t off_kbar() const { return msplit + part + lse + rulep; }
   __host__ __device__ int64_t off_kq() const { return off_kbar() + kbar; }
   __host__ __device__ int64_t off_kp() const { return off_kq() + kq; }
@@ -69,7 +73,8 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   ScoreSizes z;
   z.msplit = mfma ? align64f(int64_t(units) * s.R * 128) : 0;
   z.part = mfma ? align64f(cdiv(s.N, MFMA_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
-  z.lse = align64f(int64_t(units) * s.R * 2);
+  z.lse = align64f(int64_t(units) * s.R * (mfma ? 3 : 2));
+  z.lse_pairs = int64_t(units) * s.R * 2;
   z.rulep = mfma ? 0 : align64f(int64_t(L) * s.N);
   z.kbar = resid ? align64f(int64_t(s.N) * D) : 0;
   z.kq = resid ? align64f(int64_t(s.nq) * D) : 0;

@@ -302,6 +302,237 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
   }
 }
 
+// ------------------------------------------------------------------ ring pass (R <= 64)
+// Keys and memory rows both stream by direct global->LDS loads: three 32 KB key
+// stages and two 32 KB memory stages fill the 160 KB of LDS. With no compiler-issued
+// vector loads left in the unit loop, the waits placed by hand are the only ones.
+// The second pass seeds each accumulator with -(max + log2 Z) of its row, read by
+// scalar loads, so exp2 of the MFMA result is already the softmax weight.
+constexpr int KSTAGES = 3;
+constexpr int MSTAGE = 64 * 256;                 // bf16 per memory stage: 64 rows x 512 B
+
+// Read-only view for wave-uniform loads: the compiler issues them on the scalar unit
+// (tracked by lgkmcnt, so they never delay the vector-memory waits of the ring).
+typedef const __attribute__((address_space(4))) float cfloat;
+
+template <bool PASS_B, bool KBAR>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L,
+                                                    int Hkv, int dead, const ikv_session *__restrict__ sess,
+                                                    const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+                                                    float *__restrict__ scores, bool resid) {
+  __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
+
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int tile = blockIdx.x;
+  const int j0 = tile * MFMA_TILE;
+  if (j0 >= s.N) return;
+  const int units = L * Hkv;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int R = s.R, nsl = R >> 4;
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
+  float *part = base + z.off_part();
+  const float *nl2 = base + z.off_nl2();
+  const int32_t *S = slot_maps + s.slot_off;
+
+  // candidate flags of this lane's 32 MFMA outputs: bit blk*4 + i <-> position blk*16 + 4g + i
+  uint32_t cmask = 0;
+#pragma unroll
+  for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = j0 + blk * 16 + 4 * g + i;
+      if (j < s.N && S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe))) cmask |= 1u << (blk * 4 + i);
+    }
+
+  const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
+  const int64_t slot_stride = int64_t(Hkv) * MD;
+  const uint16_t *src[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int tok = (8 * w + k) * 4 + (lane >> 4);
+    const int j = j0 + tok;
+    const int slot = j < s.N ? S[j] : dead;
+    src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
+  }
+  auto issue_k = [&](int u) {
+    const int l = u / Hkv, h = u - l * Hkv;
+    const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
+    const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * w + k) * 4) * MD * 2)));
+  };
+  // memory rows of unit u: R rows of 512 B, 32 chunks of 16 B per row, chunk slot
+  // s of row r holds chunk s ^ (r & 15); wave w issues R/8 of the R/2 1-KB pieces
+  const int nm = R >> 3;
+  auto issue_m = [&](int u) {
+    const uint16_t *m0 = msplit + int64_t(u) * R * 256;
+    const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
+    for (int k = 0; k < nm; ++k) {
+      const int piece = w * nm + k;
+      const int r = piece * 2 + (lane >> 5);
+      const int sl = lane & 31;
+      dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+    }
+  };
+
+  float racc[8][4];
+  float kb[64];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) racc[i][k] = 0.f;
+#pragma unroll
+  for (int i = 0; i < 64; ++i) kb[i] = 0.f;
+
+  auto compute = [&](int u, const uint16_t *kl, const uint16_t *mlds) {
+    if (w < nsl) {
+      const int row = w * 16 + r16;
+      const uint16_t *mr = mlds + row * 256;
+      bf16x8 mh[4], ml[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        mh[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2) ^ r16) * 8));
+        ml[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2 + 1) ^ r16) * 8));
+      }
+      float seed = 0.f;
+      if (PASS_B) {
+        const int64_t o = int64_t(__builtin_amdgcn_readfirstlane(u * R + w * 16));
+        const cfloat *q = (cfloat *)(nl2 + o);
+        float sv[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          sv[i] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, q[i])));
+        seed = sv[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) seed = (r16 == i) ? sv[i] : seed;
+      }
+      f32x4 acc[MFMA_TILE / 16];
+#pragma unroll
+      for (int blk = 0; blk < MFMA_TILE / 16; ++blk) {
+        acc[blk] = f32x4{seed, seed, seed, seed};
+        const int tok = blk * 16 + r16;
+        const uint16_t *kr = kl + tok * MD;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const int chunk = 4 * ks + g;
+          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kr + ((chunk ^ (tok & 15)) * 8));
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, mh[ks], acc[blk], 0, 0, 0);
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ml[ks], acc[blk], 0, 0, 0);
+        }
+      }
+      if (!PASS_B) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (!((cmask >> (blk * 4 + i)) & 1u)) acc[blk][i] = -INFINITY;
+            m = fmaxf(m, acc[blk][i]);
+          }
+        const float mb = (m == -INFINITY) ? 0.f : m;
+        float zs = 0.f;
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) zs += ex2(acc[blk][i] - mb);
+#pragma unroll
+        for (int o = 16; o < 64; o <<= 1) {
+          const float m2 = __shfl_xor(m, o, WAVE);
+          const float z2 = __shfl_xor(zs, o, WAVE);
+          const float mm = fmaxf(m, m2);
+          const float a = (m == -INFINITY) ? 0.f : zs * ex2(m - mm);
+          const float c = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
+          m = mm;
+          zs = a + c;
+        }
+        if (lane < 16) *reinterpret_cast<float2 *>(part + ((int64_t(tile) * units + u) * R + row) * 2) =
+            make_float2(m, zs);
+      } else {
+#pragma unroll
+        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if ((cmask >> (blk * 4 + i)) & 1u) racc[blk][i] += ex2(acc[blk][i]);
+      }
+    }
+    if (KBAR) {
+      const int tok = 32 * w + (lane & 31);
+      const uint16_t *kr = kl + tok * MD;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int chunk = (lane >> 5) * 8 + i;
+        const uint4 v = *reinterpret_cast<const uint4 *>(kr + ((chunk ^ (tok & 15)) * 8));
+        kb[8 * i + 0] += bf_lo(v.x);
+        kb[8 * i + 1] += bf_hi(v.x);
+        kb[8 * i + 2] += bf_lo(v.y);
+        kb[8 * i + 3] += bf_hi(v.y);
+        kb[8 * i + 4] += bf_lo(v.z);
+        kb[8 * i + 5] += bf_hi(v.z);
+        kb[8 * i + 6] += bf_lo(v.w);
+        kb[8 * i + 7] += bf_hi(v.w);
+      }
+    }
+  };
+
+  // DMA order: K(0), M(0), K(1), then per unit u: M(u+1), K(u+2). At the top of unit
+  // u only K(u+1) (8 loads per wave) may still be younger than M(u) and K(u).
+  issue_k(0);
+  issue_m(0);
+  if (units > 1) issue_k(1);
+  for (int u = 0; u < units; ++u) {
+    if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (u + 1 < units) issue_m(u + 1);
+    if (u + 2 < units) issue_k(u + 2);
+    compute(u, lds + (u % KSTAGES) * STAGE, lds + KSTAGES * STAGE + (u & 1) * MSTAGE);
+  }
+  __syncthreads();
+
+  if (PASS_B) {
+    float *red = reinterpret_cast<float *>(lds);       // [4][MFMA_TILE], the loop is over
+#pragma unroll
+    for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v = racc[blk][i];
+        v += __shfl_xor(v, 1, WAVE);
+        v += __shfl_xor(v, 2, WAVE);
+        v += __shfl_xor(v, 4, WAVE);
+        v += __shfl_xor(v, 8, WAVE);
+        if (r16 == 0) red[w * MFMA_TILE + blk * 16 + 4 * g + i] = v;
+      }
+    __syncthreads();
+    if (t < MFMA_TILE) {
+      const int j = j0 + t;
+      if (j < s.N) {
+        const bool c = S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+        scores[s.slot_off + j] = c ? (red[t] + red[MFMA_TILE + t]) + (red[2 * MFMA_TILE + t] + red[3 * MFMA_TILE + t])
+                                   : -INFINITY;
+      }
+    }
+  }
+  if (KBAR) {
+    const int tok = 32 * w + (lane & 31);
+    const int j = j0 + tok;
+    if (j < s.N) {
+      const float inv = 1.0f / float(units);
+      float *dst = base + z.off_kbar() + int64_t(j) * MD + (lane >> 5) * 64;
+#pragma unroll
+      for (int e = 0; e < 64; e += 4)
+        *reinterpret_cast<float4 *>(dst + e) = make_float4(kb[e] * inv, kb[e + 1] * inv, kb[e + 2] * inv,
+                                                           kb[e + 3] * inv);
+    }
+  }
+}
+
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
 // Four threads share a row and split its tiles; they combine with two shuffles.
 __global__ void __launch_bounds__(256) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
@@ -335,6 +566,9 @@ __global__ void __launch_bounds__(256) k_lse_mfma(const ikv_session *__restrict_
     float *lse = base + z.off_lse();
     lse[2 * i] = m;
     lse[2 * i + 1] = zs > 0.0 ? float(1.0 / zs) : 0.f;
+    // -(max + log2 Z): the ring pass seeds its accumulators with it (-inf without candidates)
+    float *nl2 = base + z.off_nl2();
+    nl2[i] = (m == -INFINITY || !(zs > 0.0)) ? -INFINITY : float(-(double(m) + log2(zs)));
   }
 }
 
@@ -356,11 +590,22 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   k_fill_skipped<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.scores);
   k_msplit<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR * 4, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L,
                                                                                         p.Hkv, resid);
-  k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                               a.slot_maps, a.ws, a.scores, resid);
+  const bool ring = a.maxR <= 64;
+  if (ring)
+    k_score_ring<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.ws, a.scores, resid);
+  else
+    k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.ws, a.scores, resid);
   k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
                                                                                       resid);
-  if (resid)
+  if (ring && resid)
+    k_score_ring<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                               a.slot_maps, a.ws, a.scores, resid);
+  else if (ring)
+    k_score_ring<true, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+  else if (resid)
     k_score_mfma<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                a.slot_maps, a.ws, a.scores, resid);
   else
