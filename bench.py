@@ -162,9 +162,11 @@ def main() -> int:
 
     n_live = int(st.host("n_live")[0])
     n_keep = int(st.host("n_keep")[0])
-    import oracle
-    sets = oracle.sets(batch.S(0), s.pi, s.qs, s.qe, s.C, 0)
-    nA = int(sets["cand"].sum())
+    # candidates: live positions outside the forced prefix and query span
+    S0 = np.asarray(batch.S(0))
+    jj = np.arange(len(S0))
+    forced = (jj < s.pi) | ((jj >= s.qs) & (jj < s.qe))
+    nA = int(((S0 != st.dead) & ~forced).sum())
     t_ss = (phase_ms[2] + phase_ms[3]) / 1e3
     tokens_per_s = nA / t_ss
 

@@ -29,7 +29,8 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 // layouts: the MFMA path (D = 128, R a multiple of 16) and the VALU path.
 //   msplit [units][R][256 bf16]   memory rows pre-split into bf16 hi + lo (MFMA only)
 //   part   per-tile (max, sum exp) of every memory row:
-//            MFMA [tiles of 128][units][R][2], VALU [units][R][tiles of 256][2]
+//            MFMA [tiles of 64 or 128][units][R][2] (room for tiles of 64),
+//            VALU [units][R][tiles of 256][2]
 //   lse    [units][R][2]          (max, 1/Z) of every memory row, then (MFMA only)
 //          [units][R]             -(max + log2 Z), the seed of the second pass
 //   rulep  [L][N]                 per-layer partial rule scores (VALU only)
@@ -44,6 +45,7 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 // MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC].
 constexpr int MBAR_PARTS = 64;
 constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
+constexpr int PART_TILE = 64;       // positions per first-pass partial of the ring passes
 
 struct ScoreSizes {
   int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist;
@@ -72,7 +74,7 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
                                                   bool mfma) {
   ScoreSizes z;
   z.msplit = mfma ? align64f(int64_t(units) * s.R * 128) : 0;
-  z.part = mfma ? align64f(cdiv(s.N, MFMA_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
+  z.part = mfma ? align64f(cdiv(s.N, PART_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
   z.lse = align64f(int64_t(units) * s.R * (mfma ? 3 : 2));
   z.lse_pairs = int64_t(units) * s.R * 2;
   z.rulep = mfma ? 0 : align64f(int64_t(L) * s.N);

@@ -306,20 +306,24 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
 // Keys and memory rows both stream by direct global->LDS loads: three 32 KB key
 // stages and two 32 KB memory stages fill the 160 KB of LDS. With no compiler-issued
 // vector loads left in the unit loop, the waits placed by hand are the only ones.
-// The second pass seeds each accumulator with -(max + log2 Z) of its row, read by
-// scalar loads, so exp2 of the MFMA result is already the softmax weight.
+// Eight waves, two per SIMD: wave w takes the 16 memory rows of slice w & 3 against
+// the 64 positions of half w >> 2, so one wave's LDS reads and exp2 run under the
+// other's MFMAs. The first pass keeps one (max, sum) per 64 positions; the second
+// seeds each accumulator with -(max + log2 Z) of its row, read by scalar loads, so
+// exp2 of the MFMA result is already the softmax weight.
 constexpr int KSTAGES = 3;
 constexpr int MSTAGE = 64 * 256;                 // bf16 per memory stage: 64 rows x 512 B
+constexpr int RING_THREADS = 512;
 
 // Read-only view for wave-uniform loads: the compiler issues them on the scalar unit
 // (tracked by lgkmcnt, so they never delay the vector-memory waits of the ring).
 typedef const __attribute__((address_space(4))) float cfloat;
 
 template <bool PASS_B, bool KBAR>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L,
-                                                    int Hkv, int dead, const ikv_session *__restrict__ sess,
-                                                    const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-                                                    float *__restrict__ scores, bool resid) {
+__global__ void __launch_bounds__(RING_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
+             const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+             float *__restrict__ scores, bool resid) {
   __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
 
   const int b = blockIdx.y;
@@ -330,8 +334,14 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   if (j0 >= s.N) return;
   const int units = L * Hkv;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int rs = w & 3, half = w >> 2;             // memory-row slice, position half
   const int g = lane >> 4, r16 = lane & 15;
   const int R = s.R, nsl = R >> 4;
+  const bool act = rs < nsl;
+  const int row = rs * 16 + r16;
+  const int p0 = half * 64;                        // first position of this wave's half
+  const int ptile = tile * 2 + half;
+  const bool pstore = act && lane < 16 && int64_t(ptile) * PART_TILE < s.N;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
@@ -339,38 +349,42 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   const float *nl2 = base + z.off_nl2();
   const int32_t *S = slot_maps + s.slot_off;
 
-  // candidate flags of this lane's 32 MFMA outputs: bit blk*4 + i <-> position blk*16 + 4g + i
+  // candidate flags of this lane's 16 MFMA outputs: bit blk*4 + i <-> position p0 + blk*16 + 4g + i
   uint32_t cmask = 0;
 #pragma unroll
-  for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+  for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int j = j0 + blk * 16 + 4 * g + i;
+      const int j = j0 + p0 + blk * 16 + 4 * g + i;
       if (j < s.N && S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe))) cmask |= 1u << (blk * 4 + i);
     }
 
+  // Key DMA: wave w, instruction k loads positions (4w + k)*4 + lane/16, 16-byte slot
+  // lane%16 of the row, which holds chunk (lane%16) ^ (position%16).
   const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(lds));
   const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
   const int64_t slot_stride = int64_t(Hkv) * MD;
-  const uint16_t *src[8];
+  const uint16_t *src[4];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int tok = (8 * w + k) * 4 + (lane >> 4);
+  for (int k = 0; k < 4; ++k) {
+    const int tok = (4 * w + k) * 4 + (lane >> 4);
     const int j = j0 + tok;
-    const int slot = j < s.N ? S[j] : dead;
+    const int slot = j < s.N ? S[j] : dead;        // past the end: any valid row
     src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
   }
+  // every compiler-issued load of the set-up is complete before the first DMA
+  asm volatile("" ::"v"(cmask), "v"(src[0]), "v"(src[1]), "v"(src[2]), "v"(src[3]));
   auto issue_k = [&](int u) {
     const int l = u / Hkv, h = u - l * Hkv;
     const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
     const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * w + k) * 4) * MD * 2)));
+    for (int k = 0; k < 4; ++k)
+      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((4 * w + k) * 4) * MD * 2)));
   };
   // memory rows of unit u: R rows of 512 B, 32 chunks of 16 B per row, chunk slot
-  // s of row r holds chunk s ^ (r & 15); wave w issues R/8 of the R/2 1-KB pieces
-  const int nm = R >> 3;
+  // s of row r holds chunk s ^ (r & 15); wave w issues R/16 of the R/2 1-KB pieces
+  const int nm = R >> 4;
   auto issue_m = [&](int u) {
     const uint16_t *m0 = msplit + int64_t(u) * R * 256;
     const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
@@ -382,28 +396,35 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
   };
 
-  float racc[8][4];
-  float kb[64];
+  float racc[4][4];
+  float kb[32];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[i][k] = 0.f;
 #pragma unroll
-  for (int i = 0; i < 64; ++i) kb[i] = 0.f;
+  for (int i = 0; i < 32; ++i) kb[i] = 0.f;
+  float pm = 0.f, pz = 0.f;                        // first pass: the previous unit's (max, sum)
 
-  auto compute = [&](int u, const uint16_t *kl, const uint16_t *mlds) {
-    if (w < nsl) {
-      const int row = w * 16 + r16;
-      const uint16_t *mr = mlds + row * 256;
-      bf16x8 mh[4], ml[4];
+  auto compute = [&](int u) {
+    const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
+    if (act) {
+      const uint16_t *mr = lds + KSTAGES * STAGE + (u & 1) * MSTAGE + row * 256;
+      bf16x8 mh[4], ml[4], ka[4][4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         mh[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2) ^ r16) * 8));
         ml[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2 + 1) ^ r16) * 8));
       }
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        const uint16_t *kr = kl + (p0 + blk * 16 + r16) * MD;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kr + (((4 * ks + g) ^ r16) * 8));
+      }
       float seed = 0.f;
       if (PASS_B) {
-        const int64_t o = int64_t(__builtin_amdgcn_readfirstlane(u * R + w * 16));
+        const int64_t o = int64_t(__builtin_amdgcn_readfirstlane(u * R + rs * 16));
         const cfloat *q = (cfloat *)(nl2 + o);
         float sv[16];
 #pragma unroll
@@ -413,24 +434,21 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
 #pragma unroll
         for (int i = 1; i < 16; ++i) seed = (r16 == i) ? sv[i] : seed;
       }
-      f32x4 acc[MFMA_TILE / 16];
+      f32x4 acc[4];
 #pragma unroll
-      for (int blk = 0; blk < MFMA_TILE / 16; ++blk) {
-        acc[blk] = f32x4{seed, seed, seed, seed};
-        const int tok = blk * 16 + r16;
-        const uint16_t *kr = kl + tok * MD;
+      for (int blk = 0; blk < 4; ++blk) acc[blk] = f32x4{seed, seed, seed, seed};
+      // four independent accumulators between consecutive MFMAs
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const int chunk = 4 * ks + g;
-          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(kr + ((chunk ^ (tok & 15)) * 8));
-          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, mh[ks], acc[blk], 0, 0, 0);
-          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ml[ks], acc[blk], 0, 0, 0);
-        }
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk) acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], mh[ks], acc[blk], 0, 0, 0);
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk) acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], ml[ks], acc[blk], 0, 0, 0);
       }
       if (!PASS_B) {
         float m = -INFINITY;
 #pragma unroll
-        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+        for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             if (!((cmask >> (blk * 4 + i)) & 1u)) acc[blk][i] = -INFINITY;
@@ -439,7 +457,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
         const float mb = (m == -INFINITY) ? 0.f : m;
         float zs = 0.f;
 #pragma unroll
-        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+        for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
           for (int i = 0; i < 4; ++i) zs += ex2(acc[blk][i] - mb);
 #pragma unroll
@@ -452,23 +470,22 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
           m = mm;
           zs = a + c;
         }
-        if (lane < 16) *reinterpret_cast<float2 *>(part + ((int64_t(tile) * units + u) * R + row) * 2) =
-            make_float2(m, zs);
+        pm = m;
+        pz = zs;
       } else {
 #pragma unroll
-        for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+        for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             if ((cmask >> (blk * 4 + i)) & 1u) racc[blk][i] += ex2(acc[blk][i]);
       }
     }
     if (KBAR) {
-      const int tok = 32 * w + (lane & 31);
+      const int tok = t >> 2, q4 = t & 3;
       const uint16_t *kr = kl + tok * MD;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int chunk = (lane >> 5) * 8 + i;
-        const uint4 v = *reinterpret_cast<const uint4 *>(kr + ((chunk ^ (tok & 15)) * 8));
+      for (int i = 0; i < 4; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((q4 * 4 + i) ^ (tok & 15)) * 8));
         kb[8 * i + 0] += bf_lo(v.x);
         kb[8 * i + 1] += bf_hi(v.x);
         kb[8 * i + 2] += bf_lo(v.y);
@@ -480,26 +497,33 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
       }
     }
   };
+  auto store_part = [&](int u) {
+    if (pstore)
+      *reinterpret_cast<float2 *>(part + ((int64_t(ptile) * units + u) * R + row) * 2) = make_float2(pm, pz);
+  };
 
-  // DMA order: K(0), M(0), K(1), then per unit u: M(u+1), K(u+2). At the top of unit
-  // u only K(u+1) (8 loads per wave) may still be younger than M(u) and K(u).
+  // Issue order per wave: K(0), M(0), K(1), then per unit u: [first pass: store of
+  // unit u-1], M(u+1), K(u+2). At the top of unit u only K(u+1) (4 loads) may still
+  // be younger than M(u) and K(u).
   issue_k(0);
   issue_m(0);
   if (units > 1) issue_k(1);
   for (int u = 0; u < units; ++u) {
-    if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    if (u + 1 < units) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (!PASS_B && u > 0) store_part(u - 1);
     if (u + 1 < units) issue_m(u + 1);
     if (u + 2 < units) issue_k(u + 2);
-    compute(u, lds + (u % KSTAGES) * STAGE, lds + KSTAGES * STAGE + (u & 1) * MSTAGE);
+    compute(u);
   }
+  if (!PASS_B) store_part(units - 1);
   __syncthreads();
 
   if (PASS_B) {
-    float *red = reinterpret_cast<float *>(lds);       // [4][MFMA_TILE], the loop is over
+    float *red = reinterpret_cast<float *>(lds);   // [4][MFMA_TILE], the loop is over
 #pragma unroll
-    for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
+    for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float v = racc[blk][i];
@@ -507,7 +531,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
         v += __shfl_xor(v, 2, WAVE);
         v += __shfl_xor(v, 4, WAVE);
         v += __shfl_xor(v, 8, WAVE);
-        if (r16 == 0) red[w * MFMA_TILE + blk * 16 + 4 * g + i] = v;
+        if (r16 == 0) red[rs * MFMA_TILE + p0 + blk * 16 + 4 * g + i] = v;
       }
     __syncthreads();
     if (t < MFMA_TILE) {
@@ -520,13 +544,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
   }
   if (KBAR) {
-    const int tok = 32 * w + (lane & 31);
+    const int tok = t >> 2, q4 = t & 3;
     const int j = j0 + tok;
     if (j < s.N) {
       const float inv = 1.0f / float(units);
-      float *dst = base + z.off_kbar() + int64_t(j) * MD + (lane >> 5) * 64;
+      float *dst = base + z.off_kbar() + int64_t(j) * MD + q4 * 32;
 #pragma unroll
-      for (int e = 0; e < 64; e += 4)
+      for (int e = 0; e < 32; e += 4)
         *reinterpret_cast<float4 *>(dst + e) = make_float4(kb[e] * inv, kb[e + 1] * inv, kb[e + 2] * inv,
                                                            kb[e + 3] * inv);
     }
@@ -534,41 +558,53 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
 }
 
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
-// Four threads share a row and split its tiles; they combine with two shuffles.
-__global__ void __launch_bounds__(256) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
-                                                  int Hkv, bool resid) {
+// A workgroup takes 64 consecutive rows; its eight waves split the tiles (lane =
+// row, so each load instruction reads 512 contiguous bytes), fold them online into
+// (max, sum) and merge through LDS in a fixed order.
+__global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
+                                                  int Hkv, bool resid, int ptile) {
+  __shared__ float sm[8][64], sz[8][64];
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   const int units = L * Hkv;
   const int64_t rows = int64_t(units) * s.R;
-  const int64_t i = int64_t(blockIdx.x) * 64 + (threadIdx.x >> 2);
-  const int q = threadIdx.x & 3;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t i = int64_t(blockIdx.x) * 64 + lane;
+  if (int64_t(blockIdx.x) * 64 >= rows) return;
   const bool on = i < rows;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const float *part = base + z.off_part();
-  const int64_t tiles = cdiv(s.N, MFMA_TILE);
-  float m = -INFINITY;
+  const int64_t tiles = cdiv(s.N, ptile);
+  float m = -INFINITY, zs = 0.f;
   if (on)
-    for (int64_t k = q; k < tiles; k += 4) m = fmaxf(m, part[(k * rows + i) * 2]);
-  m = fmaxf(m, __shfl_xor(m, 1, WAVE));
-  m = fmaxf(m, __shfl_xor(m, 2, WAVE));
-  double zs = 0.0;
-  if (on && m != -INFINITY)
-    for (int64_t k = q; k < tiles; k += 4) {
-      const float mk = part[(k * rows + i) * 2];
-      if (mk != -INFINITY) zs += double(part[(k * rows + i) * 2 + 1]) * double(exp2f(mk - m));
+    for (int64_t k = w; k < tiles; k += 8) {
+      const float2 p = *reinterpret_cast<const float2 *>(part + (k * rows + i) * 2);
+      if (p.x == -INFINITY) continue;
+      if (p.x > m) {
+        zs = (m == -INFINITY ? 0.f : zs * exp2f(m - p.x)) + p.y;
+        m = p.x;
+      } else {
+        zs += p.y * exp2f(p.x - m);
+      }
     }
-  zs += __shfl_xor(zs, 1, WAVE);
-  zs += __shfl_xor(zs, 2, WAVE);
-  if (on && q == 0) {
+  sm[w][lane] = m;
+  sz[w][lane] = zs;
+  __syncthreads();
+  if (w == 0 && on) {
+    float mx = -INFINITY;
+    for (int k = 0; k < 8; ++k) mx = fmaxf(mx, sm[k][lane]);
+    double Z = 0.0;
+    if (mx != -INFINITY)
+      for (int k = 0; k < 8; ++k)
+        if (sm[k][lane] != -INFINITY) Z += double(sz[k][lane]) * double(exp2f(sm[k][lane] - mx));
     float *lse = base + z.off_lse();
-    lse[2 * i] = m;
-    lse[2 * i + 1] = zs > 0.0 ? float(1.0 / zs) : 0.f;
+    lse[2 * i] = mx;
+    lse[2 * i + 1] = Z > 0.0 ? float(1.0 / Z) : 0.f;
     // -(max + log2 Z): the ring pass seeds its accumulators with it (-inf without candidates)
     float *nl2 = base + z.off_nl2();
-    nl2[i] = (m == -INFINITY || !(zs > 0.0)) ? -INFINITY : float(-(double(m) + log2(zs)));
+    nl2[i] = (mx == -INFINITY || !(Z > 0.0)) ? -INFINITY : float(-(double(mx) + log2(Z)));
   }
 }
 
@@ -592,18 +628,18 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
                                                                                         p.Hkv, resid);
   const bool ring = a.maxR <= 64;
   if (ring)
-    k_score_ring<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+    k_score_ring<false, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                  a.slot_maps, a.ws, a.scores, resid);
   else
     k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                  a.slot_maps, a.ws, a.scores, resid);
-  k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
-                                                                                      resid);
+  k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
+                                                                                      resid, ring ? PART_TILE : MFMA_TILE);
   if (ring && resid)
-    k_score_ring<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+    k_score_ring<true, true><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                a.slot_maps, a.ws, a.scores, resid);
   else if (ring)
-    k_score_ring<true, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+    k_score_ring<true, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
                                                                 a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
   else if (resid)
     k_score_mfma<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
