@@ -131,6 +131,8 @@ ikv_status ikv_init_dead_slot(const ikv_pool *pool, void *stream);
  * row is divided by max(||row||_2, 1e-12). lambda = INFINITY drops the history
  * (the "query" scorer mode and the "- memory" ablation). In place on M.
  *   q_span: device, per session [L][Hkv*R][qe-qs][D] of the pool's kv_dtype.
+ *   M + mem_off and q_span + qspan_off must be 16-byte aligned for every session
+ *   (IKV_EINVAL otherwise): rows are read and written 16 bytes per lane.
  * Sessions with qe == qs leave M unchanged apart from the decay and projection.
  */
 ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess,

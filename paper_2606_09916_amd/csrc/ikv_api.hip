@@ -153,9 +153,13 @@ ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess, const ik
   if (!M || !q_span) return fail(IKV_EINVAL, "M / q_span is NULL");
   if (!(lambda >= 0.0f)) return fail(IKV_EINVAL, "lambda must be >= 0 (got %g)", double(lambda));
   int max_rows = 0;
+  const size_t esize = pool->kv_dtype == IKV_BF16 ? 2 : 4;
   for (int b = 0; b < B; ++b) {
     const int rows = pool->L * pool->Hkv * sess[b].R;
     max_rows = rows > max_rows ? rows : max_rows;
+    if ((reinterpret_cast<uintptr_t>(M) + size_t(sess[b].mem_off) * 4) % 16 ||
+        (reinterpret_cast<uintptr_t>(q_span) + size_t(sess[b].qspan_off) * esize) % 16)
+      return fail(IKV_EINVAL, "session %d: M + mem_off and q_span + qspan_off must be 16-byte aligned", b);
   }
   const float decay = isinf(lambda) ? 0.0f : float(exp(-double(lambda)));
   return hip_status(ikv::launch_qm_update(*pool, sess_dev, B, max_rows, M, q_span, decay, (hipStream_t)stream),

@@ -29,42 +29,80 @@ hipError_t launch_init_dead_slot(const ikv_pool &p, hipStream_t st) {
 }
 
 // One wavefront per memory row: Enc = mean of the span rows, M = decay * M + Enc,
-// then the row is divided by max(||row||, 1e-12). D is a multiple of 64, at most 256.
-template <typename T>
-__global__ void __launch_bounds__(256) k_qm_update(const ikv_session *__restrict__ sess, int L, int Hkv, int D,
+// then the row is divided by max(||row||, 1e-12). Lane (g, c) reads channels
+// 8c .. 8c+7 of span rows g, g + G, ... (G = 512 / D rows per wave step) with
+// 16-byte loads; the G row groups fold with shuffles.
+template <typename T, int D>
+__global__ void __launch_bounds__(256) k_qm_update(const ikv_session *__restrict__ sess, int L, int Hkv,
                                                    float *__restrict__ M, const T *__restrict__ q_span,
                                                    float decay) {
+  constexpr int CL = D / 8;        // lanes per span row
+  constexpr int G = WAVE / CL;     // span rows per wave step
   const ikv_session s = sess[blockIdx.y];
   const int rows = L * Hkv * s.R;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int lane = threadIdx.x & 63;
+  const int c = lane % CL, g = lane / CL;
   const int n = s.qe - s.qs;
-  float *m = M + s.mem_off + int64_t(row) * D;
-  const T *q = q_span + s.qspan_off + int64_t(row) * n * D;
-  const int per = D >> 6;
-  float x[4];
+  float *m = M + s.mem_off + int64_t(row) * D + c * 8;
+  const T *q = q_span + s.qspan_off + int64_t(row) * n * D + c * 8;
+  float e[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) e[k] = 0.f;
+  int tq = g;
+  for (; tq + 3 * G < n; tq += 4 * G) {          // four loads in flight per lane
+    float a[4][8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load8(q + int64_t(tq + u * G) * D, a[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) e[k] += a[u][k];
+  }
+  for (; tq < n; tq += G) {
+    float a[8];
+    load8(q + int64_t(tq) * D, a);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) e[k] += a[k];
+  }
+#pragma unroll
+  for (int o = CL; o < WAVE; o <<= 1)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) e[k] += __shfl_xor(e[k], o, WAVE);
+  float x[8];
   float ss = 0.f;
-  for (int k = 0; k < per; ++k) {
-    const int d = lane + 64 * k;
-    float e = 0.f;
-    for (int t = 0; t < n; ++t) e += Store<T>::ld(q + int64_t(t) * D + d);
-    if (n > 0) e /= float(n);
-    x[k] = decay * m[d] + e;
-    ss += x[k] * x[k];
+  if (g == 0) {
+    float mo[8];
+    load8(m, mo);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      x[k] = decay * mo[k] + (n > 0 ? e[k] / float(n) : 0.f);
+      ss += x[k] * x[k];
+    }
   }
   ss = wave_sum(ss);
   const float nrm = fmaxf(sqrtf(ss), 1e-12f);
-  for (int k = 0; k < per; ++k) m[lane + 64 * k] = x[k] / nrm;
+  if (g == 0) {
+    *reinterpret_cast<float4 *>(m) = make_float4(x[0] / nrm, x[1] / nrm, x[2] / nrm, x[3] / nrm);
+    *reinterpret_cast<float4 *>(m + 4) = make_float4(x[4] / nrm, x[5] / nrm, x[6] / nrm, x[7] / nrm);
+  }
+}
+
+template <typename T>
+void qm_launch(const ikv_pool &p, const ikv_session *sess_dev, dim3 grid, float *M, const void *q_span, float decay,
+               hipStream_t st) {
+  if (p.D == 128)
+    k_qm_update<T, 128><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
+  else
+    k_qm_update<T, 64><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
 }
 
 hipError_t launch_qm_update(const ikv_pool &p, const ikv_session *sess_dev, int B, int max_rows, float *M,
                             const void *q_span, float decay, hipStream_t st) {
   dim3 grid(unsigned(cdiv(max_rows, 4)), unsigned(B));
-  if (p.kv_dtype == IKV_BF16)
-    k_qm_update<uint16_t><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, p.D, M, (const uint16_t *)q_span, decay);
-  else
-    k_qm_update<float><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, p.D, M, (const float *)q_span, decay);
+  if (p.kv_dtype == IKV_BF16) qm_launch<uint16_t>(p, sess_dev, grid, M, q_span, decay, st);
+  else qm_launch<float>(p, sess_dev, grid, M, q_span, decay, st);
   return hipGetLastError();
 }
 

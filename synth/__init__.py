@@ -386,4 +386,14 @@ def alias_slots(S: np.ndarray, seed: int, pairs: int) -> np.ndarray:
     return S
 
 
-T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS = 20, 21, 22
+def slot_map(n: int, num_slots: int, seed: int, dead_frac: float = 0.1, dead: int = DEAD_SLOT) -> np.ndarray:
+    """int32 slot map of n positions: distinct slots drawn from [0, num_slots) minus the
+    dead slot, about `dead_frac` of the positions pointing at the dead slot."""
+    g = stream(seed, T_MISC_SLOTS)
+    pool = np.delete(np.arange(num_slots, dtype=np.int64), dead)
+    S = g.choice(pool, size=n, replace=False).astype(np.int32)
+    S[g.random(n) < dead_frac] = dead
+    return S
+
+
+T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS, T_MISC_SLOTS = 20, 21, 22, 23

@@ -123,6 +123,12 @@ def test_calls_reject_bad_arguments_before_launch():
                                        None) == -1
     assert L.ikv_qm_update(ctypes.byref(p), sp, fake, 1, fake, fake, -1.0, None) == -1
     assert L.ikv_qm_update(ctypes.byref(p), sp, None, 1, fake, fake, 0.5, None) == -1
+    # span rows and memory rows must be 16-byte aligned (float32 pool: offsets a multiple of 4)
+    assert L.ikv_qm_update(ctypes.byref(p), ctypes.cast(_sess(qspan_off=2), ctypes.POINTER(ikv.Session)), fake, 1,
+                           fake, fake, 0.5, None) == -1
+    assert L.ikv_qm_update(ctypes.byref(p), ctypes.cast(_sess(mem_off=2), ctypes.POINTER(ikv.Session)), fake, 1,
+                           fake, fake, 0.5, None) == -1
+    assert L.ikv_qm_update(ctypes.byref(p), sp, fake, 1, fake + 8, fake, 0.5, None) == -1
     # B = 0 is a no-op
     assert L.ikv_select_budget(sp, fake, 0, None, 0, None, None, None, None, None, 0, None) == 0
 
