@@ -4,9 +4,11 @@
 // k_decode_split: one workgroup per (session, layer, KV head, split of the live
 // list). Each wavefront takes blocks of 64 live slots: lane k computes the logits
 // of slot k for the G query heads sharing the KV head, the block's weights are
-// folded into a running (max, sum, output) per head, and the value rows are read
-// with lanes along the head dimension. The partial state of every split goes to
-// the workspace; k_decode_combine merges the splits per (session, layer, head).
+// folded into a running (max, sum, output) per head. The value rows only need the
+// slots, so they are loaded together with the key rows (16 bytes per lane, 64 / (D/8)
+// rows per load instruction); the lanes of one channel group fold their rows at the end.
+// The partial state of every split goes to the workspace; k_decode_combine merges
+// the splits per (session, layer, head).
 #include <math.h>
 
 #include "ikv_internal.hpp"
@@ -18,24 +20,28 @@ int decode_splits(int maxN) {
   return int(s < 1 ? 1 : (s > 64 ? 64 : s));
 }
 
-// CPL consecutive value channels of one lane (CPL = D / 64).
-template <typename T, int CPL> struct Chan;
-template <> struct Chan<uint16_t, 2> {
-  static __device__ __forceinline__ void ld(const uint16_t *p, float (&v)[2]) {
-    const uint32_t w = *reinterpret_cast<const uint32_t *>(p);
-    v[0] = __uint_as_float(w << 16);
-    v[1] = __uint_as_float(w & 0xffff0000u);
+// 8 consecutive elements kept as raw 16-byte words until they are used.
+template <typename T> struct Raw8 {
+  static constexpr int W = sizeof(T) / 2;      // uint4 words: 1 for bf16, 2 for float
+  uint4 r[W];
+  __device__ __forceinline__ void ld(const T *p) {
+#pragma unroll
+    for (int k = 0; k < W; ++k) r[k] = reinterpret_cast<const uint4 *>(p)[k];
   }
-};
-template <> struct Chan<float, 2> {
-  static __device__ __forceinline__ void ld(const float *p, float (&v)[2]) {
-    const float2 x = *reinterpret_cast<const float2 *>(p);
-    v[0] = x.x;
-    v[1] = x.y;
+  __device__ __forceinline__ void unpack(float (&o)[8]) const {
+    if constexpr (W == 1) {
+      const uint32_t w[4] = {r[0].x, r[0].y, r[0].z, r[0].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        o[2 * i] = __uint_as_float(w[i] << 16);
+        o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+      }
+    } else {
+      const uint32_t w[8] = {r[0].x, r[0].y, r[0].z, r[0].w, r[1].x, r[1].y, r[1].z, r[1].w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] = __uint_as_float(w[i]);
+    }
   }
-};
-template <typename T> struct Chan<T, 1> {
-  static __device__ __forceinline__ void ld(const T *p, float (&v)[1]) { v[0] = Store<T>::ld(p); }
 };
 
 template <typename T, int D, int G>
@@ -44,10 +50,10 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
                                                       const ikv_session *__restrict__ sess, const T *__restrict__ q,
                                                       const int32_t *__restrict__ live,
                                                       const int32_t *__restrict__ n_live, float *__restrict__ ws) {
-  constexpr int CPL = D / 64;          // value channels per lane
+  constexpr int LPR = D / 8;           // lanes per value row (8 channels each)
+  constexpr int RPI = WAVE / LPR;      // value rows per load instruction
   __shared__ float qs[G][D];
   __shared__ float pw[4][G][DEC_BLOCK];
-  __shared__ int sl[4][DEC_BLOCK];
   __shared__ float red[4][G][2];
   __shared__ float ored[4][G][D];
 
@@ -62,19 +68,22 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
   const int chunk = int(cdiv(n, nsplit));
   const int k0 = split * chunk, k1 = min(n, k0 + chunk);
   const float scale = 1.0f / sqrtf(float(D));
+  const int32_t *lv = live + s.slot_off;
+  int slot0 = 0;                                   // the first block's slot: loads with the query rows
+  if (k0 + w * DEC_BLOCK + lane < k1) slot0 = lv[k0 + w * DEC_BLOCK + lane];
   for (int e = t; e < G * D; e += 256) {
     const int h = e / D, d = e - h * D;
     qs[h][d] = Store<T>::ld(q + ((int64_t(b) * L + l) * Hq + g * G + h) * D + d) * scale;
   }
   __syncthreads();
-  const int32_t *lv = live + s.slot_off;
-  float m[G], lsum[G], o[G][CPL];
+  const int rq = lane / LPR, cq = lane % LPR;     // value row group, channel group
+  float m[G], lsum[G], o[G][8];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     m[h] = -INFINITY;
     lsum[h] = 0.f;
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) o[h][i] = 0.f;
+    for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
   const int64_t row_stride = int64_t(Hkv) * D;
   const T *kbase = kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
@@ -82,16 +91,27 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
   for (int base = k0 + w * DEC_BLOCK; base < k1; base += 4 * DEC_BLOCK) {
     const int kk = base + lane;
     const bool valid = kk < k1;
-    const int slot = valid ? lv[kk] : 0;
+    const int slot = base == k0 + w * DEC_BLOCK ? slot0 : (valid ? lv[kk] : 0);
+    const int nb = min(DEC_BLOCK, k1 - base);
+    Raw8<T> v[DEC_BLOCK / RPI];
+#pragma unroll
+    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
+      const int i = r * RPI + rq;
+      const int si = __shfl(slot, i, WAVE);
+      if (i < nb) v[r].ld(vbase + int64_t(si) * row_stride + cq * 8);
+    }
     float x[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) x[h] = 0.f;
     if (valid) {
       const T *kr = kbase + int64_t(slot) * row_stride;
-#pragma unroll 4
+      Raw8<T> kraw[D / 8];
+#pragma unroll
+      for (int d = 0; d < D; d += 8) kraw[d / 8].ld(kr + d);
+#pragma unroll
       for (int d = 0; d < D; d += 8) {
         float kv[8];
-        load8(kr + d, kv);
+        kraw[d / 8].unpack(kv);
 #pragma unroll
         for (int h = 0; h < G; ++h) {
           const float4 q0 = *reinterpret_cast<const float4 *>(&qs[h][d]);
@@ -107,7 +127,6 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
         }
       }
     }
-    sl[w][lane] = slot;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float xv = valid ? x[h] : -INFINITY;
@@ -118,26 +137,34 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
       m[h] = mn;
       pw[w][h][lane] = p;
 #pragma unroll
-      for (int i = 0; i < CPL; ++i) o[h][i] *= corr;
+      for (int i = 0; i < 8; ++i) o[h][i] *= corr;
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    const int nb = min(DEC_BLOCK, k1 - base);
-    for (int i = 0; i < nb; ++i) {
-      const T *vr = vbase + int64_t(sl[w][i]) * row_stride;
-      float v[CPL];
-      Chan<T, CPL>::ld(vr + lane * CPL, v);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float p = pw[w][h][i];
+    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
+      const int i = r * RPI + rq;
+      if (i < nb) {
+        float vv[8];
+        v[r].unpack(vv);
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) o[h][c] = fmaf(p, v[c], o[h][c]);
+        for (int h = 0; h < G; ++h) {
+          const float p = pw[w][h][i];
+#pragma unroll
+          for (int c = 0; c < 8; ++c) o[h][c] = fmaf(p, vv[c], o[h][c]);
+        }
       }
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   }
-  // merge the four wavefronts
+  // fold the value row groups of each wavefront, then merge the four wavefronts
+#pragma unroll
+  for (int x = LPR; x < WAVE; x <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) o[h][c] += __shfl_xor(o[h][c], x, WAVE);
   if (lane == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -151,8 +178,9 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
     float mm = -INFINITY;
     for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
     const float f = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mm);
+    if (rq == 0)
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) ored[w][h][lane * CPL + c] = o[h][c] * f;
+      for (int c = 0; c < 8; ++c) ored[w][h][cq * 8 + c] = o[h][c] * f;
   }
   __syncthreads();
   for (int e = t; e < G * (D + 2); e += 256) {

@@ -16,6 +16,7 @@ constexpr int SEL_THREADS = 1024;
 constexpr int SEL_WAVES = SEL_THREADS / WAVE;
 constexpr int SEL_LDS_KEYS = 32768;        // sessions up to this N keep their keys in LDS
 constexpr int SEL_BINS = 2048;             // radix passes of 11, 11 and 10 bits
+constexpr int SEL_U = 8;                   // loads in flight per thread: every sweep is latency-bound
 
 __device__ __forceinline__ uint64_t lanes_below() { return (uint64_t(1) << (threadIdx.x & 63)) - 1; }
 
@@ -82,7 +83,7 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t bin, bool on) 
 #pragma unroll
   for (int r = 0; r < 4 && act; ++r) {
     const int leader = __ffsll((unsigned long long)act) - 1;
-    const uint32_t lb = __shfl(bin, leader, WAVE);
+    const uint32_t lb = uint32_t(__builtin_amdgcn_readlane(int(bin), leader));
     const uint64_t same = __ballot(on && bin == lb) & act;
     if (lane == leader) atomicAdd(&hist[lb], uint32_t(__popcll(same)));
     act &= ~same;
@@ -107,20 +108,35 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(const ikv_session *__res
   uint8_t *kp = keep + s.slot_off;
   const bool cached = s.N <= SEL_LDS_KEYS;
   auto forced_at = [&](int j) { return j < s.pi || (j >= s.qs && j < s.qe); };
+  // slot and score of position j (past the end: a dead position)
+  auto load = [&](int j, int &sv, float &fv, bool need_score) {
+    sv = j < s.N ? S[j] : dead;
+    fv = (need_score && j < s.N) ? sc[j] : 0.f;
+  };
   // key of a live candidate, 0 otherwise
-  auto key_at = [&](int j) -> uint32_t {
+  auto key_of = [&](int j, int sv, float fv) -> uint32_t {
+    if (j >= s.N) return 0u;
     if (cached) return keys[j];
-    return (S[j] != dead && !forced_at(j)) ? score_key(sc[j]) : 0u;
+    return (sv != dead && !forced_at(j)) ? score_key(fv) : 0u;
   };
 
   // counts of live and forced positions; the candidates' keys go to LDS
   int nl = 0, nf = 0;
-  for (int j = t; j < s.N; j += SEL_THREADS) {
-    const bool live = S[j] != dead;
-    const bool forced = forced_at(j);
-    nl += live;
-    nf += live && forced;
-    if (cached) keys[j] = (live && !forced && s.N > s.C) ? score_key(sc[j]) : 0u;
+  for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
+    int sv[SEL_U];
+    float fv[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) load(c0 + u * SEL_THREADS + t, sv[u], fv[u], cached);
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int j = c0 + u * SEL_THREADS + t;
+      if (j >= s.N) continue;
+      const bool live = sv[u] != dead;
+      const bool forced = forced_at(j);
+      nl += live;
+      nf += live && forced;
+      if (cached) keys[j] = (live && !forced && s.N > s.C) ? score_key(fv[u]) : 0u;
+    }
   }
   nl = block_sum(nl, red);
   nf = block_sum(nf, red);
@@ -147,11 +163,19 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(const ikv_session *__res
       const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + (pass == 1 ? 11 : 10)));
       for (int i = t; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0;
       __syncthreads();
-      for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS) {
-        const int j = c0 + t;
-        const uint32_t key = j < s.N ? key_at(j) : 0u;
-        const bool on = key != 0u && (key & himask) == (prefix & himask);
-        hist_add(hist, (key >> shift) & (nbins - 1u), on);
+      for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
+        int sv[SEL_U];
+        float fv[SEL_U];
+        if (!cached)
+#pragma unroll
+          for (int u = 0; u < SEL_U; ++u) load(c0 + u * SEL_THREADS + t, sv[u], fv[u], true);
+#pragma unroll
+        for (int u = 0; u < SEL_U; ++u) {
+          const int j = c0 + u * SEL_THREADS + t;
+          const uint32_t key = key_of(j, sv[u], fv[u]);
+          const bool on = key != 0u && (key & himask) == (prefix & himask);
+          hist_add(hist, (key >> shift) & (nbins - 1u), on);
+        }
       }
       __syncthreads();
       // thread t owns bins 2t, 2t+1 (pass 2: bin t); find the bin holding the kk-th
@@ -196,32 +220,47 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(const ikv_session *__res
   wave_range(s.N, lo, hi);
   int ties = 0;
   if (take > 0)
-    for (int64_t c0 = lo; c0 < hi; c0 += WAVE) {
-      const int j = int(c0) + lane;
-      const bool eq = j < hi && key_at(j) == prefix;
-      ties += __popcll(__ballot(eq));
+    for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
+      int sv[SEL_U];
+      float fv[SEL_U];
+      if (!cached)
+#pragma unroll
+        for (int u = 0; u < SEL_U; ++u) load(int(c0) + u * WAVE + lane, sv[u], fv[u], true);
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) {
+        const int j = int(c0) + u * WAVE + lane;
+        const bool eq = j < hi && key_of(j, sv[u], fv[u]) == prefix;
+        ties += __popcll(__ballot(eq));
+      }
     }
   int all_ties;
   int rank = wave_base(ties, all_ties, red);
   int kept = 0;
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE) {
-    const int j = int(c0) + lane;
-    bool k = false, eq = false;
-    if (j < hi) {
-      const bool live = S[j] != dead;
-      if (live && forced_at(j)) {
-        k = true;
-      } else if (live && take > 0) {
-        const uint32_t key = key_at(j);
-        k = key > prefix;
-        eq = key == prefix;
+  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
+    int sv[SEL_U];
+    float fv[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) load(int(c0) + u * WAVE + lane, sv[u], fv[u], !cached);
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int j = int(c0) + u * WAVE + lane;
+      bool k = false, eq = false;
+      if (j < hi) {
+        const bool live = sv[u] != dead;
+        if (live && forced_at(j)) {
+          k = true;
+        } else if (live && take > 0) {
+          const uint32_t key = key_of(j, sv[u], fv[u]);
+          k = key > prefix;
+          eq = key == prefix;
+        }
       }
+      const uint64_t bal = __ballot(eq);
+      if (eq && rank + __popcll(bal & lanes_below()) < kk) k = true;
+      rank += __popcll(bal);
+      if (j < hi) kp[j] = k ? 1 : 0;
+      kept += k;
     }
-    const uint64_t bal = __ballot(eq);
-    if (eq && rank + __popcll(bal & lanes_below()) < kk) k = true;
-    rank += __popcll(bal);
-    if (j < hi) kp[j] = k ? 1 : 0;
-    kept += k;
   }
   kept = block_sum(kept, red);
   if (t == 0) {
@@ -290,36 +329,49 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
   int64_t lo, hi;
   wave_range(s.N, lo, hi);
   int surv = 0;
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE) {
-    const int j = int(c0) + lane;
-    bool k = false;
-    if (j < hi) {
-      const int u = S[j];
-      k = u != dead && kp[j] != 0;
-      if (k) sets.set(sets.kept, u);
+  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
+    int sv[SEL_U];
+    uint8_t kv[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const int j = int(c0) + u * WAVE + lane;
+      sv[u] = j < hi ? S[j] : dead;
+      kv[u] = j < hi ? kp[j] : 0;
     }
-    surv += __popcll(__ballot(k));
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) {
+      const bool k = sv[u] != dead && kv[u] != 0;
+      if (k) sets.set(sets.kept, sv[u]);
+      surv += __popcll(__ballot(k));
+    }
   }
   int total_live;
   int pos = wave_base(surv, total_live, red);
   sets.sync();
   // reroute dropped positions, mark freeable slots, list the survivors in position order
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE) {
-    const int j = int(c0) + lane;
-    bool k = false;
-    int u = dead;
-    if (j < hi) {
-      u = S[j];
+  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
+    int sv[SEL_U];
+    uint8_t kv[SEL_U];
+#pragma unroll
+    for (int q = 0; q < SEL_U; ++q) {
+      const int j = int(c0) + q * WAVE + lane;
+      sv[q] = j < hi ? S[j] : dead;
+      kv[q] = j < hi ? kp[j] : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < SEL_U; ++q) {
+      const int j = int(c0) + q * WAVE + lane;
+      const int u = sv[q];
       const bool alive = u != dead;
-      k = alive && kp[j] != 0;
+      const bool k = alive && kv[q] != 0;
       if (alive && !k) {
         S[j] = dead;
         if (j >= s.radix_prefix && !((sets.word(sets.kept, u >> 5) >> (u & 31)) & 1u)) sets.set(sets.freed, u);
       }
+      const uint64_t bal = __ballot(k);
+      if (k) live[s.slot_off + pos + __popcll(bal & lanes_below())] = u;
+      pos += __popcll(bal);
     }
-    const uint64_t bal = __ballot(k);
-    if (k) live[s.slot_off + pos + __popcll(bal & lanes_below())] = u;
-    pos += __popcll(bal);
   }
   if (t == 0) n_live[b] = total_live;
   sets.sync();
