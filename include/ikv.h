@@ -229,6 +229,23 @@ ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, in
 /* Message of the last error on this thread ("" if none). */
 const char *ikv_last_error(void);
 
+/*
+ * Per-kernel timing, a tracing aid for profiling the calls above.
+ * ikv_timing(1) makes every following call record a pair of HIP events around
+ * each kernel it launches, on that call's stream; ikv_timing(0) stops recording
+ * (records already taken stay until read). ikv_timing returns IKV_OK.
+ * ikv_timing_read waits for the recorded events, writes up to `cap` entries in
+ * launch order (kernel name: a static string; elapsed milliseconds), drops every
+ * record and returns how many records it held (a count above cap means the rest
+ * were not written), or IKV_EHIP if an event call failed. At most 65536 records
+ * are kept between reads; later launches are not recorded. names and ms are host
+ * memory and may be NULL when cap is 0. The record list is process-wide: switch
+ * timing on, launch and read from one thread. Event pairs add a little time
+ * between kernels; time whole calls with timing off.
+ */
+ikv_status ikv_timing(int32_t enable);
+int32_t ikv_timing_read(const char **names, float *ms, int32_t cap);
+
 #ifdef __cplusplus
 }
 #endif

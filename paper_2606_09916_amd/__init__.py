@@ -7,4 +7,4 @@ redirect and slot-map decode attention. This package is its Python binding.
 from .ikv import (CALL_DECODE, CALL_REDIRECT, CALL_SCORE, CALL_SELECT, IKV_BF16, IKV_F32,  # noqa: F401
                   IKV_NO_XATTN, IKV_RESIDUAL, SYMBOLS, IkvError, Pool, Session, Sessions, Workspace,
                   decode_attend_slotmap, init_dead_slot, lib, make_pool, qm_update, redirect_slots,
-                  score_history, select_budget, workspace_bytes)
+                  score_history, select_budget, timing, timing_read, workspace_bytes)

@@ -4,11 +4,34 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "ikv_internal.hpp"
 
 namespace {
+
+// ---- per-kernel timing (ikv_timing)
+struct TimingRec {
+  const char *name;
+  hipEvent_t a, b;
+};
+constexpr size_t kMaxTimingRecs = 65536;
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_recs;      // recorded since the last read
+std::vector<hipEvent_t> g_events;   // idle events, reused
+
+hipEvent_t take_event() {
+  if (!g_events.empty()) {
+    hipEvent_t e = g_events.back();
+    g_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
 
 thread_local std::string g_err;
 
@@ -107,6 +130,60 @@ size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
 extern "C" {
 
 const char *ikv_last_error(void) { return g_err.c_str(); }
+
+namespace ikv {
+
+KTimer::KTimer(const char *name, hipStream_t stream) : idx(-1), st(stream) {
+  if (!g_timing) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (!g_timing || g_recs.size() >= kMaxTimingRecs) return;
+  TimingRec r{name, take_event(), take_event()};
+  if (!r.a || !r.b || hipEventRecord(r.a, st) != hipSuccess) {
+    if (r.a) g_events.push_back(r.a);
+    if (r.b) g_events.push_back(r.b);
+    return;
+  }
+  g_recs.push_back(r);
+  idx = int(g_recs.size()) - 1;
+}
+
+KTimer::~KTimer() {
+  if (idx < 0) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (size_t(idx) < g_recs.size()) (void)hipEventRecord(g_recs[size_t(idx)].b, st);
+}
+
+}  // namespace ikv
+
+ikv_status ikv_timing(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = enable != 0;
+  return ok();
+}
+
+int32_t ikv_timing_read(const char **names, float *ms, int32_t cap) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (cap > 0 && (!names || !ms)) return fail(IKV_EINVAL, "names / ms is NULL with cap > 0");
+  const int32_t n = int32_t(g_recs.size());
+  hipError_t err = hipSuccess;
+  for (int32_t i = 0; i < n; ++i) {
+    TimingRec &r = g_recs[size_t(i)];
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    if (i < cap) {
+      names[i] = r.name;
+      ms[i] = t;
+    }
+    g_events.push_back(r.a);
+    g_events.push_back(r.b);
+  }
+  g_recs.clear();
+  if (err != hipSuccess) return hip_status(err, "ikv_timing_read");
+  ok();
+  return n;
+}
 
 ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, int32_t B, int32_t call,
                                uint32_t flags, size_t *bytes) {

@@ -175,6 +175,15 @@ struct ScoreArgs {
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
 };
 
+// Opt-in per-kernel timing (ikv_timing in the C ABI): every launch site holds a
+// KTimer, which, while timing is on, records a HIP event pair around its launch.
+struct KTimer {
+  int idx;
+  hipStream_t st;
+  KTimer(const char *name, hipStream_t stream);
+  ~KTimer();
+};
+
 hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);
 hipError_t launch_qm_update(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_rows,
                             float *M, const void *q_span, float decay, hipStream_t st);

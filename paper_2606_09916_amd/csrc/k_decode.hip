@@ -226,9 +226,15 @@ __global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ 
 template <typename T, int D, int G>
 static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
                                   const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
-  k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
-      (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws);
-  k_decode_combine<T, D><<<dim3(p.L * p.Hq, B), D, 0, st>>>(ws, splits, p.L, p.Hq, (T *)out);
+  {
+    KTimer kt_("k_decode_split<T, D, G>", st);
+    k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
+        (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws);
+  }
+  {
+    KTimer kt_("k_decode_combine<T, D>", st);
+    k_decode_combine<T, D><<<dim3(p.L * p.Hq, B), D, 0, st>>>(ws, splits, p.L, p.Hq, (T *)out);
+  }
   return hipGetLastError();
 }
 

@@ -20,11 +20,17 @@ hipError_t launch_init_dead_slot(const ikv_pool &p, hipStream_t st) {
   int64_t n = int64_t(p.L) * HD;
   dim3 grid(unsigned(cdiv(n, 256)));
   if (p.kv_dtype == IKV_BF16)
-    k_init_dead_slot<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)p.k_pool, (uint16_t *)p.v_pool, p.L,
-                                                      p.num_slots, HD, p.dead_slot);
+    {
+      KTimer kt_("k_init_dead_slot<uint16_t>", st);
+      k_init_dead_slot<uint16_t><<<grid, 256, 0, st>>>((uint16_t *)p.k_pool, (uint16_t *)p.v_pool, p.L,
+                                                        p.num_slots, HD, p.dead_slot);
+    }
   else
-    k_init_dead_slot<float><<<grid, 256, 0, st>>>((float *)p.k_pool, (float *)p.v_pool, p.L, p.num_slots,
-                                                   HD, p.dead_slot);
+    {
+      KTimer kt_("k_init_dead_slot<float>", st);
+      k_init_dead_slot<float><<<grid, 256, 0, st>>>((float *)p.k_pool, (float *)p.v_pool, p.L, p.num_slots,
+                                                     HD, p.dead_slot);
+    }
   return hipGetLastError();
 }
 
@@ -93,9 +99,15 @@ template <typename T>
 void qm_launch(const ikv_pool &p, const ikv_session *sess_dev, dim3 grid, float *M, const void *q_span, float decay,
                hipStream_t st) {
   if (p.D == 128)
-    k_qm_update<T, 128><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
+    {
+      KTimer kt_("k_qm_update<T, 128>", st);
+      k_qm_update<T, 128><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
+    }
   else
-    k_qm_update<T, 64><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
+    {
+      KTimer kt_("k_qm_update<T, 64>", st);
+      k_qm_update<T, 64><<<grid, 256, 0, st>>>(sess_dev, p.L, p.Hkv, M, (const T *)q_span, decay);
+    }
 }
 
 hipError_t launch_qm_update(const ikv_pool &p, const ikv_session *sess_dev, int B, int max_rows, float *M,

@@ -376,22 +376,40 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   const int64_t F = 3 * D + 1;
   const int64_t n = F * HC + (F + HC) * HIDDEN + int64_t(HIDDEN) * HC;
-  k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
-  k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);
-  k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma);
+  {
+    KTimer kt_("k_res_transpose", st);
+    k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
+  }
+  {
+    KTimer kt_("k_mbar_part<D>", st);
+    k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);
+  }
+  {
+    KTimer kt_("k_res_setup<D>", st);
+    k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma);
+  }
   if (a.maxNq > 0)
-    k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
-                                                                         a.mfma);
+    {
+      KTimer kt_("k_res_kv<D>", st);
+      k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
+                                                                           a.mfma);
+    }
   if (a.mfma_resid) {
-    k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + HC + HIDDEN, 256)), a.B), 256, 0, st>>>(
-        a.sess_dev, a.residual, a.ws, p.L, p.Hkv);
+    {
+      KTimer kt_("k_res_fold<D>", st);
+      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + HC + HIDDEN, 256)), a.B), 256, 0, st>>>(
+          a.sess_dev, a.residual, a.ws, p.L, p.Hkv);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_residual_mfma(a, st);
   }
-  k_residual<D><<<dim3(unsigned(cdiv(a.maxN, 32)), a.B), 256, 0, st>>>(
-      a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
-      (a.flags & IKV_NO_XATTN) == 0, a.mfma);
+  {
+    KTimer kt_("k_residual<D>", st);
+    k_residual<D><<<dim3(unsigned(cdiv(a.maxN, 32)), a.B), 256, 0, st>>>(
+        a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
+        (a.flags & IKV_NO_XATTN) == 0, a.mfma);
+  }
   return hipGetLastError();
 }
 

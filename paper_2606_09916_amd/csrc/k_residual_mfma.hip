@@ -293,9 +293,12 @@ __global__ void __launch_bounds__(256) k_residual_mfma(const ikv_session *__rest
 
 hipError_t launch_residual_mfma(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
-  k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, RT)), a.B), 256, 0, st>>>(
-      a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
-      (a.flags & IKV_NO_XATTN) == 0);
+  {
+    KTimer kt_("k_residual_mfma", st);
+    k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, RT)), a.B), 256, 0, st>>>(
+        a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
+        (a.flags & IKV_NO_XATTN) == 0);
+  }
   return hipGetLastError();
 }
 

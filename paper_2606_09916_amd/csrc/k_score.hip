@@ -275,19 +275,34 @@ static hipError_t launch_score_t(const ScoreArgs &a, hipStream_t st) {
   const bool resid = (a.flags & IKV_RESIDUAL) != 0;
   const unsigned tiles = unsigned(cdiv(a.maxN, SCORE_TILE));
   const T *kp = static_cast<const T *>(p.k_pool);
-  k_score_stats<T, D><<<dim3(tiles, units, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                               a.slot_maps, a.M, a.ws, resid);
-  k_score_lse<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, units,
-                                                                                       D, resid);
-  k_score_rule<T, D><<<dim3(tiles, p.L, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                            a.slot_maps, a.M, a.ws, resid);
-  k_score_finish<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.slot_maps, p.dead_slot,
-                                                                        a.scores, a.ws, p.L, units, D, resid);
+  {
+    KTimer kt_("k_score_stats<T, D>", st);
+    k_score_stats<T, D><<<dim3(tiles, units, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.M, a.ws, resid);
+  }
+  {
+    KTimer kt_("k_score_lse", st);
+    k_score_lse<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.ws, p.L, units,
+                                                                                         D, resid);
+  }
+  {
+    KTimer kt_("k_score_rule<T, D>", st);
+    k_score_rule<T, D><<<dim3(tiles, p.L, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                              a.slot_maps, a.M, a.ws, resid);
+  }
+  {
+    KTimer kt_("k_score_finish", st);
+    k_score_finish<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.slot_maps, p.dead_slot,
+                                                                          a.scores, a.ws, p.L, units, D, resid);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !resid) return e;
   constexpr int TOK = 256 / (D / 2);
-  k_kbar<T, D><<<dim3(unsigned(cdiv(a.maxN, TOK)), a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
-                                                                       a.sess_dev, a.slot_maps, a.ws);
+  {
+    KTimer kt_("k_kbar<T, D>", st);
+    k_kbar<T, D><<<dim3(unsigned(cdiv(a.maxN, TOK)), a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                         a.sess_dev, a.slot_maps, a.ws);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_residual(a, st);

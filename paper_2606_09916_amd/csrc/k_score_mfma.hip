@@ -623,30 +623,57 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   const bool resid = (a.flags & IKV_RESIDUAL) != 0;
   const unsigned tiles = unsigned(cdiv(a.maxN, MFMA_TILE));
   const uint16_t *kp = static_cast<const uint16_t *>(p.k_pool);
-  k_fill_skipped<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.scores);
-  k_msplit<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR * 4, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L,
-                                                                                        p.Hkv, resid);
+  {
+    KTimer kt_("k_fill_skipped", st);
+    k_fill_skipped<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.scores);
+  }
+  {
+    KTimer kt_("k_msplit", st);
+    k_msplit<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR * 4, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L,
+                                                                                          p.Hkv, resid);
+  }
   const bool ring = a.maxR <= 64;
   if (ring)
-    k_score_ring<false, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                 a.slot_maps, a.ws, a.scores, resid);
+    {
+      KTimer kt_("k_score_ring<false, false>", st);
+      k_score_ring<false, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                   a.slot_maps, a.ws, a.scores, resid);
+    }
   else
-    k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                 a.slot_maps, a.ws, a.scores, resid);
-  k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
-                                                                                      resid, ring ? PART_TILE : MFMA_TILE);
+    {
+      KTimer kt_("k_score_mfma<false, false>", st);
+      k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                   a.slot_maps, a.ws, a.scores, resid);
+    }
+  {
+    KTimer kt_("k_lse_mfma", st);
+    k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
+                                                                                        resid, ring ? PART_TILE : MFMA_TILE);
+  }
   if (ring && resid)
-    k_score_ring<true, true><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                               a.slot_maps, a.ws, a.scores, resid);
+    {
+      KTimer kt_("k_score_ring<true, true>", st);
+      k_score_ring<true, true><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.ws, a.scores, resid);
+    }
   else if (ring)
-    k_score_ring<true, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
-                                                                a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+    {
+      KTimer kt_("k_score_ring<true, false>", st);
+      k_score_ring<true, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                  a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+    }
   else if (resid)
-    k_score_mfma<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                               a.slot_maps, a.ws, a.scores, resid);
+    {
+      KTimer kt_("k_score_mfma<true, true>", st);
+      k_score_mfma<true, true><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.ws, a.scores, resid);
+    }
   else
-    k_score_mfma<true, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
-                                                                a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+    {
+      KTimer kt_("k_score_mfma<true, false>", st);
+      k_score_mfma<true, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                  a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+    }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !resid) return e;
   return launch_residual(a, st);

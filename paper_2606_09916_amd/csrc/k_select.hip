@@ -271,7 +271,10 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select(const ikv_session *__res
 
 hipError_t launch_select(const ikv_session *sess_dev, int B, int, const int32_t *slot_maps, int32_t dead,
                          const float *scores, uint8_t *keep, int32_t *n_keep, float *tau, hipStream_t st) {
-  k_select<<<B, SEL_THREADS, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, n_keep, tau);
+  {
+    KTimer kt_("k_select", st);
+    k_select<<<B, SEL_THREADS, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, n_keep, tau);
+  }
   return hipGetLastError();
 }
 
@@ -411,11 +414,17 @@ hipError_t launch_redirect(const ikv_session *sess_dev, int B, int64_t num_slots
                            const uint8_t *keep, int32_t *freed, int32_t *n_freed, int32_t *live, int32_t *n_live,
                            uint32_t *ws, hipStream_t st) {
   if (bitset_words(num_slots) <= RED_LDS_WORDS)
-    k_redirect<true><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
-                                                n_live, ws);
+    {
+      KTimer kt_("k_redirect<true>", st);
+      k_redirect<true><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
+                                                  n_live, ws);
+    }
   else
-    k_redirect<false><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
-                                                 n_live, ws);
+    {
+      KTimer kt_("k_redirect<false>", st);
+      k_redirect<false><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
+                                                   n_live, ws);
+    }
   return hipGetLastError();
 }
 

@@ -21,7 +21,8 @@ STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE",
 
 # Every symbol include/ikv.h declares.
 SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget",
-           "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error")
+           "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error",
+           "ikv_timing", "ikv_timing_read")
 
 
 class IkvError(RuntimeError):
@@ -65,6 +66,8 @@ def lib() -> ctypes.CDLL:
             "ikv_decode_attend_slotmap": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p],
             "ikv_workspace_bytes": [P, S, c_int32, c_int32, c_uint32, ctypes.POINTER(c_size_t)],
+            "ikv_timing": [c_int32],
+            "ikv_timing_read": [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(c_float), c_int32],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -192,3 +195,19 @@ def decode_attend_slotmap(pool: Pool, sess: Sessions, q, live, n_live, out, ws: 
                                            _ptr(live), _ptr(n_live), _ptr(out), wp, wn, _stream(stream)),
            "ikv_decode_attend_slotmap")
 
+
+# ----------------------------------------------------------------------------- timing
+
+def timing(enable: bool) -> None:
+    """Record (or stop recording) a HIP event pair around every kernel the calls launch."""
+    _check(lib().ikv_timing(1 if enable else 0), "ikv_timing")
+
+
+def timing_read(cap: int = 65536) -> list[tuple[str, float]]:
+    """Wait for the recorded kernels and return [(kernel name, ms)] in launch order."""
+    names = (ctypes.c_char_p * max(1, cap))()
+    ms = (c_float * max(1, cap))()
+    n = lib().ikv_timing_read(names, ms, cap)
+    if n < 0:
+        _check(n, "ikv_timing_read")
+    return [(names[i].decode(), float(ms[i])) for i in range(min(n, cap))]

@@ -138,3 +138,12 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(raw, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         raw.lib()
+
+
+def test_timing_toggle_and_empty_read():
+    # no kernel launched: switching timing on and reading touches no device
+    assert ikv.lib().ikv_timing(1) == 0
+    assert ikv.timing_read() == []
+    assert ikv.lib().ikv_timing_read(None, None, 0) == 0
+    assert ikv.lib().ikv_timing_read(None, None, 5) == -1
+    assert ikv.lib().ikv_timing(0) == 0
