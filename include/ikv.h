@@ -156,7 +156,8 @@ ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess,
  *     (214,274 floats at D = 128; 124,162 at D = 64). Ignored without IKV_RESIDUAL.
  *   scores: device float32, per session [N]: s_j on A, -INFINITY elsewhere.
  *   Sessions with N <= C are skipped (Appendix H): all their scores are -INFINITY.
- *   slot_maps, M, qpos: read only.
+ *   slot_maps, M, qpos: read only. M + mem_off must be 16-byte aligned for every
+ *   session (IKV_EINVAL otherwise).
  */
 ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
                              const ikv_session *sess_dev, int32_t B,

@@ -257,6 +257,8 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   if (resid && !residual) return fail(IKV_EINVAL, "IKV_RESIDUAL set but residual is NULL");
   int maxR = 0, maxNq = 0, anyq = 0;
   for (int b = 0; b < B; ++b) {
+    if ((reinterpret_cast<uintptr_t>(M) + size_t(sess[b].mem_off) * 4) % 16)
+      return fail(IKV_EINVAL, "session %d: M + mem_off must be 16-byte aligned", b);
     maxR = sess[b].R > maxR ? sess[b].R : maxR;
     maxNq = sess[b].nq > maxNq ? sess[b].nq : maxNq;
     anyq |= sess[b].nq > 0;

@@ -108,15 +108,20 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
     for (int p = 0; p < MBAR_PARTS; ++p) a += misc[int64_t(p) * D + t];
     mbar[t] = a / float(int64_t(units) * s.R);
   }
-  if (t == 0) {
+  if (t < WAVE) {   // live query positions in order: one wave, ranked by ballot
     int n = 0;
     const int32_t *S = slot_maps + s.slot_off;
     const int32_t *qp = qpos + s.qpos_off;
-    for (int i = 0; i < s.nq; ++i) {
-      const int j = qp[i];
-      if (j >= 0 && j < s.N && S[j] != dead) qlist[n++] = j;
+    for (int i0 = 0; i0 < s.nq; i0 += WAVE) {
+      const int i = i0 + t;
+      int j = -1;
+      if (i < s.nq) j = qp[i];
+      const bool ok = j >= 0 && j < s.N && S[j] != dead;
+      const uint64_t bal = __ballot(ok);
+      if (ok) qlist[n + __popcll(bal & ((uint64_t(1) << t) - 1))] = j;
+      n += __popcll(bal);
     }
-    reinterpret_cast<int *>(mbar)[D] = n;
+    if (t == 0) reinterpret_cast<int *>(mbar)[D] = n;
   }
 }
 
@@ -380,6 +385,7 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
     KTimer kt_("k_res_transpose", st);
     k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
   }
+  if (!a.mfma)   // on the matrix-core path k_msplit leaves the partial sums of mbar
   {
     KTimer kt_("k_mbar_part<D>", st);
     k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);

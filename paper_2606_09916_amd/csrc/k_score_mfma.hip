@@ -38,27 +38,73 @@ __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 
 // M' = M * log2(e) / sqrt(D) split into bf16 hi and lo. Per (unit, row), 256 bf16
 // in fragment order [g 0..3][k-step 0..3][hi 8 | lo 8], where (k-step, g) holds
 // channels (4 k-step + g) * 8 .. + 8: lane group g of an MFMA reads 128 contiguous bytes.
+// Workgroup p takes rows [p*rows/P, (p+1)*rows/P) with P = MBAR_PARTS; thread (r, c)
+// splits channel group c of rows r, r + 16, ... (32 bytes in, two 16-byte stores out),
+// a batch of rows in flight at once. With the residual head on it also sums the raw
+// rows: the workgroup's column sums are partial p of mbar.
+constexpr int MS_BATCH = 6;
+
 __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ sess, const float *__restrict__ M,
                                                 float *__restrict__ ws, int L, int Hkv, bool resid) {
+  __shared__ float red[16][MD];
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   const int units = L * Hkv;
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= int64_t(units) * s.R * 4) return;
-  const int64_t row = i >> 2;
-  const int g = int(i & 3);
+  const int64_t rows = int64_t(units) * s.R;
+  const int p = blockIdx.x;
+  const int64_t r0 = rows * p / MBAR_PARTS, r1 = rows * (p + 1) / MBAR_PARTS;
+  const int rg = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const int g = c & 3, ks = c >> 2;
   const float scale = LOG2E / sqrtf(float(MD));
-  uint16_t *dst = reinterpret_cast<uint16_t *>(ws + score_offset(sess, b, L, units, MD, resid, true)) + row * 256 +
-                  g * 64;
-  for (int ks = 0; ks < 4; ++ks) {
-    const float *src = M + s.mem_off + row * MD + (4 * ks + g) * 8;
-    for (int e = 0; e < 8; ++e) {
-      const float v = src[e] * scale;
-      const uint16_t hi = float_to_bf16_bits(v);
-      dst[ks * 16 + e] = hi;
-      dst[ks * 16 + 8 + e] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+  float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  uint16_t *dst = reinterpret_cast<uint16_t *>(base) + (g * 4 + ks) * 16;
+  const float *src = M + s.mem_off + c * 8;
+  float cs[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) cs[e] = 0.f;
+  for (int64_t r = r0 + rg; r < r1; r += 16 * MS_BATCH) {
+    float4 va[MS_BATCH], vb[MS_BATCH];
+#pragma unroll
+    for (int k = 0; k < MS_BATCH; ++k) {
+      const int64_t rr = r + 16 * k;
+      if (rr < r1) {
+        va[k] = *reinterpret_cast<const float4 *>(src + rr * MD);
+        vb[k] = *reinterpret_cast<const float4 *>(src + rr * MD + 4);
+      }
     }
+#pragma unroll
+    for (int k = 0; k < MS_BATCH; ++k) {
+      const int64_t rr = r + 16 * k;
+      if (rr >= r1) continue;
+      const float v[8] = {va[k].x, va[k].y, va[k].z, va[k].w, vb[k].x, vb[k].y, vb[k].z, vb[k].w};
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const float x0 = v[e] * scale, x1 = v[e + 1] * scale;
+        const uint16_t h0 = float_to_bf16_bits(x0), h1 = float_to_bf16_bits(x1);
+        const uint16_t l0 = float_to_bf16_bits(x0 - bf16_bits_to_float(h0));
+        const uint16_t l1 = float_to_bf16_bits(x1 - bf16_bits_to_float(h1));
+        hw[e / 2] = uint32_t(h0) | (uint32_t(h1) << 16);
+        lw[e / 2] = uint32_t(l0) | (uint32_t(l1) << 16);
+        cs[e] += v[e];
+        cs[e + 1] += v[e + 1];
+      }
+      uint16_t *d = dst + rr * 256;
+      *reinterpret_cast<uint4 *>(d) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      *reinterpret_cast<uint4 *>(d + 8) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+    }
+  }
+  if (!resid) return;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rg][c * 8 + e] = cs[e];
+  __syncthreads();
+  if (threadIdx.x < MD) {
+    float tsum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) tsum += red[k][threadIdx.x];
+    const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+    base[z.off_misc() + int64_t(p) * MD + threadIdx.x] = tsum;
   }
 }
 
@@ -578,15 +624,25 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   const float *part = base + z.off_part();
   const int64_t tiles = cdiv(s.N, ptile);
   float m = -INFINITY, zs = 0.f;
+  constexpr int LB = 8;                            // tiles in flight per thread
   if (on)
-    for (int64_t k = w; k < tiles; k += 8) {
-      const float2 p = *reinterpret_cast<const float2 *>(part + (k * rows + i) * 2);
-      if (p.x == -INFINITY) continue;
-      if (p.x > m) {
-        zs = (m == -INFINITY ? 0.f : zs * exp2f(m - p.x)) + p.y;
-        m = p.x;
-      } else {
-        zs += p.y * exp2f(p.x - m);
+    for (int64_t k0 = w; k0 < tiles; k0 += 8 * LB) {
+      float2 pv[LB];
+#pragma unroll
+      for (int q = 0; q < LB; ++q) {
+        const int64_t k = k0 + 8 * q;
+        pv[q] = k < tiles ? *reinterpret_cast<const float2 *>(part + (k * rows + i) * 2) : make_float2(-INFINITY, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < LB; ++q) {
+        const float2 p = pv[q];
+        if (p.x == -INFINITY) continue;
+        if (p.x > m) {
+          zs = (m == -INFINITY ? 0.f : zs * exp2f(m - p.x)) + p.y;
+          m = p.x;
+        } else {
+          zs += p.y * exp2f(p.x - m);
+        }
       }
     }
   sm[w][lane] = m;
@@ -629,8 +685,7 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   }
   {
     KTimer kt_("k_msplit", st);
-    k_msplit<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR * 4, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L,
-                                                                                          p.Hkv, resid);
+    k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, resid);
   }
   const bool ring = a.maxR <= 64;
   if (ring)

@@ -113,6 +113,9 @@ def test_calls_reject_bad_arguments_before_launch():
     assert L.ikv_score_history(ctypes.byref(p), sp, fake, 1, fake, fake, fake, None, 0, fake, fake, 16, None) == -3
     assert L.ikv_score_history(ctypes.byref(p), sp, fake, 1, fake, fake, fake, None, 0, fake, fake + 4, 1 << 30,
                                None) == -3
+    # memory rows must be 16-byte aligned
+    assert L.ikv_score_history(ctypes.byref(p), ctypes.cast(_sess(mem_off=1), ctypes.POINTER(ikv.Session)), fake,
+                               1, fake, fake, fake, None, 0, fake, fake, 1 << 30, None) == -1
     # null outputs
     assert L.ikv_select_budget(sp, fake, 1, fake, 0, fake, None, fake, fake, None, 0, None) == -1
     assert L.ikv_redirect_slots(sp, fake, 1, 100, fake, 0, fake, fake, fake, None, fake, fake, 1 << 20,
