@@ -103,25 +103,45 @@ __global__ void __launch_bounds__(256) k_residual_mfma(const ikv_session *__rest
   __syncthreads();
   if (!any) return;
 
-  for (int e = t; e < RT * RD; e += 256) {
-    const int r = e / RD, d = e - r * RD;
-    const int j = pos_s[r];
-    uint16_t h, l;
-    split_bf16(j >= 0 ? kbar[int64_t(j) * RD + d] : 0.f, h, l);
-    xs[0][r * XS + d] = h;
-    xs[1][r * XS + d] = l;
+  // kbar rows of the tile (and K', V' of the live query positions), split into bf16
+  // hi + lo in LDS: eight float4 loads per thread per matrix, all in flight at once
+  constexpr int NQ4 = RT * RD / 4 / 256;
+  {
+    float4 v[NQ4];
+#pragma unroll
+    for (int q = 0; q < NQ4; ++q) {
+      const int e4 = q * 256 + t, r = e4 / (RD / 4), d = (e4 % (RD / 4)) * 4;
+      const int j = pos_s[r];
+      v[q] = j >= 0 ? *reinterpret_cast<const float4 *>(kbar + int64_t(j) * RD + d) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ4; ++q) {
+      const int e4 = q * 256 + t, r = e4 / (RD / 4), d = (e4 % (RD / 4)) * 4;
+      const float x[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) split_bf16(x[k], xs[0][r * XS + d + k], xs[1][r * XS + d + k]);
+    }
   }
   const bool on = xattn && nql > 0;
   if (on) {
-    for (int e = t; e < RES_MAX_KEYS * RD; e += 256) {
-      const int key = e / RD, d = e - key * RD;
-      uint16_t h, l;
-      split_bf16(key < nql ? kp[int64_t(key) * HC + d] : 0.f, h, l);
-      kps[0][key * XS + d] = h;
-      kps[1][key * XS + d] = l;
-      split_bf16(key < nql ? vp[int64_t(key) * HC + d] : 0.f, h, l);
-      vts[0][d * PS + key] = h;
-      vts[1][d * PS + key] = l;
+    float4 kv[NQ4], vv[NQ4];
+#pragma unroll
+    for (int q = 0; q < NQ4; ++q) {
+      const int e4 = q * 256 + t, key = e4 / (RD / 4), d = (e4 % (RD / 4)) * 4;
+      const bool live = key < nql;
+      kv[q] = live ? *reinterpret_cast<const float4 *>(kp + int64_t(key) * HC + d) : make_float4(0.f, 0.f, 0.f, 0.f);
+      vv[q] = live ? *reinterpret_cast<const float4 *>(vp + int64_t(key) * HC + d) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ4; ++q) {
+      const int e4 = q * 256 + t, key = e4 / (RD / 4), d = (e4 % (RD / 4)) * 4;
+      const float xk[4] = {kv[q].x, kv[q].y, kv[q].z, kv[q].w};
+      const float xv[4] = {vv[q].x, vv[q].y, vv[q].z, vv[q].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        split_bf16(xk[k], kps[0][key * XS + d + k], kps[1][key * XS + d + k]);
+        split_bf16(xv[k], vts[0][(d + k) * PS + key], vts[1][(d + k) * PS + key]);
+      }
     }
   }
   __syncthreads();
