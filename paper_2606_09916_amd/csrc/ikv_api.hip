@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -116,6 +117,16 @@ size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flag
   return size_t(f) * sizeof(float);
 }
 
+int64_t total_positions(const ikv_session *sess, int B) {
+  int64_t total = 0;
+  for (int b = 0; b < B; ++b) total = std::max<int64_t>(total, sess[b].slot_off + sess[b].N);
+  return total;
+}
+
+size_t select_bytes(const ikv_session *sess, int B) {
+  return B > 0 ? ikv::select_workspace_bytes(sess, B, total_positions(sess, B)) : 0;
+}
+
 size_t redirect_bytes(int64_t num_slots, int B) {
   return size_t(B) * 2 * size_t(ikv::bitset_words(num_slots)) * sizeof(uint32_t);
 }
@@ -199,6 +210,8 @@ ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, in
       *bytes = score_bytes(pool, sess, B, flags);
       return ok();
     case IKV_CALL_SELECT:
+      if ((r = check_sessions(sess, sess, B))) return r;
+      *bytes = select_bytes(sess, B);
       return ok();
     case IKV_CALL_REDIRECT:
       if (!pool) return fail(IKV_EINVAL, "pool is NULL");
@@ -291,15 +304,15 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
 ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
                              const int32_t *slot_maps, int32_t dead_slot, const float *scores, uint8_t *keep,
                              int32_t *n_keep, float *tau, void *workspace, size_t workspace_bytes, void *stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   ikv_status r = check_sessions(sess, sess_dev, B);
   if (r) return r;
   if (B == 0) return ok();
   if (!slot_maps || !scores || !keep || !n_keep || !tau)
     return fail(IKV_EINVAL, "slot_maps / scores / keep / n_keep / tau is NULL");
   if (dead_slot < 0) return fail(IKV_ESHAPE, "dead_slot < 0");
-  return hip_status(ikv::launch_select(sess_dev, B, max_n(sess, B), slot_maps, dead_slot, scores, keep, n_keep, tau,
+  if ((r = check_ws(workspace, workspace_bytes, select_bytes(sess, B)))) return r;
+  return hip_status(ikv::launch_select(sess, sess_dev, B, max_n(sess, B), slot_maps, dead_slot, scores, keep, n_keep,
+                                       tau, static_cast<uint32_t *>(workspace), total_positions(sess, B),
                                        (hipStream_t)stream),
                     "ikv_select_budget");
 }

@@ -188,9 +188,10 @@ hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);
 hipError_t launch_qm_update(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_rows,
                             float *M, const void *q_span, float decay, hipStream_t st);
 hipError_t launch_score(const ScoreArgs &a, hipStream_t st);
-hipError_t launch_select(const ikv_session *sess_dev, int B, int maxN, const int32_t *slot_maps,
-                         int32_t dead, const float *scores, uint8_t *keep, int32_t *n_keep,
-                         float *tau, hipStream_t st);
+hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_dev, int B, int maxN,
+                         const int32_t *slot_maps, int32_t dead, const float *scores, uint8_t *keep,
+                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st);
+size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions);
 hipError_t launch_redirect(const ikv_session *sess_dev, int B, int64_t num_slots, int32_t *slot_maps,
                            int32_t dead, const uint8_t *keep, int32_t *freed, int32_t *n_freed,
                            int32_t *live, int32_t *n_live, uint32_t *ws, hipStream_t st);

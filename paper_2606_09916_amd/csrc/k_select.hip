@@ -14,11 +14,21 @@ namespace ikv {
 
 constexpr int SEL_THREADS = 1024;
 constexpr int SEL_WAVES = SEL_THREADS / WAVE;
-constexpr int SEL_LDS_KEYS = 32768;        // sessions up to this N keep their keys in LDS
 constexpr int SEL_BINS = 2048;             // radix passes of 11, 11 and 10 bits
 constexpr int SEL_U = 8;                   // loads in flight per thread: every sweep is latency-bound
+constexpr int SEL_CHUNK = 4096;            // positions per workgroup of k_select_keys / k_select_mark
+constexpr int SEL_PART = SEL_BINS + 64;    // workspace words per chunk: histogram, counts, padding
+constexpr int SEL_LIST = 16384;            // keys (with positions) of the threshold bin held in LDS
+constexpr int SEL_TIES = 1024;             // ties at the threshold ranked directly (else by radix passes)
 
 __device__ __forceinline__ uint64_t lanes_below() { return (uint64_t(1) << (threadIdx.x & 63)) - 1; }
+
+// Loads of a batch are issued unconditionally, from an index clamped into [0, n), and
+// masked afterwards: a load under a branch is waited on at once, inside the branch.
+template <typename T>
+__device__ __forceinline__ T ld_clamped(const T *p, int64_t i, int64_t n) {
+  return p[i < n ? i : n - 1];
+}
 
 // Sum over the workgroup; `red` holds SEL_WAVES ints. Every thread must call it.
 __device__ __forceinline__ int block_sum(int v, int *red) {
@@ -91,189 +101,351 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t bin, bool on) 
   if ((act >> lane) & 1u) atomicAdd(&hist[bin], 1u);
 }
 
-__global__ void __launch_bounds__(SEL_THREADS) k_select(const ikv_session *__restrict__ sess,
-                                                        const int32_t *__restrict__ slot_maps, int dead,
-                                                        const float *__restrict__ scores, uint8_t *__restrict__ keep,
-                                                        int32_t *__restrict__ n_keep, float *__restrict__ tau) {
-  __shared__ uint32_t keys[SEL_LDS_KEYS];
+// ---- selection in three launches. Workspace, per call:
+//   parts: per session and chunk of SEL_CHUNK positions, the chunk's 2048-bin
+//          histogram of the top 11 key bits, its live count and live forced count;
+//   keys:  the key of every position of every session at slot_off (0: not a candidate);
+//   res:   per session the threshold key and the last tied position that is kept.
+//   k_select_keys:   one workgroup per chunk: keys, initial keep (live forced positions,
+//                    or every live position when the step is skipped), chunk histogram;
+//   k_select_finish: one workgroup per session: the histograms summed, the keys of the
+//                    bin that holds the take-th largest gathered with their positions,
+//                    the exact threshold by radix passes over them, and among the keys
+//                    equal to it the position of the last one taken (radix select on
+//                    positions, smallest first);
+//   k_select_mark:   one workgroup per chunk: keep every candidate above the threshold
+//                    and every tie at or before that position.
+__host__ __device__ inline int64_t sel_chunks_before(const ikv_session *sess, int b) {
+  int64_t c = 0;
+  for (int i = 0; i < b; ++i) c += cdiv(sess[i].N, SEL_CHUNK);
+  return c;
+}
+
+__global__ void __launch_bounds__(256) k_select_keys(const ikv_session *__restrict__ sess,
+                                                     const int32_t *__restrict__ slot_maps, int dead,
+                                                     const float *__restrict__ scores, uint8_t *__restrict__ keep,
+                                                     uint32_t *__restrict__ ws, int64_t keys_off) {
   __shared__ uint32_t hist[SEL_BINS];
-  __shared__ int red[SEL_WAVES];
-  __shared__ uint32_t sh_prefix;
-  __shared__ int sh_k;
-  const int b = blockIdx.x;
+  __shared__ int cnt[2];
+  const int b = blockIdx.y;
   const ikv_session s = sess[b];
-  const int t = threadIdx.x, lane = t & 63;
+  const int64_t j0 = int64_t(blockIdx.x) * SEL_CHUNK;
+  if (j0 >= s.N) return;
+  const int t = threadIdx.x;
+  const bool skip = s.N <= s.C;
+  uint32_t *part = ws + (sel_chunks_before(sess, b) + blockIdx.x) * SEL_PART;
+  uint32_t *keys = ws + keys_off + s.slot_off;
   const int32_t *S = slot_maps + s.slot_off;
   const float *sc = scores + s.slot_off;
   uint8_t *kp = keep + s.slot_off;
-  const bool cached = s.N <= SEL_LDS_KEYS;
-  auto forced_at = [&](int j) { return j < s.pi || (j >= s.qs && j < s.qe); };
-  // slot and score of position j (past the end: a dead position)
-  auto load = [&](int j, int &sv, float &fv, bool need_score) {
-    sv = j < s.N ? S[j] : dead;
-    fv = (need_score && j < s.N) ? sc[j] : 0.f;
-  };
-  // key of a live candidate, 0 otherwise
-  auto key_of = [&](int j, int sv, float fv) -> uint32_t {
-    if (j >= s.N) return 0u;
-    if (cached) return keys[j];
-    return (sv != dead && !forced_at(j)) ? score_key(fv) : 0u;
-  };
-
-  // counts of live and forced positions; the candidates' keys go to LDS
+  for (int i = t; i < SEL_BINS; i += 256) hist[i] = 0u;
+  if (t < 2) cnt[t] = 0;
+  __syncthreads();
+  constexpr int PER = SEL_CHUNK / 256;
+  int sv[PER];
+  float fv[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int64_t j = j0 + q * 256 + t;
+    sv[q] = ld_clamped(S, j, s.N);
+    fv[q] = ld_clamped(sc, j, s.N);
+  }
   int nl = 0, nf = 0;
-  for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
-    int sv[SEL_U];
-    float fv[SEL_U];
 #pragma unroll
-    for (int u = 0; u < SEL_U; ++u) load(c0 + u * SEL_THREADS + t, sv[u], fv[u], cached);
+  for (int q = 0; q < PER; ++q) {
+    const int64_t j = j0 + q * 256 + t;
+    const bool in = j < s.N;
+    const bool live = in && sv[q] != dead;
+    const bool forced = j < s.pi || (j >= s.qs && j < s.qe);
+    nl += live;
+    nf += live && forced;
+    const bool cand = live && !forced && !skip;
+    const uint32_t key = cand ? score_key(fv[q]) : 0u;
+    if (in) {
+      kp[j] = (live && (forced || skip)) ? 1 : 0;
+      keys[j] = key;
+    }
+    hist_add(hist, key >> 21, cand);
+  }
 #pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int j = c0 + u * SEL_THREADS + t;
-      if (j >= s.N) continue;
-      const bool live = sv[u] != dead;
-      const bool forced = forced_at(j);
-      nl += live;
-      nf += live && forced;
-      if (cached) keys[j] = (live && !forced && s.N > s.C) ? score_key(fv[u]) : 0u;
+  for (int o = 32; o > 0; o >>= 1) {
+    nl += __shfl_xor(nl, o, WAVE);
+    nf += __shfl_xor(nf, o, WAVE);
+  }
+  if ((t & 63) == 0) {
+    atomicAdd(&cnt[0], nl);
+    atomicAdd(&cnt[1], nf);
+  }
+  __syncthreads();
+  for (int i = t; i < SEL_BINS; i += 256) part[i] = hist[i];
+  if (t < 2) part[SEL_BINS + t] = uint32_t(cnt[t]);
+}
+
+// The bin of `hist` (nbins bins, nbins / SEL_THREADS per thread) holding the kk-th
+// largest value, scanning from the top bin down; writes the bin and the rank inside
+// it to sh[0], sh[1]. Every thread of the workgroup must call it.
+__device__ __forceinline__ void find_bin(const uint32_t *hist, int nbins, int kk, int *red, int *sh) {
+  const int t = threadIdx.x, lane = t & 63;
+  const int per = nbins / SEL_THREADS;
+  const int hi_bin = nbins - 1 - t * per;
+  int c = 0;
+  for (int q = 0; q < per; ++q) c += int(hist[hi_bin - q]);
+  int x = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, WAVE);
+    if (lane >= o) x += y;
+  }
+  int tot;
+  const int above = wave_base(__shfl(x, 63, WAVE), tot, red) + x - c;
+  if (above < kk && kk <= above + c) {
+    int cum = above;
+    for (int q = 0; q < per; ++q) {
+      const int h = int(hist[hi_bin - q]);
+      if (cum + h >= kk) {
+        sh[0] = hi_bin - q;
+        sh[1] = kk - cum;
+        break;
+      }
+      cum += h;
     }
   }
-  nl = block_sum(nl, red);
-  nf = block_sum(nf, red);
-  const int na = nl - nf;
+  __syncthreads();
+}
 
-  if (s.N <= s.C) {   // the compression event is skipped: every live position stays
-    for (int j = t; j < s.N; j += SEL_THREADS) kp[j] = S[j] != dead;
+// The kk-th largest of n values (1 <= kk <= n), get(i) -> (value, counted): radix
+// passes of 11, 11 and 10 bits from the top, starting at pass p0 when the bits above
+// it are already known to be `prefix` for every counted value. Every thread must call it.
+template <class Get>
+__device__ uint32_t kth_largest(Get get, int n, int kk, uint32_t *hist, int *red, int *sh, int p0 = 0,
+                                uint32_t prefix = 0) {
+  const int t = threadIdx.x;
+  for (int pass = p0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const uint32_t nbins = pass == 2 ? 1024u : 2048u;
+    const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + (pass == 1 ? 11 : 10)));
+    for (int i = t; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0u;
+    __syncthreads();
+    for (int c0 = 0; c0 < n; c0 += SEL_THREADS * SEL_U) {
+      uint32_t v[SEL_U];
+      bool c[SEL_U];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) {
+        const int i = c0 + u * SEL_THREADS + t;
+        get(i < n ? i : n - 1, v[u], c[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u)
+        if (c0 + u * SEL_THREADS + t >= n) c[u] = false;
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u)
+        hist_add(hist, (v[u] >> shift) & (nbins - 1u), c[u] && (v[u] & himask) == (prefix & himask));
+    }
+    __syncthreads();
+    find_bin(hist, int(nbins), kk, red, sh);
+    prefix |= uint32_t(sh[0]) << shift;
+    kk = sh[1];
+    __syncthreads();
+  }
+  return prefix;
+}
+
+__global__ void __launch_bounds__(SEL_THREADS) k_select_finish(const ikv_session *__restrict__ sess,
+                                                               int32_t *__restrict__ n_keep, float *__restrict__ tau,
+                                                               uint32_t *__restrict__ ws, int64_t keys_off,
+                                                               int64_t res_off) {
+  __shared__ uint32_t lkey[SEL_LIST];                 // keys of the threshold's top bin
+  __shared__ uint32_t lpos[SEL_LIST];                 // their positions
+  __shared__ uint32_t hist[SEL_BINS];
+  __shared__ int red[SEL_WAVES];
+  __shared__ int sh[2];
+  __shared__ int sh_n, sh_cnt[2];
+  const int b = blockIdx.x;
+  const ikv_session s = sess[b];
+  const int t = threadIdx.x, lane = t & 63;
+  const int64_t nch = cdiv(s.N, SEL_CHUNK);
+  const uint32_t *parts = ws + sel_chunks_before(sess, b) * SEL_PART;
+  const uint32_t *keys = ws + keys_off + s.slot_off;
+  uint32_t *res = ws + res_off + int64_t(b) * 4;
+  // chunk histograms and counts summed
+  if (t < 2) sh_cnt[t] = 0;
+  __syncthreads();
+  for (int i = t; i < SEL_BINS + 2; i += SEL_THREADS) {
+    uint32_t a = 0;
+    for (int64_t c0 = 0; c0 < nch; c0 += SEL_U) {
+      uint32_t v[SEL_U];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) v[u] = parts[(c0 + u < nch ? c0 + u : nch - 1) * SEL_PART + i];
+#pragma unroll
+      for (int u = 0; u < SEL_U; ++u) a += c0 + u < nch ? v[u] : 0u;
+    }
+    if (i < SEL_BINS) hist[i] = a;
+    else sh_cnt[i - SEL_BINS] = int(a);
+  }
+  __syncthreads();
+  const int nl = sh_cnt[0], nf = sh_cnt[1];
+  const int take = s.N <= s.C ? 0 : min(max(0, s.C - nf), nl - nf);
+  if (take <= 0) {                                    // nothing to rank: the keys pass left keep final
     if (t == 0) {
-      n_keep[b] = nl;
-      tau[b] = -INFINITY;
+      n_keep[b] = s.N <= s.C ? nl : nf;
+      tau[b] = s.N <= s.C ? -INFINITY : INFINITY;
+      res[0] = 0xffffffffu;                           // above every key: the mark pass keeps nothing more
+      res[1] = 0u;
     }
     return;
   }
-  const int cstar = max(0, s.C - nf);
-  const int take = min(cstar, na);
-
-  // radix select of the take-th largest key: 11, 11 and 10 bits from the top
-  uint32_t prefix = 0;
-  int kk = take;
-  if (take > 0) {
-    for (int pass = 0; pass < 3; ++pass) {
-      const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-      const uint32_t nbins = pass == 2 ? 1024u : 2048u;
-      const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + (pass == 1 ? 11 : 10)));
-      for (int i = t; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0;
-      __syncthreads();
-      for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
-        int sv[SEL_U];
-        float fv[SEL_U];
-        if (!cached)
+  find_bin(hist, SEL_BINS, take, red, sh);
+  uint32_t prefix = uint32_t(sh[0]) << 21;            // the top 11 bits of the threshold
+  int kk = sh[1];                                     // its rank among the keys that share them
+  int cnt = int(hist[sh[0]]);
+  int level = 1;                                      // radix passes done
+  __syncthreads();
+  if (cnt > SEL_LIST) {
+    // scores concentrate: one more pass, bits 20..10, over the keys of the bin
+    for (int i = t; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0u;
+    __syncthreads();
+    for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
+      uint32_t kv[SEL_U];
 #pragma unroll
-          for (int u = 0; u < SEL_U; ++u) load(c0 + u * SEL_THREADS + t, sv[u], fv[u], true);
+      for (int u = 0; u < SEL_U; ++u) kv[u] = ld_clamped(keys, c0 + u * SEL_THREADS + t, s.N);
 #pragma unroll
-        for (int u = 0; u < SEL_U; ++u) {
-          const int j = c0 + u * SEL_THREADS + t;
-          const uint32_t key = key_of(j, sv[u], fv[u]);
-          const bool on = key != 0u && (key & himask) == (prefix & himask);
-          hist_add(hist, (key >> shift) & (nbins - 1u), on);
-        }
-      }
-      __syncthreads();
-      // thread t owns bins 2t, 2t+1 (pass 2: bin t); find the bin holding the kk-th
-      // largest by an exclusive scan over threads from the top bin down
-      const int per = pass == 2 ? 1 : 2;
-      const int hi_bin = int(nbins) - 1 - t * per;        // highest bin of this thread
-      int c = 0;
-      if (hi_bin >= 0)
-        for (int q = 0; q < per; ++q) c += int(hist[hi_bin - q]);
-      int x = c;                                          // inclusive scan in thread order
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o, WAVE);
-        if (lane >= o) x += y;
-      }
-      int tot;
-      const int wb = wave_base(__shfl(x, 63, WAVE), tot, red);
-      const int above = wb + x - c;                       // keys in bins above this thread's
-      if (hi_bin >= 0 && above < kk && kk <= above + c) {
-        int cum = above;
-        for (int q = 0; q < per; ++q) {
-          const int bin = hi_bin - q;
-          const int h = int(hist[bin]);
-          if (cum + h >= kk) {
-            sh_prefix = prefix | (uint32_t(bin) << shift);
-            sh_k = kk - cum;
-            break;
-          }
-          cum += h;
-        }
-      }
-      __syncthreads();
-      prefix = sh_prefix;
-      kk = sh_k;
-      __syncthreads();
+      for (int u = 0; u < SEL_U; ++u)
+        hist_add(hist, (kv[u] >> 10) & 2047u,
+                 c0 + u * SEL_THREADS + t < s.N && kv[u] != 0u && (kv[u] >> 21) == (prefix >> 21));
     }
+    __syncthreads();
+    find_bin(hist, SEL_BINS, kk, red, sh);
+    prefix |= uint32_t(sh[0]) << 10;
+    kk = sh[1];
+    cnt = int(hist[sh[0]]);
+    level = 2;
+    __syncthreads();
   }
-
-  // keep F, every candidate above the threshold key, and the first kk equal to it in
-  // position order: wave w ranks the ties of its own contiguous range
-  int64_t lo, hi;
-  wave_range(s.N, lo, hi);
-  int ties = 0;
-  if (take > 0)
-    for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
-      int sv[SEL_U];
-      float fv[SEL_U];
-      if (!cached)
+  const uint32_t known = level == 1 ? 0xffe00000u : 0xfffffc00u;   // bits fixed by the passes done
+  uint32_t thr, tpos;
+  if (cnt <= SEL_LIST) {
+    // gather the keys that share those bits, with their positions (any order)
+    if (t == 0) sh_n = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < s.N; c0 += SEL_THREADS * SEL_U) {
+      uint32_t kv[SEL_U];
 #pragma unroll
-        for (int u = 0; u < SEL_U; ++u) load(int(c0) + u * WAVE + lane, sv[u], fv[u], true);
+      for (int u = 0; u < SEL_U; ++u) kv[u] = ld_clamped(keys, c0 + u * SEL_THREADS + t, s.N);
 #pragma unroll
       for (int u = 0; u < SEL_U; ++u) {
-        const int j = int(c0) + u * WAVE + lane;
-        const bool eq = j < hi && key_of(j, sv[u], fv[u]) == prefix;
-        ties += __popcll(__ballot(eq));
-      }
-    }
-  int all_ties;
-  int rank = wave_base(ties, all_ties, red);
-  int kept = 0;
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
-    int sv[SEL_U];
-    float fv[SEL_U];
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) load(int(c0) + u * WAVE + lane, sv[u], fv[u], !cached);
-#pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
-      const int j = int(c0) + u * WAVE + lane;
-      bool k = false, eq = false;
-      if (j < hi) {
-        const bool live = sv[u] != dead;
-        if (live && forced_at(j)) {
-          k = true;
-        } else if (live && take > 0) {
-          const uint32_t key = key_of(j, sv[u], fv[u]);
-          k = key > prefix;
-          eq = key == prefix;
+        const bool m = c0 + u * SEL_THREADS + t < s.N && kv[u] != 0u && (kv[u] & known) == prefix;
+        const uint64_t bal = __ballot(m);
+        int base = 0;
+        if (lane == 0 && bal) base = atomicAdd(&sh_n, __popcll(bal));
+        base = __shfl(base, 0, WAVE);
+        if (m) {
+          const int at = base + __popcll(bal & lanes_below());
+          lkey[at] = kv[u];
+          lpos[at] = uint32_t(c0 + u * SEL_THREADS + t);
         }
       }
-      const uint64_t bal = __ballot(eq);
-      if (eq && rank + __popcll(bal & lanes_below()) < kk) k = true;
-      rank += __popcll(bal);
-      if (j < hi) kp[j] = k ? 1 : 0;
-      kept += k;
     }
+    __syncthreads();
+    const int n = sh_n;
+    thr = kth_largest([&](int i, uint32_t &v, bool &c) { v = lkey[i]; c = true; }, n, kk, hist, red, sh, level,
+                      prefix);
+    // keys above the threshold among them, then the ties kept: the smallest positions
+    int gt = 0, eq = 0;
+    for (int i = t; i < n; i += SEL_THREADS) {
+      gt += lkey[i] > thr;
+      eq += lkey[i] == thr;
+    }
+    gt = block_sum(gt, red);
+    eq = block_sum(eq, red);
+    const int kt = kk - gt;                           // ties taken, 1 <= kt <= eq
+    if (eq <= SEL_TIES) {
+      // few ties: list their positions, and the one with kt - 1 smaller ones is the last taken
+      uint32_t *tie = hist;                           // the histogram is free again
+      if (t == 0) sh_n = 0;
+      __syncthreads();
+      for (int i0 = 0; i0 < n; i0 += SEL_THREADS) {
+        const int i = i0 + t;
+        const bool m = i < n && lkey[i] == thr;
+        const uint64_t bal = __ballot(m);
+        int base = 0;
+        if (lane == 0 && bal) base = atomicAdd(&sh_n, __popcll(bal));
+        base = __shfl(base, 0, WAVE);
+        if (m) tie[base + __popcll(bal & lanes_below())] = lpos[i];
+      }
+      __syncthreads();
+      if (t < eq) {
+        const uint32_t p = tie[t];
+        int r = 0;
+        for (int k = 0; k < eq; ++k) r += tie[k] < p;
+        if (r == kt - 1) sh[0] = int(p);
+      }
+      __syncthreads();
+      tpos = uint32_t(sh[0]);
+    } else {
+      tpos = ~kth_largest([&](int i, uint32_t &v, bool &c) { v = ~lpos[i]; c = lkey[i] == thr; }, n, kt, hist, red,
+                          sh);
+    }
+  } else {
+    // heavy ties even after 22 bits: the remaining passes and the tie order over every key
+    thr = kth_largest([&](int i, uint32_t &v, bool &c) { v = keys[i]; c = v != 0u; }, s.N, kk, hist, red, sh, level,
+                      prefix);
+    int gt = 0;
+    for (int i = t; i < s.N; i += SEL_THREADS) gt += keys[i] > thr;
+    gt = block_sum(gt, red);
+    tpos = ~kth_largest([&](int i, uint32_t &v, bool &c) { c = keys[i] == thr; v = ~uint32_t(i); }, s.N, take - gt,
+                        hist, red, sh);
   }
-  kept = block_sum(kept, red);
   if (t == 0) {
-    n_keep[b] = kept;
-    tau[b] = take > 0 ? key_score(prefix) : INFINITY;
+    res[0] = thr;
+    res[1] = tpos;
+    n_keep[b] = nf + take;
+    tau[b] = key_score(thr);
   }
 }
 
-hipError_t launch_select(const ikv_session *sess_dev, int B, int, const int32_t *slot_maps, int32_t dead,
-                         const float *scores, uint8_t *keep, int32_t *n_keep, float *tau, hipStream_t st) {
+__global__ void __launch_bounds__(256) k_select_mark(const ikv_session *__restrict__ sess, uint8_t *__restrict__ keep,
+                                                     const uint32_t *__restrict__ ws, int64_t keys_off,
+                                                     int64_t res_off) {
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  const int64_t j0 = int64_t(blockIdx.x) * SEL_CHUNK;
+  if (j0 >= s.N) return;
+  const uint32_t thr = ws[res_off + int64_t(b) * 4], tpos = ws[res_off + int64_t(b) * 4 + 1];
+  if (thr == 0xffffffffu) return;
+  const uint32_t *keys = ws + keys_off + s.slot_off;
+  uint8_t *kp = keep + s.slot_off;
+  constexpr int PER = SEL_CHUNK / 256;
+  uint32_t kv[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) kv[q] = ld_clamped(keys, j0 + q * 256 + threadIdx.x, int64_t(s.N));
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int64_t j = j0 + q * 256 + threadIdx.x;
+    if (j < s.N && (kv[q] > thr || (kv[q] == thr && uint32_t(j) <= tpos))) kp[j] = 1;
+  }
+}
+
+size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions) {
+  return size_t(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4) * sizeof(uint32_t);
+}
+
+hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_dev, int B, int maxN,
+                         const int32_t *slot_maps, int32_t dead, const float *scores, uint8_t *keep,
+                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st) {
+  const int64_t keys_off = sel_chunks_before(sess_host, B) * SEL_PART;
+  const int64_t res_off = keys_off + total_positions;
+  const dim3 grid(unsigned(cdiv(maxN, SEL_CHUNK)), B);
+  if (maxN > 0) {
+    KTimer kt_("k_select_keys", st);
+    k_select_keys<<<grid, 256, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, ws, keys_off);
+  }
   {
-    KTimer kt_("k_select", st);
-    k_select<<<B, SEL_THREADS, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, n_keep, tau);
+    KTimer kt_("k_select_finish", st);
+    k_select_finish<<<B, SEL_THREADS, 0, st>>>(sess_dev, n_keep, tau, ws, keys_off, res_off);
+  }
+  if (maxN > 0) {
+    KTimer kt_("k_select_mark", st);
+    k_select_mark<<<grid, 256, 0, st>>>(sess_dev, keep, ws, keys_off, res_off);
   }
   return hipGetLastError();
 }
@@ -337,13 +509,13 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
     uint8_t kv[SEL_U];
 #pragma unroll
     for (int u = 0; u < SEL_U; ++u) {
-      const int j = int(c0) + u * WAVE + lane;
-      sv[u] = j < hi ? S[j] : dead;
-      kv[u] = j < hi ? kp[j] : 0;
+      const int64_t j = c0 + u * WAVE + lane;
+      sv[u] = ld_clamped(S, j, hi);
+      kv[u] = ld_clamped(kp, j, hi);
     }
 #pragma unroll
     for (int u = 0; u < SEL_U; ++u) {
-      const bool k = sv[u] != dead && kv[u] != 0;
+      const bool k = c0 + u * WAVE + lane < hi && sv[u] != dead && kv[u] != 0;
       if (k) sets.set(sets.kept, sv[u]);
       surv += __popcll(__ballot(k));
     }
@@ -357,14 +529,14 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
     uint8_t kv[SEL_U];
 #pragma unroll
     for (int q = 0; q < SEL_U; ++q) {
-      const int j = int(c0) + q * WAVE + lane;
-      sv[q] = j < hi ? S[j] : dead;
-      kv[q] = j < hi ? kp[j] : 0;
+      const int64_t j = c0 + q * WAVE + lane;
+      sv[q] = ld_clamped(S, j, hi);
+      kv[q] = ld_clamped(kp, j, hi);
     }
 #pragma unroll
     for (int q = 0; q < SEL_U; ++q) {
       const int j = int(c0) + q * WAVE + lane;
-      const int u = sv[q];
+      const int u = j < hi ? sv[q] : dead;
       const bool alive = u != dead;
       const bool k = alive && kv[q] != 0;
       if (alive && !k) {

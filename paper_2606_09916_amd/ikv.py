@@ -173,9 +173,11 @@ def score_history(pool: Pool, sess: Sessions, slot_maps, M, scores, ws: Workspac
                                    _stream(stream)), "ikv_score_history")
 
 
-def select_budget(sess: Sessions, slot_maps, dead_slot: int, scores, keep, n_keep, tau, stream=None) -> None:
+def select_budget(sess: Sessions, slot_maps, dead_slot: int, scores, keep, n_keep, tau, ws: Workspace,
+                  stream=None) -> None:
+    wp, wn = ws.get(workspace_bytes(None, sess, CALL_SELECT))
     _check(lib().ikv_select_budget(sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps), dead_slot, _ptr(scores),
-                                   _ptr(keep), _ptr(n_keep), _ptr(tau), None, 0, _stream(stream)),
+                                   _ptr(keep), _ptr(n_keep), _ptr(tau), wp, wn, _stream(stream)),
            "ikv_select_budget")
 
 

@@ -87,7 +87,7 @@ class RetentionStep:
                           residual=self.residual if f & ikv.IKV_RESIDUAL else None, flags=f)
 
     def select(self):
-        ikv.select_budget(self.sess, self.S, self.dead, self.scores, self.keep, self.n_keep, self.tau)
+        ikv.select_budget(self.sess, self.S, self.dead, self.scores, self.keep, self.n_keep, self.tau, self.ws)
 
     def redirect(self):
         ikv.redirect_slots(self.sess, self.num_slots, self.S, self.dead, self.keep, self.freed, self.n_freed,

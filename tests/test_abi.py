@@ -89,7 +89,11 @@ def test_workspace_sizes_are_consistent():
     assert st == 0 and plain > 0 and plain % 256 == 0
     st, resid = _ws(p, _sess(), ikv.CALL_SCORE, ikv.IKV_RESIDUAL)
     assert st == 0 and resid > plain
-    assert _ws(None, _sess(), ikv.CALL_SELECT) == (0, 0)
+    # selection: per chunk of 4096 positions a 2048-bin histogram + counts (2112 words),
+    # one key per position, then 4 result words per session
+    assert _ws(None, _sess(), ikv.CALL_SELECT) == (0, (2112 + 50 + 4) * 4)
+    assert _ws(None, _sess(slot_off=1000), ikv.CALL_SELECT) == (0, (2112 + 1050 + 4) * 4)
+    assert _ws(None, _sess(N=4097, qs=4000, qe=4097), ikv.CALL_SELECT) == (0, (2 * 2112 + 4097 + 4) * 4)
     st, red = _ws(p, _sess(), ikv.CALL_REDIRECT)
     assert st == 0 and red == 2 * 64 * 4          # two 100-slot bitsets, each padded to 64 words
     st, dec = _ws(p, _sess(), ikv.CALL_DECODE)
@@ -116,6 +120,8 @@ def test_calls_reject_bad_arguments_before_launch():
     # memory rows must be 16-byte aligned
     assert L.ikv_score_history(ctypes.byref(p), ctypes.cast(_sess(mem_off=1), ctypes.POINTER(ikv.Session)), fake,
                                1, fake, fake, fake, None, 0, fake, fake, 1 << 30, None) == -1
+    # selection workspace too small
+    assert L.ikv_select_budget(sp, fake, 1, fake, 0, fake, fake, fake, fake, fake, 16, None) == -3
     # null outputs
     assert L.ikv_select_budget(sp, fake, 1, fake, 0, fake, None, fake, fake, None, 0, None) == -1
     assert L.ikv_redirect_slots(sp, fake, 1, 100, fake, 0, fake, fake, fake, None, fake, fake, 1 << 20,

@@ -45,7 +45,7 @@ def _select(dev, rows, S_all, sc_all):
     keep = torch.zeros(tot, dtype=torch.uint8, device=dev)
     n_keep = torch.zeros(B, dtype=torch.int32, device=dev)
     tau = torch.zeros(B, dtype=torch.float32, device=dev)
-    ikv.select_budget(sess, S_d, DEAD, sc_d, keep, n_keep, tau)
+    ikv.select_budget(sess, S_d, DEAD, sc_d, keep, n_keep, tau, ikv.Workspace(dev))
     torch.cuda.synchronize()
     return keep.cpu().numpy(), n_keep.cpu().numpy(), tau.cpu().numpy()
 
