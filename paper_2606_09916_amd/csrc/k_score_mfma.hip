@@ -452,6 +452,60 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   for (int i = 0; i < 32; ++i) kb[i] = 0.f;
   float pm = 0.f, pz = 0.f;                        // first pass: the previous unit's (max, sum)
 
+  // The logits of a unit are finished (masked max and sum, or exp2 summed into the
+  // rule score) during the next unit, on the VALU under that unit's MFMAs: the two
+  // pipes overlap, and the epilogue reads only registers, so it may cross the barrier.
+  f32x4 accp[4];
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) accp[blk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  // Epilogue of one unit in eight steps, so that each step can run under four MFMAs
+  // of the next unit. First pass: masked max (step 0), exp2 sums (steps 1-4), the
+  // merge across the four lane groups of a row (steps 5-6). Second pass: two exp2
+  // terms of the rule score per step.
+  float em = -INFINITY, emb = 0.f, ez = 0.f;
+  auto epilogue_step = [&](f32x4 (&a)[4], int c) {
+    if (!PASS_B) {
+      if (c == 0) {
+        em = -INFINITY;
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (!((cmask >> (blk * 4 + i)) & 1u)) a[blk][i] = -INFINITY;
+            em = fmaxf(em, a[blk][i]);
+          }
+        emb = (em == -INFINITY) ? 0.f : em;
+        ez = 0.f;
+      } else if (c <= 4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ez += ex2(a[c - 1][i] - emb);
+      } else if (c <= 6) {
+        const int o = c == 5 ? 16 : 32;
+        const float m2 = __shfl_xor(em, o, WAVE);
+        const float z2 = __shfl_xor(ez, o, WAVE);
+        const float mm = fmaxf(em, m2);
+        const float x = (em == -INFINITY) ? 0.f : ez * ex2(em - mm);
+        const float y = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
+        em = mm;
+        ez = x + y;
+        if (c == 6) {
+          pm = em;
+          pz = ez;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int e = 2 * c + k, blk = e >> 2, i = e & 3;
+        racc[blk][i] += ((cmask >> e) & 1u) ? ex2(a[blk][i]) : 0.f;
+      }
+    }
+  };
+  auto epilogue = [&](f32x4 (&a)[4]) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) epilogue_step(a, c);
+  };
+
   auto compute = [&](int u) {
     const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
     if (act) {
@@ -483,48 +537,19 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
       f32x4 acc[4];
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) acc[blk] = f32x4{seed, seed, seed, seed};
-      // four independent accumulators between consecutive MFMAs
+      // chunk c: the four MFMAs of k-step c/2 (hi, then lo), then epilogue step c of
+      // the previous unit (a no-op before the first); the fences keep the interleave
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int c = 0; c < 8; ++c) {
+        const int ks = c >> 1;
 #pragma unroll
-        for (int blk = 0; blk < 4; ++blk) acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], mh[ks], acc[blk], 0, 0, 0);
-#pragma unroll
-        for (int blk = 0; blk < 4; ++blk) acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], ml[ks], acc[blk], 0, 0, 0);
+        for (int blk = 0; blk < 4; ++blk)
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[ks] : mh[ks], acc[blk], 0, 0, 0);
+        epilogue_step(accp, c);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (!PASS_B) {
-        float m = -INFINITY;
 #pragma unroll
-        for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (!((cmask >> (blk * 4 + i)) & 1u)) acc[blk][i] = -INFINITY;
-            m = fmaxf(m, acc[blk][i]);
-          }
-        const float mb = (m == -INFINITY) ? 0.f : m;
-        float zs = 0.f;
-#pragma unroll
-        for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) zs += ex2(acc[blk][i] - mb);
-#pragma unroll
-        for (int o = 16; o < 64; o <<= 1) {
-          const float m2 = __shfl_xor(m, o, WAVE);
-          const float z2 = __shfl_xor(zs, o, WAVE);
-          const float mm = fmaxf(m, m2);
-          const float a = (m == -INFINITY) ? 0.f : zs * ex2(m - mm);
-          const float c = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
-          m = mm;
-          zs = a + c;
-        }
-        pm = m;
-        pz = zs;
-      } else {
-#pragma unroll
-        for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if ((cmask >> (blk * 4 + i)) & 1u) racc[blk][i] += ex2(acc[blk][i]);
-      }
+      for (int blk = 0; blk < 4; ++blk) accp[blk] = acc[blk];
     }
     if (KBAR) {
       const int tok = t >> 2, q4 = t & 3;
@@ -549,7 +574,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   };
 
   // Issue order per wave: K(0), M(0), K(1), then per unit u: [first pass: store of
-  // unit u-1], M(u+1), K(u+2). At the top of unit u only K(u+1) (4 loads) may still
+  // unit u-2], M(u+1), K(u+2). At the top of unit u only K(u+1) (4 loads) may still
   // be younger than M(u) and K(u).
   issue_k(0);
   issue_m(0);
@@ -558,11 +583,13 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     if (u + 1 < units) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (!PASS_B && u > 0) store_part(u - 1);
+    if (!PASS_B && u >= 2) store_part(u - 2);      // finished during unit u - 1
     if (u + 1 < units) issue_m(u + 1);
     if (u + 2 < units) issue_k(u + 2);
     compute(u);
   }
+  if (!PASS_B && units >= 2) store_part(units - 2);
+  if (act) epilogue(accp);                         // the last unit
   if (!PASS_B) store_part(units - 1);
   __syncthreads();
 
