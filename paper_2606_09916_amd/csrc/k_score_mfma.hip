@@ -546,25 +546,25 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
         for (int blk = 0; blk < 4; ++blk)
           acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[ks] : mh[ks], acc[blk], 0, 0, 0);
         epilogue_step(accp, c);
+        // mean key row: wave (rs, half) sums channel quarter rs of its 64 positions
+        // from the fragments already in registers
+        if (KBAR && ks == rs && (c & 1) == 0)
+#pragma unroll
+          for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kb[blk * 8 + e] += float(ka[blk][ks][e]);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) accp[blk] = acc[blk];
     }
-    if (KBAR) {
-      const int tok = t >> 2, q4 = t & 3;
-      const uint16_t *kr = kl + tok * MD;
+    if (KBAR && !act) {                            // slices without memory rows still cover their channels
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((q4 * 4 + i) ^ (tok & 15)) * 8));
-        kb[8 * i + 0] += bf_lo(v.x);
-        kb[8 * i + 1] += bf_hi(v.x);
-        kb[8 * i + 2] += bf_lo(v.y);
-        kb[8 * i + 3] += bf_hi(v.y);
-        kb[8 * i + 4] += bf_lo(v.z);
-        kb[8 * i + 5] += bf_hi(v.z);
-        kb[8 * i + 6] += bf_lo(v.w);
-        kb[8 * i + 7] += bf_hi(v.w);
+      for (int blk = 0; blk < 4; ++blk) {
+        const uint16_t *kr = kl + (p0 + blk * 16 + r16) * MD;
+        const bf16x8 f = *reinterpret_cast<const bf16x8 *>(kr + (((4 * rs + g) ^ r16) * 8));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kb[blk * 8 + e] += float(f[e]);
       }
     }
   };
@@ -617,15 +617,16 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     }
   }
   if (KBAR) {
-    const int tok = t >> 2, q4 = t & 3;
-    const int j = j0 + tok;
-    if (j < s.N) {
-      const float inv = 1.0f / float(units);
-      float *dst = base + z.off_kbar() + int64_t(j) * MD + q4 * 32;
+    const float inv = 1.0f / float(units);
 #pragma unroll
-      for (int e = 0; e < 32; e += 4)
-        *reinterpret_cast<float4 *>(dst + e) = make_float4(kb[e] * inv, kb[e + 1] * inv, kb[e + 2] * inv,
-                                                           kb[e + 3] * inv);
+    for (int blk = 0; blk < 4; ++blk) {
+      const int j = j0 + p0 + blk * 16 + r16;
+      if (j < s.N) {
+        float *dst = base + z.off_kbar() + int64_t(j) * MD + (4 * rs + g) * 8;
+        const float *v = kb + blk * 8;
+        *reinterpret_cast<float4 *>(dst) = make_float4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
+        *reinterpret_cast<float4 *>(dst + 4) = make_float4(v[4] * inv, v[5] * inv, v[6] * inv, v[7] * inv);
+      }
     }
   }
 }
