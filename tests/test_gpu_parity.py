@@ -428,3 +428,24 @@ def test_qwen3_8b_32k_step_full(qwen3_8b):
     st.step(update_memory=False)
     ndiff = _compare_step(st, batch, 0, blob, ikv.IKV_RESIDUAL, False)
     print(f"kept-set differences inside the band: {ndiff}")
+
+
+@pytest.fixture(scope="module")
+def qwen25_14b(dev):
+    batch = synth.qwen25_14b_92k_heavy(R=64)
+    blob = synth.residual_blob(128, seed=23)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    return batch, blob, st
+
+
+def test_qwen25_14b_92k_heavy_step_full(qwen25_14b):
+    """Qwen2.5-14B-shaped step (48 layers, 8 KV heads, 92,300 positions: not a multiple
+    of any tile, budget 8192, 64 memory rows per KV head, residual head on), with 5% of
+    the non-forced keys scaled x4 on every layer and head (a heavy-tailed score
+    distribution), against the full oracle."""
+    batch, blob, st = qwen25_14b
+    st.reset()
+    st.step(update_memory=False)
+    ndiff = _compare_step(st, batch, 0, blob, ikv.IKV_RESIDUAL, False)
+    print(f"kept-set differences inside the band: {ndiff}")
