@@ -397,3 +397,57 @@ def slot_map(n: int, num_slots: int, seed: int, dead_frac: float = 0.1, dead: in
 
 
 T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS, T_MISC_SLOTS = 20, 21, 22, 23
+T_TURNS = 24
+
+
+# ----------------------------------------------------------------------------- multi-turn session
+
+def multi_turn_plan(seed: int, turns: int = 8, first: int = 4096, final: int = 49152) -> list:
+    """Token counts of a multi-turn agent session: [(appended tool tokens, query tokens)].
+
+    Turn 1 holds `first` positions, the last 32-64 of them the query. Each later turn
+    appends a tool output of ~U[2048, 8192] tokens (rescaled so that the last turn
+    ends at `final` positions) and then a 32-64 token query.
+    """
+    g = stream(seed, T_TURNS)
+    nq = g.integers(32, 65, turns)
+    tool = g.integers(2048, 8193, turns - 1).astype(np.float64)
+    target = final - first - int(nq[1:].sum())
+    tool = np.floor(tool * target / tool.sum()).astype(np.int64)
+    tool[-1] += target - int(tool.sum())
+    return [(first - int(nq[0]), int(nq[0]))] + [(int(a), int(q)) for a, q in zip(tool, nq[1:])]
+
+
+def turn_kv_rows(seed: int, turn: int, start: int, n: int, shape: Shape, kv_dtype: int = BF16):
+    """K (post-RoPE at positions start .. start+n-1) and V rows appended in one turn,
+    each [L][n][Hkv][D] in the storage type (bf16 bits or float32)."""
+    L, Hkv, D = shape.L, shape.Hkv, shape.D
+    cs = rope_cos_sin(np.arange(start, start + n), D)
+    st = np.uint16 if kv_dtype == BF16 else np.float32
+    k = np.empty((L, n, Hkv, D), st)
+    v = np.empty((L, n, Hkv, D), st)
+
+    def fill(l):
+        x = stream(seed, T_K, (turn << 16) | l).standard_normal((n, Hkv, D), dtype=np.float32)
+        k[l] = to_dtype(rope_neox(x.astype(np.float64), *cs), kv_dtype)
+        y = stream(seed, T_V, (turn << 16) | l).standard_normal((n, Hkv, D), dtype=np.float32)
+        v[l] = to_dtype(y.astype(np.float64), kv_dtype)
+
+    with ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(fill, range(L)))
+    return k, v
+
+
+def turn_span_rows(seed: int, turn: int, positions: np.ndarray, shape: Shape, R: int, kv_dtype: int = BF16):
+    """Query rows of a turn's span for the QueryMemory update: [L][Hkv*R][n][D], post-RoPE."""
+    n = len(positions)
+    q = stream(seed, T_QSPAN, turn).standard_normal((n, shape.L, shape.Hkv * R, shape.D), dtype=np.float32)
+    q = rope_neox(q.astype(np.float64), *rope_cos_sin(positions, shape.D)).transpose(1, 2, 0, 3)
+    return to_dtype(np.ascontiguousarray(q), kv_dtype)
+
+
+def turn_decode_query(seed: int, turn: int, position: int, shape: Shape, kv_dtype: int = BF16):
+    """The decode query of a turn, [L][Hq][D], post-RoPE at `position`."""
+    q = stream(seed, T_QDEC, turn).standard_normal((1, shape.L, shape.Hq, shape.D), dtype=np.float32)
+    q = rope_neox(q.astype(np.float64), *rope_cos_sin(np.array([position]), shape.D))
+    return to_dtype(q[0], kv_dtype)
