@@ -145,15 +145,34 @@ __device__ __forceinline__ void load8(const float *p, float *o) {
 }
 
 // ---------------------------------------------------------------- wave reductions
+// Sum / max over the 64 lanes by DPP row operations (VALU rate, no LDS round trip):
+// pairs within quads, half rows, rows, then the row broadcasts leave the total in
+// lane 63, which every lane reads back. Every lane of the wave must be active.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp_f(float old, float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
+                                                                CTRL, ROW_MASK, 0xf, false));
+}
+__device__ __forceinline__ float lane63(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-  return v;
+  v += dpp_f<0xB1>(0.f, v);          // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(0.f, v);          // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(0.f, v);         // row_half_mirror
+  v += dpp_f<0x140>(0.f, v);         // row_mirror
+  v += dpp_f<0x142, 0xa>(0.f, v);    // row_bcast:15 into rows 1 and 3
+  v += dpp_f<0x143, 0xc>(0.f, v);    // row_bcast:31 into rows 2 and 3
+  return lane63(v);
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
-  return v;
+  v = fmaxf(v, dpp_f<0xB1>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x4E>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x141>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x140>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x142, 0xa>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x143, 0xc>(-INFINITY, v));
+  return lane63(v);
 }
 
 // ---------------------------------------------------------------- launchers

@@ -44,6 +44,59 @@ template <typename T> struct Raw8 {
   }
 };
 
+// The end of a split: fold the value row groups of each wavefront, merge the four
+// wavefronts through LDS, and write (max, sum, output) per query head to the workspace.
+template <int D, int G>
+__device__ __forceinline__ void decode_finish(float (&m)[G], float (&lsum)[G], float (&o)[G][8], float (&red)[4][G][2],
+                                              float (&ored)[4][G][D], float *__restrict__ ws, int b, int L, int l,
+                                              int Hq, int g, int split, int nsplit) {
+  constexpr int LPR = D / 8;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int rq = lane / LPR, cq = lane % LPR;
+  // fold the value row groups of each wavefront, then merge the four wavefronts
+#pragma unroll
+  for (int x = LPR; x < WAVE; x <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) o[h][c] += __shfl_xor(o[h][c], x, WAVE);
+  if (lane == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      red[w][h][0] = m[h];
+      red[w][h][1] = lsum[h];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float mm = -INFINITY;
+    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
+    const float f = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mm);
+    if (rq == 0)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) ored[w][h][cq * 8 + c] = o[h][c] * f;
+  }
+  __syncthreads();
+  for (int e = t; e < G * (D + 2); e += 256) {
+    const int h = e / (D + 2), d = e - h * (D + 2);
+    float mm = -INFINITY;
+    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
+    float val;
+    if (d == 0) {
+      val = mm;
+    } else if (d == 1) {
+      val = 0.f;
+      for (int k = 0; k < 4; ++k)
+        if (red[k][h][0] != -INFINITY) val += red[k][h][1] * __expf(red[k][h][0] - mm);
+    } else {
+      val = (ored[0][h][d - 2] + ored[1][h][d - 2]) + (ored[2][h][d - 2] + ored[3][h][d - 2]);
+    }
+    const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
+    ws[(row * nsplit + split) * (D + 2) + d] = val;
+  }
+}
+
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpool, const T *__restrict__ vpool,
                                                       int64_t num_slots, int L, int Hkv,
@@ -158,48 +211,163 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   }
-  // fold the value row groups of each wavefront, then merge the four wavefronts
+  decode_finish<D, G>(m, lsum, o, red, ored, ws, b, L, l, Hq, g, split, nsplit);
+}
+
+// ---- matrix-core decode (bf16 pool, D = 128). The logits of 16 live positions x
+// the G query heads of a KV head are one chain of four v_mfma_f32_16x16x32_bf16:
+// the key rows are the A operand (lane (g, r) loads 16 bytes of position r), the
+// query rows the B operand (column h = query head h, zero beyond G), both exact in
+// bf16 with float32 accumulation. The block's softmax weights go to LDS as one row
+// of G per position; the value rows are summed on the VALU as in k_decode_split.
+typedef __bf16 bf16x8_d __attribute__((ext_vector_type(8)));
+typedef float f32x4_d __attribute__((ext_vector_type(4)));
+
+template <int G>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_decode_mfma(const uint16_t *__restrict__ kpool,
+                                                     const uint16_t *__restrict__ vpool, int64_t num_slots, int L,
+                                                     int Hkv, const ikv_session *__restrict__ sess,
+                                                     const uint16_t *__restrict__ q, const int32_t *__restrict__ live,
+                                                     const int32_t *__restrict__ n_live, float *__restrict__ ws) {
+  constexpr int D = 128;
+  constexpr int LPR = D / 8;           // lanes per value row (8 channels each)
+  constexpr int RPI = WAVE / LPR;      // value rows per load instruction
+  constexpr int GP = (G + 3) & ~3;     // weights per position in LDS, padded to float4
+  __shared__ __align__(16) float pw[4][DEC_BLOCK][GP];
+  __shared__ float red[4][G][2];
+  __shared__ float ored[4][G][D];
+
+  const int b = blockIdx.z;
+  const ikv_session s = sess[b];
+  const int Hq = Hkv * G;
+  const int u = blockIdx.y, l = u / Hkv, g = u - l * Hkv;
+  const int split = blockIdx.x, nsplit = gridDim.x;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int gq = lane >> 4, r16 = lane & 15;
+  int n = n_live[b];
+  n = n < 0 ? 0 : (n > s.N ? s.N : n);
+  const int chunk = int(cdiv(n, nsplit));
+  const int k0 = split * chunk, k1 = min(n, k0 + chunk);
+  const float scale = 1.0f / sqrtf(float(D));
+  const int32_t *lv = live + s.slot_off;
+  int slot0 = 0;                                   // the first block's slot: loads with the query rows
+  if (k0 + w * DEC_BLOCK + lane < k1) slot0 = lv[k0 + w * DEC_BLOCK + lane];
+  // the query rows as the B operand: lane (gq, r16) holds channels ks*32 + gq*8 .. +8 of head r16
+  bf16x8_d qb[4];
+  {
+    const uint16_t *qr = q + ((int64_t(b) * L + l) * Hq + g * G + (r16 < G ? r16 : 0)) * D + gq * 8;
 #pragma unroll
-  for (int x = LPR; x < WAVE; x <<= 1)
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int c = 0; c < 8; ++c) o[h][c] += __shfl_xor(o[h][c], x, WAVE);
-  if (lane == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      red[w][h][0] = m[h];
-      red[w][h][1] = lsum[h];
+    for (int ks = 0; ks < 4; ++ks) {
+      qb[ks] = *reinterpret_cast<const bf16x8_d *>(qr + ks * 32);
+      if (r16 >= G) qb[ks] = bf16x8_d{};
     }
   }
-  __syncthreads();
+  const int rq = lane / LPR, cq = lane % LPR;     // value row group, channel group
+  float m[G], lsum[G], o[G][8];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    float mm = -INFINITY;
-    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
-    const float f = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mm);
-    if (rq == 0)
+    m[h] = -INFINITY;
+    lsum[h] = 0.f;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) ored[w][h][cq * 8 + c] = o[h][c] * f;
+    for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
-  __syncthreads();
-  for (int e = t; e < G * (D + 2); e += 256) {
-    const int h = e / (D + 2), d = e - h * (D + 2);
-    float mm = -INFINITY;
-    for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
-    float val;
-    if (d == 0) {
-      val = mm;
-    } else if (d == 1) {
-      val = 0.f;
-      for (int k = 0; k < 4; ++k)
-        if (red[k][h][0] != -INFINITY) val += red[k][h][1] * __expf(red[k][h][0] - mm);
-    } else {
-      val = (ored[0][h][d - 2] + ored[1][h][d - 2]) + (ored[2][h][d - 2] + ored[3][h][d - 2]);
+  const int64_t row_stride = int64_t(Hkv) * D;
+  const uint16_t *kbase = kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
+  const uint16_t *vbase = vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
+  for (int base = k0 + w * DEC_BLOCK; base < k1; base += 4 * DEC_BLOCK) {
+    const int kk = base + lane;
+    const bool valid = kk < k1;
+    const int slot = base == k0 + w * DEC_BLOCK ? slot0 : (valid ? lv[kk] : 0);
+    const int nb = min(DEC_BLOCK, k1 - base);
+    // value rows (they need only the slots) and key fragments leave together
+    Raw8<uint16_t> v[DEC_BLOCK / RPI];
+#pragma unroll
+    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
+      const int i = r * RPI + rq;
+      const int si = __shfl(slot, i, WAVE);
+      if (i < nb) v[r].ld(vbase + int64_t(si) * row_stride + cq * 8);
     }
-    const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
-    ws[(row * nsplit + split) * (D + 2) + d] = val;
+    bf16x8_d kf[4][4];
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb) {
+      const int sr = __shfl(slot, bb * 16 + r16, WAVE);   // past the block: slot 0, masked below
+      const uint16_t *kr = kbase + int64_t(sr) * row_stride + gq * 8;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kf[bb][ks] = *reinterpret_cast<const bf16x8_d *>(kr + ks * 32);
+    }
+    f32x4_d acc[4];
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb) {
+      acc[bb] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bb][ks], qb[ks], acc[bb], 0, 0, 0);
+    }
+    // acc[bb][i]: logit of position bb*16 + 4gq + i for query head r16
+    float mx = -INFINITY;
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float x = (bb * 16 + 4 * gq + i < nb) ? acc[bb][i] * scale : -INFINITY;
+        acc[bb][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+    float mn[G], corr[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      mn[h] = fmaxf(m[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mx), h)));
+      corr[h] = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mn[h]);
+    }
+    float mine = mn[0];                            // the new max of this lane's head
+#pragma unroll
+    for (int h = 1; h < G; ++h) mine = (r16 == h) ? mn[h] : mine;
+    float ps = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = (acc[bb][i] == -INFINITY) ? 0.f : __expf(acc[bb][i] - mine);
+        ps += p;
+        if (r16 < G) pw[w][bb * 16 + 4 * gq + i][r16] = p;
+      }
+    ps += __shfl_xor(ps, 16, WAVE);
+    ps += __shfl_xor(ps, 32, WAVE);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      lsum[h] = lsum[h] * corr[h] + __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ps), h));
+      m[h] = mn[h];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) o[h][c] *= corr[h];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
+      const int i = r * RPI + rq;
+      if (i < nb) {
+        float vv[8];
+        v[r].unpack(vv);
+        float pv[GP];
+#pragma unroll
+        for (int h4 = 0; h4 < GP; h4 += 4) {
+          const float4 x = *reinterpret_cast<const float4 *>(&pw[w][i][h4]);
+          pv[h4] = x.x;
+          pv[h4 + 1] = x.y;
+          pv[h4 + 2] = x.z;
+          pv[h4 + 3] = x.w;
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+          for (int c = 0; c < 8; ++c) o[h][c] = fmaf(pv[h], vv[c], o[h][c]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   }
+  decode_finish<D, G>(m, lsum, o, red, ored, ws, b, L, l, Hq, g, split, nsplit);
 }
 
 template <typename T, int D>
@@ -226,7 +394,12 @@ __global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ 
 template <typename T, int D, int G>
 static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
                                   const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
-  {
+  if constexpr (sizeof(T) == 2 && D == 128) {
+    KTimer kt_("k_decode_mfma<G>", st);
+    k_decode_mfma<G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
+        (const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const uint16_t *)q,
+        live, n_live, ws);
+  } else {
     KTimer kt_("k_decode_split<T, D, G>", st);
     k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
         (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws);
