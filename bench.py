@@ -214,7 +214,7 @@ def main() -> int:
     kv_row = sh.Hkv * sh.D * 2 * sh.L                          # one position's K over all layers, bf16
     score_bytes = nA * (kv_row + 4 + 4) + sh.L * sh.Hkv * s.R * sh.D * 4 + (blob.size * 4 if flags else 0)
     score_flops = 2 * (2.0 * sh.L * sh.Hkv * s.R * sh.D) * nA
-    decode_bytes = n_live * (2 * kv_row + 4)
+    decode_bytes = n_live * (2 * kv_row + 4)                    # decode phase: split and combine kernels
     score_gbs = score_bytes / (phase_ms[2] / 1e3) / 1e9
     decode_gbs = decode_bytes / (phase_ms[5] / 1e3) / 1e9
     # split-bf16 logits: two bf16 MFMAs per product in each of the two passes
@@ -229,6 +229,7 @@ def main() -> int:
         "k_score_ring<true, true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
         "k_score_ring<true, false>": key_bytes + mem_bytes + s.N * 4,
         "k_decode_split<T, D, G>": kv_live + sh.L * sh.Hq * sh.D * 2,
+        "k_decode_mfma<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
         "k_qm_update<T, 128>": units * s.R * (s.qe - s.qs) * sh.D * 2 + 2 * mem_bytes,
         "k_select": s.N * (4 + 4 + 1),
         "k_redirect<true>": s.N * (4 + 1 + 4 + 4),

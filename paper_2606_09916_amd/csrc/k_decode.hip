@@ -119,7 +119,7 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
   int n = n_live[b];
   n = n < 0 ? 0 : (n > s.N ? s.N : n);
   const int chunk = int(cdiv(n, nsplit));
-  const int k0 = split * chunk, k1 = min(n, k0 + chunk);
+  const int k0 = min(n, split * chunk), k1 = min(n, k0 + chunk);
   const float scale = 1.0f / sqrtf(float(D));
   const int32_t *lv = live + s.slot_off;
   int slot0 = 0;                                   // the first block's slot: loads with the query rows
@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   int n = n_live[b];
   n = n < 0 ? 0 : (n > s.N ? s.N : n);
   const int chunk = int(cdiv(n, nsplit));
-  const int k0 = split * chunk, k1 = min(n, k0 + chunk);
+  const int k0 = min(n, split * chunk), k1 = min(n, k0 + chunk);
   const float scale = 1.0f / sqrtf(float(D));
   const int32_t *lv = live + s.slot_off;
   int slot0 = 0;                                   // the first block's slot: loads with the query rows
@@ -376,16 +376,30 @@ __global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ 
   const int64_t row = int64_t(blockIdx.y) * L * Hq + blockIdx.x;
   const float *p = ws + row * nsplit * (D + 2);
   const int d = threadIdx.x;
-  float mm = -INFINITY;
-  for (int k = 0; k < nsplit; ++k) mm = fmaxf(mm, p[k * (D + 2)]);
-  float lsum = 0.f, acc = 0.f;
-  if (mm != -INFINITY) {
-    for (int k = 0; k < nsplit; ++k) {
-      const float mk = p[k * (D + 2)];
-      if (mk == -INFINITY) continue;
-      const float f = expf(mk - mm);
-      lsum = fmaf(p[k * (D + 2) + 1], f, lsum);
-      acc = fmaf(p[k * (D + 2) + 2 + d], f, acc);
+  constexpr int U = 8;                             // splits in flight per thread
+  float mm = -INFINITY, lsum = 0.f, acc = 0.f;     // online over the splits
+  for (int k0 = 0; k0 < nsplit; k0 += U) {
+    float mk[U], lk[U], ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = min(k0 + u, nsplit - 1);
+      mk[u] = p[k * (D + 2)];
+      lk[u] = p[k * (D + 2) + 1];
+      ok[u] = p[k * (D + 2) + 2 + d];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (k0 + u >= nsplit || mk[u] == -INFINITY) continue;
+      if (mk[u] > mm) {
+        const float f = mm == -INFINITY ? 0.f : expf(mm - mk[u]);
+        lsum = fmaf(lsum, f, lk[u]);
+        acc = fmaf(acc, f, ok[u]);
+        mm = mk[u];
+      } else {
+        const float f = expf(mk[u] - mm);
+        lsum = fmaf(lk[u], f, lsum);
+        acc = fmaf(ok[u], f, acc);
+      }
     }
   }
   out[row * D + d] = Store<T>::from(lsum > 0.f ? acc / lsum : 0.f);
