@@ -631,6 +631,194 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   }
 }
 
+// ------------------------------------------------------------------ first pass, unit-major (R <= 64, even Hkv)
+// The first pass needs no sum over units per position, so it runs unit by unit: a
+// workgroup owns one head pair of one layer and a chunk of CH positions. The memory
+// rows of its two units sit in registers for the whole chunk and only keys stream,
+// 32 positions x 2 heads (16 KB) per stage through a 4-stage LDS ring, so two
+// workgroups share a CU. Wave w takes head w >> 1 of the pair and memory rows
+// 32 (w & 1) .. + 31 as two 16-row MFMA blocks; per row it keeps an online (max, sum
+// of exp2) over the chunk's candidates and writes one partial per (chunk, unit, row).
+// Non-candidates enter the accumulators as -inf before the MFMAs, so the epilogue
+// needs no mask.
+constexpr int ST_THREADS = 256;
+constexpr int ST_TILE = 32;                      // positions per stage
+constexpr int ST_STAGES = 4;
+constexpr int ST_STAGE = ST_TILE * 2 * MD;       // bf16 per stage: 32 positions x 2 heads
+constexpr int ST_CHMAX = 1024;                   // positions per chunk at most
+
+// 16 bytes per lane from sbase + voff (scalar base, 32-bit byte offset per lane)
+// straight into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void dma16s(const void *sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
+__global__ void __launch_bounds__(ST_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
+              const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+              bool resid, int CH) {
+  __shared__ __align__(1024) uint16_t ring[ST_STAGES * ST_STAGE];
+  __shared__ uint32_t koff[ST_CHMAX];            // byte offset of each position's key rows in the layer
+  __shared__ __align__(16) float bias[ST_CHMAX];  // 0 for a candidate, -inf otherwise
+
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int HP = L * Hkv / 2;
+  const int hp = int(blockIdx.x % unsigned(HP)), chunk = int(blockIdx.x / unsigned(HP));
+  const int c0 = chunk * CH;
+  if (c0 >= s.N) return;
+  const int npos = min(CH, s.N - c0);
+  const int T = int(cdiv(npos, ST_TILE));
+  const int l = hp / (Hkv / 2), h0 = 2 * (hp - l * (Hkv / 2));
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int hh = w >> 1, r0 = 32 * (w & 1);      // head within the pair, first memory row
+  const int g = lane >> 4, r16 = lane & 15;
+  const int R = s.R;
+  const int units = L * Hkv;
+  const int u = l * Hkv + h0 + hh;
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
+  float *part = base + z.off_part();
+  const int32_t *S = slot_maps + s.slot_off;
+  const uint32_t slot_bytes = uint32_t(Hkv) * MD * 2;
+
+  // the chunk's key offsets (dead slot past the end) and candidate biases
+  int32_t sv[ST_CHMAX / ST_THREADS];
+#pragma unroll
+  for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) sv[k] = S[c0 + min(t + k * ST_THREADS, npos - 1)];
+  // memory rows of this wave, B-operand fragments: lane (g, r16) holds row r0 + 16 rb + r16
+  // (the last row stands in for rows past R, whose results are never stored),
+  // channels (4 ks + g) * 8 .. + 8, hi then lo
+  bf16x8 mh[2][4], ml[2][4];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    const int row = min(r0 + 16 * rb + r16, R - 1);
+    const uint16_t *mp = msplit + (int64_t(u) * R + row) * 256 + g * 64;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      mh[rb][ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16);
+      ml[rb][ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16 + 8);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) {
+    const int p = t + k * ST_THREADS, j = c0 + p;
+    const bool in = p < npos;
+    const int slot = in ? sv[k] : dead;
+    const bool cand = in && slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+    koff[p] = uint32_t(slot) * slot_bytes;
+    bias[p] = cand ? 0.f : -INFINITY;
+  }
+  // every compiler-issued load of the set-up is complete before the first key load
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  // Key loads: instruction k of wave w fills 1 KB of the stage, positions 2 (4w + k)
+  // and + 1; lane -> (position, head, 16-byte slot lane & 15), and slot s of a 256-byte
+  // row holds chunk s ^ (position & 15).
+  const uint16_t *kb0 = kpool + int64_t(l) * num_slots * (int64_t(Hkv) * MD) + int64_t(h0) * MD;
+  uint32_t lconst[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int p = 2 * (4 * w + k) + (lane >> 5);
+    lconst[k] = uint32_t(((lane >> 4) & 1) * MD * 2 + (((lane & 15) ^ (p & 15)) * 16));
+  }
+  const uint32_t lds_w = __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>(ring)) + w * 4096);
+  auto issue = [&](int tt) {
+    const uint32_t st = lds_w + uint32_t((tt % ST_STAGES) * ST_STAGE * 2);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      dma16s(kb0, koff[tt * ST_TILE + 2 * (4 * w + k) + (lane >> 5)] + lconst[k], st + k * 1024);
+  };
+
+  float Mr[2] = {-INFINITY, -INFINITY}, Zr[2] = {0.f, 0.f};
+  auto compute = [&](int tt) {
+    const uint16_t *kl = ring + (tt % ST_STAGES) * ST_STAGE;
+    bf16x8 ka[2][4];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const uint16_t *kr = kl + ((16 * pb + r16) * 2 + hh) * MD;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) ka[pb][ks] = *reinterpret_cast<const bf16x8 *>(kr + (((4 * ks + g) ^ r16) * 8));
+    }
+    // lane (g, r16) of block (pb, rb) holds row r0 + 16 rb + r16 at positions 16 pb + 4 g + i
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const float4 bv = *reinterpret_cast<const float4 *>(bias + tt * ST_TILE + 16 * pb + 4 * g);
+      acc[pb][0] = acc[pb][1] = f32x4{bv.x, bv.y, bv.z, bv.w};
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          acc[pb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[pb][ks], mh[rb][ks], acc[pb][rb], 0, 0, 0);
+          acc[pb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[pb][ks], ml[rb][ks], acc[pb][rb], 0, 0, 0);
+        }
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      float m = Mr[rb];
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[pb][rb][i]);
+      const float e0 = (m == -INFINITY) ? 0.f : m;   // nothing seen yet: every term below is 0
+      float zs = Zr[rb] * ex2(Mr[rb] - e0);
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) zs += ex2(acc[pb][rb][i] - e0);
+      Zr[rb] = zs;
+      Mr[rb] = m;
+    }
+  };
+
+  for (int k = 0; k < ST_STAGES - 1 && k < T; ++k) issue(k);
+  for (int tt = 0; tt < T; ++tt) {
+    // tile tt's four loads per wave are done once at most those of the later tiles
+    // already issued (four each) are outstanding
+    const int later = min(ST_STAGES - 2, T - 1 - tt);
+    if (later >= 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (later == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tt + ST_STAGES - 1 < T) issue(tt + ST_STAGES - 1);
+    compute(tt);
+  }
+
+  // merge the four lane groups of each row and store the chunk's partial
+  const int64_t rows = int64_t(units) * R;
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+#pragma unroll
+    for (int o = 16; o < 64; o <<= 1) {
+      const float m2 = __shfl_xor(Mr[rb], o, WAVE), z2 = __shfl_xor(Zr[rb], o, WAVE);
+      const float mm = fmaxf(Mr[rb], m2);
+      const float x = (Mr[rb] == -INFINITY) ? 0.f : Zr[rb] * ex2(Mr[rb] - mm);
+      const float y = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
+      Mr[rb] = mm;
+      Zr[rb] = x + y;
+    }
+    const int row = r0 + 16 * rb + r16;
+    if (g == 0 && row < R)
+      *reinterpret_cast<float2 *>(part + (int64_t(chunk) * rows + int64_t(u) * R + row) * 2) = make_float2(Mr[rb], Zr[rb]);
+  }
+}
+
+// Positions per chunk of the unit-major first pass: about nine rounds of two
+// workgroups per CU at the largest sizes, whole 64-position multiples.
+inline int stats_chunk(int maxN, int head_pairs) {
+  const int64_t c = cdiv(cdiv(int64_t(maxN) * head_pairs, 4608), 64) * 64;
+  return int(std::min<int64_t>(std::max<int64_t>(c, 64), 1024));
+}
+
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
 // A workgroup takes 64 consecutive rows; its eight waves split the tiles (lane =
 // row, so each load instruction reads 512 contiguous bytes), fold them online into
@@ -716,7 +904,16 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, resid);
   }
   const bool ring = a.maxR <= 64;
-  if (ring)
+  // the unit-major first pass addresses a layer's keys with 32-bit offsets
+  const bool stats = ring && p.Hkv % 2 == 0 && p.num_slots * p.Hkv * MD * 2 <= int64_t(UINT32_MAX);
+  const int chunk = stats ? stats_chunk(a.maxN, units / 2) : 0;
+  if (stats)
+    {
+      KTimer kt_("k_score_stats", st);
+      k_score_stats<<<dim3(unsigned(units / 2 * cdiv(a.maxN, chunk)), a.B), ST_THREADS, 0, st>>>(
+          kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, resid, chunk);
+    }
+  else if (ring)
     {
       KTimer kt_("k_score_ring<false, false>", st);
       k_score_ring<false, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
@@ -731,7 +928,7 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   {
     KTimer kt_("k_lse_mfma", st);
     k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
-                                                                                        resid, ring ? PART_TILE : MFMA_TILE);
+                                                                                        resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE);
   }
   if (ring && resid)
     {
