@@ -379,7 +379,8 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   const int j0 = tile * MFMA_TILE;
   if (j0 >= s.N) return;
   const int units = L * Hkv;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform: branches on it stay scalar
   const int rs = w & 3, half = w >> 2;             // memory-row slice, position half
   const int g = lane >> 4, r16 = lane & 15;
   const int R = s.R, nsl = R >> 4;
@@ -443,13 +444,22 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   };
 
   float racc[4][4];
-  float kb[32];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[i][k] = 0.f;
+  // Mean key row on the matrix cores: the MFMA of a key fragment (channels 32 rs .. + 31)
+  // with the B operand eye0 (eye1) copies channels 32 rs + n (32 rs + 16 + n) of its 16
+  // positions into column n, so summing over units is the accumulation itself.
+  f32x4 kacc[4][2];
+  bf16x8 eye0, eye1;
 #pragma unroll
-  for (int i = 0; i < 32; ++i) kb[i] = 0.f;
+  for (int blk = 0; blk < 4; ++blk) kacc[blk][0] = kacc[blk][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    eye0[e] = (8 * g + e == r16) ? __bf16(1.0f) : __bf16(0.0f);
+    eye1[e] = (8 * g + e == r16 + 16) ? __bf16(1.0f) : __bf16(0.0f);
+  }
   float pm = 0.f, pz = 0.f;                        // first pass: the previous unit's (max, sum)
 
   // The logits of a unit are finished (masked max and sum, or exp2 summed into the
@@ -494,10 +504,11 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
         }
       }
     } else {
+      // non-candidates are summed too and dropped at the store
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int e = 2 * c + k, blk = e >> 2, i = e & 3;
-        racc[blk][i] += ((cmask >> e) & 1u) ? ex2(a[blk][i]) : 0.f;
+        racc[blk][i] += ex2(a[blk][i]);
       }
     }
   };
@@ -546,13 +557,14 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
         for (int blk = 0; blk < 4; ++blk)
           acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[ks] : mh[ks], acc[blk], 0, 0, 0);
         epilogue_step(accp, c);
-        // mean key row: wave (rs, half) sums channel quarter rs of its 64 positions
+        // mean key row: wave (rs, half) sums channels 32 rs .. + 31 of its 64 positions
         // from the fragments already in registers
         if (KBAR && ks == rs && (c & 1) == 0)
 #pragma unroll
-          for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) kb[blk * 8 + e] += float(ka[blk][ks][e]);
+          for (int blk = 0; blk < 4; ++blk) {
+            kacc[blk][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], eye0, kacc[blk][0], 0, 0, 0);
+            kacc[blk][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], eye1, kacc[blk][1], 0, 0, 0);
+          }
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
@@ -563,8 +575,8 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
       for (int blk = 0; blk < 4; ++blk) {
         const uint16_t *kr = kl + (p0 + blk * 16 + r16) * MD;
         const bf16x8 f = *reinterpret_cast<const bf16x8 *>(kr + (((4 * rs + g) ^ r16) * 8));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kb[blk * 8 + e] += float(f[e]);
+        kacc[blk][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, eye0, kacc[blk][0], 0, 0, 0);
+        kacc[blk][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, eye1, kacc[blk][1], 0, 0, 0);
       }
     }
   };
@@ -617,17 +629,19 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     }
   }
   if (KBAR) {
+    // lane (g, r16) of kacc[blk][hf] holds positions p0 + 16 blk + 4 g + i, channel 32 rs + 16 hf + r16
     const float inv = 1.0f / float(units);
+    float *kbar = base + z.off_kbar() + 32 * rs + r16;
 #pragma unroll
-    for (int blk = 0; blk < 4; ++blk) {
-      const int j = j0 + p0 + blk * 16 + r16;
-      if (j < s.N) {
-        float *dst = base + z.off_kbar() + int64_t(j) * MD + (4 * rs + g) * 8;
-        const float *v = kb + blk * 8;
-        *reinterpret_cast<float4 *>(dst) = make_float4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
-        *reinterpret_cast<float4 *>(dst + 4) = make_float4(v[4] * inv, v[5] * inv, v[6] * inv, v[7] * inv);
+    for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = j0 + p0 + blk * 16 + 4 * g + i;
+        if (j < s.N) {
+          kbar[int64_t(j) * MD] = kacc[blk][0][i] * inv;
+          kbar[int64_t(j) * MD + 16] = kacc[blk][1][i] * inv;
+        }
       }
-    }
   }
 }
 
