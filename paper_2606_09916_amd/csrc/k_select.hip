@@ -85,8 +85,8 @@ __device__ __forceinline__ float key_score(uint32_t k) {
 }
 
 // hist[bin] += 1 for every lane with `on`. Lanes that share a bin are counted by
-// their leader with one atomic (scores cluster in a few bins); after four rounds
-// the remaining lanes add individually.
+// their leader with one atomic (scores cluster in a few bins); after four rounds,
+// or once a round finds at most two lanes on its bin, the rest add individually.
 __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t bin, bool on) {
   const int lane = threadIdx.x & 63;
   uint64_t act = __ballot(on);
@@ -97,6 +97,7 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t bin, bool on) 
     const uint64_t same = __ballot(on && bin == lb) & act;
     if (lane == leader) atomicAdd(&hist[lb], uint32_t(__popcll(same)));
     act &= ~same;
+    if (__popcll(same) <= 2) break;                   // the bins are spread: no more rounds
   }
   if ((act >> lane) & 1u) atomicAdd(&hist[bin], 1u);
 }
@@ -425,6 +426,137 @@ __global__ void __launch_bounds__(256) k_select_mark(const ikv_session *__restri
   }
 }
 
+// ---- selection in one launch for sessions of at most SEL_SMALL positions: one
+// workgroup per session holds every key in LDS, so the radix passes and the tie
+// ranking never leave the CU. Thread t takes positions t + 1024 q; wave w's 64
+// consecutive positions of sweep q give one 64-bit ballot of the initial keep flags.
+// Scores concentrate in a narrow range, so the passes bin the keys still in play,
+// [lo, hi], by their offset from lo: 11 bits of the actual spread per pass.
+constexpr int SEL_SMALL = 32768;
+constexpr int SEL_SU = 16;                 // loads in flight per thread while the keys are read
+
+__device__ __forceinline__ uint32_t block_min(uint32_t v, int *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, uint32_t(__shfl_xor(int(v), o, WAVE)));
+  if (lane == 0) red[wave] = int(v);
+  __syncthreads();
+  uint32_t r = 0xffffffffu;
+#pragma unroll
+  for (int w = 0; w < SEL_WAVES; ++w) r = min(r, uint32_t(red[w]));
+  __syncthreads();
+  return r;
+}
+
+__global__ void __launch_bounds__(SEL_THREADS) k_select_small(const ikv_session *__restrict__ sess,
+                                                              const int32_t *__restrict__ slot_maps, int dead,
+                                                              const float *__restrict__ scores,
+                                                              uint8_t *__restrict__ keep, int32_t *__restrict__ n_keep,
+                                                              float *__restrict__ tau) {
+  __shared__ uint32_t keys[SEL_SMALL];                // 0: not a candidate
+  __shared__ uint64_t kbits[SEL_SMALL / 64];          // live forced positions (every live one when skipped)
+  __shared__ uint32_t hist[SEL_BINS];
+  __shared__ int red[SEL_WAVES];
+  __shared__ int sh[2];
+  constexpr int Q = SEL_SMALL / SEL_THREADS;
+  const int b = blockIdx.x;
+  const ikv_session s = sess[b];
+  const int t = threadIdx.x, lane = t & 63;
+  const int N = s.N;
+  const bool skip = N <= s.C;
+  const int32_t *S = slot_maps + s.slot_off;
+  const float *sc = scores + s.slot_off;
+  uint8_t *kp = keep + s.slot_off;
+  int nl = 0, nf = 0;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;             // over the candidates
+  for (int q0 = 0; q0 < Q; q0 += SEL_SU) {
+    if (q0 * SEL_THREADS >= N) break;
+    int sv[SEL_SU];
+    float fv[SEL_SU];
+#pragma unroll
+    for (int u = 0; u < SEL_SU; ++u) {
+      const int j = (q0 + u) * SEL_THREADS + t;
+      sv[u] = ld_clamped(S, j, N);
+      fv[u] = ld_clamped(sc, j, N);
+    }
+#pragma unroll
+    for (int u = 0; u < SEL_SU; ++u) {
+      const int j = (q0 + u) * SEL_THREADS + t;
+      const bool in = j < N;
+      const bool live = in && sv[u] != dead;
+      const bool forced = j < s.pi || (j >= s.qs && j < s.qe);
+      nl += live;
+      nf += live && forced;
+      const bool cand = live && !forced && !skip;
+      const uint32_t key = cand ? score_key(fv[u]) : 0u;
+      keys[j] = key;
+      if (cand) {
+        kmin = min(kmin, key);
+        kmax = max(kmax, key);
+      }
+      const uint64_t kb = __ballot(live && (forced || skip));
+      if (lane == 0) kbits[j >> 6] = kb;
+    }
+  }
+  nl = block_sum(nl, red);
+  nf = block_sum(nf, red);
+  const int take = skip ? 0 : min(max(0, s.C - nf), nl - nf);
+  uint32_t thr = 0xffffffffu, tpos = 0u;              // above every key: nothing beyond the initial keep
+  if (take > 0) {
+    // the take-th largest key: shrink [lo, hi] until it holds one value
+    uint32_t lo = block_min(kmin, red), hi = ~block_min(~kmax, red);
+    int kk = take;                                    // its rank from the top among keys in [lo, hi]
+    const int n = min(N, SEL_SMALL);
+    while (hi > lo) {
+      const int span = 32 - __clz(int(hi - lo));      // bits of hi - lo
+      const int shift = max(0, span - 11);
+      for (int i = t; i < SEL_BINS; i += SEL_THREADS) hist[i] = 0u;
+      __syncthreads();
+      for (int i0 = 0; i0 < n; i0 += SEL_THREADS * SEL_U) {
+        uint32_t kv[SEL_U];
+#pragma unroll
+        for (int u = 0; u < SEL_U; ++u) kv[u] = keys[min(i0 + u * SEL_THREADS + t, n - 1)];
+#pragma unroll
+        for (int u = 0; u < SEL_U; ++u) {
+          const bool on = i0 + u * SEL_THREADS + t < n && kv[u] >= lo && kv[u] <= hi;
+          hist_add(hist, on ? (kv[u] - lo) >> shift : 0u, on);
+        }
+      }
+      __syncthreads();
+      find_bin(hist, SEL_BINS, kk, red, sh);
+      const uint32_t nlo = lo + (uint32_t(sh[0]) << shift);
+      hi = shift == 0 ? nlo : min(hi, nlo + ((1u << shift) - 1u));
+      lo = nlo;
+      kk = sh[1];
+      __syncthreads();
+    }
+    thr = lo;
+    int gt = 0, eq = 0;
+    for (int i = t; i < n; i += SEL_THREADS) {
+      gt += keys[i] > thr;
+      eq += keys[i] == thr;
+    }
+    gt = block_sum(gt, red);
+    eq = block_sum(eq, red);
+    const int kt = take - gt;                         // ties taken, 1 <= kt <= eq
+    // all ties taken: any position passes; else the kt-th smallest tied position
+    tpos = kt == eq ? 0xffffffffu
+                    : ~kth_largest([&](int i, uint32_t &v, bool &c) { v = ~uint32_t(i); c = keys[i] == thr; }, n, kt,
+                                   hist, red, sh);
+  }
+  for (int q = 0; q < Q; ++q) {
+    const int j = q * SEL_THREADS + t;
+    if (j >= N) break;
+    const uint32_t k = keys[j];
+    const bool sel = k != 0u && (k > thr || (k == thr && uint32_t(j) <= tpos));
+    kp[j] = uint8_t(sel || ((kbits[j >> 6] >> lane) & 1u));
+  }
+  if (t == 0) {
+    n_keep[b] = skip ? nl : nf + take;
+    tau[b] = skip ? -INFINITY : (take > 0 ? key_score(thr) : INFINITY);
+  }
+}
+
 size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions) {
   return size_t(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4) * sizeof(uint32_t);
 }
@@ -434,6 +566,11 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
                          int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st) {
   const int64_t keys_off = sel_chunks_before(sess_host, B) * SEL_PART;
   const int64_t res_off = keys_off + total_positions;
+  if (maxN <= SEL_SMALL) {
+    KTimer kt_("k_select_small", st);
+    k_select_small<<<B, SEL_THREADS, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, n_keep, tau);
+    return hipGetLastError();
+  }
   const dim3 grid(unsigned(cdiv(maxN, SEL_CHUNK)), B);
   if (maxN > 0) {
     KTimer kt_("k_select_keys", st);
