@@ -39,19 +39,23 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 //   kp/vp  [nq][HC]               W_K kq + b_K, W_V kq + b_V (residual only)
 //   misc   [MBAR_PARTS][D] + [D] + 64   partial and final mbar, live query count (residual only)
 //   fold   folded first-layer weights [HC+HIDDEN][D] as bf16 hi + lo, then the
-//          constant terms q0 [HC], h0 [HIDDEN] (residual on the MFMA path only)
+//          constant terms q0 [HC], h0 [HIDDEN], then the rule column of W_Q and W_1
+//          [HC+HIDDEN] (residual on the MFMA path only)
 //   qlist  [nq] live query positions (residual only)
+//   kvf    K' and V' of up to 64 live query positions as bf16 hi + lo MFMA fragments,
+//          zero past the live ones (residual on the MFMA path only)
 // followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN], and on the
-// MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC].
+// MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC], columns
+// ordered within each 32-wide head as perm32 below.
 constexpr int MBAR_PARTS = 64;
 constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
 constexpr int PART_TILE = 64;       // positions per first-pass partial of the ring passes
 
 struct ScoreSizes {
-  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist;
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf;
   int64_t lse_pairs;   // units * R * 2: the (max, 1/Z) pairs at the start of lse
   __host__ __device__ int64_t total() const {
-    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist;
+    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf;
   }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
@@ -65,10 +69,24 @@ struct ScoreSizes {
   __host__ __device__ int64_t off_misc() const { return off_vp() + vp; }
   __host__ __device__ int64_t off_fold() const { return off_misc() + misc; }
   __host__ __device__ int64_t off_qlist() const { return off_fold() + fold; }
+  __host__ __device__ int64_t off_kvf() const { return off_qlist() + qlist; }
 };
 
-// Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0).
-__host__ __device__ inline int64_t fold_floats(int D) { return int64_t(HC + HIDDEN) * D + HC + HIDDEN; }
+// Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0,
+// then the rule column).
+__host__ __device__ inline int64_t fold_floats(int D) { return int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN); }
+
+// Residual cross-attention fragments: K' and V' of RES_KEYS live query positions.
+constexpr int RES_KEYS = 64;
+constexpr int KVF_BF16 = 2 * HC_HEADS * 4 * 2 * 64 * 8;       // K' then V', 16 KB bf16 each
+// Within a 32-wide block, the channel (or key) that MFMA k index 8 g + e stands for:
+// lane group g of a 16x16 output block holds rows 4 g .. 4 g + 3 of the block, so the
+// two 16-row halves of a 32-wide block give it 4 g + e and 16 + 4 g + e - 4.
+__host__ __device__ inline int perm32(int g, int e) { return e < 4 ? 4 * g + e : 16 + 4 * g + (e - 4); }
+// and its inverse: channel c of a 32-wide block -> k index 8 g + e
+__host__ __device__ inline int perm32_inv(int c) {
+  return c < 16 ? 8 * (c >> 2) + (c & 3) : 8 * ((c - 16) >> 2) + 4 + ((c - 16) & 3);
+}
 
 __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid,
                                                   bool mfma) {
@@ -85,6 +103,7 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   z.misc = resid ? align64f(int64_t(MBAR_PARTS + 1) * D + 64) : 0;
   z.fold = resid && mfma ? align64f(fold_floats(D)) : 0;
   z.qlist = resid ? align64f(s.nq) : 0;
+  z.kvf = resid && mfma ? align64f(KVF_BF16 / 2) : 0;
   return z;
 }
 

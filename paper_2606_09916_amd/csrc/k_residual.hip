@@ -34,7 +34,8 @@ struct ResLayout {
 int64_t residual_floats(int D) { return ResLayout(D).total; }
 
 // W_Q^T [F][HC] and W_1^T [F+HC][HIDDEN] so that consecutive threads read consecutive
-// outputs, and the cross-attention columns of W_1 as bf16 hi [HIDDEN][HC] then lo.
+// outputs, and the cross-attention columns of W_1 as bf16 hi [HIDDEN][HC] then lo,
+// each 32-wide head block in the MFMA k order of perm32.
 __global__ void k_res_transpose(const float *__restrict__ blob, float *__restrict__ shared, int D) {
   const ResLayout lay(D);
   const int64_t F = 3 * D + 1;
@@ -55,8 +56,9 @@ __global__ void k_res_transpose(const float *__restrict__ blob, float *__restric
     const int64_t o = k / HC, c = k - o * HC;
     const float v = blob[lay.W1 + o * (F + HC) + F + c];
     const uint16_t hi = float_to_bf16_bits(v);
-    w1c[k] = hi;
-    w1c[nc + k] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+    const int64_t at = o * HC + (c & ~int64_t(31)) + perm32_inv(int(c & 31));
+    w1c[at] = hi;
+    w1c[nc + at] = float_to_bf16_bits(v - bf16_bits_to_float(hi));
   }
 }
 
@@ -126,9 +128,15 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
 }
 
 // K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup.
+// With `frag` (D = 128, at most RES_KEYS rows) the grid covers all RES_KEYS rows and
+// also writes them as bf16 hi + lo MFMA fragments, zeros past the live rows:
+//   K' [head][key block kb][hi|lo][lane 16 g + i][8]: key 16 kb + i, channels
+//      32 head + perm32(g, e) (the A operand of the logits block);
+//   V' [head][channel block nb][key step ks][hi|lo][lane 16 g + i][8]: channel
+//      32 head + 16 nb + i, keys 32 ks + perm32(g, e) (the A operand of the context).
 template <int D>
 __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                                float *__restrict__ ws, int L, int Hkv, bool mfma) {
+                                                float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
@@ -142,7 +150,7 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
   const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
   const int *qlist = reinterpret_cast<const int *>(base + z.off_qlist());
   const int i0 = blockIdx.x * 4;
-  if (i0 >= n) return;
+  if (i0 >= n && !frag) return;
   __shared__ float kq[4][D];
   const int t = threadIdx.x;
   for (int e = t; e < 4 * D; e += 256) {
@@ -164,13 +172,35 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
 #pragma unroll
   for (int r = 0; r < 4; ++r)
     if (i0 + r < n) dst[int64_t(i0 + r) * HC + o] = a[r];
+  if (!frag) return;
+  uint16_t *kf = reinterpret_cast<uint16_t *>(base + z.off_kvf());
+  uint16_t *vf = kf + KVF_BF16 / 2;
+  const int head = o >> 5, c = o & 31;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int key = i0 + r;
+    const float v = key < n ? a[r] : 0.f;
+    const uint16_t hi = float_to_bf16_bits(v), lo = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+    if (!isv) {
+      const int k = perm32_inv(c), kb = key >> 4, lane = 16 * (k >> 3) + (key & 15);
+      const int64_t at = int64_t((head * 4 + kb) * 2) * 512 + lane * 8 + (k & 7);
+      kf[at] = hi;
+      kf[at + 512] = lo;
+    } else {
+      const int nb = c >> 4, ks = key >> 5, k = perm32_inv(key & 31), lane = 16 * (k >> 3) + (c & 15);
+      const int64_t at = int64_t(((head * 2 + nb) * 2 + ks) * 2) * 512 + lane * 8 + (k & 7);
+      vf[at] = hi;
+      vf[at + 512] = lo;
+    }
+  }
 }
 
 // Folded first layer of one session (exact in real arithmetic):
 //   W_Q phi + b_Q  = (W_Q^k + W_Q^km diag(mbar)) kbar + (W_Q^m mbar + b_Q) + w_Q^r rule
 //   W_1 [phi; c] + b_1 = (W_1^k + W_1^km diag(mbar)) kbar + (W_1^m mbar + b_1) + w_1^r rule + W_1^c c
 // Rows 0..HC-1 of the folded matrix are the W_Q part, rows HC.. the W_1 part; stored
-// as bf16 hi [HC+HIDDEN][D] then lo, then q0 [HC] and h0 [HIDDEN] in float32.
+// as bf16 hi [HC+HIDDEN][D] then lo, then q0 [HC] and h0 [HIDDEN] in float32, then
+// the rule column w_Q^r [HC] and w_1^r [HIDDEN].
 template <int D>
 __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
                                                   float *__restrict__ ws, int L, int Hkv) {
@@ -202,6 +232,10 @@ __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict_
     float a = o < HC ? blob[lay.bQ + o] : blob[lay.b1 + (o - HC)];
     for (int d = 0; d < D; ++d) a = fmaf(row[D + d], mbar[d], a);
     q0[o] = a;
+  } else if (i < nw + 2 * (HC + HIDDEN)) {          // the rule column
+    const int64_t o = i - nw - (HC + HIDDEN);
+    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
+    q0[HC + HIDDEN + o] = row[3 * D];
   }
 }
 
@@ -394,16 +428,16 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
     KTimer kt_("k_res_setup<D>", st);
     k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma);
   }
-  if (a.maxNq > 0)
+  if (a.maxNq > 0 || a.mfma_resid)
     {
       KTimer kt_("k_res_kv<D>", st);
-      k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
-                                                                           a.mfma);
+      k_res_kv<D><<<dim3(unsigned(a.mfma_resid ? RES_KEYS / 4 : cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(
+          a.sess_dev, a.residual, a.ws, p.L, p.Hkv, a.mfma, a.mfma_resid);
     }
   if (a.mfma_resid) {
     {
       KTimer kt_("k_res_fold<D>", st);
-      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + HC + HIDDEN, 256)), a.B), 256, 0, st>>>(
+      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN), 256)), a.B), 256, 0, st>>>(
           a.sess_dev, a.residual, a.ws, p.L, p.Hkv);
     }
     hipError_t e = hipGetLastError();
