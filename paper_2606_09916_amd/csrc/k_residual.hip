@@ -155,7 +155,9 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
   const int t = threadIdx.x;
   for (int e = t; e < 4 * D; e += 256) {
     const int r = e / D, d = e - r * D;
-    kq[r][d] = (i0 + r < n) ? kbar[int64_t(qlist[i0 + r]) * D + d] : 0.f;
+    const int q = n > 0 ? qlist[min(i0 + r, n - 1)] : 0;   // a live row (or row 0) stands in past n
+    const float v = kbar[int64_t(q) * D + d];
+    kq[r][d] = (i0 + r < n) ? v : 0.f;
   }
   __syncthreads();
   const int o = t & (HC - 1);
@@ -163,10 +165,16 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
   const float *W = blob + (isv ? lay.WV : lay.WK) + int64_t(o) * D;
   const float bias = blob[(isv ? lay.bV : lay.bK) + o];
   float a[4] = {bias, bias, bias, bias};
-  for (int d = 0; d < D; ++d) {
-    const float wv = W[d];
+  constexpr int WB = 64;                              // weights in flight per thread
+#pragma unroll 1
+  for (int d0 = 0; d0 < D; d0 += WB) {
+    float wv[WB];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) a[r] = fmaf(wv, kq[r][d], a[r]);
+    for (int d = 0; d < WB; ++d) wv[d] = W[d0 + d];
+#pragma unroll
+    for (int d = 0; d < WB; ++d)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a[r] = fmaf(wv[d], kq[r][d0 + d], a[r]);
   }
   float *dst = isv ? vp : kp;
 #pragma unroll
@@ -203,10 +211,12 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
 // the rule column w_Q^r [HC] and w_1^r [HIDDEN].
 template <int D>
 __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                                  float *__restrict__ ws, int L, int Hkv) {
+                                                  float *__restrict__ ws, float *__restrict__ shared, int L, int Hkv) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
-  if (s.N <= s.C) return;
+  uint16_t *w1c = reinterpret_cast<uint16_t *>(shared + align64f(int64_t(3 * D + 1) * HC) +
+                                                align64f(int64_t(3 * D + 1 + HC) * HIDDEN));
+  if (s.N <= s.C && b != 0) return;
   const int units = L * Hkv;
   const ResLayout lay(D);
   const int64_t F = 3 * D + 1;
@@ -219,6 +229,7 @@ __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict_
   float *q0 = fold + int64_t(HC + HIDDEN) * D;
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   const int64_t nw = int64_t(HC + HIDDEN) * D;
+  if (s.N <= s.C && i < nw + 2 * (HC + HIDDEN)) return;   // skipped session: only the shared part
   if (i < nw) {
     const int64_t o = i / D, d = i - o * D;
     const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
@@ -230,12 +241,26 @@ __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict_
     const int64_t o = i - nw;
     const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
     float a = o < HC ? blob[lay.bQ + o] : blob[lay.b1 + (o - HC)];
-    for (int d = 0; d < D; ++d) a = fmaf(row[D + d], mbar[d], a);
+    float rv[D];                                      // the whole row in flight at once
+#pragma unroll
+    for (int d = 0; d < D; ++d) rv[d] = row[D + d];
+#pragma unroll
+    for (int d = 0; d < D; ++d) a = fmaf(rv[d], mbar[d], a);
     q0[o] = a;
   } else if (i < nw + 2 * (HC + HIDDEN)) {          // the rule column
     const int64_t o = i - nw - (HC + HIDDEN);
     const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
     q0[HC + HIDDEN + o] = row[3 * D];
+  } else if (b == 0 && i < nw + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC) {
+    // shared by every session: the cross-attention columns of W_1 as bf16 hi + lo
+    // [HIDDEN][HC], each 32-wide head block in the MFMA k order of perm32
+    const int64_t k = i - nw - 2 * (HC + HIDDEN), nc = int64_t(HIDDEN) * HC;
+    const int64_t o = k / HC, c = k - o * HC;
+    const float v = blob[lay.W1 + o * (F + HC) + F + c];
+    const uint16_t h = float_to_bf16_bits(v);
+    const int64_t at = o * HC + (c & ~int64_t(31)) + perm32_inv(int(c & 31));
+    w1c[at] = h;
+    w1c[nc + at] = float_to_bf16_bits(v - bf16_bits_to_float(h));
   }
 }
 
@@ -415,10 +440,11 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   const int64_t F = 3 * D + 1;
   const int64_t n = F * HC + (F + HC) * HIDDEN + int64_t(HIDDEN) * HC;
-  {
-    KTimer kt_("k_res_transpose", st);
-    k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
-  }
+  if (!a.mfma_resid)
+    {
+      KTimer kt_("k_res_transpose", st);
+      k_res_transpose<<<unsigned(cdiv(n, 256)), 256, 0, st>>>(a.residual, a.ws_shared, D);
+    }
   if (!a.mfma)   // on the matrix-core path k_msplit leaves the partial sums of mbar
   {
     KTimer kt_("k_mbar_part<D>", st);
@@ -437,8 +463,8 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   if (a.mfma_resid) {
     {
       KTimer kt_("k_res_fold<D>", st);
-      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN), 256)), a.B), 256, 0, st>>>(
-          a.sess_dev, a.residual, a.ws, p.L, p.Hkv);
+      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC, 256)),
+                           a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, a.ws_shared, p.L, p.Hkv);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -40,19 +40,25 @@ __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 
 // channels (4 k-step + g) * 8 .. + 8: lane group g of an MFMA reads 128 contiguous bytes.
 // Workgroup p takes rows [p*rows/P, (p+1)*rows/P) with P = MBAR_PARTS; thread (r, c)
 // splits channel group c of rows r, r + 16, ... (32 bytes in, two 16-byte stores out),
-// a batch of rows in flight at once. With the residual head on it also sums the raw
-// rows: the workgroup's column sums are partial p of mbar.
-constexpr int MS_BATCH = 6;
+// a batch of rows in flight at once (loads from row indices clamped into the range and
+// masked afterwards, so that none waits inside a branch). With the residual head on it
+// also sums the raw rows: the workgroup's column sums are partial p of mbar. For a
+// session at or under its budget it only fills the scores with -inf (the gate).
+constexpr int MS_BATCH = 9;
 
 __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ sess, const float *__restrict__ M,
-                                                float *__restrict__ ws, int L, int Hkv, bool resid) {
+                                                float *__restrict__ ws, float *__restrict__ scores, int L, int Hkv,
+                                                bool resid) {
   __shared__ float red[16][MD];
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
-  if (s.N <= s.C) return;
+  const int p = blockIdx.x;
+  if (s.N <= s.C) {
+    for (int j = p * 256 + int(threadIdx.x); j < s.N; j += MBAR_PARTS * 256) scores[s.slot_off + j] = -INFINITY;
+    return;
+  }
   const int units = L * Hkv;
   const int64_t rows = int64_t(units) * s.R;
-  const int p = blockIdx.x;
   const int64_t r0 = rows * p / MBAR_PARTS, r1 = rows * (p + 1) / MBAR_PARTS;
   const int rg = threadIdx.x >> 4, c = threadIdx.x & 15;
   const int g = c & 3, ks = c >> 2;
@@ -67,11 +73,9 @@ __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ 
     float4 va[MS_BATCH], vb[MS_BATCH];
 #pragma unroll
     for (int k = 0; k < MS_BATCH; ++k) {
-      const int64_t rr = r + 16 * k;
-      if (rr < r1) {
-        va[k] = *reinterpret_cast<const float4 *>(src + rr * MD);
-        vb[k] = *reinterpret_cast<const float4 *>(src + rr * MD + 4);
-      }
+      const int64_t rr = min(r + 16 * k, r1 - 1);
+      va[k] = *reinterpret_cast<const float4 *>(src + rr * MD);
+      vb[k] = *reinterpret_cast<const float4 *>(src + rr * MD + 4);
     }
 #pragma unroll
     for (int k = 0; k < MS_BATCH; ++k) {
@@ -861,7 +865,8 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
 #pragma unroll
       for (int q = 0; q < LB; ++q) {
         const int64_t k = k0 + 8 * q;
-        pv[q] = k < tiles ? *reinterpret_cast<const float2 *>(part + (k * rows + i) * 2) : make_float2(-INFINITY, 0.f);
+        pv[q] = *reinterpret_cast<const float2 *>(part + (min(k, tiles - 1) * rows + i) * 2);
+        if (k >= tiles) pv[q] = make_float2(-INFINITY, 0.f);
       }
 #pragma unroll
       for (int q = 0; q < LB; ++q) {
@@ -894,13 +899,6 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   }
 }
 
-// The gate: sessions with N <= C get -inf everywhere (the passes skip them).
-__global__ void k_fill_skipped(const ikv_session *__restrict__ sess, float *__restrict__ scores) {
-  const ikv_session s = sess[blockIdx.y];
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (s.N <= s.C && j < s.N) scores[s.slot_off + j] = -INFINITY;
-}
-
 hipError_t launch_residual(const ScoreArgs &a, hipStream_t st);
 
 hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
@@ -910,12 +908,8 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   const unsigned tiles = unsigned(cdiv(a.maxN, MFMA_TILE));
   const uint16_t *kp = static_cast<const uint16_t *>(p.k_pool);
   {
-    KTimer kt_("k_fill_skipped", st);
-    k_fill_skipped<<<dim3(unsigned(cdiv(a.maxN, 256)), a.B), 256, 0, st>>>(a.sess_dev, a.scores);
-  }
-  {
     KTimer kt_("k_msplit", st);
-    k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, resid);
+    k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, a.scores, p.L, p.Hkv, resid);
   }
   const bool ring = a.maxR <= 64;
   // the unit-major first pass addresses a layer's keys with 32-bit offsets
