@@ -32,8 +32,8 @@ CALIB_BYTES = 256 << 20        # the calibration copy (bytes read = bytes writte
 # scaled by what it reads for the calibration copy) on one workload, for the kernel
 # as built from the hashed sources; reported only while those sources are unchanged.
 MEASURED_TRAFFIC = {
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ring<true, true>"): (2513811948, "dab941fffc8574fd"),
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ring<false, false>"): (2566899601, "dab941fffc8574fd"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ring<true, true>"): (2509678055, "693cd3ee9ea02893"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2570847174, "693cd3ee9ea02893"),
 }
 TRAFFIC_SOURCES = ("paper_2606_09916_amd/csrc/k_score_mfma.hip", "paper_2606_09916_amd/csrc/ikv_internal.hpp")
 
@@ -224,7 +224,9 @@ def main() -> int:
     key_bytes = nA * units * sh.D * 2                          # candidate key rows, bf16, one pass
     mem_bytes = units * s.R * sh.D * 4                         # memory rows, float32
     kv_live = n_live * units * sh.D * 2 * 2                    # live K and V rows, bf16
+    stats_parts = -(-s.N // 1024) * units * s.R * 8            # one (max, sum) per chunk and memory row
     algo = {
+        "k_score_stats": key_bytes + mem_bytes + stats_parts,
         "k_score_ring<false, false>": key_bytes + mem_bytes,
         "k_score_ring<true, true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
         "k_score_ring<true, false>": key_bytes + mem_bytes + s.N * 4,
@@ -232,6 +234,8 @@ def main() -> int:
         "k_decode_mfma<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
         "k_qm_update<T, 128>": units * s.R * (s.qe - s.qs) * sh.D * 2 + 2 * mem_bytes,
         "k_select": s.N * (4 + 4 + 1),
+        "k_select_small": s.N * (4 + 4 + 1),
+        "k_residual_mfma": nA * (sh.D * 4 + 4 + 4),
         "k_redirect<true>": s.N * (4 + 1 + 4 + 4),
     }
     kernels = {}
