@@ -433,7 +433,7 @@ __global__ void __launch_bounds__(256) k_select_mark(const ikv_session *__restri
 // Scores concentrate in a narrow range, so the passes bin the keys still in play,
 // [lo, hi], by their offset from lo: 11 bits of the actual spread per pass.
 constexpr int SEL_SMALL = 32768;
-constexpr int SEL_SU = 16;                 // loads in flight per thread while the keys are read
+constexpr int SEL_SU = 32;                 // loads in flight per thread while the keys are read
 
 __device__ __forceinline__ uint32_t block_min(uint32_t v, int *red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -557,8 +557,287 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select_small(const ikv_session 
   }
 }
 
+// ---- selection across workgroups (a cooperative launch: every workgroup of the grid
+// is resident at once). Each session's positions split into chunks of SC_CHUNK, one
+// workgroup each, holding its keys in LDS; the workgroups of a session meet at
+// barriers on a counter in the workspace. Counts, key range and the radix histograms
+// are summed with integer device-scope atomics (order-free, so the result is
+// deterministic), and every workgroup then takes the same decisions from the same
+// totals: the passes bin the keys still in play by their offset from the smallest
+// candidate key, 11 bits of the actual spread per pass; ties at the threshold are
+// ranked by the same passes over positions.
+constexpr int SC_THREADS = 256;
+constexpr int SC_WAVES = SC_THREADS / WAVE;
+constexpr int SC_PER = 4;                              // positions per thread
+constexpr int SC_CHUNK = SC_THREADS * SC_PER;
+constexpr int SC_MAXN = 131072;                        // positions per session on this path
+constexpr int SC_HIST = 5;                             // histograms: 3 key passes, 2 position passes
+constexpr int SC_WORDS = 64 + SC_HIST * SEL_BINS;      // per session: counters, then histograms
+// counter words: barrier, live count, live forced count, ~(min key), max key
+enum { SC_BAR = 0, SC_NL = 1, SC_NF = 2, SC_NMIN = 3, SC_MAX = 4 };
+
+__device__ __forceinline__ uint32_t ald(const uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void aadd(uint32_t *p, uint32_t v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void amax(uint32_t *p, uint32_t v) {
+  __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The k-th barrier of a session's G workgroups: wait until the counter reaches k * G.
+// Everything the workgroups exchange is a device-scope atomic, so the barrier needs
+// no cache write-back or invalidation: each thread's atomics are complete once its
+// vector-memory count drains, then one thread adds to the counter and polls it with
+// coherent loads. Every workgroup of the grid is resident (cooperative launch), so the
+// count is reached; the poll is bounded all the same.
+__device__ __forceinline__ void sc_barrier(uint32_t *bar, uint32_t target) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    aadd(bar, 1u);
+    for (uint32_t spin = 0; spin < (1u << 24); ++spin) {
+      if (ald(bar) >= target) break;
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+}
+
+// Sum and maximum over the workgroup of SC_THREADS threads.
+__device__ __forceinline__ uint32_t sc_umax(uint32_t v, int *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, uint32_t(__shfl_xor(int(v), o, WAVE)));
+  if (lane == 0) red[wave] = int(v);
+  __syncthreads();
+  uint32_t r = 0u;
+#pragma unroll
+  for (int w = 0; w < SC_WAVES; ++w) r = max(r, uint32_t(red[w]));
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ int sc_sum(int v, int *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  int tot = 0;
+#pragma unroll
+  for (int w = 0; w < SC_WAVES; ++w) tot += red[w];
+  __syncthreads();
+  return tot;
+}
+
+// The bin of the session histogram `gh` holding the kk-th largest (scanning from the
+// top bin); copies the histogram into `lh` and writes the bin and the rank inside it
+// to sh[0], sh[1]. Every thread must call it.
+__device__ __forceinline__ void sc_find_bin(const uint32_t *gh, uint32_t *lh, int kk, int *red, int *sh) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  constexpr int per = SEL_BINS / SC_THREADS;
+  const int hi_bin = SEL_BINS - 1 - t * per;
+  uint32_t v[per];
+#pragma unroll
+  for (int q = 0; q < per; ++q) v[q] = ald(gh + hi_bin - q);
+  int c = 0;
+#pragma unroll
+  for (int q = 0; q < per; ++q) {
+    lh[hi_bin - q] = v[q];
+    c += int(v[q]);
+  }
+  int x = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, WAVE);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) red[wave] = x;
+  __syncthreads();
+  int base = 0;
+#pragma unroll
+  for (int w = 0; w < SC_WAVES; ++w) base += w < wave ? red[w] : 0;
+  const int above = base + x - c;
+  if (above < kk && kk <= above + c) {
+    int cum = above;
+#pragma unroll
+    for (int q = 0; q < per; ++q) {
+      const int h = int(v[q]);
+      if (cum < kk && cum + h >= kk) {
+        sh[0] = hi_bin - q;
+        sh[1] = kk - cum;
+      }
+      cum += h;
+    }
+  }
+  __syncthreads();
+}
+
+// The kk-th largest of this chunk's values get(i) among those counted, merged with
+// the session's other chunks: [lo, hi] holds it and kk is its rank from the top among
+// the values in [lo, hi]; pass p uses histogram hist0 + p. Every workgroup of the
+// session calls it with the same arguments and takes the same passes. Returns the
+// value; *cnt is the number of counted values equal to it.
+template <class Get>
+__device__ uint32_t sc_kth(Get get, uint32_t lo, uint32_t hi, int kk, uint32_t *cw, int hist0, uint32_t *lh,
+                           int *red, int *sh, int &nbar, int G, int &cnt) {
+  const int t = threadIdx.x;
+  int pass = 0;
+  cnt = -1;
+  while (hi > lo) {
+    const int span = 32 - __clz(int(hi - lo));
+    const int shift = max(0, span - 11);
+    for (int i = t; i < SEL_BINS; i += SC_THREADS) lh[i] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < SC_PER; ++q) {
+      uint32_t v;
+      bool c;
+      get(q * SC_THREADS + t, v, c);
+      const bool on = c && v >= lo && v <= hi;
+      hist_add(lh, on ? (v - lo) >> shift : 0u, on);
+    }
+    __syncthreads();
+    uint32_t *gh = cw + 64 + (hist0 + pass) * SEL_BINS;
+    for (int i = t; i < SEL_BINS; i += SC_THREADS)
+      if (lh[i]) aadd(gh + i, lh[i]);
+    sc_barrier(cw + SC_BAR, uint32_t(++nbar * G));
+    sc_find_bin(gh, lh, kk, red, sh);
+    const uint32_t nlo = lo + (uint32_t(sh[0]) << shift);
+    hi = shift == 0 ? nlo : min(hi, nlo + ((1u << shift) - 1u));
+    lo = nlo;
+    kk = sh[1];
+    cnt = int(lh[sh[0]]);
+    ++pass;
+    __syncthreads();
+  }
+  return lo;
+}
+
+__global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *__restrict__ sess,
+                                                            const int32_t *__restrict__ slot_maps, int dead,
+                                                            const float *__restrict__ scores,
+                                                            uint8_t *__restrict__ keep, int32_t *__restrict__ n_keep,
+                                                            float *__restrict__ tau, uint32_t *__restrict__ coop) {
+  __shared__ uint32_t ck[SC_CHUNK];                  // keys of this chunk (0: not a candidate)
+  __shared__ uint32_t lh[SEL_BINS];
+  __shared__ int red[SC_WAVES];
+  __shared__ int sh[2];
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  const int N = s.N;
+  const int G = max(1, int(cdiv(N, SC_CHUNK)));     // an empty session still writes its counts
+  const int wg = blockIdx.x;
+  if (wg >= G) return;                               // not one of this session's workgroups
+  const int t = threadIdx.x;
+  uint32_t *cw = coop + int64_t(b) * SC_WORDS;
+  const bool skip = N <= s.C;
+  const int j0 = wg * SC_CHUNK;
+  const int32_t *S = slot_maps + s.slot_off;
+  const float *sc = scores + s.slot_off;
+  uint8_t *kp = keep + s.slot_off;
+
+  // keys, initial keep flags (live forced, or every live position when skipped), counts, key range
+  int sv[SC_PER];
+  float fv[SC_PER];
+#pragma unroll
+  for (int q = 0; q < SC_PER; ++q) {
+    const int j = j0 + q * SC_THREADS + t;
+    sv[q] = ld_clamped(S, j, N);
+    fv[q] = ld_clamped(sc, j, N);
+  }
+  int nl = 0, nf = 0;
+  uint32_t nmin = 0u, kmax = 0u, kflag = 0u;         // nmin: complement of the smallest key
+#pragma unroll
+  for (int q = 0; q < SC_PER; ++q) {
+    const int j = j0 + q * SC_THREADS + t;
+    const bool live = j < N && sv[q] != dead;
+    const bool forced = j < s.pi || (j >= s.qs && j < s.qe);
+    nl += live;
+    nf += live && forced;
+    const bool cand = live && !forced && !skip;
+    const uint32_t key = cand ? score_key(fv[q]) : 0u;
+    ck[q * SC_THREADS + t] = key;
+    kflag |= uint32_t(live && (forced || skip)) << q;
+    if (cand) {
+      nmin = max(nmin, ~key);
+      kmax = max(kmax, key);
+    }
+  }
+  nl = sc_sum(nl, red);
+  nf = sc_sum(nf, red);
+  nmin = sc_umax(nmin, red);
+  kmax = sc_umax(kmax, red);
+  if (t == 0) {
+    aadd(cw + SC_NL, uint32_t(nl));
+    aadd(cw + SC_NF, uint32_t(nf));
+    amax(cw + SC_NMIN, nmin);
+    amax(cw + SC_MAX, kmax);
+  }
+  int nbar = 0;
+  sc_barrier(cw + SC_BAR, uint32_t(++nbar * G));
+  const int tl = int(ald(cw + SC_NL)), tf = int(ald(cw + SC_NF));
+  const int take = skip ? 0 : min(max(0, s.C - tf), tl - tf);
+  uint32_t thr = 0xffffffffu, tpos = 0u;             // above every key: nothing beyond the initial keep
+  if (take > 0) {
+    int cnt;
+    thr = sc_kth([&](int i, uint32_t &v, bool &c) { v = ck[i]; c = v != 0u; }, ~ald(cw + SC_NMIN), ald(cw + SC_MAX),
+                 take, cw, 0, lh, red, sh, nbar, G, cnt);
+    // rank of the threshold among the keys equal to it, and how many there are
+    const int eq = cnt < 0 ? tl - tf : cnt;           // no pass: every candidate has the same key
+    const int kt = cnt < 0 ? take : sh[1];
+    // all ties taken: any position passes; else the kt-th smallest tied position
+    if (kt == eq) {
+      tpos = 0xffffffffu;
+    } else {
+      int c2;
+      tpos = ~sc_kth([&](int i, uint32_t &v, bool &c) { v = ~uint32_t(j0 + i); c = ck[i] == thr; },
+                     ~uint32_t(N - 1), 0xffffffffu, kt, cw, 3, lh, red, sh, nbar, G, c2);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < SC_PER; ++q) {
+    const int j = j0 + q * SC_THREADS + t;
+    if (j < N) {
+      const uint32_t k = ck[q * SC_THREADS + t];
+      const bool sel = k != 0u && (k > thr || (k == thr && uint32_t(j) <= tpos));
+      kp[j] = uint8_t(sel || ((kflag >> q) & 1u));
+    }
+  }
+  if (wg == 0 && t == 0) {
+    n_keep[b] = skip ? tl : tf + take;
+    tau[b] = skip ? -INFINITY : (take > 0 ? key_score(thr) : INFINITY);
+  }
+}
+
+__global__ void k_select_coop_zero(uint32_t *__restrict__ coop, int64_t words) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i < words) __hip_atomic_store(coop + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions) {
-  return size_t(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4) * sizeof(uint32_t);
+  return size_t(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4 + int64_t(B) * SC_WORDS) *
+         sizeof(uint32_t);
+}
+
+// Workgroups of k_select_coop that the current device holds at once (0: no cooperative launch).
+static int coop_capacity() {
+  static int cap[64];
+  static bool known[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!known[dev]) {
+    int per_cu = 0, cus = 0, coop = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_select_coop, SC_THREADS, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess)
+      per_cu = cus = coop = 0;
+    cap[dev] = coop ? per_cu * cus : 0;
+    known[dev] = true;
+  }
+  return cap[dev];
 }
 
 hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_dev, int B, int maxN,
@@ -566,6 +845,22 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
                          int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st) {
   const int64_t keys_off = sel_chunks_before(sess_host, B) * SEL_PART;
   const int64_t res_off = keys_off + total_positions;
+  const int64_t gmax = cdiv(maxN, SC_CHUNK);
+  if (maxN > 0 && maxN <= SC_MAXN && gmax * B <= coop_capacity()) {
+    uint32_t *coop = ws + res_off + int64_t(B) * 4;
+    const int64_t words = int64_t(B) * SC_WORDS;
+    {
+      KTimer kt_("k_select_coop_zero", st);
+      k_select_coop_zero<<<unsigned(cdiv(words, 256)), 256, 0, st>>>(coop, words);
+    }
+    KTimer kt_("k_select_coop", st);
+    void *args[] = {(void *)&sess_dev, (void *)&slot_maps, (void *)&dead, (void *)&scores, (void *)&keep,
+                    (void *)&n_keep, (void *)&tau, (void *)&coop};
+    hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_select_coop), dim3(unsigned(gmax), B),
+                                              dim3(SC_THREADS), args, 0, st);
+    if (e != hipSuccess) return e;
+    return hipGetLastError();
+  }
   if (maxN <= SEL_SMALL) {
     KTimer kt_("k_select_small", st);
     k_select_small<<<B, SEL_THREADS, 0, st>>>(sess_dev, slot_maps, dead, scores, keep, n_keep, tau);
@@ -592,6 +887,7 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
 // pool has at most RED_LDS_WORDS * 32 slots, else in the caller's workspace, where
 // the workgroup's waves reach each other through device-scope atomics and fences.
 constexpr int RED_LDS_WORDS = 16384;        // two bitsets of 64 KB: pools up to 524288 slots
+constexpr int RED_U = 16;                   // positions in flight per lane in the two sweeps
 
 template <bool LDS_SETS>
 struct SlotSets {
@@ -641,17 +937,17 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
   int64_t lo, hi;
   wave_range(s.N, lo, hi);
   int surv = 0;
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
-    int sv[SEL_U];
-    uint8_t kv[SEL_U];
+  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * RED_U) {
+    int sv[RED_U];
+    uint8_t kv[RED_U];
 #pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
+    for (int u = 0; u < RED_U; ++u) {
       const int64_t j = c0 + u * WAVE + lane;
       sv[u] = ld_clamped(S, j, hi);
       kv[u] = ld_clamped(kp, j, hi);
     }
 #pragma unroll
-    for (int u = 0; u < SEL_U; ++u) {
+    for (int u = 0; u < RED_U; ++u) {
       const bool k = c0 + u * WAVE + lane < hi && sv[u] != dead && kv[u] != 0;
       if (k) sets.set(sets.kept, sv[u]);
       surv += __popcll(__ballot(k));
@@ -661,17 +957,17 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
   int pos = wave_base(surv, total_live, red);
   sets.sync();
   // reroute dropped positions, mark freeable slots, list the survivors in position order
-  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * SEL_U) {
-    int sv[SEL_U];
-    uint8_t kv[SEL_U];
+  for (int64_t c0 = lo; c0 < hi; c0 += WAVE * RED_U) {
+    int sv[RED_U];
+    uint8_t kv[RED_U];
 #pragma unroll
-    for (int q = 0; q < SEL_U; ++q) {
+    for (int q = 0; q < RED_U; ++q) {
       const int64_t j = c0 + q * WAVE + lane;
       sv[q] = ld_clamped(S, j, hi);
       kv[q] = ld_clamped(kp, j, hi);
     }
 #pragma unroll
-    for (int q = 0; q < SEL_U; ++q) {
+    for (int q = 0; q < RED_U; ++q) {
       const int j = int(c0) + q * WAVE + lane;
       const int u = j < hi ? sv[q] : dead;
       const bool alive = u != dead;
