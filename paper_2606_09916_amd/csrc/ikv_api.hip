@@ -293,6 +293,8 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.ws = static_cast<float *>(workspace);
   a.mfma = use_mfma(pool, sess, B);
   a.mfma_resid = a.mfma && resid && maxNq <= 64;
+  a.stats = a.mfma && maxR <= 64 && pool->Hkv % 2 == 0 &&
+            int64_t(pool->num_slots) * pool->Hkv * pool->D * 2 <= int64_t(UINT32_MAX);
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.maxR = maxR;

@@ -44,6 +44,8 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 //   qlist  [nq] live query positions (residual only)
 //   kvf    K' and V' of up to 64 live query positions as bf16 hi + lo MFMA fragments,
 //          zero past the live ones (residual on the MFMA path only)
+//   mbp    [units / 2][D] column sums of the memory rows per head pair, the partials
+//          of mbar when the unit-major first pass runs (residual on the MFMA path only)
 // followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN], and on the
 // MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC], columns
 // ordered within each 32-wide head as perm32 below.
@@ -52,10 +54,10 @@ constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score
 constexpr int PART_TILE = 64;       // positions per first-pass partial of the ring passes
 
 struct ScoreSizes {
-  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf;
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp;
   int64_t lse_pairs;   // units * R * 2: the (max, 1/Z) pairs at the start of lse
   __host__ __device__ int64_t total() const {
-    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf;
+    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf + mbp;
   }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
@@ -70,6 +72,7 @@ struct ScoreSizes {
   __host__ __device__ int64_t off_fold() const { return off_misc() + misc; }
   __host__ __device__ int64_t off_qlist() const { return off_fold() + fold; }
   __host__ __device__ int64_t off_kvf() const { return off_qlist() + qlist; }
+  __host__ __device__ int64_t off_mbp() const { return off_kvf() + kvf; }
 };
 
 // Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0,
@@ -104,6 +107,7 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   z.fold = resid && mfma ? align64f(fold_floats(D)) : 0;
   z.qlist = resid ? align64f(s.nq) : 0;
   z.kvf = resid && mfma ? align64f(KVF_BF16 / 2) : 0;
+  z.mbp = resid && mfma ? align64f(int64_t(units / 2) * D) : 0;
   return z;
 }
 
@@ -210,6 +214,7 @@ struct ScoreArgs {
   float *ws_shared;
   int maxN, maxR, maxNq;
   bool mfma;           // MFMA score passes (D = 128 and every R a multiple of 16)
+  bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
 };
 

@@ -89,12 +89,13 @@ __global__ void __launch_bounds__(256) k_mbar_part(const ikv_session *__restrict
   }
 }
 
-// Per session: mbar (from the partial sums) and the list of live query positions.
+// Per session: mbar (from the partial sums: MBAR_PARTS row ranges, or with `pairs`
+// one per head pair) and the list of live query positions.
 template <int D>
 __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict__ sess,
                                                    const int32_t *__restrict__ slot_maps,
                                                    const int32_t *__restrict__ qpos, int dead, float *__restrict__ ws,
-                                                   int L, int Hkv, bool mfma) {
+                                                   int L, int Hkv, bool mfma, bool pairs) {
   const int b = blockIdx.x;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
@@ -105,10 +106,30 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
   float *mbar = misc + int64_t(MBAR_PARTS) * D;
   int *qlist = reinterpret_cast<int *>(base + z.off_qlist());
   const int t = threadIdx.x;
-  if (t < D) {
+  {
+    // 256 / D threads per channel, eight partials in flight each, merged in a fixed order
+    constexpr int TPC = 256 / D;
+    __shared__ float red[TPC][D];
+    const float *parts = pairs ? base + z.off_mbp() : misc;
+    const int np = pairs ? units / 2 : MBAR_PARTS;
+    const int c = t % D, grp = t / D;
     float a = 0.f;
-    for (int p = 0; p < MBAR_PARTS; ++p) a += misc[int64_t(p) * D + t];
-    mbar[t] = a / float(int64_t(units) * s.R);
+    for (int p0 = grp; p0 < np; p0 += 8 * TPC) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = parts[int64_t(min(p0 + q * TPC, np - 1)) * D + c];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (p0 + q * TPC < np) a += v[q];
+    }
+    red[grp][c] = a;
+    __syncthreads();
+    if (t < D) {
+      float tot = 0.f;
+#pragma unroll
+      for (int k = 0; k < TPC; ++k) tot += red[k][t];
+      mbar[t] = tot / float(int64_t(units) * s.R);
+    }
   }
   if (t < WAVE) {   // live query positions in order: one wave, ranked by ballot
     int n = 0;
@@ -452,7 +473,8 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
   }
   {
     KTimer kt_("k_res_setup<D>", st);
-    k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma);
+    k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma,
+                                        a.stats);
   }
   if (a.maxNq > 0 || a.mfma_resid)
     {

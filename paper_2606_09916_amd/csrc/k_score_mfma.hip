@@ -658,7 +658,10 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 // 32 (w & 1) .. + 31 as two 16-row MFMA blocks; per row it keeps an online (max, sum
 // of exp2) over the chunk's candidates and writes one partial per (chunk, unit, row).
 // Non-candidates enter the accumulators as -inf before the MFMAs, so the epilogue
-// needs no mask.
+// needs no mask. The memory rows are read as float32 and split in registers; the
+// workgroups of chunk 0 also store the split rows of their units for the second pass
+// and, with the residual head on, the column sums of their rows (a partial of mbar).
+// For a session at or under its budget the pass only fills the scores with -inf.
 constexpr int ST_THREADS = 256;
 constexpr int ST_TILE = 32;                      // positions per stage
 constexpr int ST_STAGES = 4;
@@ -677,18 +680,22 @@ __device__ __forceinline__ void dma16s(const void *sbase, uint32_t voff, uint32_
 __global__ void __launch_bounds__(ST_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
               const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-              bool resid, int CH) {
+              const float *__restrict__ M, float *__restrict__ scores, bool resid, int CH) {
   __shared__ __align__(1024) uint16_t ring[ST_STAGES * ST_STAGE];
   __shared__ uint32_t koff[ST_CHMAX];            // byte offset of each position's key rows in the layer
   __shared__ __align__(16) float bias[ST_CHMAX];  // 0 for a candidate, -inf otherwise
 
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
-  if (s.N <= s.C) return;
   const int HP = L * Hkv / 2;
   const int hp = int(blockIdx.x % unsigned(HP)), chunk = int(blockIdx.x / unsigned(HP));
   const int c0 = chunk * CH;
   if (c0 >= s.N) return;
+  if (s.N <= s.C) {                              // the gate: nothing is scored
+    if (hp == 0)
+      for (int j = c0 + int(threadIdx.x); j < min(s.N, c0 + CH); j += ST_THREADS) scores[s.slot_off + j] = -INFINITY;
+    return;
+  }
   const int npos = min(CH, s.N - c0);
   const int T = int(cdiv(npos, ST_TILE));
   const int l = hp / (Hkv / 2), h0 = 2 * (hp - l * (Hkv / 2));
@@ -700,7 +707,7 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   const int u = l * Hkv + h0 + hh;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
-  const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
+  uint16_t *msplit = reinterpret_cast<uint16_t *>(base);
   float *part = base + z.off_part();
   const int32_t *S = slot_maps + s.slot_off;
   const uint32_t slot_bytes = uint32_t(Hkv) * MD * 2;
@@ -709,19 +716,51 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   int32_t sv[ST_CHMAX / ST_THREADS];
 #pragma unroll
   for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) sv[k] = S[c0 + min(t + k * ST_THREADS, npos - 1)];
-  // memory rows of this wave, B-operand fragments: lane (g, r16) holds row r0 + 16 rb + r16
-  // (the last row stands in for rows past R, whose results are never stored),
-  // channels (4 ks + g) * 8 .. + 8, hi then lo
+  // memory rows of this wave as B-operand fragments: lane (g, r16) holds row r0 + 16 rb + r16
+  // (the last row stands in for rows past R, whose results are never stored), channels
+  // (4 ks + g) * 8 .. + 8 of M * log2(e) / sqrt(D), split into bf16 hi + lo (both rounded
+  // to nearest even)
   bf16x8 mh[2][4], ml[2][4];
+  {
+    const float mscale = LOG2E / sqrtf(float(MD));
+    float4 mv[2][4][2];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const int row = min(r0 + 16 * rb + r16, R - 1);
-    const uint16_t *mp = msplit + (int64_t(u) * R + row) * 256 + g * 64;
+    for (int rb = 0; rb < 2; ++rb) {
+      const int row = min(r0 + 16 * rb + r16, R - 1);
+      const float *mp = M + s.mem_off + (int64_t(u) * R + row) * MD + g * 8;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      mh[rb][ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16);
-      ml[rb][ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16 + 8);
+      for (int ks = 0; ks < 4; ++ks) {
+        mv[rb][ks][0] = *reinterpret_cast<const float4 *>(mp + ks * 32);
+        mv[rb][ks][1] = *reinterpret_cast<const float4 *>(mp + ks * 32 + 4);
+      }
     }
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const float x[8] = {mv[rb][ks][0].x, mv[rb][ks][0].y, mv[rb][ks][0].z, mv[rb][ks][0].w,
+                            mv[rb][ks][1].x, mv[rb][ks][1].y, mv[rb][ks][1].z, mv[rb][ks][1].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = x[e] * mscale;
+          mh[rb][ks][e] = __bf16(v);
+          ml[rb][ks][e] = __bf16(v - float(mh[rb][ks][e]));
+        }
+      }
+    // chunk 0 keeps the split rows for the second pass, in the layout of k_msplit
+    if (chunk == 0)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int row = r0 + 16 * rb + r16;
+        if (row < R) {
+          uint16_t *dp = msplit + (int64_t(u) * R + row) * 256;
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16) = mh[rb][ks];
+            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16 + 8) = ml[rb][ks];
+          }
+        }
+      }
   }
 #pragma unroll
   for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) {
@@ -809,6 +848,19 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
     __syncthreads();
     if (tt + ST_STAGES - 1 < T) issue(tt + ST_STAGES - 1);
     compute(tt);
+  }
+
+  // chunk 0 with the residual head: column sums of the head pair's 2 R memory rows
+  if (resid && chunk == 0) {
+    float *red = reinterpret_cast<float *>(ring);  // the ring is free: every wave is past its last tile
+    __syncthreads();
+    const int c = t & (MD - 1), half = t >> 7;
+    const float *mp = M + s.mem_off + int64_t(l * Hkv + h0) * R * MD + c;
+    float a = 0.f;
+    for (int r = half; r < 2 * R; r += 2) a += mp[int64_t(r) * MD];
+    red[t] = a;
+    __syncthreads();
+    if (t < MD) base[z.off_mbp() + int64_t(hp) * MD + t] = red[t] + red[MD + t];
   }
 
   // merge the four lane groups of each row and store the chunk's partial
@@ -907,19 +959,19 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   const bool resid = (a.flags & IKV_RESIDUAL) != 0;
   const unsigned tiles = unsigned(cdiv(a.maxN, MFMA_TILE));
   const uint16_t *kp = static_cast<const uint16_t *>(p.k_pool);
-  {
-    KTimer kt_("k_msplit", st);
-    k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, a.scores, p.L, p.Hkv, resid);
-  }
   const bool ring = a.maxR <= 64;
-  // the unit-major first pass addresses a layer's keys with 32-bit offsets
-  const bool stats = ring && p.Hkv % 2 == 0 && p.num_slots * p.Hkv * MD * 2 <= int64_t(UINT32_MAX);
+  const bool stats = a.stats;                      // the unit-major pass splits the memory rows itself
+  if (!stats)
+    {
+      KTimer kt_("k_msplit", st);
+      k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, a.scores, p.L, p.Hkv, resid);
+    }
   const int chunk = stats ? stats_chunk(a.maxN, units / 2) : 0;
   if (stats)
     {
       KTimer kt_("k_score_stats", st);
       k_score_stats<<<dim3(unsigned(units / 2 * cdiv(a.maxN, chunk)), a.B), ST_THREADS, 0, st>>>(
-          kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, resid, chunk);
+          kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, a.M, a.scores, resid, chunk);
     }
   else if (ring)
     {
