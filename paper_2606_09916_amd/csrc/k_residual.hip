@@ -8,6 +8,7 @@
 #include <math.h>
 
 #include "ikv_internal.hpp"
+#include "res_setup.hpp"
 
 namespace ikv {
 
@@ -89,63 +90,13 @@ __global__ void __launch_bounds__(256) k_mbar_part(const ikv_session *__restrict
   }
 }
 
-// Per session: mbar (from the partial sums: MBAR_PARTS row ranges, or with `pairs`
-// one per head pair) and the list of live query positions.
+// Per session: mbar and the live query positions (res_setup_body), one workgroup each.
 template <int D>
 __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict__ sess,
                                                    const int32_t *__restrict__ slot_maps,
                                                    const int32_t *__restrict__ qpos, int dead, float *__restrict__ ws,
                                                    int L, int Hkv, bool mfma, bool pairs) {
-  const int b = blockIdx.x;
-  const ikv_session s = sess[b];
-  if (s.N <= s.C) return;
-  const int units = L * Hkv;
-  const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
-  float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
-  float *misc = base + z.off_misc();
-  float *mbar = misc + int64_t(MBAR_PARTS) * D;
-  int *qlist = reinterpret_cast<int *>(base + z.off_qlist());
-  const int t = threadIdx.x;
-  {
-    // 256 / D threads per channel, eight partials in flight each, merged in a fixed order
-    constexpr int TPC = 256 / D;
-    __shared__ float red[TPC][D];
-    const float *parts = pairs ? base + z.off_mbp() : misc;
-    const int np = pairs ? units / 2 : MBAR_PARTS;
-    const int c = t % D, grp = t / D;
-    float a = 0.f;
-    for (int p0 = grp; p0 < np; p0 += 8 * TPC) {
-      float v[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = parts[int64_t(min(p0 + q * TPC, np - 1)) * D + c];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (p0 + q * TPC < np) a += v[q];
-    }
-    red[grp][c] = a;
-    __syncthreads();
-    if (t < D) {
-      float tot = 0.f;
-#pragma unroll
-      for (int k = 0; k < TPC; ++k) tot += red[k][t];
-      mbar[t] = tot / float(int64_t(units) * s.R);
-    }
-  }
-  if (t < WAVE) {   // live query positions in order: one wave, ranked by ballot
-    int n = 0;
-    const int32_t *S = slot_maps + s.slot_off;
-    const int32_t *qp = qpos + s.qpos_off;
-    for (int i0 = 0; i0 < s.nq; i0 += WAVE) {
-      const int i = i0 + t;
-      int j = -1;
-      if (i < s.nq) j = qp[i];
-      const bool ok = j >= 0 && j < s.N && S[j] != dead;
-      const uint64_t bal = __ballot(ok);
-      if (ok) qlist[n + __popcll(bal & ((uint64_t(1) << t) - 1))] = j;
-      n += __popcll(bal);
-    }
-    if (t == 0) reinterpret_cast<int *>(mbar)[D] = n;
-  }
+  res_setup_body<D>(sess, int(blockIdx.x), slot_maps, qpos, dead, ws, L, Hkv, mfma, pairs);
 }
 
 // K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup.
@@ -156,8 +107,8 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
 //   V' [head][channel block nb][key step ks][hi|lo][lane 16 g + i][8]: channel
 //      32 head + 16 nb + i, keys 32 ks + perm32(g, e) (the A operand of the context).
 template <int D>
-__global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                                float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
+__device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restrict__ sess, const float *__restrict__ blob,
+                                            float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
@@ -170,7 +121,7 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
   float *vp = base + z.off_vp();
   const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
   const int *qlist = reinterpret_cast<const int *>(base + z.off_qlist());
-  const int i0 = blockIdx.x * 4;
+  const int i0 = bx * 4;
   if (i0 >= n && !frag) return;
   __shared__ float kq[4][D];
   const int t = threadIdx.x;
@@ -224,6 +175,12 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
   }
 }
 
+template <int D>
+__global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
+                                                float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
+  res_kv_body<D>(int(blockIdx.x), sess, blob, ws, L, Hkv, mfma, frag);
+}
+
 // Folded first layer of one session (exact in real arithmetic):
 //   W_Q phi + b_Q  = (W_Q^k + W_Q^km diag(mbar)) kbar + (W_Q^m mbar + b_Q) + w_Q^r rule
 //   W_1 [phi; c] + b_1 = (W_1^k + W_1^km diag(mbar)) kbar + (W_1^m mbar + b_1) + w_1^r rule + W_1^c c
@@ -231,8 +188,8 @@ __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ 
 // as bf16 hi [HC+HIDDEN][D] then lo, then q0 [HC] and h0 [HIDDEN] in float32, then
 // the rule column w_Q^r [HC] and w_1^r [HIDDEN].
 template <int D>
-__global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                                  float *__restrict__ ws, float *__restrict__ shared, int L, int Hkv) {
+__device__ __forceinline__ void res_fold_body(int bx, const ikv_session *__restrict__ sess, const float *__restrict__ blob,
+                                              float *__restrict__ ws, float *__restrict__ shared, int L, int Hkv) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   uint16_t *w1c = reinterpret_cast<uint16_t *>(shared + align64f(int64_t(3 * D + 1) * HC) +
@@ -248,7 +205,7 @@ __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict_
   uint16_t *hi = reinterpret_cast<uint16_t *>(fold);
   uint16_t *lo = hi + int64_t(HC + HIDDEN) * D;
   float *q0 = fold + int64_t(HC + HIDDEN) * D;
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t i = int64_t(bx) * 256 + threadIdx.x;
   const int64_t nw = int64_t(HC + HIDDEN) * D;
   if (s.N <= s.C && i < nw + 2 * (HC + HIDDEN)) return;   // skipped session: only the shared part
   if (i < nw) {
@@ -283,6 +240,17 @@ __global__ void __launch_bounds__(256) k_res_fold(const ikv_session *__restrict_
     w1c[at] = h;
     w1c[nc + at] = float_to_bf16_bits(v - bf16_bits_to_float(h));
   }
+}
+
+// The fold (res_fold_body, first nfold workgroups) and, after it in the same launch,
+// K' and V' of the live query rows as fragments (res_kv_body, RES_KEYS / 4 workgroups):
+// both need only the set-up and the mean key rows.
+template <int D>
+__global__ void __launch_bounds__(256) k_res_fold_kv(const ikv_session *__restrict__ sess,
+                                                     const float *__restrict__ blob, float *__restrict__ ws,
+                                                     float *__restrict__ shared, int L, int Hkv, int nfold) {
+  if (int(blockIdx.x) < nfold) res_fold_body<D>(int(blockIdx.x), sess, blob, ws, shared, L, Hkv);
+  else res_kv_body<D>(int(blockIdx.x) - nfold, sess, blob, ws, L, Hkv, true, true);
 }
 
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
@@ -471,22 +439,24 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
     KTimer kt_("k_mbar_part<D>", st);
     k_mbar_part<D><<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, p.L, p.Hkv, a.mfma);
   }
-  {
-    KTimer kt_("k_res_setup<D>", st);
-    k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma,
-                                        a.stats);
-  }
-  if (a.maxNq > 0 || a.mfma_resid)
+  if (!a.mfma)   // on the matrix-core path the row-statistics launch did the set-up
+    {
+      KTimer kt_("k_res_setup<D>", st);
+      k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma,
+                                          a.stats);
+    }
+  if (a.maxNq > 0 && !a.mfma_resid)
     {
       KTimer kt_("k_res_kv<D>", st);
-      k_res_kv<D><<<dim3(unsigned(a.mfma_resid ? RES_KEYS / 4 : cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(
-          a.sess_dev, a.residual, a.ws, p.L, p.Hkv, a.mfma, a.mfma_resid);
+      k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
+                                                                         a.mfma, false);
     }
   if (a.mfma_resid) {
     {
-      KTimer kt_("k_res_fold<D>", st);
-      k_res_fold<D><<<dim3(unsigned(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC, 256)),
-                           a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, a.ws_shared, p.L, p.Hkv);
+      const int nfold = int(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC, 256));
+      KTimer kt_("k_res_fold_kv<D>", st);
+      k_res_fold_kv<D><<<dim3(unsigned(nfold + RES_KEYS / 4), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws,
+                                                                                 a.ws_shared, p.L, p.Hkv, nfold);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

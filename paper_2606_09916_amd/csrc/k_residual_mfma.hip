@@ -1,7 +1,7 @@
 // Residual head of Eq. 4 (features Eq. 5, cross-attention Eq. 6) on the matrix cores,
 // for D = 128 and at most 64 live query positions per session.
 //
-// With mbar folded into the first-layer weights (k_res_fold), the head of one
+// With mbar folded into the first-layer weights (k_res_fold_kv), the head of one
 // candidate is a chain of small products on v_mfma_f32_16x16x32_bf16. Each wave owns
 // 16 candidates and keeps its activations in registers: the products run transposed
 // (weights as the A operand, candidates as the columns), so that the accumulator of

@@ -22,6 +22,7 @@
 #include <math.h>
 
 #include "ikv_internal.hpp"
+#include "res_setup.hpp"
 
 namespace ikv {
 
@@ -892,11 +893,18 @@ inline int stats_chunk(int maxN, int head_pairs) {
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
 // A workgroup takes 64 consecutive rows; its eight waves split the tiles (lane =
 // row, so each load instruction reads 512 contiguous bytes), fold them online into
-// (max, sum) and merge through LDS in a fixed order.
+// (max, sum) and merge through LDS in a fixed order. With the residual head on, the
+// last workgroup of each session does the head's set-up instead (res_setup_body),
+// which needs only the first pass.
 __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
-                                                  int Hkv, bool resid, int ptile) {
+                                                  int Hkv, bool resid, int ptile, const int32_t *__restrict__ slot_maps,
+                                                  const int32_t *__restrict__ qpos, int dead, bool pairs) {
   __shared__ float sm[8][64], sz[8][64];
   const int b = blockIdx.y;
+  if (resid && blockIdx.x == gridDim.x - 1) {
+    res_setup_body<MD>(sess, b, slot_maps, qpos, dead, ws, L, Hkv, true, pairs);
+    return;
+  }
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   const int units = L * Hkv;
@@ -987,8 +995,9 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     }
   {
     KTimer kt_("k_lse_mfma", st);
-    k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv,
-                                                                                        resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE);
+    k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64) + (resid ? 1 : 0)), a.B), 512, 0, st>>>(
+        a.sess_dev, a.ws, p.L, p.Hkv, resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE, a.slot_maps, a.qpos,
+        p.dead_slot, a.stats);
   }
   if (ring && resid)
     {
