@@ -522,34 +522,22 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     for (int c = 0; c < 8; ++c) epilogue_step(a, c);
   };
 
-  auto compute = [&](int u) {
+  auto compute = [&](int u, float seed) {     // seed: this lane's row, second pass only
     const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
     if (act) {
       const uint16_t *mr = lds + KSTAGES * STAGE + (u & 1) * MSTAGE + row * 256;
+      // fragments of k-step ks: memory row hi/lo and the four key blocks; k-step 0 now,
+      // each later one two chunks before its MFMAs, so that the eight waves' LDS reads
+      // spread over the unit instead of all landing at its start
       bf16x8 mh[4], ml[4], ka[4][4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      auto read_ks = [&](int ks) {
         mh[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2) ^ r16) * 8));
         ml[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2 + 1) ^ r16) * 8));
-      }
 #pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        const uint16_t *kr = kl + (p0 + blk * 16 + r16) * MD;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kr + (((4 * ks + g) ^ r16) * 8));
-      }
-      float seed = 0.f;
-      if (PASS_B) {
-        const int64_t o = int64_t(__builtin_amdgcn_readfirstlane(u * R + rs * 16));
-        const cfloat *q = (cfloat *)(nl2 + o);
-        float sv[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          sv[i] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, q[i])));
-        seed = sv[0];
-#pragma unroll
-        for (int i = 1; i < 16; ++i) seed = (r16 == i) ? sv[i] : seed;
-      }
+        for (int blk = 0; blk < 4; ++blk)
+          ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kl + (p0 + blk * 16 + r16) * MD + (((4 * ks + g) ^ r16) * 8));
+      };
+      read_ks(0);
       f32x4 acc[4];
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) acc[blk] = f32x4{seed, seed, seed, seed};
@@ -558,6 +546,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const int ks = c >> 1;
+        if ((c & 1) == 0 && ks + 1 < 4) read_ks(ks + 1);
 #pragma unroll
         for (int blk = 0; blk < 4; ++blk)
           acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[ks] : mh[ks], acc[blk], 0, 0, 0);
@@ -597,13 +586,28 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   issue_m(0);
   if (units > 1) issue_k(1);
   for (int u = 0; u < units; ++u) {
+    // second pass: -(max + log2 Z) of this wave's 16 memory rows, by scalar loads issued
+    // before the unit's waits, which they outlast (tracked by lgkmcnt, not vmcnt)
+    float sv[16];
+    if (PASS_B && act) {
+      const cfloat *q = (cfloat *)(nl2 + int64_t(__builtin_amdgcn_readfirstlane(u * R + rs * 16)));
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        sv[i] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, q[i])));
+    }
     if (u + 1 < units) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (!PASS_B && u >= 2) store_part(u - 2);      // finished during unit u - 1
     if (u + 1 < units) issue_m(u + 1);
     if (u + 2 < units) issue_k(u + 2);
-    compute(u);
+    float seed = 0.f;
+    if (PASS_B && act) {
+      seed = sv[0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) seed = (r16 == i) ? sv[i] : seed;
+    }
+    compute(u, seed);
   }
   if (!PASS_B && units >= 2) store_part(units - 2);
   if (act) epilogue(accp);                         // the last unit
