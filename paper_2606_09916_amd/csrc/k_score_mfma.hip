@@ -426,25 +426,40 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   }
   // every compiler-issued load of the set-up is complete before the first DMA
   asm volatile("" ::"v"(cmask), "v"(src[0]), "v"(src[1]), "v"(src[2]), "v"(src[3]));
-  auto issue_k = [&](int u) {
+  auto issue_k_piece = [&](int u, int k) {
     const int l = u / Hkv, h = u - l * Hkv;
     const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
     const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
+    dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((4 * w + k) * 4) * MD * 2)));
+  };
+  auto issue_k = [&](int u) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((4 * w + k) * 4) * MD * 2)));
+    for (int k = 0; k < 4; ++k) issue_k_piece(u, k);
   };
   // memory rows of unit u: R rows of 512 B, 32 chunks of 16 B per row, chunk slot
   // s of row r holds chunk s ^ (r & 15); wave w issues R/16 of the R/2 1-KB pieces
   const int nm = R >> 4;
-  auto issue_m = [&](int u) {
+  auto issue_m_piece = [&](int u, int k) {
     const uint16_t *m0 = msplit + int64_t(u) * R * 256;
     const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
-    for (int k = 0; k < nm; ++k) {
-      const int piece = w * nm + k;
-      const int r = piece * 2 + (lane >> 5);
-      const int sl = lane & 31;
-      dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+    const int piece = w * nm + k;
+    const int r = piece * 2 + (lane >> 5);
+    const int sl = lane & 31;
+    dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+  };
+  // The loads of the next stages during unit u, spread over its eight MFMA chunks: the
+  // memory-row pieces of unit u + 1 in chunks 0-1, the key pieces of unit u + 2 in
+  // chunks 2-5. The address unit accepts one 1-KB instruction every 16 clocks or so,
+  // so eight waves issuing all of theirs at once would hold every wave for about a
+  // thousand clocks before its MFMAs. The order (memory rows first) keeps the count
+  // the top of each unit waits for.
+  auto dma_chunk = [&](int u, int c) {
+    if (c < 2) {
+#pragma unroll
+      for (int k = 2 * c; k < 2 * c + 2; ++k)
+        if (k < nm && u + 1 < units) issue_m_piece(u + 1, k);
+    } else if (c < 6) {
+      if (u + 2 < units) issue_k_piece(u + 2, c - 2);
     }
   };
 
@@ -537,6 +552,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
         for (int blk = 0; blk < 4; ++blk)
           ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kl + (p0 + blk * 16 + r16) * MD + (((4 * ks + g) ^ r16) * 8));
       };
+      dma_chunk(u, 0);
       read_ks(0);
       f32x4 acc[4];
 #pragma unroll
@@ -546,6 +562,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const int ks = c >> 1;
+        if (c > 0) dma_chunk(u, c);
         if ((c & 1) == 0 && ks + 1 < 4) read_ks(ks + 1);
 #pragma unroll
         for (int blk = 0; blk < 4; ++blk)
@@ -564,6 +581,9 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) accp[blk] = acc[blk];
     }
+    if (!act)
+#pragma unroll
+      for (int c = 0; c < 6; ++c) dma_chunk(u, c);
     if (KBAR && !act) {                            // slices without memory rows still cover their channels
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) {
@@ -580,10 +600,10 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   };
 
   // Issue order per wave: K(0), M(0), K(1), then per unit u: [first pass: store of
-  // unit u-2], M(u+1), K(u+2). At the top of unit u only K(u+1) (4 loads) may still
-  // be younger than M(u) and K(u).
+  // unit u-2], M(u+1), K(u+2), the last two spread over the unit's MFMA chunks. At
+  // the top of unit u only K(u+1) (4 loads) may still be younger than M(u) and K(u).
   issue_k(0);
-  issue_m(0);
+  for (int k = 0; k < nm; ++k) issue_m_piece(0, k);
   if (units > 1) issue_k(1);
   for (int u = 0; u < units; ++u) {
     // second pass: -(max + log2 Z) of this wave's 16 memory rows, by scalar loads issued
@@ -599,8 +619,6 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (!PASS_B && u >= 2) store_part(u - 2);      // finished during unit u - 1
-    if (u + 1 < units) issue_m(u + 1);
-    if (u + 2 < units) issue_k(u + 2);
     float seed = 0.f;
     if (PASS_B && act) {
       seed = sv[0];
@@ -651,6 +669,230 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
           kbar[int64_t(j) * MD + 16] = kacc[blk][1][i] * inv;
         }
       }
+  }
+}
+
+// ------------------------------------------------------------------ second pass, warp-specialised (R <= 64)
+// The second pass as producer and consumer waves. A wave that issues a load into LDS can
+// stall until the CU's address unit takes it, and the ring's 64 KB per unit keep that unit
+// busy most of the time; when the waves that issue the loads are also the ones running the
+// MFMAs, those stalls leave the matrix cores idle. Here waves 4-7 (producers) issue every
+// load of the ring and sum the mean key row on the VALU; waves 0-3 (consumers, one per
+// SIMD) only read LDS, run the logit MFMAs and fold exp2 of the logits into the rule score.
+// Consumer c takes memory rows 32 (c & 1) .. + 31 against positions 64 (c >> 1) .. + 63,
+// which reads 128 KB of LDS per unit instead of the 192 KB of sixteen-row waves.
+constexpr int WS_THREADS = 512;
+
+template <bool KBAR>
+__global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
+           const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+           float *__restrict__ scores, bool resid) {
+  __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
+
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int tile = blockIdx.x;
+  const int j0 = tile * MFMA_TILE;
+  if (j0 >= s.N) return;
+  const int units = L * Hkv;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int g = lane >> 4, r16 = lane & 15;
+  const int R = s.R;
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  const int32_t *S = slot_maps + s.slot_off;
+  const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+
+  if (w >= 4) {
+    // ---------------- producers: the ring's loads, and the mean key row
+    const int pw = w - 4;
+    const int64_t slot_stride = int64_t(Hkv) * MD;
+    // key instruction k of producer pw loads positions (8 pw + k) * 4 + lane / 16, 16-byte
+    // slot lane % 16 of the row, which holds chunk (lane % 16) ^ (position % 16)
+    const uint16_t *src[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int tok = (8 * pw + k) * 4 + (lane >> 4);
+      const int j = j0 + tok;
+      const int slot = j < s.N ? S[j] : dead;      // past the end: any valid row
+      src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
+    }
+    asm volatile("" ::"v"(src[0]), "v"(src[7]));   // the slot loads are complete before the first DMA
+    auto issue_k = [&](int u) {
+      const int l = u / Hkv, h = u - l * Hkv;
+      const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
+      const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * pw + k) * 4) * MD * 2)));
+    };
+    // memory rows of unit u: R rows of 512 B, chunk slot c of row r holds chunk c ^ (r & 15);
+    // producer pw issues R/8 of the R/2 1-KB pieces (two rows each)
+    const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
+    const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
+    const int npc = R >> 3;
+    auto issue_m = [&](int u) {
+      const uint16_t *m0 = msplit + int64_t(u) * R * 256;
+      const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
+      for (int k = 0; k < npc; ++k) {
+        const int piece = pw * npc + k;
+        const int r = piece * 2 + (lane >> 5);
+        const int sl = lane & 31;
+        dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+      }
+    };
+    // mean key row: lane (position 32 pw + lane % 32, channels 64 (lane / 32) .. + 63)
+    const int pp = 32 * pw + (lane & 31), hc = lane >> 5;
+    float kb[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) kb[i] = 0.f;
+
+    // Issue order: K(0), M(0), K(1), then per unit u: M(u+1), K(u+2). At the top of unit u
+    // only K(u+1) (8 loads) may still be younger than M(u) and K(u).
+    issue_k(0);
+    issue_m(0);
+    if (units > 1) issue_k(1);
+    for (int u = 0; u < units; ++u) {
+      if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (u + 1 < units) issue_m(u + 1);
+      if (u + 2 < units) issue_k(u + 2);
+      if (KBAR) {
+        const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((8 * hc + c) ^ (pp & 15)) * 8));
+          const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {              // bf16 -> float is exact: the high half of the word
+            kb[8 * c + 2 * e] += __uint_as_float(q[e] << 16);
+            kb[8 * c + 2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
+          }
+        }
+      }
+    }
+    __syncthreads();                                 // matches the consumers' reduction barrier
+    __syncthreads();
+    if (KBAR) {
+      const int j = j0 + pp;
+      if (j < s.N) {
+        const float inv = 1.0f / float(units);
+        float4 *kbar = reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(j) * MD + 64 * hc);
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          kbar[q] = make_float4(kb[4 * q] * inv, kb[4 * q + 1] * inv, kb[4 * q + 2] * inv, kb[4 * q + 3] * inv);
+      }
+    }
+    return;
+  }
+
+  // ---------------- consumers: logits on the matrix cores, exp2 folded into the rule score
+  const int rh = w & 1, p0 = (w >> 1) * 64;         // memory-row half, first position of the half
+  const int nsl = R >> 4;
+  const bool act[2] = {2 * rh < nsl, 2 * rh + 1 < nsl};
+  const float *nl2 = base + z.off_nl2();
+  // seeds -(max + log2 Z) of this lane's two rows (-inf for rows past R: those slices
+  // multiply zero fragments, so exp2 of their accumulators is 0)
+  auto load_seeds = [&](int u, float &s0, float &s1) {
+    const int row0 = 32 * rh + r16, row1 = row0 + 16;
+    s0 = row0 < R ? nl2[int64_t(u) * R + row0] : -INFINITY;
+    s1 = row1 < R ? nl2[int64_t(u) * R + row1] : -INFINITY;
+  };
+  float racc[4][4];
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) racc[blk][i] = 0.f;
+  f32x4 accp[2][4];
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) accp[sl][blk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  // step c (0-7) of the previous unit's epilogue: exp2 of four of its 32 logits per lane
+  auto epilogue_step = [&](int c) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int e = 4 * c + k, sl = e >> 4, blk = (e >> 2) & 3, i = e & 3;
+      racc[blk][i] += ex2(accp[sl][blk][i]);
+    }
+  };
+  float sd0, sd1;
+  load_seeds(0, sd0, sd1);
+  for (int u = 0; u < units; ++u) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this unit's seeds
+    const float seed0 = sd0, seed1 = sd1;
+    __syncthreads();
+    if (u + 1 < units) load_seeds(u + 1, sd0, sd1);
+    const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
+    const uint16_t *mb = lds + KSTAGES * STAGE + (u & 1) * MSTAGE;
+    const uint16_t *mr0 = mb + (32 * rh + r16) * 256, *mr1 = mr0 + 16 * 256;
+    // fragments of k-step ks: memory rows (hi, lo) of both slices, the four key blocks
+    bf16x8 mh[2][4], ml[2][4], ka[4][4];
+    auto read_ks = [&](int ks) {
+      const int ch = ((g * 8 + ks * 2) ^ r16) * 8, cl = ((g * 8 + ks * 2 + 1) ^ r16) * 8;
+      mh[0][ks] = *reinterpret_cast<const bf16x8 *>(mr0 + ch);
+      ml[0][ks] = *reinterpret_cast<const bf16x8 *>(mr0 + cl);
+      mh[1][ks] = *reinterpret_cast<const bf16x8 *>(mr1 + ch);
+      ml[1][ks] = *reinterpret_cast<const bf16x8 *>(mr1 + cl);
+      if (!act[0]) mh[0][ks] = ml[0][ks] = bf16x8{};
+      if (!act[1]) mh[1][ks] = ml[1][ks] = bf16x8{};
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+        ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kl + (p0 + blk * 16 + r16) * MD + (((4 * ks + g) ^ r16) * 8));
+    };
+    read_ks(0);
+    f32x4 acc[2][4];
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      acc[0][blk] = f32x4{seed0, seed0, seed0, seed0};
+      acc[1][blk] = f32x4{seed1, seed1, seed1, seed1};
+    }
+    // chunk c: the eight MFMAs of k-step c/2 (hi, then lo) for both slices, then step c of
+    // the previous unit's epilogue; the fences keep the interleave
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int ks = c >> 1;
+      if ((c & 1) == 0 && ks + 1 < 4) read_ks(ks + 1);
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+          acc[sl][blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[sl][ks] : mh[sl][ks],
+                                                                 acc[sl][blk], 0, 0, 0);
+      epilogue_step(c);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) accp[sl][blk] = acc[sl][blk];
+  }
+#pragma unroll
+  for (int c = 0; c < 8; ++c) epilogue_step(c);      // the last unit
+  __syncthreads();                                   // the ring is free: reuse it for the reduction
+  float *red = reinterpret_cast<float *>(lds);       // [2][MFMA_TILE]
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = racc[blk][i];                        // position p0 + 16 blk + 4 g + i, row r16 of both slices
+      v += __shfl_xor(v, 1, WAVE);
+      v += __shfl_xor(v, 2, WAVE);
+      v += __shfl_xor(v, 4, WAVE);
+      v += __shfl_xor(v, 8, WAVE);
+      if (r16 == 0) red[rh * MFMA_TILE + p0 + blk * 16 + 4 * g + i] = v;
+    }
+  __syncthreads();
+  if (t < MFMA_TILE) {
+    const int j = j0 + t;
+    if (j < s.N) {
+      const bool c = S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+      scores[s.slot_off + j] = c ? red[t] + red[MFMA_TILE + t] : -INFINITY;
+    }
   }
 }
 
@@ -1005,15 +1247,15 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   }
   if (ring && resid)
     {
-      KTimer kt_("k_score_ring<true, true>", st);
-      k_score_ring<true, true><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                 a.slot_maps, a.ws, a.scores, resid);
+      KTimer kt_("k_score_ws<true>", st);
+      k_score_ws<true><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                a.slot_maps, a.ws, a.scores, resid);
     }
   else if (ring)
     {
-      KTimer kt_("k_score_ring<true, false>", st);
-      k_score_ring<true, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
-                                                                  a.sess_dev, a.slot_maps, a.ws, a.scores, resid);
+      KTimer kt_("k_score_ws<false>", st);
+      k_score_ws<false><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                                 a.slot_maps, a.ws, a.scores, resid);
     }
   else if (resid)
     {
