@@ -721,28 +721,31 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
     }
     asm volatile("" ::"v"(src[0]), "v"(src[7]));   // the slot loads are complete before the first DMA
-    auto issue_k = [&](int u) {
+    auto issue_k_piece = [&](int u, int k) {
       const int l = u / Hkv, h = u - l * Hkv;
       const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
       const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
+      dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * pw + k) * 4) * MD * 2)));
+    };
+    auto issue_k = [&](int u) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * pw + k) * 4) * MD * 2)));
+      for (int k = 0; k < 8; ++k) issue_k_piece(u, k);
     };
     // memory rows of unit u: R rows of 512 B, chunk slot c of row r holds chunk c ^ (r & 15);
     // producer pw issues R/8 of the R/2 1-KB pieces (two rows each)
     const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
     const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
     const int npc = R >> 3;
-    auto issue_m = [&](int u) {
+    auto issue_m_piece = [&](int u, int k) {
       const uint16_t *m0 = msplit + int64_t(u) * R * 256;
       const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
-      for (int k = 0; k < npc; ++k) {
-        const int piece = pw * npc + k;
-        const int r = piece * 2 + (lane >> 5);
-        const int sl = lane & 31;
-        dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
-      }
+      const int piece = pw * npc + k;
+      const int r = piece * 2 + (lane >> 5);
+      const int sl = lane & 31;
+      dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+    };
+    auto issue_m = [&](int u) {
+      for (int k = 0; k < npc; ++k) issue_m_piece(u, k);
     };
     // mean key row: lane (position 32 pw + lane % 32, channels 64 (lane / 32) .. + 63)
     const int pp = 32 * pw + (lane & 31), hc = lane >> 5;
@@ -751,7 +754,10 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
     for (int i = 0; i < 64; ++i) kb[i] = 0.f;
 
     // Issue order: K(0), M(0), K(1), then per unit u: M(u+1), K(u+2). At the top of unit u
-    // only K(u+1) (8 loads) may still be younger than M(u) and K(u).
+    // only K(u+1) (8 loads) may still be younger than M(u) and K(u). Within a unit the
+    // loads alternate with the mean-key-row steps (memory-row pieces in steps 0-3, two
+    // each, key pieces in steps 4-7), so that the VALU work fills the time a wave waits
+    // for the address unit to take its next load.
     issue_k(0);
     issue_m(0);
     if (units > 1) issue_k(1);
@@ -759,12 +765,18 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
-      if (u + 1 < units) issue_m(u + 1);
-      if (u + 2 < units) issue_k(u + 2);
-      if (KBAR) {
-        const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
+      const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
+      for (int c = 0; c < 8; ++c) {
+        if (c < 4) {
+#pragma unroll
+          for (int k = 2 * c; k < 2 * c + 2; ++k)
+            if (k < npc && u + 1 < units) issue_m_piece(u + 1, k);
+        } else if (u + 2 < units) {
+          issue_k_piece(u + 2, 2 * (c - 4));
+          issue_k_piece(u + 2, 2 * (c - 4) + 1);
+        }
+        if (KBAR) {
           const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((8 * hc + c) ^ (pp & 15)) * 8));
           const uint32_t q[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -773,6 +785,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
             kb[8 * c + 2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     __syncthreads();                                 // matches the consumers' reduction barrier
@@ -793,15 +806,8 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   // ---------------- consumers: logits on the matrix cores, exp2 folded into the rule score
   const int rh = w & 1, p0 = (w >> 1) * 64;         // memory-row half, first position of the half
   const int nsl = R >> 4;
-  const bool act[2] = {2 * rh < nsl, 2 * rh + 1 < nsl};
+  const bool act0 = 2 * rh < nsl, act1 = 2 * rh + 1 < nsl;   // slices of this wave within R
   const float *nl2 = base + z.off_nl2();
-  // seeds -(max + log2 Z) of this lane's two rows (-inf for rows past R: those slices
-  // multiply zero fragments, so exp2 of their accumulators is 0)
-  auto load_seeds = [&](int u, float &s0, float &s1) {
-    const int row0 = 32 * rh + r16, row1 = row0 + 16;
-    s0 = row0 < R ? nl2[int64_t(u) * R + row0] : -INFINITY;
-    s1 = row1 < R ? nl2[int64_t(u) * R + row1] : -INFINITY;
-  };
   float racc[4][4];
 #pragma unroll
   for (int blk = 0; blk < 4; ++blk)
@@ -820,13 +826,16 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       racc[blk][i] += ex2(accp[sl][blk][i]);
     }
   };
-  float sd0, sd1;
-  load_seeds(0, sd0, sd1);
-  for (int u = 0; u < units; ++u) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this unit's seeds
-    const float seed0 = sd0, seed1 = sd1;
+  // Seeds -(max + log2 Z) of the lane's two rows, loaded two units ahead at the end of
+  // a unit's MFMAs: issued right after the barrier, a load would queue behind the
+  // producers' ring loads at the address unit. Rows past R take -inf against zero
+  // fragments, so exp2 of their logits is 0.
+  const int row0 = 32 * rh + r16, row1 = row0 + 16;
+  auto seed_ld = [&](int u, int row) { return nl2[int64_t(u) * R + min(row, R - 1)]; };
+  // one unit: seeds s0, s1 as loaded (rows past R take -inf here)
+  auto unit_step = [&](int u, float s0, float s1) {
+    const float seed0 = row0 < R ? s0 : -INFINITY, seed1 = row1 < R ? s1 : -INFINITY;
     __syncthreads();
-    if (u + 1 < units) load_seeds(u + 1, sd0, sd1);
     const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
     const uint16_t *mb = lds + KSTAGES * STAGE + (u & 1) * MSTAGE;
     const uint16_t *mr0 = mb + (32 * rh + r16) * 256, *mr1 = mr0 + 16 * 256;
@@ -838,8 +847,8 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       ml[0][ks] = *reinterpret_cast<const bf16x8 *>(mr0 + cl);
       mh[1][ks] = *reinterpret_cast<const bf16x8 *>(mr1 + ch);
       ml[1][ks] = *reinterpret_cast<const bf16x8 *>(mr1 + cl);
-      if (!act[0]) mh[0][ks] = ml[0][ks] = bf16x8{};
-      if (!act[1]) mh[1][ks] = ml[1][ks] = bf16x8{};
+      if (!act0) mh[0][ks] = ml[0][ks] = bf16x8{};
+      if (!act1) mh[1][ks] = ml[1][ks] = bf16x8{};
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
         ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kl + (p0 + blk * 16 + r16) * MD + (((4 * ks + g) ^ r16) * 8));
@@ -870,6 +879,27 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
     for (int sl = 0; sl < 2; ++sl)
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) accp[sl][blk] = acc[sl][blk];
+  };
+  // Even and odd units keep their own seed registers (unrolled by two), so that no
+  // register that a load is still filling has to be copied.
+  float a0 = seed_ld(0, row0), a1 = seed_ld(0, row1), b0 = 0.f, b1 = 0.f;
+  if (units > 1) {
+    b0 = seed_ld(1, row0);
+    b1 = seed_ld(1, row1);
+  }
+  for (int u = 0; u < units; u += 2) {
+    unit_step(u, a0, a1);
+    if (u + 2 < units) {
+      a0 = seed_ld(u + 2, row0);
+      a1 = seed_ld(u + 2, row1);
+    }
+    if (u + 1 < units) {
+      unit_step(u + 1, b0, b1);
+      if (u + 3 < units) {
+        b0 = seed_ld(u + 3, row0);
+        b1 = seed_ld(u + 3, row1);
+      }
+    }
   }
 #pragma unroll
   for (int c = 0; c < 8; ++c) epilogue_step(c);      // the last unit
