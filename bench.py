@@ -32,8 +32,8 @@ CALIB_BYTES = 256 << 20        # the calibration copy (bytes read = bytes writte
 # scaled by what it reads for the calibration copy) on one workload, for the kernel
 # as built from the hashed sources; reported only while those sources are unchanged.
 MEASURED_TRAFFIC = {
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ring<true, true>"): (2509678055, "693cd3ee9ea02893"),
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2570847174, "693cd3ee9ea02893"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ws<true>"): (2509193672, "d289b7d9da93adb8"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2682181323, "d289b7d9da93adb8"),
 }
 TRAFFIC_SOURCES = ("paper_2606_09916_amd/csrc/k_score_mfma.hip", "paper_2606_09916_amd/csrc/ikv_internal.hpp")
 
@@ -227,9 +227,9 @@ def main() -> int:
     stats_parts = -(-s.N // 1024) * units * s.R * 8            # one (max, sum) per chunk and memory row
     algo = {
         "k_score_stats": key_bytes + mem_bytes + stats_parts,
-        "k_score_ring<false, false>": key_bytes + mem_bytes,
-        "k_score_ring<true, true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
-        "k_score_ring<true, false>": key_bytes + mem_bytes + s.N * 4,
+        "k_score_ring": key_bytes + mem_bytes,
+        "k_score_ws<true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
+        "k_score_ws<false>": key_bytes + mem_bytes + s.N * 4,
         "k_decode_split<T, D, G>": kv_live + sh.L * sh.Hq * sh.D * 2,
         "k_decode_mfma<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
         "k_qm_update<T, 128>": units * s.R * (s.qe - s.qs) * sh.D * 2 + 2 * mem_bytes,

@@ -180,7 +180,9 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
  *   workspace: ikv_workspace_bytes(IKV_CALL_SELECT) bytes (per-session histograms
  *   and one 4-byte key per position, and per session the counters and histograms of
  *   the multi-workgroup path). The call may be a cooperative launch (every workgroup
- *   resident at once); concurrent calls must not share a workspace.
+ *   resident at once); concurrent calls must not share a workspace. With the
+ *   environment variable IKV_NO_COOP=1 the call never launches cooperatively (for
+ *   tools that cannot follow such a launch); the result is the same.
  */
 ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev,
                              int32_t B, const int32_t *slot_maps, int32_t dead_slot,

@@ -51,7 +51,7 @@ __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int6
 // ordered within each 32-wide head as perm32 below.
 constexpr int MBAR_PARTS = 64;
 constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
-constexpr int PART_TILE = 64;       // positions per first-pass partial of the ring passes
+constexpr int PART_TILE = 64;       // positions per partial of the position-major first pass
 
 struct ScoreSizes {
   int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp;

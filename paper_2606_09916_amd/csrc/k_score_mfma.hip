@@ -353,28 +353,25 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
   }
 }
 
-// ------------------------------------------------------------------ ring pass (R <= 64)
+// ------------------------------------------------------------------ first pass, position-major (R <= 64, odd Hkv)
 // Keys and memory rows both stream by direct global->LDS loads: three 32 KB key
 // stages and two 32 KB memory stages fill the 160 KB of LDS. With no compiler-issued
 // vector loads left in the unit loop, the waits placed by hand are the only ones.
 // Eight waves, two per SIMD: wave w takes the 16 memory rows of slice w & 3 against
 // the 64 positions of half w >> 2, so one wave's LDS reads and exp2 run under the
-// other's MFMAs. The first pass keeps one (max, sum) per 64 positions; the second
-// seeds each accumulator with -(max + log2 Z) of its row, read by scalar loads, so
-// exp2 of the MFMA result is already the softmax weight.
+// other's MFMAs. Each (64 positions, unit, row) leaves one (max, sum) in the log2
+// domain. The unit-major pass below is used instead whenever Hkv is even.
 constexpr int KSTAGES = 3;
 constexpr int MSTAGE = 64 * 256;                 // bf16 per memory stage: 64 rows x 512 B
 constexpr int RING_THREADS = 512;
 
-// Read-only view for wave-uniform loads: the compiler issues them on the scalar unit
-// (tracked by lgkmcnt, so they never delay the vector-memory waits of the ring).
+// Read-only view for wave-uniform loads: the compiler issues them on the scalar unit.
 typedef const __attribute__((address_space(4))) float cfloat;
 
-template <bool PASS_B, bool KBAR>
 __global__ void __launch_bounds__(RING_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
              const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-             float *__restrict__ scores, bool resid) {
+             bool resid) {
   __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
 
   const int b = blockIdx.y;
@@ -398,7 +395,6 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
   float *part = base + z.off_part();
-  const float *nl2 = base + z.off_nl2();
   const int32_t *S = slot_maps + s.slot_off;
 
   // candidate flags of this lane's 16 MFMA outputs: bit blk*4 + i <-> position p0 + blk*16 + 4g + i
@@ -449,10 +445,8 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   };
   // The loads of the next stages during unit u, spread over its eight MFMA chunks: the
   // memory-row pieces of unit u + 1 in chunks 0-1, the key pieces of unit u + 2 in
-  // chunks 2-5. The address unit accepts one 1-KB instruction every 16 clocks or so,
-  // so eight waves issuing all of theirs at once would hold every wave for about a
-  // thousand clocks before its MFMAs. The order (memory rows first) keeps the count
-  // the top of each unit waits for.
+  // chunks 2-5. The order (memory rows first) keeps the count the top of each unit
+  // waits for.
   auto dma_chunk = [&](int u, int c) {
     if (c < 2) {
 #pragma unroll
@@ -463,72 +457,44 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     }
   };
 
-  float racc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) racc[i][k] = 0.f;
-  // Mean key row on the matrix cores: the MFMA of a key fragment (channels 32 rs .. + 31)
-  // with the B operand eye0 (eye1) copies channels 32 rs + n (32 rs + 16 + n) of its 16
-  // positions into column n, so summing over units is the accumulation itself.
-  f32x4 kacc[4][2];
-  bf16x8 eye0, eye1;
-#pragma unroll
-  for (int blk = 0; blk < 4; ++blk) kacc[blk][0] = kacc[blk][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    eye0[e] = (8 * g + e == r16) ? __bf16(1.0f) : __bf16(0.0f);
-    eye1[e] = (8 * g + e == r16 + 16) ? __bf16(1.0f) : __bf16(0.0f);
-  }
-  float pm = 0.f, pz = 0.f;                        // first pass: the previous unit's (max, sum)
-
-  // The logits of a unit are finished (masked max and sum, or exp2 summed into the
-  // rule score) during the next unit, on the VALU under that unit's MFMAs: the two
-  // pipes overlap, and the epilogue reads only registers, so it may cross the barrier.
+  float pm = 0.f, pz = 0.f;                        // the previous unit's (max, sum)
+  // The logits of a unit are finished (masked max and sum) during the next unit, on
+  // the VALU under that unit's MFMAs: the two pipes overlap, and the epilogue reads
+  // only registers, so it may cross the barrier.
   f32x4 accp[4];
 #pragma unroll
   for (int blk = 0; blk < 4; ++blk) accp[blk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
   // Epilogue of one unit in eight steps, so that each step can run under four MFMAs
-  // of the next unit. First pass: masked max (step 0), exp2 sums (steps 1-4), the
-  // merge across the four lane groups of a row (steps 5-6). Second pass: two exp2
-  // terms of the rule score per step.
+  // of the next unit: masked max (step 0), exp2 sums (steps 1-4), the merge across the
+  // four lane groups of a row (steps 5-6).
   float em = -INFINITY, emb = 0.f, ez = 0.f;
   auto epilogue_step = [&](f32x4 (&a)[4], int c) {
-    if (!PASS_B) {
-      if (c == 0) {
-        em = -INFINITY;
+    if (c == 0) {
+      em = -INFINITY;
 #pragma unroll
-        for (int blk = 0; blk < 4; ++blk)
+      for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (!((cmask >> (blk * 4 + i)) & 1u)) a[blk][i] = -INFINITY;
-            em = fmaxf(em, a[blk][i]);
-          }
-        emb = (em == -INFINITY) ? 0.f : em;
-        ez = 0.f;
-      } else if (c <= 4) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) ez += ex2(a[c - 1][i] - emb);
-      } else if (c <= 6) {
-        const int o = c == 5 ? 16 : 32;
-        const float m2 = __shfl_xor(em, o, WAVE);
-        const float z2 = __shfl_xor(ez, o, WAVE);
-        const float mm = fmaxf(em, m2);
-        const float x = (em == -INFINITY) ? 0.f : ez * ex2(em - mm);
-        const float y = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
-        em = mm;
-        ez = x + y;
-        if (c == 6) {
-          pm = em;
-          pz = ez;
+        for (int i = 0; i < 4; ++i) {
+          if (!((cmask >> (blk * 4 + i)) & 1u)) a[blk][i] = -INFINITY;
+          em = fmaxf(em, a[blk][i]);
         }
-      }
-    } else {
-      // non-candidates are summed too and dropped at the store
+      emb = (em == -INFINITY) ? 0.f : em;
+      ez = 0.f;
+    } else if (c <= 4) {
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int e = 2 * c + k, blk = e >> 2, i = e & 3;
-        racc[blk][i] += ex2(a[blk][i]);
+      for (int i = 0; i < 4; ++i) ez += ex2(a[c - 1][i] - emb);
+    } else if (c <= 6) {
+      const int o = c == 5 ? 16 : 32;
+      const float m2 = __shfl_xor(em, o, WAVE);
+      const float z2 = __shfl_xor(ez, o, WAVE);
+      const float mm = fmaxf(em, m2);
+      const float x = (em == -INFINITY) ? 0.f : ez * ex2(em - mm);
+      const float y = (m2 == -INFINITY) ? 0.f : z2 * ex2(m2 - mm);
+      em = mm;
+      ez = x + y;
+      if (c == 6) {
+        pm = em;
+        pz = ez;
       }
     }
   };
@@ -537,7 +503,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
     for (int c = 0; c < 8; ++c) epilogue_step(a, c);
   };
 
-  auto compute = [&](int u, float seed) {     // seed: this lane's row, second pass only
+  auto compute = [&](int u) {
     const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
     if (act) {
       const uint16_t *mr = lds + KSTAGES * STAGE + (u & 1) * MSTAGE + row * 256;
@@ -556,7 +522,7 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
       read_ks(0);
       f32x4 acc[4];
 #pragma unroll
-      for (int blk = 0; blk < 4; ++blk) acc[blk] = f32x4{seed, seed, seed, seed};
+      for (int blk = 0; blk < 4; ++blk) acc[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
       // chunk c: the four MFMAs of k-step c/2 (hi, then lo), then epilogue step c of
       // the previous unit (a no-op before the first); the fences keep the interleave
 #pragma unroll
@@ -568,30 +534,13 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
         for (int blk = 0; blk < 4; ++blk)
           acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], (c & 1) ? ml[ks] : mh[ks], acc[blk], 0, 0, 0);
         epilogue_step(accp, c);
-        // mean key row: wave (rs, half) sums channels 32 rs .. + 31 of its 64 positions
-        // from the fragments already in registers
-        if (KBAR && ks == rs && (c & 1) == 0)
-#pragma unroll
-          for (int blk = 0; blk < 4; ++blk) {
-            kacc[blk][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], eye0, kacc[blk][0], 0, 0, 0);
-            kacc[blk][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], eye1, kacc[blk][1], 0, 0, 0);
-          }
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) accp[blk] = acc[blk];
-    }
-    if (!act)
+    } else {
 #pragma unroll
       for (int c = 0; c < 6; ++c) dma_chunk(u, c);
-    if (KBAR && !act) {                            // slices without memory rows still cover their channels
-#pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        const uint16_t *kr = kl + (p0 + blk * 16 + r16) * MD;
-        const bf16x8 f = *reinterpret_cast<const bf16x8 *>(kr + (((4 * rs + g) ^ r16) * 8));
-        kacc[blk][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, eye0, kacc[blk][0], 0, 0, 0);
-        kacc[blk][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f, eye1, kacc[blk][1], 0, 0, 0);
-      }
     }
   };
   auto store_part = [&](int u) {
@@ -599,77 +548,22 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
       *reinterpret_cast<float2 *>(part + ((int64_t(ptile) * units + u) * R + row) * 2) = make_float2(pm, pz);
   };
 
-  // Issue order per wave: K(0), M(0), K(1), then per unit u: [first pass: store of
-  // unit u-2], M(u+1), K(u+2), the last two spread over the unit's MFMA chunks. At
-  // the top of unit u only K(u+1) (4 loads) may still be younger than M(u) and K(u).
+  // Issue order per wave: K(0), M(0), K(1), then per unit u: the store of unit u-2,
+  // M(u+1), K(u+2), the last two spread over the unit's MFMA chunks. At the top of
+  // unit u only K(u+1) (4 loads) may still be younger than M(u) and K(u).
   issue_k(0);
   for (int k = 0; k < nm; ++k) issue_m_piece(0, k);
   if (units > 1) issue_k(1);
   for (int u = 0; u < units; ++u) {
-    // second pass: -(max + log2 Z) of this wave's 16 memory rows, by scalar loads issued
-    // before the unit's waits, which they outlast (tracked by lgkmcnt, not vmcnt)
-    float sv[16];
-    if (PASS_B && act) {
-      const cfloat *q = (cfloat *)(nl2 + int64_t(__builtin_amdgcn_readfirstlane(u * R + rs * 16)));
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        sv[i] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, q[i])));
-    }
     if (u + 1 < units) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (!PASS_B && u >= 2) store_part(u - 2);      // finished during unit u - 1
-    float seed = 0.f;
-    if (PASS_B && act) {
-      seed = sv[0];
-#pragma unroll
-      for (int i = 1; i < 16; ++i) seed = (r16 == i) ? sv[i] : seed;
-    }
-    compute(u, seed);
+    if (u >= 2) store_part(u - 2);                 // finished during unit u - 1
+    compute(u);
   }
-  if (!PASS_B && units >= 2) store_part(units - 2);
+  if (units >= 2) store_part(units - 2);
   if (act) epilogue(accp);                         // the last unit
-  if (!PASS_B) store_part(units - 1);
-  __syncthreads();
-
-  if (PASS_B) {
-    float *red = reinterpret_cast<float *>(lds);   // [4][MFMA_TILE], the loop is over
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v = racc[blk][i];
-        v += __shfl_xor(v, 1, WAVE);
-        v += __shfl_xor(v, 2, WAVE);
-        v += __shfl_xor(v, 4, WAVE);
-        v += __shfl_xor(v, 8, WAVE);
-        if (r16 == 0) red[rs * MFMA_TILE + p0 + blk * 16 + 4 * g + i] = v;
-      }
-    __syncthreads();
-    if (t < MFMA_TILE) {
-      const int j = j0 + t;
-      if (j < s.N) {
-        const bool c = S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
-        scores[s.slot_off + j] = c ? (red[t] + red[MFMA_TILE + t]) + (red[2 * MFMA_TILE + t] + red[3 * MFMA_TILE + t])
-                                   : -INFINITY;
-      }
-    }
-  }
-  if (KBAR) {
-    // lane (g, r16) of kacc[blk][hf] holds positions p0 + 16 blk + 4 g + i, channel 32 rs + 16 hf + r16
-    const float inv = 1.0f / float(units);
-    float *kbar = base + z.off_kbar() + 32 * rs + r16;
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int j = j0 + p0 + blk * 16 + 4 * g + i;
-        if (j < s.N) {
-          kbar[int64_t(j) * MD] = kacc[blk][0][i] * inv;
-          kbar[int64_t(j) * MD + 16] = kacc[blk][1][i] * inv;
-        }
-      }
-  }
+  store_part(units - 1);
 }
 
 // ------------------------------------------------------------------ second pass, warp-specialised (R <= 64)
@@ -788,16 +682,28 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __syncthreads();                                 // matches the consumers' reduction barrier
+    __syncthreads();                                 // the ring is free (matches the consumers)
+    // The mean key rows go out through LDS, so that each store writes two whole
+    // 512-byte rows: stored straight from the lanes, every line would leave L2 in
+    // 16-byte pieces. Rows of 132 floats keep the lanes' writes on distinct banks;
+    // the region starts past the consumers' reduction buffer.
+    float *kt = reinterpret_cast<float *>(lds) + 2 * MFMA_TILE;
+    constexpr int KT_ROW = MD + 4;
+    if (KBAR) {
+      const float inv = 1.0f / float(units);
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        *reinterpret_cast<float4 *>(kt + pp * KT_ROW + 64 * hc + 4 * q) =
+            make_float4(kb[4 * q] * inv, kb[4 * q + 1] * inv, kb[4 * q + 2] * inv, kb[4 * q + 3] * inv);
+    }
     __syncthreads();
     if (KBAR) {
-      const int j = j0 + pp;
-      if (j < s.N) {
-        const float inv = 1.0f / float(units);
-        float4 *kbar = reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(j) * MD + 64 * hc);
+      // producer pw stores positions 32 pw .. + 31: two rows (32 lanes x 16 B each) per instruction
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
-          kbar[q] = make_float4(kb[4 * q] * inv, kb[4 * q + 1] * inv, kb[4 * q + 2] * inv, kb[4 * q + 3] * inv);
+      for (int q = 0; q < 16; ++q) {
+        const int pr = 32 * pw + 2 * q + (lane >> 5), j = j0 + pr;
+        const float4 v = *reinterpret_cast<const float4 *>(kt + pr * KT_ROW + 4 * (lane & 31));
+        if (j < s.N) reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(j) * MD)[lane & 31] = v;
       }
     }
     return;
@@ -1229,7 +1135,7 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
     float *lse = base + z.off_lse();
     lse[2 * i] = mx;
     lse[2 * i + 1] = Z > 0.0 ? float(1.0 / Z) : 0.f;
-    // -(max + log2 Z): the ring pass seeds its accumulators with it (-inf without candidates)
+    // -(max + log2 Z): the second pass seeds its accumulators with it (-inf without candidates)
     float *nl2 = base + z.off_nl2();
     nl2[i] = (mx == -INFINITY || !(Z > 0.0)) ? -INFINITY : float(-(double(mx) + log2(Z)));
   }
@@ -1259,9 +1165,9 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     }
   else if (ring)
     {
-      KTimer kt_("k_score_ring<false, false>", st);
-      k_score_ring<false, false><<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                   a.slot_maps, a.ws, a.scores, resid);
+      KTimer kt_("k_score_ring", st);
+      k_score_ring<<<dim3(tiles, a.B), RING_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                             a.slot_maps, a.ws, resid);
     }
   else
     {

@@ -8,6 +8,8 @@
 // a ballot ranks the lanes, so the workgroup needs one cross-wave scan per sweep.
 #include <math.h>
 
+#include <stdlib.h>
+
 #include "ikv_internal.hpp"
 
 namespace ikv {
@@ -823,11 +825,18 @@ size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_posi
 }
 
 // Workgroups of k_select_coop that the current device holds at once (0: no cooperative launch).
+// Workgroups a cooperative launch of k_select_coop may have on the current device
+// (0: not available). IKV_NO_COOP=1 in the environment turns the cooperative path off,
+// for tools that cannot follow a cooperative launch; the selection is the same.
 static int coop_capacity() {
   static int cap[64];
   static bool known[64];
+  static const bool off = [] {
+    const char *e = getenv("IKV_NO_COOP");
+    return e != nullptr && e[0] != '\0' && e[0] != '0';
+  }();
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (off || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   if (!known[dev]) {
     int per_cu = 0, cus = 0, coop = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_select_coop, SC_THREADS, 0) != hipSuccess ||

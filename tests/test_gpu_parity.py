@@ -123,6 +123,23 @@ def test_rule_scores_d128_matrix_cores(dev, R, N):
     check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
 
 
+@pytest.mark.parametrize("R,N,Hkv,flags", [(64, 1000, 3, 0), (16, 700, 1, 0), (48, 1300, 3, ikv.IKV_RESIDUAL)])
+def test_scores_d128_odd_kv_heads(dev, R, N, Hkv, flags):
+    """An odd number of KV heads: the first pass runs position-major over all units
+    (64-position partials), the second pass as for even Hkv."""
+    batch = small_d128(R=R, N=N, seed=3 * R + N, L=3, Hkv=Hkv, G=2)
+    blob = synth.residual_blob(128, seed=R) if flags else None
+    st = RetentionStep(batch, dev, residual=blob, flags=flags)
+    st.init_dead_slot()
+    st.score(flags=flags)
+    want, sets = oracle_scores(batch, 0, blob, flags)
+    rel = check_scores(st.host("scores"), want, sets["cand"])
+    assert rel < 1e-5, rel
+    st.select()
+    keep_o, n_o, tau_o = oracle.select_budget(want, sets)
+    check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
+
+
 @pytest.mark.parametrize("R,flags,nq", [(16, ikv.IKV_RESIDUAL, 16), (64, ikv.IKV_RESIDUAL, 16),
                                         (64, ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN, 16),
                                         (32, ikv.IKV_RESIDUAL, 64), (48, ikv.IKV_RESIDUAL, 100)])
