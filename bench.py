@@ -236,7 +236,7 @@ def main() -> int:
         "k_select": s.N * (4 + 4 + 1),
         "k_select_small": s.N * (4 + 4 + 1),
         "k_residual_mfma": nA * (sh.D * 4 + 4 + 4),
-        "k_redirect<true>": s.N * (4 + 1 + 4 + 4),
+        "k_redirect<bytes>": s.N * (4 + 1 + 4 + 4),
     }
     kernels = {}
     for name, v in per_kernel.items():

@@ -892,40 +892,71 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
 }
 
 // ------------------------------------------------------------------ redirect
-// The two slot bitsets (slots of kept positions, freed slots) live in LDS when the
-// pool has at most RED_LDS_WORDS * 32 slots, else in the caller's workspace, where
-// the workgroup's waves reach each other through device-scope atomics and fences.
+// Two slot sets: slots of kept positions, freed slots. Where they live (RED_MODE):
+//   RED_BYTES (pools up to 65,536 slots): one LDS byte per slot, set by plain byte
+//     stores. Every writer stores the same 1, so no atomics are needed; an LDS atomic
+//     OR serialises the lanes that hit one word, and the 16 positions of a page do.
+//   RED_LDS_BITS (up to RED_LDS_WORDS * 32 slots): LDS bitsets, set by atomic OR.
+//   RED_GLOBAL_BITS: bitsets in the caller's workspace, where the workgroup's waves
+//     reach each other through device-scope atomics and fences.
 constexpr int RED_LDS_WORDS = 16384;        // two bitsets of 64 KB: pools up to 524288 slots
+constexpr int RED_BYTE_SLOTS = 65536;       // two byte maps of 64 KB
 constexpr int RED_U = 16;                   // positions in flight per lane in the two sweeps
+enum { RED_BYTES = 0, RED_LDS_BITS = 1, RED_GLOBAL_BITS = 2 };
 
-template <bool LDS_SETS>
+template <int MODE>
 struct SlotSets {
   uint32_t *kept, *freed;
   __device__ __forceinline__ void set(uint32_t *w, int u) const {
-    if (LDS_SETS) atomicOr(w + (u >> 5), 1u << (u & 31));
+    if (MODE == RED_BYTES) *reinterpret_cast<volatile uint8_t *>(reinterpret_cast<uint8_t *>(w) + u) = 1;
+    else if (MODE == RED_LDS_BITS) atomicOr(w + (u >> 5), 1u << (u & 31));
     else __hip_atomic_fetch_or(w + (u >> 5), 1u << (u & 31), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  // bit k of word i <-> slot 32 i + k
   __device__ __forceinline__ uint32_t word(const uint32_t *w, int64_t i) const {
-    if (LDS_SETS) return w[i];
+    if (MODE == RED_BYTES) {
+      const uint4 *p = reinterpret_cast<const uint4 *>(w) + 2 * i;
+      const uint4 a = p[0], c = p[1];
+      const uint32_t x[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+      uint32_t m = 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        m |= ((x[k] & 1u) | ((x[k] >> 7) & 2u) | ((x[k] >> 14) & 4u) | ((x[k] >> 21) & 8u)) << (4 * k);
+      return m;
+    }
+    if (MODE == RED_LDS_BITS) return w[i];
     return __hip_atomic_load(w + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __device__ __forceinline__ void clear(uint32_t *w, int64_t i) const {
-    if (LDS_SETS) w[i] = 0u;
-    else __hip_atomic_store(w + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __device__ __forceinline__ bool test(const uint32_t *w, int u) const {
+    if (MODE == RED_BYTES) return reinterpret_cast<const uint8_t *>(w)[u] != 0;
+    return (word(w, u >> 5) >> (u & 31)) & 1u;
+  }
+  // every word of both sets (words = 32-slot groups), cleared by the workgroup
+  __device__ __forceinline__ void clear_all(int64_t words, int t) const {
+    const int64_t n = MODE == RED_BYTES ? words * 8 : words;   // 32-bit stores per set
+    for (int64_t i = t; i < n; i += SEL_THREADS) {
+      if (MODE == RED_GLOBAL_BITS) {
+        __hip_atomic_store(kept + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(freed + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        kept[i] = 0u;
+        freed[i] = 0u;
+      }
+    }
   }
   __device__ __forceinline__ void sync() const {
-    if (!LDS_SETS) __threadfence();
+    if (MODE == RED_GLOBAL_BITS) __threadfence();
     __syncthreads();
   }
 };
 
-template <bool LDS_SETS>
+template <int MODE>
 __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__restrict__ sess, int64_t num_slots,
                                                           int32_t *__restrict__ slot_maps, int dead,
                                                           const uint8_t *__restrict__ keep, int32_t *__restrict__ freed,
                                                           int32_t *__restrict__ n_freed, int32_t *__restrict__ live,
                                                           int32_t *__restrict__ n_live, uint32_t *__restrict__ ws) {
-  __shared__ uint32_t lds_sets[LDS_SETS ? 2 * RED_LDS_WORDS : 1];
+  __shared__ __align__(16) uint32_t lds_sets[MODE != RED_GLOBAL_BITS ? 2 * RED_LDS_WORDS : 1];
   __shared__ int red[SEL_WAVES];
   const int b = blockIdx.x;
   const ikv_session s = sess[b];
@@ -933,14 +964,10 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
   int32_t *S = slot_maps + s.slot_off;
   const uint8_t *kp = keep + s.slot_off;
   const int64_t words = bitset_words(num_slots);
-  SlotSets<LDS_SETS> sets;
-  sets.kept = LDS_SETS ? lds_sets : ws + int64_t(b) * 2 * words;
-  sets.freed = sets.kept + words;
-
-  for (int64_t i = t; i < words; i += SEL_THREADS) {
-    sets.clear(sets.kept, i);
-    sets.clear(sets.freed, i);
-  }
+  SlotSets<MODE> sets;
+  sets.kept = MODE != RED_GLOBAL_BITS ? lds_sets : ws + int64_t(b) * 2 * words;
+  sets.freed = sets.kept + (MODE == RED_BYTES ? words * 8 : words);
+  sets.clear_all(words, t);
   sets.sync();
   // slots of the kept positions, and the survivors of each wave's range
   int64_t lo, hi;
@@ -983,7 +1010,7 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
       const bool k = alive && kv[q] != 0;
       if (alive && !k) {
         S[j] = dead;
-        if (j >= s.radix_prefix && !((sets.word(sets.kept, u >> 5) >> (u & 31)) & 1u)) sets.set(sets.freed, u);
+        if (j >= s.radix_prefix && !sets.test(sets.kept, u)) sets.set(sets.freed, u);
       }
       const uint64_t bal = __ballot(k);
       if (k) live[s.slot_off + pos + __popcll(bal & lanes_below())] = u;
@@ -1001,25 +1028,32 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
   for (int o = 32; o > 0; o >>= 1) nbits += __shfl_xor(nbits, o, WAVE);
   int total_freed;
   int fpos = wave_base(nbits, total_freed, red);
-  for (int64_t c0 = wlo; c0 < whi; c0 += WAVE) {
-    const int64_t i = c0 + lane;
-    const uint32_t bits = i < whi ? sets.word(sets.freed, i) : 0u;
-    const int c = __popc(bits);
-    int x = c;                                      // inclusive scan over the lanes
+  // The freed slots of a step go out as one run, in slot order: lane = slot (64 per
+  // step) on bitsets; with byte maps lane l takes slots 4l .. 4l+3 of the step (256
+  // per step, one 32-bit LDS read), each slot's place from four ballots.
+  if (MODE == RED_BYTES) {
+    const uint8_t *fb = reinterpret_cast<const uint8_t *>(sets.freed);
+    const uint64_t below = lanes_below();
+    for (int64_t base = wlo * 32; base < whi * 32; base += 4 * WAVE) {
+      const int64_t u0 = base + 4 * lane;
+      const uint32_t x = u0 < whi * 32 ? *reinterpret_cast<const uint32_t *>(fb + u0) : 0u;
+      const uint64_t b0 = __ballot(x & 0xffu), b1 = __ballot(x & 0xff00u), b2 = __ballot(x & 0xff0000u),
+                     b3 = __ballot(x & 0xff000000u);
+      int r = fpos + __popcll(b0 & below) + __popcll(b1 & below) + __popcll(b2 & below) + __popcll(b3 & below);
+      int32_t *out = freed + s.slot_off;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, WAVE);
-      if (lane >= o) x += y;
+      for (int k = 0; k < 4; ++k)
+        if ((x >> (8 * k)) & 0xffu) out[r++] = int32_t(u0 + k);
+      fpos += __popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3);
     }
-    int r = fpos + x - c;
-    uint32_t m = bits;
-    while (m) {
-      const int bit = __ffs(m) - 1;
-      m &= m - 1;
-      freed[s.slot_off + r] = int32_t(i * 32 + bit);
-      ++r;
+  } else {
+    for (int64_t base = wlo * 32; base < whi * 32; base += WAVE) {
+      const int64_t u = base + lane;
+      const bool f = u < whi * 32 && sets.test(sets.freed, int(u));
+      const uint64_t bal = __ballot(f);
+      if (f) freed[s.slot_off + fpos + __popcll(bal & lanes_below())] = int32_t(u);
+      fpos += __popcll(bal);
     }
-    fpos += __shfl(x, 63, WAVE);
   }
   if (t == 0) n_freed[b] = total_freed;
 }
@@ -1027,17 +1061,23 @@ __global__ void __launch_bounds__(SEL_THREADS) k_redirect(const ikv_session *__r
 hipError_t launch_redirect(const ikv_session *sess_dev, int B, int64_t num_slots, int32_t *slot_maps, int32_t dead,
                            const uint8_t *keep, int32_t *freed, int32_t *n_freed, int32_t *live, int32_t *n_live,
                            uint32_t *ws, hipStream_t st) {
-  if (bitset_words(num_slots) <= RED_LDS_WORDS)
+  if (num_slots <= RED_BYTE_SLOTS)
     {
-      KTimer kt_("k_redirect<true>", st);
-      k_redirect<true><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
-                                                  n_live, ws);
+      KTimer kt_("k_redirect<bytes>", st);
+      k_redirect<RED_BYTES><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed,
+                                                       live, n_live, ws);
+    }
+  else if (bitset_words(num_slots) <= RED_LDS_WORDS)
+    {
+      KTimer kt_("k_redirect<lds>", st);
+      k_redirect<RED_LDS_BITS><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed,
+                                                          live, n_live, ws);
     }
   else
     {
-      KTimer kt_("k_redirect<false>", st);
-      k_redirect<false><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed, n_freed, live,
-                                                   n_live, ws);
+      KTimer kt_("k_redirect<global>", st);
+      k_redirect<RED_GLOBAL_BITS><<<B, SEL_THREADS, 0, st>>>(sess_dev, num_slots, slot_maps, dead, keep, freed,
+                                                             n_freed, live, n_live, ws);
     }
   return hipGetLastError();
 }
