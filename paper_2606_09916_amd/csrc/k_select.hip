@@ -831,12 +831,10 @@ size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_posi
 static int coop_capacity() {
   static int cap[64];
   static bool known[64];
-  static const bool off = [] {
-    const char *e = getenv("IKV_NO_COOP");
-    return e != nullptr && e[0] != '\0' && e[0] != '0';
-  }();
+  const char *e = getenv("IKV_NO_COOP");           // read on every call
+  if (e != nullptr && e[0] != '\0' && e[0] != '0') return 0;
   int dev = 0;
-  if (off || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   if (!known[dev]) {
     int per_cu = 0, cus = 0, coop = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_select_coop, SC_THREADS, 0) != hipSuccess ||

@@ -68,9 +68,23 @@ def test_select_long_sessions_exact(dev, lengths, ties):
         assert tau[b] == t_o or (math.isnan(tau[b]) and math.isnan(t_o))
 
 
-@pytest.mark.parametrize("n,C", [(50000, 20000), (3000, 1000), (40000, 39990)])
-def test_select_all_scores_equal(dev, n, C):
+@pytest.mark.parametrize("lengths,ties,coop", [((140000, 3000), False, True), ((200000,), True, True),
+                                               ((32768, 20000, 7), True, False), ((40000, 9000), False, False)])
+def test_select_paths_exact(dev, lengths, ties, coop, monkeypatch):
+    """Sessions past the cooperative path's limit (131,072 positions) take the
+    three-kernel path; with IKV_NO_COOP=1 sessions up to 32,768 positions take the
+    one-workgroup kernel and longer ones the three-kernel path."""
+    if not coop:
+        monkeypatch.setenv("IKV_NO_COOP", "1")
+    test_select_long_sessions_exact(dev, lengths, ties)
+
+
+@pytest.mark.parametrize("n,C,coop", [(50000, 20000, True), (3000, 1000, True), (40000, 39990, True),
+                                      (3000, 1000, False), (50000, 20000, False), (150000, 60000, True)])
+def test_select_all_scores_equal(dev, n, C, coop, monkeypatch):
     # every candidate ties at the threshold: the budget fills in position order
+    if not coop:
+        monkeypatch.setenv("IKV_NO_COOP", "1")
     rows = _rows((n,), C=C, pi=7)
     S = synth.slot_map(n, n + 1, seed=5, dead_frac=0.2)
     sc = np.full(n, 0.375, np.float32)
