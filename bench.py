@@ -231,7 +231,7 @@ def main() -> int:
         "k_score_ws<true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
         "k_score_ws<false>": key_bytes + mem_bytes + s.N * 4,
         "k_decode_split<T, D, G>": kv_live + sh.L * sh.Hq * sh.D * 2,
-        "k_decode_mfma<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
+        "k_decode_heads<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
         "k_qm_update<T, 128>": units * s.R * (s.qe - s.qs) * sh.D * 2 + 2 * mem_bytes,
         "k_select": s.N * (4 + 4 + 1),
         "k_select_small": s.N * (4 + 4 + 1),

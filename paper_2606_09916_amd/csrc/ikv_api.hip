@@ -131,8 +131,21 @@ size_t redirect_bytes(int64_t num_slots, int B) {
   return size_t(B) * 2 * size_t(ikv::bitset_words(num_slots)) * sizeof(uint32_t);
 }
 
+// An upper bound on the live positions a session holds after a retention event:
+// the forced set (at most pi + qe - qs positions) plus the budget, and never more
+// than N. A slot map that was never pruned may hold more; the decode is then still
+// exact, only with longer splits.
+int live_bound(const ikv_session *s, int B) {
+  int64_t m = 1;
+  for (int b = 0; b < B; ++b) {
+    const int64_t forced = int64_t(std::max(0, s[b].pi)) + std::max(0, s[b].qe - s[b].qs);
+    m = std::max<int64_t>(m, std::min<int64_t>(s[b].N, std::max<int64_t>(s[b].C, forced)));
+  }
+  return int(m);
+}
+
 size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
-  const int splits = ikv::decode_splits(max_n(s, B));
+  const int splits = ikv::decode_splits(live_bound(s, B));
   return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
 }
 
@@ -345,7 +358,7 @@ ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *se
   if (B == 0) return ok();
   if (!q || !live || !n_live || !out) return fail(IKV_EINVAL, "q / live / n_live / out is NULL");
   if ((r = check_ws(workspace, workspace_bytes, decode_bytes(pool, sess, B)))) return r;
-  const int splits = ikv::decode_splits(max_n(sess, B));
+  const int splits = ikv::decode_splits(live_bound(sess, B));
   return hip_status(ikv::launch_decode(*pool, sess_dev, B, splits, q, live, n_live, out,
                                        static_cast<float *>(workspace), (hipStream_t)stream),
                     "ikv_decode_attend_slotmap");

@@ -1,6 +1,10 @@
 // GQA decode attention over the live slots of each session (the kept entries read
 // through the slot map with the sentinel stripped, Sec. 3.4 and Appendix C.2).
 //
+// Two kernels write the partial state of each split: k_decode_heads (bf16 pool,
+// D = 128; logits on the matrix cores, described where it is defined) and
+// k_decode_split (every other pool), below.
+//
 // k_decode_split: one workgroup per (session, layer, KV head, split of the live
 // list). Each wavefront takes blocks of 64 live slots: lane k computes the logits
 // of slot k for the G query heads sharing the KV head, the block's weights are
@@ -15,8 +19,10 @@
 
 namespace ikv {
 
-int decode_splits(int maxN) {
-  const int64_t s = cdiv(maxN, 1024);
+// Splits of the live list: about 256 live positions each (four blocks of 64 per wave
+// in the head-group kernel), at most 64 splits.
+int decode_splits(int live_bound) {
+  const int64_t s = cdiv(live_bound, 256);
   return int(s < 1 ? 1 : (s > 64 ? 64 : s));
 }
 
@@ -214,55 +220,58 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
   decode_finish<D, G>(m, lsum, o, red, ored, ws, b, L, l, Hq, g, split, nsplit);
 }
 
-// ---- matrix-core decode (bf16 pool, D = 128). The logits of 16 live positions x
-// the G query heads of a KV head are one chain of four v_mfma_f32_16x16x32_bf16:
-// the key rows are the A operand (lane (g, r) loads 16 bytes of position r), the
-// query rows the B operand (column h = query head h, zero beyond G), both exact in
-// bf16 with float32 accumulation. The block's softmax weights go to LDS as one row
-// of G per position; the value rows are summed on the VALU as in k_decode_split.
 typedef __bf16 bf16x8_d __attribute__((ext_vector_type(8)));
 typedef float f32x4_d __attribute__((ext_vector_type(4)));
 
-template <int G>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_decode_mfma(const uint16_t *__restrict__ kpool,
-                                                     const uint16_t *__restrict__ vpool, int64_t num_slots, int L,
-                                                     int Hkv, const ikv_session *__restrict__ sess,
-                                                     const uint16_t *__restrict__ q, const int32_t *__restrict__ live,
-                                                     const int32_t *__restrict__ n_live, float *__restrict__ ws) {
+// ---- head-group decode (bf16 pool, D = 128). A workgroup owns a group of `hpw`
+// adjacent KV heads of one layer (hpw * 256 contiguous bytes of every key and value
+// row) and one split of the live list; wave w owns KV head g0 + w and walks the
+// whole split in blocks of 64 live slots, so the waves of a workgroup read adjacent
+// pieces of the same rows together. The loads of block i+1 are issued while block i
+// is computed: the key fragments right after block i's logits, the value rows right
+// after its weighted sum. Each wave writes its own (max, sum, output) per query head.
+template <int G, bool O32>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_decode_heads(const uint16_t *__restrict__ kpool,
+                                                      const uint16_t *__restrict__ vpool, int64_t num_slots, int L,
+                                                      int Hkv, int hpw, const ikv_session *__restrict__ sess,
+                                                      const uint16_t *__restrict__ q, const int32_t *__restrict__ live,
+                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws) {
   constexpr int D = 128;
   constexpr int LPR = D / 8;           // lanes per value row (8 channels each)
   constexpr int RPI = WAVE / LPR;      // value rows per load instruction
+  constexpr int NV = DEC_BLOCK / RPI;  // value loads per block
   constexpr int GP = (G + 3) & ~3;     // weights per position in LDS, padded to float4
   __shared__ __align__(16) float pw[4][DEC_BLOCK][GP];
-  __shared__ float red[4][G][2];
-  __shared__ float ored[4][G][D];
+  __shared__ __align__(16) bf16x8_d qsh[4][4][WAVE];   // query fragments, read before every block's MFMAs
 
   const int b = blockIdx.z;
   const ikv_session s = sess[b];
   const int Hq = Hkv * G;
-  const int u = blockIdx.y, l = u / Hkv, g = u - l * Hkv;
+  const int ngrp = Hkv / hpw;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int l = blockIdx.y / ngrp, g = (blockIdx.y - l * ngrp) * hpw + w;
   const int split = blockIdx.x, nsplit = gridDim.x;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int gq = lane >> 4, r16 = lane & 15;
+  const int rq = lane / LPR, cq = lane % LPR;     // value row group, channel group
   int n = n_live[b];
   n = n < 0 ? 0 : (n > s.N ? s.N : n);
-  const int chunk = int(cdiv(n, nsplit));
+  const int chunk = int(cdiv(cdiv(n, nsplit), DEC_BLOCK)) * DEC_BLOCK;
   const int k0 = min(n, split * chunk), k1 = min(n, k0 + chunk);
   const float scale = 1.0f / sqrtf(float(D));
   const int32_t *lv = live + s.slot_off;
-  int slot0 = 0;                                   // the first block's slot: loads with the query rows
-  if (k0 + w * DEC_BLOCK + lane < k1) slot0 = lv[k0 + w * DEC_BLOCK + lane];
-  // the query rows as the B operand: lane (gq, r16) holds channels ks*32 + gq*8 .. +8 of head r16
-  bf16x8_d qb[4];
+  int slot = (k0 + lane < k1) ? lv[k0 + lane] : 0;
+  // the query rows as the B operand: lane (gq, r16) holds channels ks*32 + gq*8 .. +8 of head r16.
+  // They stay in LDS (no registers to spare beside two blocks of key and value loads).
   {
     const uint16_t *qr = q + ((int64_t(b) * L + l) * Hq + g * G + (r16 < G ? r16 : 0)) * D + gq * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      qb[ks] = *reinterpret_cast<const bf16x8_d *>(qr + ks * 32);
-      if (r16 >= G) qb[ks] = bf16x8_d{};
+      bf16x8_d x = *reinterpret_cast<const bf16x8_d *>(qr + ks * 32);
+      if (r16 >= G) x = bf16x8_d{};
+      qsh[w][ks][lane] = x;
     }
   }
-  const int rq = lane / LPR, cq = lane % LPR;     // value row group, channel group
   float m[G], lsum[G], o[G][8];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -272,36 +281,59 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
   const int64_t row_stride = int64_t(Hkv) * D;
-  const uint16_t *kbase = kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
-  const uint16_t *vbase = vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D;
-  for (int base = k0 + w * DEC_BLOCK; base < k1; base += 4 * DEC_BLOCK) {
-    const int kk = base + lane;
-    const bool valid = kk < k1;
-    const int slot = base == k0 + w * DEC_BLOCK ? slot0 : (valid ? lv[kk] : 0);
-    const int nb = min(DEC_BLOCK, k1 - base);
-    // value rows (they need only the slots) and key fragments leave together
-    Raw8<uint16_t> v[DEC_BLOCK / RPI];
-#pragma unroll
-    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
-      const int i = r * RPI + rq;
-      const int si = __shfl(slot, i, WAVE);
-      if (i < nb) v[r].ld(vbase + int64_t(si) * row_stride + cq * 8);
-    }
-    bf16x8_d kf[4][4];
+  // wave-uniform bases (this wave's head in layer l); a row is reached by a per-lane
+  // byte offset, 32 bits wide when a layer of the pool spans less than 4 GB
+  const char *kbase = reinterpret_cast<const char *>(kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
+  const char *vbase = reinterpret_cast<const char *>(vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
+  const uint32_t row_bytes = uint32_t(row_stride) * 2;
+  auto row_off = [&](int sl, int within) -> uint64_t {
+    if constexpr (O32) return uint32_t(sl) * row_bytes + uint32_t(within);
+    else return uint64_t(uint32_t(sl)) * row_bytes + uint32_t(within);
+  };
+  Raw8<uint16_t> v[NV];
+  bf16x8_d kf[4][4];
+  // lanes past the end of a block hold slot 0, a valid row; their logits are masked
+  auto load_k = [&](int sl, int nb) {
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
-      const int sr = __shfl(slot, bb * 16 + r16, WAVE);   // past the block: slot 0, masked below
-      const uint16_t *kr = kbase + int64_t(sr) * row_stride + gq * 8;
+      const int sr = __shfl(sl, bb * 16 + r16, WAVE);
+      const char *kr = kbase + row_off(sr, gq * 16);
+      if (bb * 16 < nb)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kf[bb][ks] = *reinterpret_cast<const bf16x8_d *>(kr + ks * 32);
+        for (int ks = 0; ks < 4; ++ks) kf[bb][ks] = *reinterpret_cast<const bf16x8_d *>(kr + ks * 64);
     }
+  };
+  auto load_v = [&](int sl, int nb) {
+#pragma unroll
+    for (int r = 0; r < NV; ++r) {
+      const int i = r * RPI + rq;
+      const int si = __shfl(sl, i, WAVE);
+      if (i < nb) v[r].ld(reinterpret_cast<const uint16_t *>(vbase + row_off(si, cq * 16)));
+    }
+  };
+  if (k0 < k1) {
+    load_v(slot, min(DEC_BLOCK, k1 - k0));
+    load_k(slot, min(DEC_BLOCK, k1 - k0));
+  }
+  for (int base = k0; base < k1; base += DEC_BLOCK) {
+    const int nb = min(DEC_BLOCK, k1 - base);
+    const int nbase = base + DEC_BLOCK;
+    const int nnb = min(DEC_BLOCK, k1 - nbase);  // <= 0 past the last block
+    const int nslot = (nbase + lane < k1) ? lv[nbase + lane] : 0;
+    asm volatile("" ::: "memory");                 // re-read the query fragments every block
+    bf16x8_d qb[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qb[ks] = qsh[w][ks][lane];
     f32x4_d acc[4];
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
       acc[bb] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+      if (bb * 16 < nb)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bb][ks], qb[ks], acc[bb], 0, 0, 0);
+        for (int ks = 0; ks < 4; ++ks)
+          acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bb][ks], qb[ks], acc[bb], 0, 0, 0);
     }
+    if (nnb > 0) load_k(nslot, nnb);
     // acc[bb][i]: logit of position bb*16 + 4gq + i for query head r16
     float mx = -INFINITY;
 #pragma unroll
@@ -344,7 +376,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 #pragma unroll
-    for (int r = 0; r < DEC_BLOCK / RPI; ++r) {
+    for (int r = 0; r < NV; ++r) {
       const int i = r * RPI + rq;
       if (i < nb) {
         float vv[8];
@@ -366,8 +398,29 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    if (nnb > 0) load_v(nslot, nnb);
+    slot = nslot;
   }
-  decode_finish<D, G>(m, lsum, o, red, ored, ws, b, L, l, Hq, g, split, nsplit);
+  // fold the value row groups; lanes 0..LPR-1 then hold channels cq*8 .. +8
+#pragma unroll
+  for (int x = LPR; x < WAVE; x <<= 1)
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) o[h][c] += __shfl_xor(o[h][c], x, WAVE);
+  if (lane < LPR) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
+      float *p = ws + (row * nsplit + split) * (D + 2);
+      if (lane == 0) {
+        p[0] = m[h];
+        p[1] = lsum[h];
+      }
+#pragma unroll
+      for (int c = 0; c < 8; ++c) p[2 + cq * 8 + c] = o[h][c];
+    }
+  }
 }
 
 template <typename T, int D>
@@ -409,10 +462,17 @@ template <typename T, int D, int G>
 static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
                                   const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
   if constexpr (sizeof(T) == 2 && D == 128) {
-    KTimer kt_("k_decode_mfma<G>", st);
-    k_decode_mfma<G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
-        (const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const uint16_t *)q,
-        live, n_live, ws);
+    const int hpw = p.Hkv % 4 == 0 ? 4 : (p.Hkv % 2 == 0 ? 2 : 1);
+    const dim3 grid(splits, p.L * (p.Hkv / hpw), B);
+    KTimer kt_("k_decode_heads<G>", st);
+    if (p.num_slots * p.Hkv * D * 2 < (int64_t(1) << 32))
+      k_decode_heads<G, true><<<grid, 64 * hpw, 0, st>>>((const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool,
+                                                         p.num_slots, p.L, p.Hkv, hpw, sess_dev, (const uint16_t *)q,
+                                                         live, n_live, ws);
+    else
+      k_decode_heads<G, false><<<grid, 64 * hpw, 0, st>>>((const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool,
+                                                          p.num_slots, p.L, p.Hkv, hpw, sess_dev, (const uint16_t *)q,
+                                                          live, n_live, ws);
   } else {
     KTimer kt_("k_decode_split<T, D, G>", st);
     k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
