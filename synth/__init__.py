@@ -172,6 +172,22 @@ def _workers() -> int:
     return max(1, min(16, os.cpu_count() or 1))
 
 
+def paged_slots(Ns, seed: int, page: int = 16, spare_pages: int = 0):
+    """Physical slots of sessions of lengths ``Ns`` in one paged pool: pages of ``page``
+    slots dealt in order from a seeded shuffle of all pages (slot 0 stays the dead
+    slot). Returns (list of int64 slot arrays, num_slots)."""
+    pages_per = [(int(n) + page - 1) // page for n in Ns]
+    total_pages = sum(pages_per) + spare_pages
+    order = stream(seed, T_PAGES).permutation(total_pages).astype(np.int64)
+    alloc, p0 = [], 0
+    for n, pp in zip(Ns, pages_per):
+        pages = order[p0:p0 + pp]
+        p0 += pp
+        j = np.arange(int(n), dtype=np.int64)
+        alloc.append(1 + pages[j // page] * page + (j % page))
+    return alloc, 1 + total_pages * page
+
+
 def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
                layout: str = "paged", page: int = 16, spare_pages: int = 0) -> Batch:
     """Draw a batch of sessions sharing one paged pool.
@@ -195,16 +211,7 @@ def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
         else:
             alloc.append(1 + stream(seed, T_SHUF).permutation(n).astype(np.int64))
     else:
-        pages_per = [(n + page - 1) // page for n in Ns]
-        total_pages = sum(pages_per) + spare_pages
-        order = stream(seed, T_PAGES).permutation(total_pages).astype(np.int64)
-        num_slots = 1 + total_pages * page
-        p0 = 0
-        for n, pp in zip(Ns, pages_per):
-            pages = order[p0:p0 + pp]
-            p0 += pp
-            j = np.arange(n, dtype=np.int64)
-            alloc.append(1 + pages[j // page] * page + (j % page))
+        alloc, num_slots = paged_slots(Ns, seed, page, spare_pages)
 
     # --- slot maps with already-dead positions ---------------------------------
     slot_off = np.zeros(B, dtype=np.int64)
@@ -398,6 +405,7 @@ def slot_map(n: int, num_slots: int, seed: int, dead_frac: float = 0.1, dead: in
 
 T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS, T_MISC_SLOTS = 20, 21, 22, 23
 T_TURNS = 24
+T_TABLE_K, T_TABLE_V = 25, 26
 
 
 # ----------------------------------------------------------------------------- multi-turn session
@@ -451,3 +459,95 @@ def turn_decode_query(seed: int, turn: int, position: int, shape: Shape, kv_dtyp
     q = stream(seed, T_QDEC, turn).standard_normal((1, shape.L, shape.Hq, shape.D), dtype=np.float32)
     q = rope_neox(q.astype(np.float64), *rope_cos_sin(np.array([position]), shape.D))
     return to_dtype(q[0], kv_dtype)
+
+
+# ----------------------------------------------------------------------------- table rows
+# Pools too large to draw on the host (the batched one-GPU share: about 219 GB of keys
+# and values) are filled on the GPU from a table: row (l, slot, h) is the window
+# table[o : o + D] of T + D N(0,1) values in bf16, at o = splitmix64(key + (r + 1) *
+# GAMMA) >> (64 - log2 T), r = (l * num_slots + slot) * Hkv + h (SplitMix64's output
+# function: Steele, Lea and Flood, OOPSLA 2014). The device kernel (table_rows.hip)
+# and table_rows() below produce the same bytes, so the oracle regenerates any row on
+# the host. Every row holds D N(0,1) values; rows whose windows overlap share values,
+# shifted. No RoPE is applied: a rotation of i.i.d. N(0,1) pairs is again i.i.d. N(0,1).
+
+TABLE_LOG2 = 24
+_GAMMA = np.uint64(0x9E3779B97F4A7C15)
+_SYNTH_LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsynth.so")
+
+
+def table(seed: int, tensor: int, D: int, log2_T: int = TABLE_LOG2) -> np.ndarray:
+    """2^log2_T + D N(0,1) values rounded to bf16 (nearest even), as uint16 bits."""
+    x = stream(seed, tensor).standard_normal((1 << log2_T) + D, dtype=np.float32)
+    u = x.view(np.uint32)
+    return ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+
+
+def table_key(seed: int, tensor: int) -> int:
+    return (int(seed) << 32) | int(tensor)
+
+
+def _splitmix64(z: np.ndarray) -> np.ndarray:
+    z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+    z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+    return z ^ (z >> np.uint64(31))
+
+
+def table_offsets(l: int, num_slots: int, Hkv: int, slots, key: int, log2_T: int = TABLE_LOG2) -> np.ndarray:
+    """Window offsets of rows (l, slots[k], h): int64 [len(slots)][Hkv]."""
+    slots = np.asarray(slots, dtype=np.uint64)
+    r = (np.uint64(l) * np.uint64(num_slots) + slots)[:, None] * np.uint64(Hkv) + np.arange(Hkv, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        z = np.uint64(key) + (r + np.uint64(1)) * _GAMMA
+        return (_splitmix64(z) >> np.uint64(64 - log2_T)).astype(np.int64)
+
+
+def table_rows(tab: np.ndarray, L: int, num_slots: int, Hkv: int, D: int, slots, key: int,
+               log2_T: int = TABLE_LOG2) -> np.ndarray:
+    """Host copy of pool rows [L][len(slots)][Hkv][D] (uint16 bf16 bits), the same bytes
+    as the device fill."""
+    slots = np.asarray(slots)
+    out = np.empty((L, len(slots), Hkv, D), dtype=np.uint16)
+    d = np.arange(D, dtype=np.int64)
+    for l in range(L):
+        o = table_offsets(l, num_slots, Hkv, slots, key, log2_T)
+        out[l] = tab[o[:, :, None] + d]
+    return out
+
+
+def device_table_rows(pool, L: int, num_slots: int, Hkv: int, D: int, slots, tab_dev, key: int,
+                      log2_T: int = TABLE_LOG2, stream_=None) -> None:
+    """Fill rows of a device bf16 pool tensor [L][num_slots][Hkv][D] from a device table:
+    every slot (slots=None) or the slots of a device int32 tensor."""
+    import ctypes
+    import torch
+    if not os.path.exists(_SYNTH_LIB):
+        raise RuntimeError(f"{_SYNTH_LIB} is missing: run __graft_entry__.build()")
+    lib = ctypes.CDLL(_SYNTH_LIB)
+    fn = lib.synth_table_rows
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                   ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_uint64, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    st = (stream_ or torch.cuda.current_stream()).cuda_stream
+    n = num_slots if slots is None else int(slots.numel())
+    err = fn(pool.data_ptr(), L, num_slots, Hkv, D, None if slots is None else slots.data_ptr(), n,
+             tab_dev.data_ptr(), log2_T, key, st)
+    if err != 0:
+        raise RuntimeError(f"synth_table_rows failed with HIP error {err}")
+
+
+def build_native(verbose: bool = False) -> str:
+    """Compile table_rows.hip into synth/libsynth.so (gfx950)."""
+    import shutil
+    import subprocess
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    src = os.path.join(os.path.dirname(_SYNTH_LIB), "table_rows.hip")
+    cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Xclang", "-target-feature",
+           "-Xclang", "-packed-fp32-ops", src, "-o", _SYNTH_LIB + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on table_rows.hip:\n{r.stdout}\n{r.stderr}")
+    os.replace(_SYNTH_LIB + ".tmp", _SYNTH_LIB)
+    if verbose:
+        print(f"built {_SYNTH_LIB}")
+    return _SYNTH_LIB
