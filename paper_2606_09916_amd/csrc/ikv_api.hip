@@ -281,8 +281,9 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   if (!slot_maps || !M || !scores) return fail(IKV_EINVAL, "slot_maps / M / scores is NULL");
   const bool resid = (flags & IKV_RESIDUAL) != 0;
   if (resid && !residual) return fail(IKV_EINVAL, "IKV_RESIDUAL set but residual is NULL");
-  int maxR = 0, maxNq = 0, anyq = 0;
+  int maxR = 0, minR = INT32_MAX, maxNq = 0, anyq = 0;
   for (int b = 0; b < B; ++b) {
+    minR = sess[b].R < minR ? sess[b].R : minR;
     if ((reinterpret_cast<uintptr_t>(M) + size_t(sess[b].mem_off) * 4) % 16)
       return fail(IKV_EINVAL, "session %d: M + mem_off must be 16-byte aligned", b);
     maxR = sess[b].R > maxR ? sess[b].R : maxR;
@@ -306,11 +307,12 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.ws = static_cast<float *>(workspace);
   a.mfma = use_mfma(pool, sess, B);
   a.mfma_resid = a.mfma && resid && maxNq <= 64;
-  a.stats = a.mfma && maxR <= 64 && pool->Hkv % 2 == 0 &&
+  a.stats = a.mfma && maxR <= 128 && pool->Hkv % 2 == 0 &&
             int64_t(pool->num_slots) * pool->Hkv * pool->D * 2 <= int64_t(UINT32_MAX);
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.maxR = maxR;
+  a.minR = minR;
   a.maxNq = maxNq;
   if (a.maxN == 0) return ok();
   return hip_status(ikv::launch_score(a, (hipStream_t)stream), "ikv_score_history");

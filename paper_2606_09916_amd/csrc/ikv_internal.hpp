@@ -212,7 +212,7 @@ struct ScoreArgs {
   float *scores;
   float *ws;           // session blocks, then the shared block
   float *ws_shared;
-  int maxN, maxR, maxNq;
+  int maxN, maxR, minR, maxNq;
   bool mfma;           // MFMA score passes (D = 128 and every R a multiple of 16)
   bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)

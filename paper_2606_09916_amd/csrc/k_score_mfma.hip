@@ -363,6 +363,21 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
 // domain. The unit-major pass below is used instead whenever Hkv is even.
 constexpr int KSTAGES = 3;
 constexpr int MSTAGE = 64 * 256;                 // bf16 per memory stage: 64 rows x 512 B
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..12
+__device__ __forceinline__ void vm_wait(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+}
+
 constexpr int RING_THREADS = 512;
 
 // Read-only view for wave-uniform loads: the compiler issues them on the scalar unit.
@@ -577,16 +592,21 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 // which reads 128 KB of LDS per unit instead of the 192 KB of sixteen-row waves.
 constexpr int WS_THREADS = 512;
 
-template <bool KBAR>
+// RH row halves per unit: 1 for sessions of up to 64 memory rows; 2 for up to 128,
+// where every unit's rows stream as two halves of 64 through the same two-stage ring
+// (half h in stage h) against the one key stage of the unit. A batch holding both
+// kinds runs one launch of each; `big` as in k_score_stats.
+template <bool KBAR, int RH>
 __global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
            const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-           float *__restrict__ scores, bool resid) {
+           float *__restrict__ scores, bool resid, int big) {
   __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
 
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
+  if ((big == 1 && s.R > 64) || (big == 2 && s.R <= 64)) return;   // the other launch's session
   const int tile = blockIdx.x;
   const int j0 = tile * MFMA_TILE;
   if (j0 >= s.N) return;
@@ -615,32 +635,35 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
     }
     asm volatile("" ::"v"(src[0]), "v"(src[7]));   // the slot loads are complete before the first DMA
-    auto issue_k_piece = [&](int u, int k) {
+    auto issue_k_piece = [&](int u, int k) __attribute__((always_inline)) {
       const int l = u / Hkv, h = u - l * Hkv;
       const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
       const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
       dma16(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * pw + k) * 4) * MD * 2)));
     };
-    auto issue_k = [&](int u) {
+    auto issue_k = [&](int u) __attribute__((always_inline)) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) issue_k_piece(u, k);
     };
-    // memory rows of unit u: R rows of 512 B, chunk slot c of row r holds chunk c ^ (r & 15);
-    // producer pw issues R/8 of the R/2 1-KB pieces (two rows each)
+    // memory rows of unit u (half hf): up to 64 rows of 512 B, chunk slot c of row r
+    // holds chunk c ^ (r & 15); producer pw issues a quarter of the half's 1-KB pieces
+    // (two rows each), npc(hf) of them
     const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
     const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
-    const int npc = R >> 3;
-    auto issue_m_piece = [&](int u, int k) {
-      const uint16_t *m0 = msplit + int64_t(u) * R * 256;
-      const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
+    auto npc_of = [&](int hf) __attribute__((always_inline)) { return min(64, max(0, R - 64 * hf)) >> 3; };
+    auto issue_m_piece = [&](int u, int hf, int k) __attribute__((always_inline)) {
+      const int npc = npc_of(hf);
+      const uint16_t *m0 = msplit + (int64_t(u) * R + 64 * hf) * 256;
+      const uint32_t st = mlds0 + uint32_t((RH == 1 ? (u & 1) : hf) * MSTAGE * 2);
       const int piece = pw * npc + k;
       const int r = piece * 2 + (lane >> 5);
       const int sl = lane & 31;
       dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
     };
-    auto issue_m = [&](int u) {
-      for (int k = 0; k < npc; ++k) issue_m_piece(u, k);
+    auto issue_m = [&](int u, int hf) __attribute__((always_inline)) {
+      for (int k = 0; k < npc_of(hf); ++k) issue_m_piece(u, hf, k);
     };
+    const int npc = npc_of(0);
     // mean key row: lane (position 32 pw + lane % 32, channels 64 (lane / 32) .. + 63)
     const int pp = 32 * pw + (lane & 31), hc = lane >> 5;
     float kb[64];
@@ -652,35 +675,66 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
     // loads alternate with the mean-key-row steps (memory-row pieces in steps 0-3, two
     // each, key pieces in steps 4-7), so that the VALU work fills the time a wave waits
     // for the address unit to take its next load.
+    auto kbar_step = [&](const uint16_t *kr, int c) __attribute__((always_inline)) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((8 * hc + c) ^ (pp & 15)) * 8));
+      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {                  // bf16 -> float is exact: the high half of the word
+        kb[8 * c + 2 * e] += __uint_as_float(q[e] << 16);
+        kb[8 * c + 2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
+      }
+    };
     issue_k(0);
-    issue_m(0);
+    issue_m(0, 0);
     if (units > 1) issue_k(1);
-    for (int u = 0; u < units; ++u) {
-      if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
+    if constexpr (RH == 1) {
+      for (int u = 0; u < units; ++u) {
+        if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        if (c < 4) {
+        for (int c = 0; c < 8; ++c) {
+          if (c < 4) {
 #pragma unroll
-          for (int k = 2 * c; k < 2 * c + 2; ++k)
-            if (k < npc && u + 1 < units) issue_m_piece(u + 1, k);
-        } else if (u + 2 < units) {
-          issue_k_piece(u + 2, 2 * (c - 4));
-          issue_k_piece(u + 2, 2 * (c - 4) + 1);
+            for (int k = 2 * c; k < 2 * c + 2; ++k)
+              if (k < npc && u + 1 < units) issue_m_piece(u + 1, 0, k);
+          } else if (u + 2 < units) {
+            issue_k_piece(u + 2, 2 * (c - 4));
+            issue_k_piece(u + 2, 2 * (c - 4) + 1);
+          }
+          if (KBAR) kbar_step(kr, c);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        if (KBAR) {
-          const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((8 * hc + c) ^ (pp & 15)) * 8));
-          const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+      }
+    } else {
+      // Per half hf of unit u: the next half's rows (M(u, 1), then M(u + 1, 0)) in
+      // steps 0-1, then key pieces 4 hf .. 4 hf + 3 of K(u + 2) in steps 2-3; the mean
+      // key row takes channel chunks 4 hf .. 4 hf + 3. At the top of a half only the
+      // key pieces issued after its rows may be outstanding: K(1) (8) at the first,
+      // four after that, none once the keys run out.
+      for (int u = 0; u < units; ++u)
+        for (int hf = 0; hf < 2; ++hf) {
+          const int after = hf == 0 ? (u == 0 ? (units > 1 ? 8 : 0) : (u + 1 < units ? 4 : 0))
+                                    : (u + 2 < units ? 4 : 0);
+          vm_wait(after);
+          __syncthreads();
+          const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
+          const int nu = hf == 0 ? u : u + 1, nh = hf ^ 1, nn = npc_of(nh);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {              // bf16 -> float is exact: the high half of the word
-            kb[8 * c + 2 * e] += __uint_as_float(q[e] << 16);
-            kb[8 * c + 2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
+          for (int c4 = 0; c4 < 4; ++c4) {
+            if (c4 < 2) {
+#pragma unroll
+              for (int k = 4 * c4; k < 4 * c4 + 4; ++k)
+                if (k < nn && nu < units) issue_m_piece(nu, nh, k);
+            } else if (u + 2 < units) {
+              issue_k_piece(u + 2, 4 * hf + 2 * (c4 - 2));
+              issue_k_piece(u + 2, 4 * hf + 2 * (c4 - 2) + 1);
+            }
+            if (KBAR) kbar_step(kr, 4 * hf + c4);
+            __builtin_amdgcn_sched_barrier(0);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
-      }
     }
     __syncthreads();                                 // the ring is free (matches the consumers)
     // The mean key rows go out through LDS, so that each store writes two whole
@@ -712,7 +766,6 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   // ---------------- consumers: logits on the matrix cores, exp2 folded into the rule score
   const int rh = w & 1, p0 = (w >> 1) * 64;         // memory-row half, first position of the half
   const int nsl = R >> 4;
-  const bool act0 = 2 * rh < nsl, act1 = 2 * rh + 1 < nsl;   // slices of this wave within R
   const float *nl2 = base + z.off_nl2();
   float racc[4][4];
 #pragma unroll
@@ -725,29 +778,31 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) accp[sl][blk] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
   // step c (0-7) of the previous unit's epilogue: exp2 of four of its 32 logits per lane
-  auto epilogue_step = [&](int c) {
+  auto epilogue_step = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int e = 4 * c + k, sl = e >> 4, blk = (e >> 2) & 3, i = e & 3;
       racc[blk][i] += ex2(accp[sl][blk][i]);
     }
   };
-  // Seeds -(max + log2 Z) of the lane's two rows, loaded two units ahead at the end of
-  // a unit's MFMAs: issued right after the barrier, a load would queue behind the
-  // producers' ring loads at the address unit. Rows past R take -inf against zero
-  // fragments, so exp2 of their logits is 0.
-  const int row0 = 32 * rh + r16, row1 = row0 + 16;
-  auto seed_ld = [&](int u, int row) { return nl2[int64_t(u) * R + min(row, R - 1)]; };
-  // one unit: seeds s0, s1 as loaded (rows past R take -inf here)
-  auto unit_step = [&](int u, float s0, float s1) {
-    const float seed0 = row0 < R ? s0 : -INFINITY, seed1 = row1 < R ? s1 : -INFINITY;
+  // Seeds -(max + log2 Z) of the lane's two rows, loaded two (virtual) units ahead at
+  // the end of a unit's MFMAs: issued right after the barrier, a load would queue behind
+  // the producers' ring loads at the address unit. Rows past R take -inf against zero
+  // fragments, so exp2 of their logits is 0. Virtual unit v is half v % RH of unit v / RH.
+  auto rowv = [&](int v, int k) __attribute__((always_inline)) { return 64 * (v % RH) + 32 * rh + 16 * k + r16; };
+  auto seed_ld = [&](int v, int k) __attribute__((always_inline)) { return nl2[int64_t(v / RH) * R + min(rowv(v, k), R - 1)]; };
+  // one virtual unit: seeds s0, s1 as loaded (rows past R take -inf here)
+  auto unit_step = [&](int v, float s0, float s1) __attribute__((always_inline)) {
+    const int u = v / RH, hf = v % RH;
+    const float seed0 = rowv(v, 0) < R ? s0 : -INFINITY, seed1 = rowv(v, 1) < R ? s1 : -INFINITY;
+    const bool act0 = 4 * hf + 2 * rh < nsl, act1 = 4 * hf + 2 * rh + 1 < nsl;   // slices within R
     __syncthreads();
     const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
-    const uint16_t *mb = lds + KSTAGES * STAGE + (u & 1) * MSTAGE;
+    const uint16_t *mb = lds + KSTAGES * STAGE + (RH == 1 ? (u & 1) : hf) * MSTAGE;
     const uint16_t *mr0 = mb + (32 * rh + r16) * 256, *mr1 = mr0 + 16 * 256;
     // fragments of k-step ks: memory rows (hi, lo) of both slices, the four key blocks
     bf16x8 mh[2][4], ml[2][4], ka[4][4];
-    auto read_ks = [&](int ks) {
+    auto read_ks = [&](int ks) __attribute__((always_inline)) {
       const int ch = ((g * 8 + ks * 2) ^ r16) * 8, cl = ((g * 8 + ks * 2 + 1) ^ r16) * 8;
       mh[0][ks] = *reinterpret_cast<const bf16x8 *>(mr0 + ch);
       ml[0][ks] = *reinterpret_cast<const bf16x8 *>(mr0 + cl);
@@ -786,24 +841,25 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) accp[sl][blk] = acc[sl][blk];
   };
-  // Even and odd units keep their own seed registers (unrolled by two), so that no
-  // register that a load is still filling has to be copied.
-  float a0 = seed_ld(0, row0), a1 = seed_ld(0, row1), b0 = 0.f, b1 = 0.f;
-  if (units > 1) {
-    b0 = seed_ld(1, row0);
-    b1 = seed_ld(1, row1);
+  // Even and odd virtual units keep their own seed registers (unrolled by two), so
+  // that no register that a load is still filling has to be copied.
+  const int V = units * RH;
+  float a0 = seed_ld(0, 0), a1 = seed_ld(0, 1), b0 = 0.f, b1 = 0.f;
+  if (V > 1) {
+    b0 = seed_ld(1, 0);
+    b1 = seed_ld(1, 1);
   }
-  for (int u = 0; u < units; u += 2) {
-    unit_step(u, a0, a1);
-    if (u + 2 < units) {
-      a0 = seed_ld(u + 2, row0);
-      a1 = seed_ld(u + 2, row1);
+  for (int v = 0; v < V; v += 2) {
+    unit_step(v, a0, a1);
+    if (v + 2 < V) {
+      a0 = seed_ld(v + 2, 0);
+      a1 = seed_ld(v + 2, 1);
     }
-    if (u + 1 < units) {
-      unit_step(u + 1, b0, b1);
-      if (u + 3 < units) {
-        b0 = seed_ld(u + 3, row0);
-        b1 = seed_ld(u + 3, row1);
+    if (v + 1 < V) {
+      unit_step(v + 1, b0, b1);
+      if (v + 3 < V) {
+        b0 = seed_ld(v + 3, 0);
+        b1 = seed_ld(v + 3, 1);
       }
     }
   }
@@ -845,11 +901,10 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 // workgroups of chunk 0 also store the split rows of their units for the second pass
 // and, with the residual head on, the column sums of their rows (a partial of mbar).
 // For a session at or under its budget the pass only fills the scores with -inf.
-constexpr int ST_THREADS = 256;
 constexpr int ST_TILE = 32;                      // positions per stage
-constexpr int ST_STAGES = 4;
 constexpr int ST_STAGE = ST_TILE * 2 * MD;       // bf16 per stage: 32 positions x 2 heads
 constexpr int ST_CHMAX = 1024;                   // positions per chunk at most
+
 
 // 16 bytes per lane from sbase + voff (scalar base, 32-bit byte offset per lane)
 // straight into LDS at lds_base + 16 * lane.
@@ -860,16 +915,26 @@ __device__ __forceinline__ void dma16s(const void *sbase, uint32_t voff, uint32_
                : "memory", "m0");
 }
 
-__global__ void __launch_bounds__(ST_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// NW waves per head, each holding 32 rows: 2 for sessions of up to 64 memory rows
+// (256 threads, two waves per SIMD), 4 for up to 128 (512 threads, four waves per
+// SIMD); either way two workgroups share a CU. A batch that holds both kinds of
+// session runs one launch of each, and each launch skips the other's sessions
+// (`big`: 0 every session, 1 only R <= 64, 2 only R > 64).
+template <int NW>
+__global__ void __launch_bounds__(128 * NW) __attribute__((amdgpu_waves_per_eu(NW, NW)))
 k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
               const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-              const float *__restrict__ M, float *__restrict__ scores, bool resid, int CH) {
+              const float *__restrict__ M, float *__restrict__ scores, bool resid, int CH, int big) {
+  constexpr int ST_THREADS = 128 * NW;
+  constexpr int ST_STAGES = 4;
+  constexpr int KI = 8 / NW;                     // key loads (1 KB each) per wave per stage
   __shared__ __align__(1024) uint16_t ring[ST_STAGES * ST_STAGE];
   __shared__ uint32_t koff[ST_CHMAX];            // byte offset of each position's key rows in the layer
   __shared__ __align__(16) float bias[ST_CHMAX];  // 0 for a candidate, -inf otherwise
 
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
+  if ((big == 1 && s.R > 64) || (big == 2 && s.R <= 64)) return;   // the other launch's session
   const int HP = L * Hkv / 2;
   const int hp = int(blockIdx.x % unsigned(HP)), chunk = int(blockIdx.x / unsigned(HP));
   const int c0 = chunk * CH;
@@ -883,7 +948,7 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   const int T = int(cdiv(npos, ST_TILE));
   const int l = hp / (Hkv / 2), h0 = 2 * (hp - l * (Hkv / 2));
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int hh = w >> 1, r0 = 32 * (w & 1);      // head within the pair, first memory row
+  const int hh = w / NW, r0 = 32 * (w % NW);     // head within the pair, first memory row
   const int g = lane >> 4, r16 = lane & 15;
   const int R = s.R;
   const int units = L * Hkv;
@@ -958,22 +1023,23 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // Key loads: instruction k of wave w fills 1 KB of the stage, positions 2 (4w + k)
+  // Key loads: instruction k of wave w fills 1 KB of the stage, positions 2 (KI w + k)
   // and + 1; lane -> (position, head, 16-byte slot lane & 15), and slot s of a 256-byte
   // row holds chunk s ^ (position & 15).
   const uint16_t *kb0 = kpool + int64_t(l) * num_slots * (int64_t(Hkv) * MD) + int64_t(h0) * MD;
-  uint32_t lconst[4];
+  uint32_t lconst[KI];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int p = 2 * (4 * w + k) + (lane >> 5);
+  for (int k = 0; k < KI; ++k) {
+    const int p = 2 * (KI * w + k) + (lane >> 5);
     lconst[k] = uint32_t(((lane >> 4) & 1) * MD * 2 + (((lane & 15) ^ (p & 15)) * 16));
   }
-  const uint32_t lds_w = __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>(ring)) + w * 4096);
+  const uint32_t lds_w =
+      __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>(ring)) + w * KI * 1024);
   auto issue = [&](int tt) {
     const uint32_t st = lds_w + uint32_t((tt % ST_STAGES) * ST_STAGE * 2);
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      dma16s(kb0, koff[tt * ST_TILE + 2 * (4 * w + k) + (lane >> 5)] + lconst[k], st + k * 1024);
+    for (int k = 0; k < KI; ++k)
+      dma16s(kb0, koff[tt * ST_TILE + 2 * (KI * w + k) + (lane >> 5)] + lconst[k], st + k * 1024);
   };
 
   float Mr[2] = {-INFINITY, -INFINITY}, Zr[2] = {0.f, 0.f};
@@ -1020,30 +1086,34 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
     }
   };
 
+  const bool act = __builtin_amdgcn_readfirstlane(r0) < R;   // a wave past the last row only loads
   for (int k = 0; k < ST_STAGES - 1 && k < T; ++k) issue(k);
   for (int tt = 0; tt < T; ++tt) {
-    // tile tt's four loads per wave are done once at most those of the later tiles
-    // already issued (four each) are outstanding
-    const int later = min(ST_STAGES - 2, T - 1 - tt);
-    if (later >= 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (later == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // tile tt's KI loads per wave are done once at most those of the later tiles
+    // already issued (KI each) are outstanding
+    vm_wait(KI * min(ST_STAGES - 2, T - 1 - tt));
     __syncthreads();
     if (tt + ST_STAGES - 1 < T) issue(tt + ST_STAGES - 1);
-    compute(tt);
+    if (act) compute(tt);
   }
 
   // chunk 0 with the residual head: column sums of the head pair's 2 R memory rows
   if (resid && chunk == 0) {
     float *red = reinterpret_cast<float *>(ring);  // the ring is free: every wave is past its last tile
     __syncthreads();
-    const int c = t & (MD - 1), half = t >> 7;
+    constexpr int NP = ST_THREADS / MD;          // row classes summed apart, then in order
+    const int c = t & (MD - 1), part = t / MD;
     const float *mp = M + s.mem_off + int64_t(l * Hkv + h0) * R * MD + c;
     float a = 0.f;
-    for (int r = half; r < 2 * R; r += 2) a += mp[int64_t(r) * MD];
+    for (int r = part; r < 2 * R; r += NP) a += mp[int64_t(r) * MD];
     red[t] = a;
     __syncthreads();
-    if (t < MD) base[z.off_mbp() + int64_t(hp) * MD + t] = red[t] + red[MD + t];
+    if (t < MD) {
+      float tot = 0.f;
+#pragma unroll
+      for (int q = 0; q < NP; ++q) tot += red[q * MD + t];
+      base[z.off_mbp() + int64_t(hp) * MD + t] = tot;
+    }
   }
 
   // merge the four lane groups of each row and store the chunk's partial
@@ -1160,8 +1230,14 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   if (stats)
     {
       KTimer kt_("k_score_stats", st);
-      k_score_stats<<<dim3(unsigned(units / 2 * cdiv(a.maxN, chunk)), a.B), ST_THREADS, 0, st>>>(
-          kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, a.M, a.scores, resid, chunk);
+      const dim3 grid(unsigned(units / 2 * cdiv(a.maxN, chunk)), a.B);
+      const bool small = a.minR <= 64, large = a.maxR > 64;
+      if (small)
+        k_score_stats<2><<<grid, 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps,
+                                               a.ws, a.M, a.scores, resid, chunk, large ? 1 : 0);
+      if (large)
+        k_score_stats<4><<<grid, 512, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps,
+                                               a.ws, a.M, a.scores, resid, chunk, small ? 2 : 0);
     }
   else if (ring)
     {
@@ -1181,17 +1257,32 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
         a.sess_dev, a.ws, p.L, p.Hkv, resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE, a.slot_maps, a.qpos,
         p.dead_slot, a.stats);
   }
-  if (ring && resid)
+  // the producer/consumer second pass up to 128 memory rows: one launch per kind of
+  // session (up to 64 rows, up to 128)
+  const bool ws_small = a.minR <= 64, ws_large = a.maxR > 64;
+  if (a.maxR <= 128 && resid)
     {
       KTimer kt_("k_score_ws<true>", st);
-      k_score_ws<true><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                a.slot_maps, a.ws, a.scores, resid);
+      if (ws_small)
+        k_score_ws<true, 1><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                    a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
+                                                                    ws_large ? 1 : 0);
+      if (ws_large)
+        k_score_ws<true, 2><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                    a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
+                                                                    ws_small ? 2 : 0);
     }
-  else if (ring)
+  else if (a.maxR <= 128)
     {
       KTimer kt_("k_score_ws<false>", st);
-      k_score_ws<false><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
-                                                                 a.slot_maps, a.ws, a.scores, resid);
+      if (ws_small)
+        k_score_ws<false, 1><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                     a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
+                                                                     ws_large ? 1 : 0);
+      if (ws_large)
+        k_score_ws<false, 2><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+                                                                     a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
+                                                                     ws_small ? 2 : 0);
     }
   else if (resid)
     {

@@ -108,7 +108,8 @@ def small_d128(R=64, N=1000, seed=31, dead_frac=0.1, C=300, L=2, Hkv=2, G=4):
                             layout="paged")
 
 
-@pytest.mark.parametrize("R,N", [(16, 1000), (48, 777), (64, 1000), (80, 333), (128, 1280), (64, 129)])
+@pytest.mark.parametrize("R,N", [(16, 1000), (48, 777), (64, 1000), (80, 333), (96, 900), (112, 1500), (128, 1280),
+                                 (64, 129)])
 def test_rule_scores_d128_matrix_cores(dev, R, N):
     """Head dimension 128, bf16 pool, R a multiple of 16: the MFMA score passes."""
     batch = small_d128(R=R, N=N, seed=R + N)
@@ -123,7 +124,8 @@ def test_rule_scores_d128_matrix_cores(dev, R, N):
     check_keep(st.host("keep"), int(st.host("n_keep")[0]), keep_o, n_o, want, tau_o, sets["cand"])
 
 
-@pytest.mark.parametrize("R,N,Hkv,flags", [(64, 1000, 3, 0), (16, 700, 1, 0), (48, 1300, 3, ikv.IKV_RESIDUAL)])
+@pytest.mark.parametrize("R,N,Hkv,flags", [(64, 1000, 3, 0), (16, 700, 1, 0), (48, 1300, 3, ikv.IKV_RESIDUAL),
+                                            (96, 800, 3, ikv.IKV_RESIDUAL)])
 def test_scores_d128_odd_kv_heads(dev, R, N, Hkv, flags):
     """An odd number of KV heads: the first pass runs position-major over all units
     (64-position partials), the second pass as for even Hkv."""
@@ -142,7 +144,8 @@ def test_scores_d128_odd_kv_heads(dev, R, N, Hkv, flags):
 
 @pytest.mark.parametrize("R,flags,nq", [(16, ikv.IKV_RESIDUAL, 16), (64, ikv.IKV_RESIDUAL, 16),
                                         (64, ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN, 16),
-                                        (32, ikv.IKV_RESIDUAL, 64), (48, ikv.IKV_RESIDUAL, 100)])
+                                        (32, ikv.IKV_RESIDUAL, 64), (48, ikv.IKV_RESIDUAL, 100),
+                                        (128, ikv.IKV_RESIDUAL, 16)])
 def test_residual_scores_d128_matrix_cores(dev, R, flags, nq):
     """Residual head at D = 128: on the matrix cores up to 64 live query positions,
     on the vector units beyond."""
