@@ -11,6 +11,12 @@ K/V, history 32,768 positions, budget 8192, 64 memory rows per KV head, residual
 head on. Prints one JSON line on stdout; progress goes to stderr.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                    [--workload qwen3_8b_32k | qwen25_14b_92k | c5_share | tiny]
+
+c5_share: 64 sessions of the Qwen2.5-14B tensor-parallel share (48 layers, 20 / 4
+heads), 4k-64k positions each (2.29 M), 32-128 memory rows, budget 8192, one pool of
+210 GiB filled on the GPU; one score + select + redirect + decode step over the
+batch (no memory update).
 """
 from __future__ import annotations
 
@@ -32,8 +38,8 @@ CALIB_BYTES = 256 << 20        # the calibration copy (bytes read = bytes writte
 # scaled by what it reads for the calibration copy) on one workload, for the kernel
 # as built from the hashed sources; reported only while those sources are unchanged.
 MEASURED_TRAFFIC = {
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ws<true>"): (2509193672, "d289b7d9da93adb8"),
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2682181323, "d289b7d9da93adb8"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ws<true>"): (2509194612, "21c06e7bc1325d07"),
+    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2673057917, "21c06e7bc1325d07"),
 }
 TRAFFIC_SOURCES = ("paper_2606_09916_amd/csrc/k_score_mfma.hip", "paper_2606_09916_amd/csrc/ikv_internal.hpp")
 
@@ -57,33 +63,50 @@ def workload(name: str, R: int):
         return synth.qwen3_8b_32k(R=R), "qwen3_8b_shape_hist32768_budget8192"
     if name == "qwen25_14b_92k":
         return synth.qwen25_14b_92k_heavy(R=R), "qwen2.5_14b_shape_hist92300_budget8192_heavy_tail"
+    if name == "c5_share":
+        return synth.batched_share_full(), "qwen2.5_14b_tp2_share_64_sessions_4k_64k_budget8192"
     if name == "tiny":
         return synth.tiny_single_layer(R=R), "tiny_single_layer_hist2048_budget512"
     raise SystemExit(f"unknown workload {name}")
 
 
+def scored(s) -> bool:
+    return s.N > s.C                                 # at or under the budget the event is skipped
+
+
 def cpu_baseline(batch, blob, flags, layers: int):
     """The float64 oracle on a bounded sample: the per-layer work (rule score and key
     mean) on `layers` of the L layers for every candidate, scaled by L / layers, plus
-    the residual MLP and the selection over every candidate, done once."""
+    the residual MLP and the selection over every candidate, done once. On one session
+    (the longest); a batch's rate is that session's, the oracle working one session at
+    a time."""
     import oracle
+    import synth
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    s = batch.sessions[0]
+    b = int(np.argmax([x.N for x in batch.sessions]))
+    s = batch.sessions[b]
     sh = batch.shape
-    S = batch.S(0)
+    S = batch.S(b)
     sets = oracle.sets(S, s.pi, s.qs, s.qe, s.C, 0)
     idx = np.nonzero(sets["cand"])[0]
     Ls = min(layers, sh.L)
-    kp = batch.k_pool[:Ls]
-    M = batch.M_of(0)[:Ls]
+    if batch.k_pool is None:                         # pool on the GPU only: rebuild the sample's rows
+        kc = np.zeros((Ls, s.N + 1, sh.Hkv, sh.D), np.uint16)
+        kc[:, 1:] = synth.table_rows(synth.table(5, synth.T_TABLE_K, sh.D), Ls, batch.num_slots, sh.Hkv, sh.D,
+                                     S, synth.table_key(5, synth.T_TABLE_K))
+        kp, S = kc, np.arange(1, s.N + 1, dtype=np.int32)
+        vp = None
+    else:
+        kp, vp = batch.k_pool[:Ls], batch.v_pool[:Ls]
+    M = batch.M_of(b)[:Ls]
     t0 = time.perf_counter()
     rule = oracle.rule_scores(kp, S, sets["cand"], M, sh.Hkv, s.R)
     kb = oracle.kbar(kp, S, idx)
-    kq = oracle.kbar(kp, S, batch.qpos_of(0))
+    kq = oracle.kbar(kp, S, batch.qpos_of(b))
     t_layers = time.perf_counter() - t0
     t0 = time.perf_counter()
     sc = rule.copy()
@@ -94,7 +117,7 @@ def cpu_baseline(batch, blob, flags, layers: int):
     t_score_select = t_layers * sh.L / Ls + t_once
     t0 = time.perf_counter()
     live = S[np.nonzero(sets["live"])[0][: s.C]]
-    oracle.decode(batch.q_dec[0][:Ls], batch.k_pool[:Ls], batch.v_pool[:Ls], live)
+    oracle.decode(batch.q_dec[b][:Ls], kp, kp if vp is None else vp, live)
     t_dec = (time.perf_counter() - t0) * sh.L / Ls
     return {"value": len(idx) / t_score_select, "unit": "history tokens/s", "cores": int(threads),
             "kind": "oracle",
@@ -113,7 +136,8 @@ def main() -> int:
     ap.add_argument("--R", type=int, default=64)
     ap.add_argument("--no-residual", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=36)
+    ap.add_argument("--cpu-layers", type=int, default=None,
+                    help="layers of the CPU baseline sample (default 36; 8 for a pool drawn on the GPU)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path is single-GPU by design.",
@@ -136,8 +160,14 @@ def main() -> int:
     s = batch.sessions[0]
     flags = 0 if args.no_residual else ikv.IKV_RESIDUAL
     blob = synth.residual_blob(sh.D, seed=22)
+    mem_update = len(batch.q_span) > 0              # a workload without span rows has no memory update
     log("uploading")
-    st = RetentionStep(batch, dev, residual=blob, flags=flags)
+    k_dev = v_dev = None
+    if batch.k_pool is None:                         # too large for the host: keys and values drawn on the GPU
+        k_dev = torch.empty((sh.L, batch.num_slots, sh.Hkv, sh.D), dtype=torch.bfloat16, device=dev)
+        v_dev = torch.empty_like(k_dev)
+        synth.fill_share_pools(k_dev, v_dev, batch)
+    st = RetentionStep(batch, dev, residual=blob, flags=flags, k_dev=k_dev, v_dev=v_dev)
     st.init_dead_slot()
     torch.cuda.synchronize()
 
@@ -148,7 +178,8 @@ def main() -> int:
         evs[0].record()
         st.reset()
         evs[1].record()
-        st.qm_update()
+        if mem_update:
+            st.qm_update()
         evs[2].record()
         st.score()
         evs[3].record()
@@ -199,21 +230,29 @@ def main() -> int:
     for name, ms in recs:
         per_kernel.setdefault(name, []).append(ms)
 
-    n_live = int(st.host("n_live")[0])
-    n_keep = int(st.host("n_keep")[0])
-    # candidates: live positions outside the forced prefix and query span
-    S0 = np.asarray(batch.S(0))
-    jj = np.arange(len(S0))
-    forced = (jj < s.pi) | ((jj >= s.qs) & (jj < s.qe))
-    nA = int(((S0 != st.dead) & ~forced).sum())
+    n_live_all = st.host("n_live").astype(np.int64)
+    n_keep_all = st.host("n_keep").astype(np.int64)
+    n_live, n_keep = int(n_live_all.sum()), int(n_keep_all.sum())
+    # candidates of each session that is scored: live positions outside the forced prefix and query span
+    nA_b, sc_b = [], []
+    for b, x in enumerate(batch.sessions):
+        Sb = np.asarray(batch.S(b))
+        jj = np.arange(len(Sb))
+        forced = (jj < x.pi) | ((jj >= x.qs) & (jj < x.qe))
+        nA_b.append(int(((Sb != st.dead) & ~forced).sum()) if scored(x) else 0)
+        sc_b.append(scored(x))
+    nA = sum(nA_b)
     t_ss = (phase_ms[2] + phase_ms[3]) / 1e3
     tokens_per_s = nA / t_ss
 
-    # algorithmic bytes / flops (per step)
+    # algorithmic bytes / flops (per step), summed over the scored sessions
     units = sh.L * sh.Hkv
     kv_row = sh.Hkv * sh.D * 2 * sh.L                          # one position's K over all layers, bf16
-    score_bytes = nA * (kv_row + 4 + 4) + sh.L * sh.Hkv * s.R * sh.D * 4 + (blob.size * 4 if flags else 0)
-    score_flops = 2 * (2.0 * sh.L * sh.Hkv * s.R * sh.D) * nA
+    Rs = [x.R for x in batch.sessions]
+    Ns = [x.N for x in batch.sessions]
+    mem_bytes = sum(units * R * sh.D * 4 for R, c in zip(Rs, sc_b) if c)    # memory rows, float32
+    score_bytes = nA * (kv_row + 4 + 4) + mem_bytes + (blob.size * 4 if flags else 0)
+    score_flops = sum(2 * (2.0 * sh.L * sh.Hkv * R * sh.D) * a for R, a in zip(Rs, nA_b))
     decode_bytes = n_live * (2 * kv_row + 4)                    # decode phase: split and combine kernels
     score_gbs = score_bytes / (phase_ms[2] / 1e3) / 1e9
     decode_gbs = decode_bytes / (phase_ms[5] / 1e3) / 1e9
@@ -222,21 +261,24 @@ def main() -> int:
     # Algorithmic HBM bytes of one launch of the main kernels: what the arithmetic must
     # read and write, independent of how the kernel stages it.
     key_bytes = nA * units * sh.D * 2                          # candidate key rows, bf16, one pass
-    mem_bytes = units * s.R * sh.D * 4                         # memory rows, float32
     kv_live = n_live * units * sh.D * 2 * 2                    # live K and V rows, bf16
-    stats_parts = -(-s.N // 1024) * units * s.R * 8            # one (max, sum) per chunk and memory row
+    # one (max, sum) per 1024-position chunk and memory row
+    stats_parts = sum(-(-N // 1024) * units * R * 8 for N, R, c in zip(Ns, Rs, sc_b) if c)
+    n_scored = sum(N for N, c in zip(Ns, sc_b) if c)
+    q_rows = sh.L * sh.Hq * sh.D * 2 * len(batch.sessions)    # decode queries, bf16
+    span_bytes = sum(units * x.R * (x.qe - x.qs) * sh.D * 2 + 2 * units * x.R * sh.D * 4 for x in batch.sessions)
     algo = {
         "k_score_stats": key_bytes + mem_bytes + stats_parts,
         "k_score_ring": key_bytes + mem_bytes,
-        "k_score_ws<true>": key_bytes + mem_bytes + s.N * 4 + s.N * sh.D * 4,
-        "k_score_ws<false>": key_bytes + mem_bytes + s.N * 4,
-        "k_decode_split<T, D, G>": kv_live + sh.L * sh.Hq * sh.D * 2,
-        "k_decode_heads<G>": kv_live + sh.L * sh.Hq * sh.D * 2,
-        "k_qm_update<T, 128>": units * s.R * (s.qe - s.qs) * sh.D * 2 + 2 * mem_bytes,
-        "k_select": s.N * (4 + 4 + 1),
-        "k_select_small": s.N * (4 + 4 + 1),
+        "k_score_ws<true>": key_bytes + mem_bytes + n_scored * 4 + n_scored * sh.D * 4,
+        "k_score_ws<false>": key_bytes + mem_bytes + n_scored * 4,
+        "k_decode_split<T, D, G>": kv_live + q_rows,
+        "k_decode_heads<G>": kv_live + q_rows,
+        "k_qm_update<T, 128>": span_bytes,
+        "k_select": sum(Ns) * (4 + 4 + 1),
+        "k_select_small": sum(Ns) * (4 + 4 + 1),
         "k_residual_mfma": nA * (sh.D * 4 + 4 + 4),
-        "k_redirect<bytes>": s.N * (4 + 1 + 4 + 4),
+        "k_redirect<bytes>": sum(Ns) * (4 + 1 + 4 + 4),
     }
     kernels = {}
     for name, v in per_kernel.items():
@@ -264,9 +306,11 @@ def main() -> int:
         "value": round(tokens_per_s, 1), "unit": "history tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": wname, "L": sh.L, "Hq": sh.Hq, "Hkv": sh.Hkv, "D": sh.D, "N": s.N, "C": s.C,
-                   "R": s.R, "kv_storage": "bf16" if batch.kv_dtype == synth.BF16 else "f32",
-                   "residual": bool(flags), "memory_update": True, "candidates": nA, "n_keep": n_keep,
+        "config": {"workload": wname, "L": sh.L, "Hq": sh.Hq, "Hkv": sh.Hkv, "D": sh.D,
+                   "sessions": len(batch.sessions), "N": s.N if len(Ns) == 1 else [min(Ns), max(Ns)],
+                   "positions": sum(Ns), "C": s.C, "R": s.R if len(set(Rs)) == 1 else [min(Rs), max(Rs)],
+                   "kv_storage": "bf16" if batch.kv_dtype == synth.BF16 else "f32",
+                   "residual": bool(flags), "memory_update": mem_update, "candidates": nA, "n_keep": n_keep,
                    "n_live": n_live},
         "decode_attn_gbs": round(decode_gbs, 1), "decode_hbm_frac": round(decode_gbs / HBM_PEAK_GBS, 4),
         "phase_ms": {n: round(float(v), 4) for n, v in zip(names, phase_ms)},
@@ -275,8 +319,9 @@ def main() -> int:
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        log(f"cpu baseline (oracle, {args.cpu_layers} layers)")
-        out["cpu_baseline"] = cpu_baseline(batch, blob, flags, args.cpu_layers)
+        layers = args.cpu_layers if args.cpu_layers is not None else (36 if batch.k_pool is not None else 8)
+        log(f"cpu baseline (oracle, {layers} layers)")
+        out["cpu_baseline"] = cpu_baseline(batch, blob, flags, layers)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -30,7 +30,8 @@ class RetentionStep:
     qpos_off, q_dec.
     """
 
-    def __init__(self, batch, device, residual=None, flags: int = 0, lam: float = 0.5, dead_slot: int = 0):
+    def __init__(self, batch, device, residual=None, flags: int = 0, lam: float = 0.5, dead_slot: int = 0,
+                 k_dev=None, v_dev=None):
         import torch
         self.device = device
         sh = batch.shape
@@ -39,8 +40,9 @@ class RetentionStep:
         self.dead = dead_slot
         self.lam = lam
         self.flags = flags
-        self.k_pool = _t(batch.k_pool, device)
-        self.v_pool = _t(batch.v_pool, device)
+        # pools already on the device (too large to draw on the host) or uploaded here
+        self.k_pool = k_dev if k_dev is not None else _t(batch.k_pool, device)
+        self.v_pool = v_dev if v_dev is not None else _t(batch.v_pool, device)
         self.pool = ikv.make_pool(self.k_pool, self.v_pool, sh.L, sh.Hq, sh.Hkv, sh.D, batch.num_slots, dead_slot)
         self.S0 = _t(batch.slot_maps.astype(np.int32), device)
         self.S = self.S0.clone()

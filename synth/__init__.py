@@ -476,11 +476,15 @@ _GAMMA = np.uint64(0x9E3779B97F4A7C15)
 _SYNTH_LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsynth.so")
 
 
+def f32_to_bf16(x) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest even), as uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+
+
 def table(seed: int, tensor: int, D: int, log2_T: int = TABLE_LOG2) -> np.ndarray:
     """2^log2_T + D N(0,1) values rounded to bf16 (nearest even), as uint16 bits."""
-    x = stream(seed, tensor).standard_normal((1 << log2_T) + D, dtype=np.float32)
-    u = x.view(np.uint32)
-    return ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+    return f32_to_bf16(stream(seed, tensor).standard_normal((1 << log2_T) + D, dtype=np.float32))
 
 
 def table_key(seed: int, tensor: int) -> int:
@@ -551,3 +555,52 @@ def build_native(verbose: bool = False) -> str:
     if verbose:
         print(f"built {_SYNTH_LIB}")
     return _SYNTH_LIB
+
+
+# ----------------------------------------------------------------------------- the batched share
+def batched_share_full(seed: int = 5, B: int = 64) -> Batch:
+    """The batched one-GPU share at full size: B sessions in the shape of one GPU's half of
+    a Qwen2.5-14B tensor-parallel pair (48 layers, 20 query / 4 KV heads, D = 128), N ~
+    U{4096..65536}, R ~ 16 U{2..8}, budget 8192, the last 64 positions the query span and
+    the cross-attention queries, one shared paged pool. Keys and values are not drawn
+    here (k_pool = v_pool = None): fill_share_pools() writes them on the GPU, and
+    share_rows() regenerates any rows on the host. No span rows (no memory update)."""
+    g = stream(seed, T_TURNS, 2)
+    Ns = [int(n) for n in g.integers(4096, 65537, B)]
+    Rs = [int(r) for r in 16 * g.integers(2, 9, B)]
+    shape = Shape(L=48, Hq=20, Hkv=4, D=128)
+    alloc, num_slots = paged_slots(Ns, seed, 16, spare_pages=64)
+    sessions = [SessionSpec(N=n, C=8192, pi=0, qs=n - 64, qe=n, R=r) for n, r in zip(Ns, Rs)]
+    slot_maps = np.concatenate(alloc).astype(np.int32)
+    slot_off = np.concatenate([[0], np.cumsum(Ns)[:-1]]).astype(np.int64)
+    Ms, mem_off, om = [], np.zeros(B, np.int64), 0
+    for b in range(B):
+        mem_off[b] = om
+        Ms.append(stream(seed, T_M, b).standard_normal((shape.L, shape.Hkv * Rs[b], shape.D), dtype=np.float32).ravel())
+        om += Ms[-1].size
+    qpos = np.concatenate([np.arange(n - 64, n) for n in Ns]).astype(np.int32)
+    q_dec = np.stack([f32_to_bf16(stream(seed, T_QDEC, b).standard_normal((shape.L, shape.Hq, shape.D),
+                                                                          dtype=np.float32)) for b in range(B)])
+    return Batch(shape=shape, kv_dtype=BF16, sessions=sessions, num_slots=num_slots, k_pool=None, v_pool=None,
+                 slot_maps=slot_maps, slot_off=slot_off, M=np.concatenate(Ms), mem_off=mem_off,
+                 q_span=np.zeros(0, np.uint16), qspan_off=np.zeros(B, np.int64), qpos=qpos,
+                 qpos_off=64 * np.arange(B, dtype=np.int64), q_dec=q_dec)
+
+
+def fill_share_pools(k, v, batch: Batch, seed: int = 5) -> None:
+    """Write every key and value row of the batched share's pool on the GPU (device bf16
+    tensors [L][num_slots][Hkv][D]) from the seeded tables."""
+    import torch
+    sh = batch.shape
+    for pool, tensor in ((k, T_TABLE_K), (v, T_TABLE_V)):
+        tab = table(seed, tensor, sh.D)
+        tab_dev = torch.from_numpy(tab.view(np.int16)).to(pool.device)
+        device_table_rows(pool, sh.L, batch.num_slots, sh.Hkv, sh.D, None, tab_dev, table_key(seed, tensor))
+
+
+def share_rows(batch: Batch, slots, values: bool = False, seed: int = 5) -> np.ndarray:
+    """Host copy of the batched share's key (or value) rows at `slots`: [L][len][Hkv][D]."""
+    sh = batch.shape
+    tensor = T_TABLE_V if values else T_TABLE_K
+    return table_rows(table(seed, tensor, sh.D), sh.L, batch.num_slots, sh.Hkv, sh.D, slots,
+                      table_key(seed, tensor))
