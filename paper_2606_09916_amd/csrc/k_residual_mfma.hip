@@ -26,7 +26,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int RD = 128;          // head dimension of this path
 constexpr int RW = 16;           // candidates per wave
-constexpr int RT = 4 * RW;       // candidates per workgroup
+constexpr int RWAVES = 8;        // waves per workgroup (one workgroup per CU)
+constexpr int RT = RWAVES * RW;  // candidates per workgroup
+constexpr int RKI = 16 / RWAVES; // 1-KB loads per wave per weight stage
 static_assert(HC == 128 && HC_HEADS == 4 && HIDDEN == 256, "fragment layout of this path");
 
 __device__ __forceinline__ bf16x8 ld8(const uint16_t *p) { return *reinterpret_cast<const bf16x8 *>(p); }
@@ -61,14 +63,15 @@ __device__ __forceinline__ float erf_as(float x) {
 
 __device__ __forceinline__ float gelu_as(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 
-// The weights stream once per workgroup through a 4-stage LDS ring of 16 KB stages
-// (direct global->LDS loads, waits placed by hand), shared by the four waves:
+// The weights stream once per workgroup through a 9-stage LDS ring of 16 KB stages
+// (direct global->LDS loads, eight stages in flight, waits placed by hand), shared by
+// the eight waves:
 //   stages 0..3    rows 32 s .. + 31 of A_Q, hi then lo;
 //   stages 4..7    K' then V' fragments of head s - 4;
 //   stages 8..23   rows 16 ob .. + 15 of A_1 (hi, lo) and of W_1^c (hi, lo), ob = s - 8.
 // Weight rows are 256 B with 16-byte chunk c of row r at slot c ^ (r & 15), so the 16
 // rows of a fragment read hit distinct banks.
-constexpr int RS_STAGES = 4;
+constexpr int RS_STAGES = 9;
 constexpr int RS_STAGE = 8192;                   // bf16 per stage (16 KB)
 constexpr int RS_NSTAGE = 24;
 
@@ -79,7 +82,21 @@ __device__ __forceinline__ void dma16r(const void *g, uint32_t lds_base) {
                : "memory", "m0");
 }
 
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+// s_waitcnt vmcnt(n) for a wave-uniform even n in 0..14
+__device__ __forceinline__ void rs_wait(int n) {
+  switch (n) {
+    case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+    case 14: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+}
+
+__global__ void __launch_bounds__(64 * RWAVES) __attribute__((amdgpu_waves_per_eu(2)))
 k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, int dead,
                 float *__restrict__ scores, const float *__restrict__ ws, const float *__restrict__ shared,
                 const float *__restrict__ blob, int L, int Hkv, bool xattn) {
@@ -120,8 +137,8 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
   const bool cand = j < s.N && slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
   if (!__syncthreads_or(cand)) return;
   const float rule = out[jc];
-  for (int k = t; k < 2 * (HC + HIDDEN); k += 256) cst[k] = c0[k];
-  for (int k = t; k < HIDDEN; k += 256) cst[2 * (HC + HIDDEN) + k] = blob[oW2 + k];
+  for (int k = t; k < 2 * (HC + HIDDEN); k += 64 * RWAVES) cst[k] = c0[k];
+  for (int k = t; k < HIDDEN; k += 64 * RWAVES) cst[2 * (HC + HIDDEN) + k] = blob[oW2 + k];
 
   // kbar^T as the B operand: lane (g, i) holds channels 32 ks + 8 g .. + 7 of its candidate
   bf16x8 xh[4], xl[4];
@@ -144,14 +161,14 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // stage st, wave w, instruction k fills 1 KB: n = 4 w + k
+  // stage st, wave w, instruction k fills 1 KB: n = RKI w + k
   const uint32_t ring0 = uint32_t(reinterpret_cast<uintptr_t>(ring));
   auto issue = [&](int st) {
     if (st >= RS_NSTAGE) return;
     const uint32_t dst = ring0 + uint32_t((st % RS_STAGES) * RS_STAGE * 2);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int n = 4 * w + k;
+    for (int k = 0; k < RKI; ++k) {
+      const int n = RKI * w + k;
       const uint16_t *src;
       if (st < 4) {                                // 32 rows of A_Q: hi (n < 8), lo
         const int r = 4 * (n & 7) + (lane >> 4);
@@ -168,12 +185,9 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
     }
   };
   // top of stage st: its loads are done once at most those of the later stages already
-  // issued (four each) are outstanding; the barrier also frees the buffer of stage st - 1
+  // issued (RKI each) are outstanding; the barrier also frees the buffer of stage st - 1
   auto advance = [&](int st) {
-    const int later = min(RS_STAGES - 2, RS_NSTAGE - 1 - st);
-    if (later >= 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (later == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    rs_wait(RKI * min(RS_STAGES - 2, RS_NSTAGE - 1 - st));
     __syncthreads();
     issue(st + RS_STAGES - 1);
     return ring + (st % RS_STAGES) * RS_STAGE;
@@ -305,7 +319,7 @@ hipError_t launch_residual_mfma(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   {
     KTimer kt_("k_residual_mfma", st);
-    k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, RT)), a.B), 256, 0, st>>>(
+    k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, RT)), a.B), 64 * RWAVES, 0, st>>>(
         a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
         (a.flags & IKV_NO_XATTN) == 0);
   }
