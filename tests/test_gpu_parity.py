@@ -189,6 +189,26 @@ def test_step_batched_d128_matrix_cores(dev):
         _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, True)
 
 
+def test_step_batched_d128_mixed_row_counts(dev):
+    """Sessions of up to 64 and of more memory rows in one batch: each score pass runs
+    one launch per kind, and each launch skips the other kind's sessions. One session is
+    at its budget (skipped), others carry dead positions, a forced prefix and a
+    protected radix prefix."""
+    shape = synth.Shape(L=2, Hq=8, Hkv=2, D=128)
+    sessions = [synth.SessionSpec(N=1100, C=300, pi=8, qs=1080, qe=1100, R=96, dead_frac=0.1),
+                synth.SessionSpec(N=700, C=200, pi=0, qs=650, qe=700, R=32),
+                synth.SessionSpec(N=400, C=400, pi=0, qs=380, qe=400, R=128),
+                synth.SessionSpec(N=1500, C=150, pi=16, qs=1440, qe=1500, R=128, radix_prefix=16),
+                synth.SessionSpec(N=900, C=500, pi=0, qs=860, qe=900, R=16, dead_frac=0.2)]
+    batch = synth.make_batch(shape, sessions, seed=43, kv_dtype=synth.BF16, layout="paged", spare_pages=4)
+    blob = synth.residual_blob(128, seed=44)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    st.step(update_memory=True)
+    for b in range(len(sessions)):
+        _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, True)
+
+
 # ============================================================================ Eqs. 4-6
 
 @pytest.mark.parametrize("variant,flags", [("random", ikv.IKV_RESIDUAL), ("random", ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN),
