@@ -134,7 +134,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_8b_32k")
     ap.add_argument("--R", type=int, default=64)
-    ap.add_argument("--no-residual", action="store_true")
+    ap.add_argument("--no-residual", action="store_true", help="the rule score alone (the '- residual' ablation)")
+    ap.add_argument("--no-xattn", action="store_true", help="residual head without its cross-attention")
+    ap.add_argument("--query-mode", action="store_true", help="memory update with lambda = inf (no history)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=None,
                     help="layers of the CPU baseline sample (default 36; 8 for a pool drawn on the GPU)")
@@ -158,7 +160,7 @@ def main() -> int:
     batch, wname = workload(args.workload, args.R)
     sh = batch.shape
     s = batch.sessions[0]
-    flags = 0 if args.no_residual else ikv.IKV_RESIDUAL
+    flags = 0 if args.no_residual else ikv.IKV_RESIDUAL | (ikv.IKV_NO_XATTN if args.no_xattn else 0)
     blob = synth.residual_blob(sh.D, seed=22)
     mem_update = len(batch.q_span) > 0              # a workload without span rows has no memory update
     log("uploading")
@@ -179,7 +181,7 @@ def main() -> int:
         st.reset()
         evs[1].record()
         if mem_update:
-            st.qm_update()
+            st.qm_update(float("inf") if args.query_mode else None)
         evs[2].record()
         st.score()
         evs[3].record()
@@ -310,7 +312,9 @@ def main() -> int:
                    "sessions": len(batch.sessions), "N": s.N if len(Ns) == 1 else [min(Ns), max(Ns)],
                    "positions": sum(Ns), "C": s.C, "R": s.R if len(set(Rs)) == 1 else [min(Rs), max(Rs)],
                    "kv_storage": "bf16" if batch.kv_dtype == synth.BF16 else "f32",
-                   "residual": bool(flags), "memory_update": mem_update, "candidates": nA, "n_keep": n_keep,
+                   "residual": bool(flags), "cross_attention": bool(flags) and not args.no_xattn,
+                   "memory_update": "query mode" if (mem_update and args.query_mode) else mem_update,
+                   "candidates": nA, "n_keep": n_keep,
                    "n_live": n_live},
         "decode_attn_gbs": round(decode_gbs, 1), "decode_hbm_frac": round(decode_gbs / HBM_PEAK_GBS, 4),
         "phase_ms": {n: round(float(v), 4) for n, v in zip(names, phase_ms)},
