@@ -96,8 +96,7 @@ def cpu_baseline(batch, blob, flags, layers: int):
     Ls = min(layers, sh.L)
     if batch.k_pool is None:                         # pool on the GPU only: rebuild the sample's rows
         kc = np.zeros((Ls, s.N + 1, sh.Hkv, sh.D), np.uint16)
-        kc[:, 1:] = synth.table_rows(synth.table(5, synth.T_TABLE_K, sh.D), Ls, batch.num_slots, sh.Hkv, sh.D,
-                                     S, synth.table_key(5, synth.T_TABLE_K))
+        kc[:, 1:] = synth.share_rows(batch, S, layers=Ls)
         kp, S = kc, np.arange(1, s.N + 1, dtype=np.int32)
         vp = None
     else:

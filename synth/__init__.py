@@ -581,26 +581,30 @@ def batched_share_full(seed: int = 5, B: int = 64) -> Batch:
     qpos = np.concatenate([np.arange(n - 64, n) for n in Ns]).astype(np.int32)
     q_dec = np.stack([f32_to_bf16(stream(seed, T_QDEC, b).standard_normal((shape.L, shape.Hq, shape.D),
                                                                           dtype=np.float32)) for b in range(B)])
-    return Batch(shape=shape, kv_dtype=BF16, sessions=sessions, num_slots=num_slots, k_pool=None, v_pool=None,
-                 slot_maps=slot_maps, slot_off=slot_off, M=np.concatenate(Ms), mem_off=mem_off,
-                 q_span=np.zeros(0, np.uint16), qspan_off=np.zeros(B, np.int64), qpos=qpos,
-                 qpos_off=64 * np.arange(B, dtype=np.int64), q_dec=q_dec)
+    batch = Batch(shape=shape, kv_dtype=BF16, sessions=sessions, num_slots=num_slots, k_pool=None, v_pool=None,
+                  slot_maps=slot_maps, slot_off=slot_off, M=np.concatenate(Ms), mem_off=mem_off,
+                  q_span=np.zeros(0, np.uint16), qspan_off=np.zeros(B, np.int64), qpos=qpos,
+                  qpos_off=64 * np.arange(B, dtype=np.int64), q_dec=q_dec)
+    batch.table_seed = seed                        # the seed of the tables its rows come from
+    return batch
 
 
-def fill_share_pools(k, v, batch: Batch, seed: int = 5) -> None:
+def fill_share_pools(k, v, batch: Batch) -> None:
     """Write every key and value row of the batched share's pool on the GPU (device bf16
     tensors [L][num_slots][Hkv][D]) from the seeded tables."""
     import torch
     sh = batch.shape
     for pool, tensor in ((k, T_TABLE_K), (v, T_TABLE_V)):
-        tab = table(seed, tensor, sh.D)
+        tab = table(batch.table_seed, tensor, sh.D)
         tab_dev = torch.from_numpy(tab.view(np.int16)).to(pool.device)
-        device_table_rows(pool, sh.L, batch.num_slots, sh.Hkv, sh.D, None, tab_dev, table_key(seed, tensor))
+        device_table_rows(pool, sh.L, batch.num_slots, sh.Hkv, sh.D, None, tab_dev,
+                          table_key(batch.table_seed, tensor))
 
 
-def share_rows(batch: Batch, slots, values: bool = False, seed: int = 5) -> np.ndarray:
-    """Host copy of the batched share's key (or value) rows at `slots`: [L][len][Hkv][D]."""
+def share_rows(batch: Batch, slots, values: bool = False, layers: int | None = None) -> np.ndarray:
+    """Host copy of the batched share's key (or value) rows at `slots`: [layers][len][Hkv][D]
+    (the first `layers` layers, every layer by default)."""
     sh = batch.shape
     tensor = T_TABLE_V if values else T_TABLE_K
-    return table_rows(table(seed, tensor, sh.D), sh.L, batch.num_slots, sh.Hkv, sh.D, slots,
-                      table_key(seed, tensor))
+    return table_rows(table(batch.table_seed, tensor, sh.D), sh.L if layers is None else layers, batch.num_slots,
+                      sh.Hkv, sh.D, slots, table_key(batch.table_seed, tensor))

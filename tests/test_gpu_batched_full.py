@@ -4,10 +4,11 @@ of a Qwen2.5-14B tensor-parallel pair (48 layers, 20 query / 4 KV heads, D = 128
 last 64 positions the query span and the cross-attention queries, residual head on;
 one scoring + selection + redirect + decode pass over the whole batch, as one call
 each. The pool holds 210 GiB of bf16 keys and values, too much to draw on the host:
-keys and values are filled on the GPU from seeded tables (synth.fill_share_pools). Every session's kept count, slot map, freed
-list and live list are checked against their definitions; four sessions (the longest,
-the shortest, the shortest above its budget, one with the most memory rows) against the
-float64 oracle on rows regenerated on the host (synth.table_rows)."""
+they are filled on the GPU from seeded tables (synth.fill_share_pools). Every session's
+kept count, slot map, freed list and live list are checked against their definitions;
+four sessions (the longest, the shortest, the shortest above its budget, one with the
+most memory rows) against the float64 oracle on rows regenerated on the host
+(synth.share_rows)."""
 import numpy as np
 import pytest
 
@@ -66,12 +67,12 @@ def test_batched_share_full_size(dev):
 
     k = torch.empty((L, num_slots, HKV, D), dtype=torch.bfloat16, device=dev)
     v = torch.empty((L, num_slots, HKV, D), dtype=torch.bfloat16, device=dev)
-    synth.fill_share_pools(k, v, batch, SEED)
+    synth.fill_share_pools(k, v, batch)
     lap("fill keys and values")
     # spot check of the fill: rows of the last layer at a few slots, against the host
     probe = np.array([1, num_slots // 2, num_slots - 1])
     got = k[L - 1, torch.from_numpy(probe).to(dev)].view(torch.int16).cpu().numpy().view(np.uint16)
-    assert np.array_equal(got, synth.share_rows(batch, probe, seed=SEED)[L - 1])
+    assert np.array_equal(got, synth.share_rows(batch, probe)[L - 1])
     st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL, k_dev=k, v_dev=v)
     st.init_dead_slot()
     lap("inputs")
@@ -117,7 +118,7 @@ def test_batched_share_full_size(dev):
         sl = slice(slot_off[b], slot_off[b] + N)
         Sb = slot_maps[sl]
         kc = np.zeros((L, N + 1, HKV, D), np.uint16)     # compact pool: position j at row j + 1
-        kc[:, 1:] = synth.share_rows(batch, Sb, seed=SEED)
+        kc[:, 1:] = synth.share_rows(batch, Sb)
         Sc = np.arange(1, N + 1, dtype=np.int32)
         sets = oracle.sets(Sc, 0, N - SPAN, N, C, 0)
         want = oracle.scores(kc, Sc, sets, batch.M_of(b), HKV, R, blob, oracle.FLAG_RESIDUAL,
@@ -135,8 +136,8 @@ def test_batched_share_full_size(dev):
         assert np.array_equal(fr[slot_off[b]:slot_off[b] + nf[b]], freed_o)
         kl = np.zeros((L, n + 1, HKV, D), np.uint16)
         vl = np.zeros((L, n + 1, HKV, D), np.uint16)
-        kl[:, 1:] = synth.share_rows(batch, live_o, seed=SEED)
-        vl[:, 1:] = synth.share_rows(batch, live_o, values=True, seed=SEED)
+        kl[:, 1:] = synth.share_rows(batch, live_o)
+        vl[:, 1:] = synth.share_rows(batch, live_o, values=True)
         o_o = oracle.decode(batch.q_dec[b], kl, vl, np.arange(1, n + 1))
         err = check_attention(synth.widen(o_all[b]), o_o, bf16=True)
         print(f"session {b}: N={N} R={R} score rel err {rel:.2e}, attention err {err:.2e}", flush=True)
