@@ -329,6 +329,25 @@ def test_decode_isolated(dev, kind, frac):
     check_attention(got, want, bf16=(kind == "bf16"))
 
 
+@pytest.mark.parametrize("Hkv,G,n_live", [(1, 1, 700), (2, 2, 129), (3, 3, 64), (4, 4, 1000), (8, 5, 300),
+                                          (2, 6, 513), (4, 7, 77), (8, 8, 2100)])
+def test_decode_heads_kernel_variants(dev, Hkv, G, n_live):
+    """bf16 pool, D = 128: the head-group decode with one, two or four KV heads per
+    workgroup (Hkv odd, 2 mod 4, 0 mod 4), G from 1 to 8, live lists that end inside
+    a 64-slot block or on its boundary, against the oracle."""
+    torch = _torch()
+    batch = small_d128(R=16, N=max(2400, n_live + 100), seed=7 * Hkv + G, dead_frac=0.0, L=2, Hkv=Hkv, G=G)
+    S = batch.S(0)
+    live = S[synth.stream(8, synth.T_MISC_KEEP, Hkv * 16 + G).permutation(len(S))[:n_live]].astype(np.int32)
+    st = RetentionStep(batch, dev)
+    st.init_dead_slot()
+    st.live[:len(live)].copy_(torch.from_numpy(live).to(dev))
+    st.n_live.fill_(len(live))
+    st.decode()
+    want = oracle.decode(batch.q_dec[0], batch.k_pool, batch.v_pool, live)
+    check_attention(synth.widen(st.host("out")[0]), want, bf16=True)
+
+
 def test_decode_empty_live_list(dev):
     batch = synth.tiny_single_layer()
     st = RetentionStep(batch, dev)
