@@ -12,26 +12,6 @@
 
 namespace ikv {
 
-// Offsets (floats) of the parameter blocks in the packed blob.
-struct ResLayout {
-  int64_t WQ, bQ, WK, bK, WV, bV, W1, b1, w2, b2, alpha, total;
-  __host__ __device__ explicit ResLayout(int D) {
-    const int64_t F = 3 * D + 1;
-    WQ = 0;
-    bQ = WQ + HC * F;
-    WK = bQ + HC;
-    bK = WK + int64_t(HC) * D;
-    WV = bK + HC;
-    bV = WV + int64_t(HC) * D;
-    W1 = bV + HC;
-    b1 = W1 + int64_t(HIDDEN) * (F + HC);
-    w2 = b1 + HIDDEN;
-    b2 = w2 + HIDDEN;
-    alpha = b2 + 1;
-    total = alpha + 1;
-  }
-};
-
 int64_t residual_floats(int D) { return ResLayout(D).total; }
 
 // W_Q^T [F][HC] and W_1^T [F+HC][HIDDEN] so that consecutive threads read consecutive
@@ -99,16 +79,11 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
   res_setup_body<D>(sess, int(blockIdx.x), slot_maps, qpos, dead, ws, L, Hkv, mfma, pairs);
 }
 
-// K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup.
-// With `frag` (D = 128, at most RES_KEYS rows) the grid covers all RES_KEYS rows and
-// also writes them as bf16 hi + lo MFMA fragments, zeros past the live rows:
-//   K' [head][key block kb][hi|lo][lane 16 g + i][8]: key 16 kb + i, channels
-//      32 head + perm32(g, e) (the A operand of the logits block);
-//   V' [head][channel block nb][key step ks][hi|lo][lane 16 g + i][8]: channel
-//      32 head + 16 nb + i, keys 32 ks + perm32(g, e) (the A operand of the context).
+// K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup,
+// kq = kbar at the live query positions (from the second pass).
 template <int D>
 __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                            float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
+                                            float *__restrict__ ws, int L, int Hkv, bool mfma) {
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
@@ -122,12 +97,12 @@ __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restric
   const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
   const int *qlist = reinterpret_cast<const int *>(base + z.off_qlist());
   const int i0 = bx * 4;
-  if (i0 >= n && !frag) return;
+  if (i0 >= n) return;
   __shared__ float kq[4][D];
   const int t = threadIdx.x;
   for (int e = t; e < 4 * D; e += 256) {
     const int r = e / D, d = e - r * D;
-    const int q = n > 0 ? qlist[min(i0 + r, n - 1)] : 0;   // a live row (or row 0) stands in past n
+    const int q = qlist[min(i0 + r, n - 1)];          // a live row stands in past n
     const float v = kbar[int64_t(q) * D + d];
     kq[r][d] = (i0 + r < n) ? v : 0.f;
   }
@@ -152,105 +127,12 @@ __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restric
 #pragma unroll
   for (int r = 0; r < 4; ++r)
     if (i0 + r < n) dst[int64_t(i0 + r) * HC + o] = a[r];
-  if (!frag) return;
-  uint16_t *kf = reinterpret_cast<uint16_t *>(base + z.off_kvf());
-  uint16_t *vf = kf + KVF_BF16 / 2;
-  const int head = o >> 5, c = o & 31;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int key = i0 + r;
-    const float v = key < n ? a[r] : 0.f;
-    const uint16_t hi = float_to_bf16_bits(v), lo = float_to_bf16_bits(v - bf16_bits_to_float(hi));
-    if (!isv) {
-      const int k = perm32_inv(c), kb = key >> 4, lane = 16 * (k >> 3) + (key & 15);
-      const int64_t at = int64_t((head * 4 + kb) * 2) * 512 + lane * 8 + (k & 7);
-      kf[at] = hi;
-      kf[at + 512] = lo;
-    } else {
-      const int nb = c >> 4, ks = key >> 5, k = perm32_inv(key & 31), lane = 16 * (k >> 3) + (c & 15);
-      const int64_t at = int64_t(((head * 2 + nb) * 2 + ks) * 2) * 512 + lane * 8 + (k & 7);
-      vf[at] = hi;
-      vf[at + 512] = lo;
-    }
-  }
 }
 
 template <int D>
 __global__ void __launch_bounds__(256) k_res_kv(const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                                float *__restrict__ ws, int L, int Hkv, bool mfma, bool frag) {
-  res_kv_body<D>(int(blockIdx.x), sess, blob, ws, L, Hkv, mfma, frag);
-}
-
-// Folded first layer of one session (exact in real arithmetic):
-//   W_Q phi + b_Q  = (W_Q^k + W_Q^km diag(mbar)) kbar + (W_Q^m mbar + b_Q) + w_Q^r rule
-//   W_1 [phi; c] + b_1 = (W_1^k + W_1^km diag(mbar)) kbar + (W_1^m mbar + b_1) + w_1^r rule + W_1^c c
-// Rows 0..HC-1 of the folded matrix are the W_Q part, rows HC.. the W_1 part; stored
-// as bf16 hi [HC+HIDDEN][D] then lo, then q0 [HC] and h0 [HIDDEN] in float32, then
-// the rule column w_Q^r [HC] and w_1^r [HIDDEN].
-template <int D>
-__device__ __forceinline__ void res_fold_body(int bx, const ikv_session *__restrict__ sess, const float *__restrict__ blob,
-                                              float *__restrict__ ws, float *__restrict__ shared, int L, int Hkv) {
-  const int b = blockIdx.y;
-  const ikv_session s = sess[b];
-  uint16_t *w1c = reinterpret_cast<uint16_t *>(shared + align64f(int64_t(3 * D + 1) * HC) +
-                                                align64f(int64_t(3 * D + 1 + HC) * HIDDEN));
-  if (s.N <= s.C && b != 0) return;
-  const int units = L * Hkv;
-  const ResLayout lay(D);
-  const int64_t F = 3 * D + 1;
-  const ScoreSizes z = score_sizes(s, L, units, D, true, true);
-  float *base = ws + score_offset(sess, b, L, units, D, true, true);
-  const float *mbar = base + z.off_misc() + int64_t(MBAR_PARTS) * D;
-  float *fold = base + z.off_fold();
-  uint16_t *hi = reinterpret_cast<uint16_t *>(fold);
-  uint16_t *lo = hi + int64_t(HC + HIDDEN) * D;
-  float *q0 = fold + int64_t(HC + HIDDEN) * D;
-  const int64_t i = int64_t(bx) * 256 + threadIdx.x;
-  const int64_t nw = int64_t(HC + HIDDEN) * D;
-  if (s.N <= s.C && i < nw + 2 * (HC + HIDDEN)) return;   // skipped session: only the shared part
-  if (i < nw) {
-    const int64_t o = i / D, d = i - o * D;
-    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
-    const float v = fmaf(row[2 * D + d], mbar[d], row[d]);
-    const uint16_t h = float_to_bf16_bits(v);
-    hi[i] = h;
-    lo[i] = float_to_bf16_bits(v - bf16_bits_to_float(h));
-  } else if (i < nw + HC + HIDDEN) {
-    const int64_t o = i - nw;
-    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
-    float a = o < HC ? blob[lay.bQ + o] : blob[lay.b1 + (o - HC)];
-    float rv[D];                                      // the whole row in flight at once
-#pragma unroll
-    for (int d = 0; d < D; ++d) rv[d] = row[D + d];
-#pragma unroll
-    for (int d = 0; d < D; ++d) a = fmaf(rv[d], mbar[d], a);
-    q0[o] = a;
-  } else if (i < nw + 2 * (HC + HIDDEN)) {          // the rule column
-    const int64_t o = i - nw - (HC + HIDDEN);
-    const float *row = o < HC ? blob + lay.WQ + o * F : blob + lay.W1 + (o - HC) * (F + HC);
-    q0[HC + HIDDEN + o] = row[3 * D];
-  } else if (b == 0 && i < nw + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC) {
-    // shared by every session: the cross-attention columns of W_1 as bf16 hi + lo
-    // [HIDDEN][HC], each 32-wide head block in the MFMA k order of perm32
-    const int64_t k = i - nw - 2 * (HC + HIDDEN), nc = int64_t(HIDDEN) * HC;
-    const int64_t o = k / HC, c = k - o * HC;
-    const float v = blob[lay.W1 + o * (F + HC) + F + c];
-    const uint16_t h = float_to_bf16_bits(v);
-    const int64_t at = o * HC + (c & ~int64_t(31)) + perm32_inv(int(c & 31));
-    w1c[at] = h;
-    w1c[nc + at] = float_to_bf16_bits(v - bf16_bits_to_float(h));
-  }
-}
-
-// The fold (res_fold_body, first nfold workgroups) and, after it in the same launch,
-// K' and V' of the live query rows as fragments (res_kv_body, RES_KEYS / 4 workgroups):
-// both need only the set-up and the mean key rows.
-template <int D>
-__global__ void __launch_bounds__(256) k_res_fold_kv(const ikv_session *__restrict__ sess,
-                                                     const float *__restrict__ blob, float *__restrict__ ws,
-                                                     float *__restrict__ shared, int L, int Hkv, int nfold) {
-  if (int(blockIdx.x) < nfold) res_fold_body<D>(int(blockIdx.x), sess, blob, ws, shared, L, Hkv);
-  else res_kv_body<D>(int(blockIdx.x) - nfold, sess, blob, ws, L, Hkv, true, true);
+                                                float *__restrict__ ws, int L, int Hkv, bool mfma) {
+  res_kv_body<D>(int(blockIdx.x), sess, blob, ws, L, Hkv, mfma);
 }
 
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
@@ -449,19 +331,11 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
     {
       KTimer kt_("k_res_kv<D>", st);
       k_res_kv<D><<<dim3(unsigned(cdiv(a.maxNq, 4)), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws, p.L, p.Hkv,
-                                                                         a.mfma, false);
+                                                                         a.mfma);
     }
-  if (a.mfma_resid) {
-    {
-      const int nfold = int(cdiv(int64_t(HC + HIDDEN) * D + 2 * (HC + HIDDEN) + int64_t(HIDDEN) * HC, 256));
-      KTimer kt_("k_res_fold_kv<D>", st);
-      k_res_fold_kv<D><<<dim3(unsigned(nfold + RES_KEYS / 4), a.B), 256, 0, st>>>(a.sess_dev, a.residual, a.ws,
-                                                                                 a.ws_shared, p.L, p.Hkv, nfold);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_residual_mfma(a, st);
-  }
+  // on the matrix-core path the row-statistics launch also folded the first layer and
+  // built the K', V' fragments
+  if (a.mfma_resid) return launch_residual_mfma(a, st);
   {
     KTimer kt_("k_residual<D>", st);
     k_residual<D><<<dim3(unsigned(cdiv(a.maxN, 32)), a.B), 256, 0, st>>>(

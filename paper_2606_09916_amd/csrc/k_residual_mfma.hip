@@ -1,13 +1,13 @@
 // Residual head of Eq. 4 (features Eq. 5, cross-attention Eq. 6) on the matrix cores,
 // for D = 128 and at most 64 live query positions per session.
 //
-// With mbar folded into the first-layer weights (k_res_fold_kv), the head of one
-// candidate is a chain of small products on v_mfma_f32_16x16x32_bf16. Each wave owns
-// 16 candidates and keeps its activations in registers: the products run transposed
-// (weights as the A operand, candidates as the columns), so that the accumulator of
-// one product is, lane for lane, the B operand of the next, up to the order of the
-// contraction index inside each 32-wide block (perm32), which the pre-arranged K',
-// V' and W_1^c fragments follow:
+// With mbar folded into the first-layer weights (res_fold_wg, which runs in the
+// row-statistics launch), the head of one candidate is a chain of small products on
+// v_mfma_f32_16x16x32_bf16. Each wave owns 16 candidates and keeps its activations in
+// registers: the products run transposed (weights as the A operand, candidates as the
+// columns), so that the accumulator of one product is, lane for lane, the B operand
+// of the next, up to the order of the contraction index inside each 32-wide block
+// (perm32), which the pre-arranged K', V' and W_1^c fragments follow:
 //   1. Q^T = A_Q kbar^T + q0 + w_Q^r rule                      (128 x 16, K = 128)
 //   2. logits_h^T = K'_h Q_h^T / sqrt(32)                      (per head, 64 x 16, K = 32)
 //   3. c_h^T = V'_h^T softmax(logits_h)^T                      (per head, 32 x 16, K = 64)

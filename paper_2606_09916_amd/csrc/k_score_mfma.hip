@@ -1146,15 +1146,29 @@ inline int stats_chunk(int maxN, int head_pairs) {
 // A workgroup takes 64 consecutive rows; its eight waves split the tiles (lane =
 // row, so each load instruction reads 512 contiguous bytes), fold them online into
 // (max, sum) and merge through LDS in a fixed order. With the residual head on, the
-// last workgroup of each session does the head's set-up instead (res_setup_body),
-// which needs only the first pass.
+// first workgroups of each session do the head's set-up instead, which needs only the
+// first pass: with `kv` (the matrix-core head) RES_KEYS workgroups build K' and V' of
+// one live query row each from the keys (res_kv_keys_wg) and `nfold` fold the first
+// layer (res_fold_wg), then one workgroup writes mbar and the live query positions
+// (res_setup_body).
 __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
                                                   int Hkv, bool resid, int ptile, const int32_t *__restrict__ slot_maps,
-                                                  const int32_t *__restrict__ qpos, int dead, bool pairs) {
+                                                  const int32_t *__restrict__ qpos, int dead, bool pairs, bool kv,
+                                                  int nfold, const uint16_t *__restrict__ kpool, int64_t num_slots,
+                                                  const float *__restrict__ blob, float *__restrict__ shared) {
   __shared__ float sm[8][64], sz[8][64];
   const int b = blockIdx.y;
-  if (resid && blockIdx.x == gridDim.x - 1) {
-    res_setup_body<MD>(sess, b, slot_maps, qpos, dead, ws, L, Hkv, true, pairs);
+  const int nkv = kv ? RES_KEYS : 0;
+  const int extra = resid ? nkv + nfold + 1 : 0;
+  const int bx = int(blockIdx.x) - extra;
+  if (bx < 0) {
+    const int x = int(blockIdx.x);
+    if (x < nkv)
+      res_kv_keys_wg<MD>(x, sess, b, kpool, num_slots, L, Hkv, slot_maps, qpos, dead, blob, ws);
+    else if (x < nkv + nfold)
+      res_fold_wg<MD>(x - nkv, sess, b, blob, ws, shared, L, Hkv, pairs);
+    else
+      res_setup_body<MD>(sess, b, slot_maps, qpos, dead, ws, L, Hkv, true, pairs);
     return;
   }
   const ikv_session s = sess[b];
@@ -1162,8 +1176,8 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   const int units = L * Hkv;
   const int64_t rows = int64_t(units) * s.R;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t i = int64_t(blockIdx.x) * 64 + lane;
-  if (int64_t(blockIdx.x) * 64 >= rows) return;
+  const int64_t i = int64_t(bx) * 64 + lane;
+  if (int64_t(bx) * 64 >= rows) return;
   const bool on = i < rows;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
@@ -1252,10 +1266,16 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
                                                                    a.slot_maps, a.ws, a.scores, resid);
     }
   {
+    // with the matrix-core residual head, this launch also folds its first layer (one
+    // item of fold_items() per thread) and builds K', V'
+    constexpr int FOLD_WGS = int((fold_items<MD>() + 511) / 512);
+    const bool kv = a.mfma_resid;
+    const int nfold = kv ? FOLD_WGS : 0;
+    const int extra = resid ? (kv ? RES_KEYS : 0) + nfold + 1 : 0;
     KTimer kt_("k_lse_mfma", st);
-    k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64) + (resid ? 1 : 0)), a.B), 512, 0, st>>>(
+    k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64) + extra), a.B), 512, 0, st>>>(
         a.sess_dev, a.ws, p.L, p.Hkv, resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE, a.slot_maps, a.qpos,
-        p.dead_slot, a.stats);
+        p.dead_slot, a.stats, kv, nfold, kp, p.num_slots, a.residual, a.ws_shared);
   }
   // the producer/consumer second pass up to 128 memory rows: one launch per kind of
   // session (up to 64 rows, up to 128)
