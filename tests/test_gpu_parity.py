@@ -209,6 +209,39 @@ def test_step_batched_d128_mixed_row_counts(dev):
         _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, True)
 
 
+def test_step_batched_d128_residual_setup_edges(dev):
+    """The residual head's set-up, fold and K', V' on the matrix-core path, at its edges:
+    session 0 at its budget (its workgroups write only the weights every session shares),
+    query lists holding dead positions (the live ones keep their list order), a list
+    with no live position (no cross-attention), and one with exactly 64 live positions
+    (every key row of the fragments)."""
+    shape = synth.Shape(L=2, Hq=8, Hkv=2, D=128)
+    specs = [synth.SessionSpec(N=300, C=300, pi=0, qs=280, qe=300, R=32),
+             synth.SessionSpec(N=1200, C=300, pi=0, qs=1180, qe=1200, R=64, dead_frac=0.3,
+                               qpos=np.zeros(48, np.int32)),
+             synth.SessionSpec(N=900, C=200, pi=0, qs=890, qe=900, R=16, dead_frac=0.3,
+                               qpos=np.zeros(12, np.int32)),
+             synth.SessionSpec(N=1000, C=250, pi=0, qs=936, qe=1000, R=48)]
+    batch = synth.make_batch(shape, specs, seed=47, kv_dtype=synth.BF16, layout="paged", spare_pages=2)
+    dead = [np.flatnonzero(batch.S(b) == synth.DEAD_SLOT) for b in range(len(specs))]
+    live = [np.flatnonzero(batch.S(b) != synth.DEAD_SLOT) for b in range(len(specs))]
+    rng = np.random.default_rng(48)
+    # session 1: 24 dead and 24 live history positions, shuffled; session 2: dead only
+    q1 = np.concatenate([rng.choice(dead[1], 24, replace=False), rng.choice(live[1][:1000], 24, replace=False)])
+    rng.shuffle(q1)
+    q2 = rng.choice(dead[2], 12, replace=False)
+    for b, q in ((1, q1), (2, q2)):
+        specs[b].qpos = q.astype(np.int32)
+        o = int(batch.qpos_off[b])
+        batch.qpos[o:o + len(q)] = q
+    blob = synth.residual_blob(128, seed=49)
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL)
+    st.init_dead_slot()
+    st.step(update_memory=False)
+    for b in range(len(specs)):
+        _compare_step(st, batch, b, blob, ikv.IKV_RESIDUAL, False)
+
+
 # ============================================================================ Eqs. 4-6
 
 @pytest.mark.parametrize("variant,flags", [("random", ikv.IKV_RESIDUAL), ("random", ikv.IKV_RESIDUAL | ikv.IKV_NO_XATTN),
