@@ -10,6 +10,8 @@
 
 #include <stdlib.h>
 
+#include <atomic>
+
 #include "ikv_internal.hpp"
 
 namespace ikv {
@@ -562,45 +564,67 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select_small(const ikv_session 
 // ---- selection across workgroups (a cooperative launch: every workgroup of the grid
 // is resident at once). Each session's positions split into chunks of SC_CHUNK, one
 // workgroup each, holding its keys in LDS; the workgroups of a session meet at
-// barriers on a counter in the workspace. Counts, key range and the radix histograms
-// are summed with integer device-scope atomics (order-free, so the result is
-// deterministic), and every workgroup then takes the same decisions from the same
-// totals: the passes bin the keys still in play by their offset from the smallest
-// candidate key, 11 bits of the actual spread per pass; ties at the threshold are
-// ranked by the same passes over positions.
+// barriers on flags in the workspace. Counts and key range go through per-workgroup
+// partials, the radix histograms are summed with integer device-scope atomics
+// (order-free, so the result is deterministic), and every workgroup then takes the same
+// decisions from the same totals: the passes bin the keys still in play by their
+// offset from the smallest candidate key, 11 bits of the actual spread per pass; ties
+// at the threshold are ranked by the same passes over positions. Nothing in the
+// workspace needs to be cleared beforehand: each workgroup clears its share of the
+// histograms before the first barrier, and the barrier flags carry a stamp that the
+// host draws afresh for every call.
 constexpr int SC_THREADS = 256;
 constexpr int SC_WAVES = SC_THREADS / WAVE;
 constexpr int SC_PER = 4;                              // positions per thread
 constexpr int SC_CHUNK = SC_THREADS * SC_PER;
 constexpr int SC_MAXN = 131072;                        // positions per session on this path
+constexpr int SC_MAXG = SC_MAXN / SC_CHUNK;            // workgroups per session
 constexpr int SC_HIST = 5;                             // histograms: 3 key passes, 2 position passes
-constexpr int SC_WORDS = 64 + SC_HIST * SEL_BINS;      // per session: counters, then histograms
-// counter words: barrier, live count, live forced count, ~(min key), max key
-enum { SC_BAR = 0, SC_NL = 1, SC_NF = 2, SC_NMIN = 3, SC_MAX = 4 };
+constexpr int SC_BARS = 8;                             // stamps per call (at most 1 + 5 barriers)
+// per session: a 64-bit barrier flag per workgroup, four partial words per workgroup
+// (live count, live forced count, ~(min key), max key), then the histograms
+constexpr int SC_PART = 2 * SC_MAXG;
+constexpr int SC_HIST0 = SC_PART + 4 * SC_MAXG;
+constexpr int SC_WORDS = SC_HIST0 + SC_HIST * SEL_BINS;
+static_assert(SC_MAXG <= 2 * WAVE, "the barrier poll reads at most two flags per lane");
 
 __device__ __forceinline__ uint32_t ald(const uint32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void ast(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ void aadd(uint32_t *p, uint32_t v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void amax(uint32_t *p, uint32_t v) {
-  __hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
-// The k-th barrier of a session's G workgroups: wait until the counter reaches k * G.
-// Everything the workgroups exchange is a device-scope atomic, so the barrier needs
-// no cache write-back or invalidation: each thread's atomics are complete once its
-// vector-memory count drains, then one thread adds to the counter and polls it with
-// coherent loads. Every workgroup of the grid is resident (cooperative launch), so the
-// count is reached; the poll is bounded all the same.
-__device__ __forceinline__ void sc_barrier(uint32_t *bar, uint32_t target) {
+// Barrier of a session's G workgroups, stamped `stamp`: workgroup wg sets its flag to
+// the stamp and waits until every flag of the session lies in [stamp, last], the
+// stamps of this barrier and of the call's later ones (a workgroup may already have
+// moved on). The host draws the call's stamps above every earlier call's, so a flag
+// left by an earlier call never passes; one left by other data passes with odds of
+// about 2^-61. Everything the workgroups exchange is a device-scope atomic, so the
+// barrier needs no cache write-back or invalidation: each thread's atomics are
+// complete once its vector-memory count drains, then one thread sets the flag and one
+// wave polls the flags with coherent loads. Every workgroup of the grid is resident
+// (cooperative launch), so every flag is set; the poll is bounded all the same.
+__device__ __forceinline__ void sc_barrier(uint64_t *flags, int G, int wg, uint64_t stamp, uint64_t last) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (threadIdx.x == 0) {
-    aadd(bar, 1u);
+  const int t = threadIdx.x;
+  if (t < WAVE) {
+    if (t == 0) __hip_atomic_store(flags + wg, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     for (uint32_t spin = 0; spin < (1u << 24); ++spin) {
-      if (ald(bar) >= target) break;
+      bool ok = true;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int j = t + k * WAVE;
+        if (j < G) {
+          const uint64_t f = __hip_atomic_load(flags + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ok = ok && f >= stamp && f <= last;
+        }
+      }
+      if (__all(ok)) break;
       __builtin_amdgcn_s_sleep(1);
     }
   }
@@ -684,7 +708,7 @@ __device__ __forceinline__ void sc_find_bin(const uint32_t *gh, uint32_t *lh, in
 // value; *cnt is the number of counted values equal to it.
 template <class Get>
 __device__ uint32_t sc_kth(Get get, uint32_t lo, uint32_t hi, int kk, uint32_t *cw, int hist0, uint32_t *lh,
-                           int *red, int *sh, int &nbar, int G, int &cnt) {
+                           int *red, int *sh, uint64_t &stamp, uint64_t last, int G, int wg, int &cnt) {
   const int t = threadIdx.x;
   int pass = 0;
   cnt = -1;
@@ -702,10 +726,10 @@ __device__ uint32_t sc_kth(Get get, uint32_t lo, uint32_t hi, int kk, uint32_t *
       hist_add(lh, on ? (v - lo) >> shift : 0u, on);
     }
     __syncthreads();
-    uint32_t *gh = cw + 64 + (hist0 + pass) * SEL_BINS;
+    uint32_t *gh = cw + SC_HIST0 + (hist0 + pass) * SEL_BINS;
     for (int i = t; i < SEL_BINS; i += SC_THREADS)
       if (lh[i]) aadd(gh + i, lh[i]);
-    sc_barrier(cw + SC_BAR, uint32_t(++nbar * G));
+    sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last);
     sc_find_bin(gh, lh, kk, red, sh);
     const uint32_t nlo = lo + (uint32_t(sh[0]) << shift);
     hi = shift == 0 ? nlo : min(hi, nlo + ((1u << shift) - 1u));
@@ -722,7 +746,8 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
                                                             const int32_t *__restrict__ slot_maps, int dead,
                                                             const float *__restrict__ scores,
                                                             uint8_t *__restrict__ keep, int32_t *__restrict__ n_keep,
-                                                            float *__restrict__ tau, uint32_t *__restrict__ coop) {
+                                                            float *__restrict__ tau, uint32_t *__restrict__ coop,
+                                                            uint64_t epoch) {
   __shared__ uint32_t ck[SC_CHUNK];                  // keys of this chunk (0: not a candidate)
   __shared__ uint32_t lh[SEL_BINS];
   __shared__ int red[SC_WAVES];
@@ -772,21 +797,29 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
   nf = sc_sum(nf, red);
   nmin = sc_umax(nmin, red);
   kmax = sc_umax(kmax, red);
-  if (t == 0) {
-    aadd(cw + SC_NL, uint32_t(nl));
-    aadd(cw + SC_NF, uint32_t(nf));
-    amax(cw + SC_NMIN, nmin);
-    amax(cw + SC_MAX, kmax);
+  uint32_t *part = cw + SC_PART;
+  if (t < 4) ast(part + 4 * wg + t, t == 0 ? uint32_t(nl) : t == 1 ? uint32_t(nf) : t == 2 ? nmin : kmax);
+  // this workgroup's share of the session's histograms starts at zero
+  for (int i = wg * SC_THREADS + t; i < SC_HIST * SEL_BINS; i += G * SC_THREADS) ast(cw + SC_HIST0 + i, 0u);
+  uint64_t stamp = epoch * SC_BARS;
+  const uint64_t last = stamp + SC_BARS - 1;
+  sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last);
+  // the session's totals from every workgroup's partials (the same in every workgroup)
+  uint32_t p0 = 0u, p1 = 0u, p2 = 0u, p3 = 0u;
+  if (t < G) {
+    p0 = ald(part + 4 * t);
+    p1 = ald(part + 4 * t + 1);
+    p2 = ald(part + 4 * t + 2);
+    p3 = ald(part + 4 * t + 3);
   }
-  int nbar = 0;
-  sc_barrier(cw + SC_BAR, uint32_t(++nbar * G));
-  const int tl = int(ald(cw + SC_NL)), tf = int(ald(cw + SC_NF));
+  const int tl = sc_sum(int(p0), red), tf = sc_sum(int(p1), red);
+  const uint32_t lo_key = ~sc_umax(p2, red), hi_key = sc_umax(p3, red);
   const int take = skip ? 0 : min(max(0, s.C - tf), tl - tf);
   uint32_t thr = 0xffffffffu, tpos = 0u;             // above every key: nothing beyond the initial keep
   if (take > 0) {
     int cnt;
-    thr = sc_kth([&](int i, uint32_t &v, bool &c) { v = ck[i]; c = v != 0u; }, ~ald(cw + SC_NMIN), ald(cw + SC_MAX),
-                 take, cw, 0, lh, red, sh, nbar, G, cnt);
+    thr = sc_kth([&](int i, uint32_t &v, bool &c) { v = ck[i]; c = v != 0u; }, lo_key, hi_key,
+                 take, cw, 0, lh, red, sh, stamp, last, G, wg, cnt);
     // rank of the threshold among the keys equal to it, and how many there are
     const int eq = cnt < 0 ? tl - tf : cnt;           // no pass: every candidate has the same key
     const int kt = cnt < 0 ? take : sh[1];
@@ -796,7 +829,7 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
     } else {
       int c2;
       tpos = ~sc_kth([&](int i, uint32_t &v, bool &c) { v = ~uint32_t(j0 + i); c = ck[i] == thr; },
-                     ~uint32_t(N - 1), 0xffffffffu, kt, cw, 3, lh, red, sh, nbar, G, c2);
+                     ~uint32_t(N - 1), 0xffffffffu, kt, cw, 3, lh, red, sh, stamp, last, G, wg, c2);
     }
   }
 #pragma unroll
@@ -814,14 +847,13 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
   }
 }
 
-__global__ void k_select_coop_zero(uint32_t *__restrict__ coop, int64_t words) {
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (i < words) __hip_atomic_store(coop + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Words before the cooperative path's block (which starts 256-byte aligned).
+static int64_t select_coop_off(const ikv_session *sess, int B, int64_t total_positions) {
+  return align64f(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4);
 }
 
 size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions) {
-  return size_t(sel_chunks_before(sess, B) * SEL_PART + total_positions + int64_t(B) * 4 + int64_t(B) * SC_WORDS) *
-         sizeof(uint32_t);
+  return size_t(select_coop_off(sess, B, total_positions) + int64_t(B) * SC_WORDS) * sizeof(uint32_t);
 }
 
 // Workgroups of k_select_coop that the current device holds at once (0: no cooperative launch).
@@ -854,15 +886,13 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
   const int64_t res_off = keys_off + total_positions;
   const int64_t gmax = cdiv(maxN, SC_CHUNK);
   if (maxN > 0 && maxN <= SC_MAXN && gmax * B <= coop_capacity()) {
-    uint32_t *coop = ws + res_off + int64_t(B) * 4;
-    const int64_t words = int64_t(B) * SC_WORDS;
-    {
-      KTimer kt_("k_select_coop_zero", st);
-      k_select_coop_zero<<<unsigned(cdiv(words, 256)), 256, 0, st>>>(coop, words);
-    }
+    uint32_t *coop = ws + select_coop_off(sess_host, B, total_positions);
+    // the barrier stamps of this call, above every earlier call's
+    static std::atomic<uint64_t> calls{1};
+    uint64_t epoch = calls.fetch_add(1);
     KTimer kt_("k_select_coop", st);
     void *args[] = {(void *)&sess_dev, (void *)&slot_maps, (void *)&dead, (void *)&scores, (void *)&keep,
-                    (void *)&n_keep, (void *)&tau, (void *)&coop};
+                    (void *)&n_keep, (void *)&tau, (void *)&coop, (void *)&epoch};
     hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_select_coop), dim3(unsigned(gmax), B),
                                               dim3(SC_THREADS), args, 0, st);
     if (e != hipSuccess) return e;

@@ -90,11 +90,16 @@ def test_workspace_sizes_are_consistent():
     st, resid = _ws(p, _sess(), ikv.CALL_SCORE, ikv.IKV_RESIDUAL)
     assert st == 0 and resid > plain
     # selection: per chunk of 4096 positions a 2048-bin histogram + counts (2112 words),
-    # one key per position, then 4 result words per session
-    coop = 64 + 5 * 2048        # per session: counters and five histograms of the cooperative path
-    assert _ws(None, _sess(), ikv.CALL_SELECT) == (0, (2112 + 50 + 4 + coop) * 4)
-    assert _ws(None, _sess(slot_off=1000), ikv.CALL_SELECT) == (0, (2112 + 1050 + 4 + coop) * 4)
-    assert _ws(None, _sess(N=4097, qs=4000, qe=4097), ikv.CALL_SELECT) == (0, (2 * 2112 + 4097 + 4 + coop) * 4)
+    # one key per position, then 4 result words per session, padded to 64 words; then per
+    # session the cooperative path's block: 128 barrier flags of 64 bits, 128 x 4 partial
+    # count words and five 2048-bin histograms
+    coop = 2 * 128 + 4 * 128 + 5 * 2048
+
+    def pad(w):
+        return (w + 63) // 64 * 64
+    assert _ws(None, _sess(), ikv.CALL_SELECT) == (0, (pad(2112 + 50 + 4) + coop) * 4)
+    assert _ws(None, _sess(slot_off=1000), ikv.CALL_SELECT) == (0, (pad(2112 + 1050 + 4) + coop) * 4)
+    assert _ws(None, _sess(N=4097, qs=4000, qe=4097), ikv.CALL_SELECT) == (0, (pad(2 * 2112 + 4097 + 4) + coop) * 4)
     st, red = _ws(p, _sess(), ikv.CALL_REDIRECT)
     assert st == 0 and red == 2 * 64 * 4          # two 100-slot bitsets, each padded to 64 words
     st, dec = _ws(p, _sess(), ikv.CALL_DECODE)
