@@ -178,9 +178,11 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
  *   Sessions with N <= C keep every live position (n_keep = live count,
  *   tau = -INFINITY).
  *   workspace: ikv_workspace_bytes(IKV_CALL_SELECT) bytes (per-session histograms
- *   and one 4-byte key per position, and per session the counters and histograms of
- *   the multi-workgroup path). The call may be a cooperative launch (every workgroup
- *   resident at once); concurrent calls must not share a workspace. With the
+ *   and one 4-byte key per position, and per session the barrier flags, partial
+ *   counts and histograms of the multi-workgroup path). Its contents on entry do not
+ *   matter: nothing in it has to be cleared between calls. The call may be a
+ *   cooperative launch (every workgroup resident at once); concurrent calls must not
+ *   share a workspace. With the
  *   environment variable IKV_NO_COOP=1 the call never launches cooperatively (for
  *   tools that cannot follow such a launch); the result is the same.
  */
