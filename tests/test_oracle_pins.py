@@ -548,3 +548,111 @@ def test_cross_attention_per_head_scale():
     c = oracle.ikv_oracle.cross_attention(Qc, kq, W)
     np.testing.assert_allclose(c[0, :32], 5.0, rtol=1e-14)
     np.testing.assert_allclose(c[0, 32:], 6.0, rtol=1e-14)
+
+
+# ============================================================================ Eqs. 4-6, hand-worked
+
+def _hand_residual(b_K=0.7, b_V=0.5, b_Q=1.0, b_1=-1.0, b_2=0.25, alpha=1.0):
+    """A residual head whose every output is worked out by hand (Sec. 3.3, Eqs. 4-6).
+
+    Two layers, one KV head, one memory row, D = 4; positions 0 and 1 are the
+    candidates, 2 and 3 the query span (the live cross-attention keys), 4 a dead
+    query position whose sentinel row would dominate if it were read. Layer-1 rows
+    are 3x layer-0 rows, so k-bar (the mean over layers) is 2x the layer-0 row:
+        k-bar_0 = e0, k-bar_1 = e1, k-bar_2 = 2 e2, k-bar_3 = 2 e3.
+    M = 0, so every row's softmax over the two candidates is uniform: rule = 1.
+    Weights (all else zero): W_Q[0, 0] = 1 (one-hot: query channel 0 reads
+    k-bar_j[0]), b_Q[0]; W_K[0, 2] = g = sqrt(32) ln 3 / 4, b_K[0]; W_V[0, 2] = 1,
+    b_V[0]; W_1[0, 3D + 1] = 1 (hidden unit 0 reads c_j[0]), b_1[0]; w_2[0] = 1, b_2.
+    Head 0 (channels 0..31, scale 1/sqrt(32)): the logit gap between query keys 2 and
+    3 is Q_j[0] * 2g / sqrt(32) = Q_j[0] ln 3 / 2, with Q_j[0] = k-bar_j[0] + b_Q[0].
+    """
+    D = 4
+    kb = np.array([[1, 0, 0, 0], [0, 1, 0, 0], [0, 0, 2, 0], [0, 0, 0, 2]], dtype=np.float64)
+    K = np.zeros((2, 6, 1, D), dtype=np.float32)          # pool [L][slots][Hkv][D]; slot 0 the sentinel
+    K[0, 1:5, 0] = kb / 2
+    K[1, 1:5, 0] = 3 * kb / 2
+    K[:, 0, 0] = [0.0, 0.0, 50.0, 0.0]                     # read only if a dead query position leaked in
+    S = np.array([1, 2, 3, 4, 0], dtype=np.int32)
+    M = np.zeros((2, 1, D))
+    st = oracle.sets(S, pi=0, qs=2, qe=4, C=3, dead=0)
+    g = math.sqrt(32.0) * math.log(3.0) / 4.0
+    blob = np.zeros(oracle.residual_param_count(D))
+    WQ = np.zeros((128, 3 * D + 1))
+    WQ[0, 0] = 1.0
+    WK = np.zeros((128, D))
+    WK[0, 2] = g
+    WV = np.zeros((128, D))
+    WV[0, 2] = 1.0
+    W1 = np.zeros((256, 3 * D + 1 + 128))
+    W1[0, 3 * D + 1] = 1.0
+    vec = lambda i, x, n: np.eye(n)[i] * x                 # noqa: E731
+    for name, val in (("W_Q", WQ), ("b_Q", vec(0, b_Q, 128)), ("W_K", WK), ("b_K", vec(0, b_K, 128)),
+                      ("W_V", WV), ("b_V", vec(0, b_V, 128)), ("W_1", W1), ("b_1", vec(0, b_1, 256)),
+                      ("w_2", vec(0, 1.0, 256)), ("b_2", [b_2]), ("alpha", [alpha])):
+        _set_block(blob, D, name, val)
+    s = oracle.scores(K, S, st, M, 1, 1, blob, oracle.FLAG_RESIDUAL, np.array([2, 3, 4]), 0)
+    return s, st
+
+
+def _gelu_hand(x):
+    return 0.5 * x * (1.0 + math.erf(x / math.sqrt(2.0)))
+
+
+def test_residual_hand_worked_two_query_keys():
+    """Candidate 0: Q = 1 + 1 = 2, gap ln 3: weights (3/4, 1/4) on V'[0] = (2.5, 0.5), so
+    c_0[0] = 2 and s_0 = 1 + GELU(2 - 1) + 0.25. Candidate 1: Q = 0 + 1 = 1, gap ln 3 / 2:
+    weights (sqrt3, 1) / (1 + sqrt3), c_1[0] = (2.5 sqrt3 + 0.5) / (1 + sqrt3)."""
+    s, st = _hand_residual()
+    assert np.nonzero(st["cand"])[0].tolist() == [0, 1]
+    r3 = math.sqrt(3.0)
+    c1 = (2.5 * r3 + 0.5) / (1.0 + r3)
+    assert math.isclose(c1, 1.7679491924311228, rel_tol=1e-15)
+    assert math.isclose(s[0], 1.0 + 0.8413447460685429 + 0.25, rel_tol=1e-14)      # GELU(1) = Phi(1)
+    assert math.isclose(s[0], 2.091344746068543, rel_tol=1e-14)
+    assert math.isclose(s[1], 1.0 + _gelu_hand(c1 - 1.0) + 0.25, rel_tol=1e-14)
+    assert math.isclose(s[1], 1.8480337638176736, rel_tol=1e-13)
+    assert np.all(np.isneginf(s[2:]))
+
+
+@pytest.mark.parametrize("kw,want", [
+    # b_Q = 0: both candidates see Q = k-bar_j[0]: candidate 0 the ln 3 / 2 gap, candidate 1 a uniform mix
+    (dict(b_Q=0.0), (1.25 + _gelu_hand((2.5 * math.sqrt(3) + 0.5) / (1 + math.sqrt(3)) - 1), 1.25 + _gelu_hand(0.5))),
+    # b_V = 0: V'[0] = (2, 0): c_0[0] = 1.5, c_1[0] = 2 sqrt3 / (1 + sqrt3)
+    (dict(b_V=0.0), (1.25 + _gelu_hand(0.5), 1.25 + _gelu_hand(2 * math.sqrt(3) / (1 + math.sqrt(3)) - 1))),
+    # b_1 = 0: the hidden unit sees c_j[0] itself
+    (dict(b_1=0.0), (1.25 + _gelu_hand(2.0), 1.25 + _gelu_hand((2.5 * math.sqrt(3) + 0.5) / (1 + math.sqrt(3))))),
+    # b_2 = -1 and alpha = -2: s = rule - 2 (GELU(c - 1) - 1)
+    (dict(b_2=-1.0, alpha=-2.0), (1.0 - 2 * (_gelu_hand(1.0) - 1.0),
+                                  1.0 - 2 * (_gelu_hand((2.5 * math.sqrt(3) + 0.5) / (1 + math.sqrt(3)) - 1) - 1.0))),
+])
+def test_residual_hand_worked_biases(kw, want):
+    s, _ = _hand_residual(**kw)
+    np.testing.assert_allclose(s[:2], want, rtol=1e-14)
+
+
+def test_residual_key_bias_cancels_in_the_softmax():
+    """b_K adds Q_j . b_K / sqrt(32) to every logit of candidate j alike, so the softmax
+    over the query keys, and hence every score, does not depend on it."""
+    a, _ = _hand_residual(b_K=0.7)
+    b, _ = _hand_residual(b_K=-13.0)
+    np.testing.assert_allclose(a, b, rtol=1e-14)
+
+
+def test_gate_counts_dead_positions():
+    """Appendix H skips the event when N <= C with N counting dead positions too. With
+    N > C but only C live positions the event still runs: candidates are scored and
+    every live one is kept, the threshold being the lowest candidate score."""
+    rng = np.random.default_rng(18)
+    L, N, Hkv, D, R = 1, 12, 1, 4, 2
+    pool, S = rand_pool(rng, L, N, Hkv, D)
+    S[[1, 4, 6]] = 0                                    # 9 live positions, N = 12
+    M = rng.standard_normal((L, Hkv * R, D))
+    st = oracle.sets(S, 0, 10, 12, C=9, dead=0)
+    assert not st["skip"] and st["Cstar"] == 7 and int(st["cand"].sum()) == 7
+    s = oracle.scores(pool, S, st, M, Hkv, R)
+    assert np.all(np.isfinite(s[st["cand"]]))
+    keep, n_keep, tau = oracle.select_budget(s, st)
+    assert np.array_equal(keep, st["live"]) and n_keep == 9 and tau == s[st["cand"]].min()
+    st12 = oracle.sets(S, 0, 10, 12, C=12, dead=0)
+    assert st12["skip"] and np.all(np.isneginf(oracle.scores(pool, S, st12, M, Hkv, R)))
