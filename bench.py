@@ -311,7 +311,7 @@ def main() -> int:
         "metric": "history tokens scored+selected/s and slot-map decode attn HBM GB/s, 32k hist/8k budget",
         "value": round(tokens_per_s, 1), "unit": "history tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "vs_baseline": None, "dtype": "bf16 MFMA (memory rows split hi+lo), f32 accumulate", "data": "synthetic",
         "config": {"workload": wname, "L": sh.L, "Hq": sh.Hq, "Hkv": sh.Hkv, "D": sh.D,
                    "sessions": len(batch.sessions), "N": s.N if len(Ns) == 1 else [min(Ns), max(Ns)],
                    "positions": sum(Ns), "C": s.C, "R": s.R if len(set(Rs)) == 1 else [min(Rs), max(Rs)],

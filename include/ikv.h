@@ -19,7 +19,8 @@
  *    memory. Sessions are passed twice: `sess` (host copy, validated and used
  *    for launch geometry) and `sess_dev` (a byte-identical device copy read by
  *    the kernels). The caller owns every buffer; the library keeps no pointer
- *    after a call returns and allocates nothing.
+ *    to them after a call returns and allocates no device memory (the one
+ *    allocation it makes is a word of pinned host memory, see ikv_select_budget).
  *  - `stream` is a hipStream_t (NULL = the default stream). Validation runs
  *    synchronously on the host; all device work is enqueued on `stream` and the
  *    call returns without synchronising.
@@ -34,7 +35,8 @@
  *  - Return value: IKV_OK, or a negative ikv_status; ikv_last_error() then gives
  *    a message (thread-local, valid until the next call on the same thread).
  *    On an error return nothing has been enqueued, except for IKV_EHIP, which
- *    reports a failed launch.
+ *    reports a failed launch, or a fault that a kernel of an earlier call reported
+ *    (see ikv_select_budget); a call that returns such a fault enqueues nothing.
  *  - Slot ids in slot maps and live lists must lie in [0, num_slots); the
  *    kernels do not check them.
  */
@@ -185,6 +187,13 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
  *   share a workspace. With the
  *   environment variable IKV_NO_COOP=1 the call never launches cooperatively (for
  *   tools that cannot follow such a launch); the result is the same.
+ *   The workgroups of a cooperative launch meet at grid barriers whose waits are
+ *   bounded (2^24 polls, or IKV_SELECT_SPINS from the environment, read on every
+ *   call). Every workgroup is resident, so a wait ends well before the bound; if one
+ *   ever gives up, the kernel still exits, the call's keep / n_keep / tau are not
+ *   valid, and the library's next call returns IKV_EHIP (the fault travels through
+ *   a word of pinned host memory that the first cooperative call allocates and the
+ *   process keeps).
  */
 ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev,
                              int32_t B, const int32_t *slot_maps, int32_t dead_slot,
@@ -220,6 +229,9 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
  *   q, out: device [B][L][Hq][D] of the pool's kv_dtype (out rounded to nearest
  *   even). live, n_live: device, as written by ikv_redirect_slots;
  *   n_live[b] must not exceed sess[b].N.
+ *   The live lists are split across workgroups by a bound known on the host,
+ *   min(N, max(C, pi + qe - qs)) over the sessions (what a retention event leaves
+ *   live); a longer list is still attended exactly, with longer splits.
  */
 ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess,
                                      const ikv_session *sess_dev, int32_t B,

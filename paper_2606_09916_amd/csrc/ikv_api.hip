@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -50,6 +51,9 @@ ikv_status ok() {
   g_err.clear();
   return IKV_OK;
 }
+
+// A fault a kernel of an earlier call reported through the host fault word.
+ikv_status pending_fault();
 
 ikv_status hip_status(hipError_t e, const char *what) {
   if (e == hipSuccess) return ok();
@@ -101,12 +105,10 @@ int max_n(const ikv_session *s, int B) {
   return m;
 }
 
-// The MFMA score passes need D = 128 and every session's R a multiple of 16.
-bool use_mfma(const ikv_pool *p, const ikv_session *s, int B) {
-  if (p->D != 128 || p->kv_dtype != IKV_BF16) return false;
-  for (int b = 0; b < B; ++b)
-    if (s[b].R % 16) return false;
-  return true;
+// The MFMA score passes need D = 128 and a bf16 pool; any R (each session's memory
+// rows run in 16-row slices, the last one padded).
+bool use_mfma(const ikv_pool *p, const ikv_session *, int) {
+  return p->D == 128 && p->kv_dtype == IKV_BF16;
 }
 
 size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flags) {
@@ -149,13 +151,50 @@ size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
   return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
 }
 
+ikv_status pending_fault() {
+  if (ikv::take_host_fault())
+    return fail(IKV_EHIP, "a grid barrier of an earlier ikv_select_budget call gave up waiting; "
+                          "that call's kept set is not valid");
+  return IKV_OK;
+}
+
 }  // namespace
+
+namespace ikv {
+
+namespace {
+std::mutex g_fault_mu;
+std::atomic<uint32_t *> g_fault_host{nullptr};   // pinned, mapped; never freed
+uint32_t *g_fault_dev = nullptr;                 // the same word as kernels address it
+}  // namespace
+
+uint32_t *host_fault_word() {
+  std::lock_guard<std::mutex> lk(g_fault_mu);
+  if (!g_fault_host) {
+    void *h = nullptr, *d = nullptr;
+    if (hipHostMalloc(&h, 64, hipHostMallocMapped | hipHostMallocPortable | hipHostMallocCoherent) != hipSuccess)
+      return nullptr;
+    *static_cast<volatile uint32_t *>(h) = 0u;
+    if (hipHostGetDevicePointer(&d, h, 0) != hipSuccess) d = h;
+    g_fault_dev = static_cast<uint32_t *>(d);
+    g_fault_host.store(static_cast<uint32_t *>(h), std::memory_order_release);
+  }
+  return g_fault_dev;
+}
+
+bool take_host_fault() {
+  uint32_t *h = g_fault_host.load(std::memory_order_acquire);
+  return h != nullptr && __atomic_exchange_n(h, 0u, __ATOMIC_ACQ_REL) != 0u;
+}
+
+}  // namespace ikv
 
 extern "C" {
 
 const char *ikv_last_error(void) { return g_err.c_str(); }
 
 namespace ikv {
+
 
 KTimer::KTimer(const char *name, hipStream_t stream) : idx(-1), st(stream) {
   if (!g_timing) return;
@@ -242,6 +281,7 @@ ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, in
 }
 
 ikv_status ikv_init_dead_slot(const ikv_pool *pool, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_pool(pool);
   if (r) return r;
   return hip_status(ikv::launch_init_dead_slot(*pool, (hipStream_t)stream), "ikv_init_dead_slot");
@@ -249,6 +289,7 @@ ikv_status ikv_init_dead_slot(const ikv_pool *pool, void *stream) {
 
 ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
                          float *M, const void *q_span, float lambda, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_pool(pool);
   if (r) return r;
   if ((r = check_sessions(sess, sess_dev, B))) return r;
@@ -273,6 +314,7 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
                              const int32_t *slot_maps, const float *M, const int32_t *qpos, const float *residual,
                              uint32_t flags, float *scores, void *workspace, size_t workspace_bytes,
                              void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_pool(pool);
   if (r) return r;
   if ((r = check_sessions(sess, sess_dev, B))) return r;
@@ -321,6 +363,7 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
 ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
                              const int32_t *slot_maps, int32_t dead_slot, const float *scores, uint8_t *keep,
                              int32_t *n_keep, float *tau, void *workspace, size_t workspace_bytes, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_sessions(sess, sess_dev, B);
   if (r) return r;
   if (B == 0) return ok();
@@ -338,6 +381,7 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
                               int32_t *slot_maps, int32_t dead_slot, const uint8_t *keep, int32_t *freed,
                               int32_t *n_freed, int32_t *live, int32_t *n_live, void *workspace,
                               size_t workspace_bytes, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_sessions(sess, sess_dev, B);
   if (r) return r;
   if (B == 0) return ok();
@@ -354,6 +398,7 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
 ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev,
                                      int32_t B, const void *q, const int32_t *live, const int32_t *n_live, void *out,
                                      void *workspace, size_t workspace_bytes, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
   ikv_status r = check_pool(pool);
   if (r) return r;
   if ((r = check_sessions(sess, sess_dev, B))) return r;

@@ -25,9 +25,13 @@ constexpr int MAX_R = 256;          // memory rows per KV head
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t align64f(int64_t n) { return (n + 63) & ~int64_t(63); }   // floats -> 256 B
 
+// Memory rows per KV head rounded up to whole 16-row MFMA slices.
+__host__ __device__ inline int pad16(int R) { return (R + 15) & ~15; }
+
 // Score workspace, per session b (floats, each block 256-byte aligned). Two
-// layouts: the MFMA path (D = 128, R a multiple of 16) and the VALU path.
-//   msplit [units][R][256 bf16]   memory rows pre-split into bf16 hi + lo (MFMA only)
+// layouts: the MFMA path (D = 128, bf16 pool) and the VALU path.
+//   msplit [units][pad16(R)][256 bf16]  memory rows pre-split into bf16 hi + lo, the
+//          rows past R zero (MFMA only)
 //   part   per-tile (max, sum exp) of every memory row:
 //            MFMA [tiles of 64 or 128][units][R][2] (room for tiles of 64),
 //            VALU [units][R][tiles of 256][2]
@@ -94,7 +98,7 @@ __host__ __device__ inline int perm32_inv(int c) {
 __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid,
                                                   bool mfma) {
   ScoreSizes z;
-  z.msplit = mfma ? align64f(int64_t(units) * s.R * 128) : 0;
+  z.msplit = mfma ? align64f(int64_t(units) * pad16(s.R) * 128) : 0;
   z.part = mfma ? align64f(cdiv(s.N, PART_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
   z.lse = align64f(int64_t(units) * s.R * (mfma ? 3 : 2));
   z.lse_pairs = int64_t(units) * s.R * 2;
@@ -213,7 +217,7 @@ struct ScoreArgs {
   float *ws;           // session blocks, then the shared block
   float *ws_shared;
   int maxN, maxR, minR, maxNq;
-  bool mfma;           // MFMA score passes (D = 128 and every R a multiple of 16)
+  bool mfma;           // MFMA score passes (D = 128, bf16 pool)
   bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
 };
@@ -243,5 +247,12 @@ hipError_t launch_decode(const ikv_pool &pool, const ikv_session *sess_dev, int 
                          float *ws, hipStream_t st);
 
 int decode_splits(int maxN);
+
+// A word of pinned host memory that kernels set (system scope) to report a fault the
+// host cannot see otherwise (a grid barrier that gave up). Allocated on first use and
+// kept for the life of the process; nullptr if the allocation failed. take_host_fault()
+// returns whether it was set and clears it.
+uint32_t *host_fault_word();
+bool take_host_fault();
 
 }  // namespace ikv

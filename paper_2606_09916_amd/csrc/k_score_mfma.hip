@@ -39,7 +39,8 @@ __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 
 // M' = M * log2(e) / sqrt(D) split into bf16 hi and lo. Per (unit, row), 256 bf16
 // in fragment order [g 0..3][k-step 0..3][hi 8 | lo 8], where (k-step, g) holds
 // channels (4 k-step + g) * 8 .. + 8: lane group g of an MFMA reads 128 contiguous bytes.
-// Workgroup p takes rows [p*rows/P, (p+1)*rows/P) with P = MBAR_PARTS; thread (r, c)
+// Each unit's rows are padded to whole 16-row slices (pad16), the pad rows zero.
+// Workgroup p takes padded rows [p*rows/P, (p+1)*rows/P) with P = MBAR_PARTS; thread (r, c)
 // splits channel group c of rows r, r + 16, ... (32 bytes in, two 16-byte stores out),
 // a batch of rows in flight at once (loads from row indices clamped into the range and
 // masked afterwards, so that none waits inside a branch). With the residual head on it
@@ -59,7 +60,8 @@ __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ 
     return;
   }
   const int units = L * Hkv;
-  const int64_t rows = int64_t(units) * s.R;
+  const int R = s.R, R16 = pad16(R);
+  const int64_t rows = int64_t(units) * R16;
   const int64_t r0 = rows * p / MBAR_PARTS, r1 = rows * (p + 1) / MBAR_PARTS;
   const int rg = threadIdx.x >> 4, c = threadIdx.x & 15;
   const int g = c & 3, ks = c >> 2;
@@ -75,14 +77,19 @@ __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ 
 #pragma unroll
     for (int k = 0; k < MS_BATCH; ++k) {
       const int64_t rr = min(r + 16 * k, r1 - 1);
-      va[k] = *reinterpret_cast<const float4 *>(src + rr * MD);
-      vb[k] = *reinterpret_cast<const float4 *>(src + rr * MD + 4);
+      const int64_t u = rr / R16, row = min<int64_t>(rr - u * R16, R - 1);   // pad rows read the last row
+      va[k] = *reinterpret_cast<const float4 *>(src + (u * R + row) * MD);
+      vb[k] = *reinterpret_cast<const float4 *>(src + (u * R + row) * MD + 4);
     }
 #pragma unroll
     for (int k = 0; k < MS_BATCH; ++k) {
       const int64_t rr = r + 16 * k;
       if (rr >= r1) continue;
-      const float v[8] = {va[k].x, va[k].y, va[k].z, va[k].w, vb[k].x, vb[k].y, vb[k].z, vb[k].w};
+      const bool real = rr - (rr / R16) * R16 < R;
+      float v[8] = {va[k].x, va[k].y, va[k].z, va[k].w, vb[k].x, vb[k].y, vb[k].z, vb[k].w};
+      if (!real)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
       uint32_t hw[4], lw[4];
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
@@ -155,7 +162,7 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
   if (j0 >= s.N) return;
   const int units = L * Hkv;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int R = s.R, nsl = R >> 4;
+  const int R = s.R, R16 = pad16(R), nsl = R16 >> 4;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
@@ -195,7 +202,7 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
   };
   auto mload = [&](int u, bf16x8 (&mh)[4], bf16x8 (&ml)[4], int sl) {
     if (u >= units || sl >= nsl) return;
-    const uint16_t *mp = msplit + (int64_t(u) * R + sl * 16 + (lane & 15)) * 256 + (lane >> 4) * 64;
+    const uint16_t *mp = msplit + (int64_t(u) * R16 + sl * 16 + (lane & 15)) * 256 + (lane >> 4) * 64;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       mh[ks] = *reinterpret_cast<const bf16x8 *>(mp + ks * 16);
@@ -265,14 +272,15 @@ __global__ void __launch_bounds__(256) k_score_mfma(const uint16_t *__restrict__
           m = mm;
           zs = a + c;
         }
-        if (lane < 16) {
+        if (lane < 16 && row < R) {                 // pad rows of the last slice are not stored
           float *p = part + ((int64_t(tile) * units + u) * R + row) * 2;
           p[0] = m;
           p[1] = zs;
         }
       } else {
-        const float mrow = lse[(int64_t(u) * R + row) * 2];
-        const float iz = lse[(int64_t(u) * R + row) * 2 + 1];
+        const int rowc = min(row, R - 1);
+        const float mrow = lse[(int64_t(u) * R + rowc) * 2];
+        const float iz = row < R ? lse[(int64_t(u) * R + rowc) * 2 + 1] : 0.f;   // pad rows add nothing
 #pragma unroll
         for (int blk = 0; blk < MFMA_TILE / 16; ++blk)
 #pragma unroll
@@ -410,12 +418,12 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform: branches on it stay scalar
   const int rs = w & 3, half = w >> 2;             // memory-row slice, position half
   const int g = lane >> 4, r16 = lane & 15;
-  const int R = s.R, nsl = R >> 4;
+  const int R = s.R, R16 = pad16(R), nsl = R16 >> 4;
   const bool act = rs < nsl;
   const int row = rs * 16 + r16;
   const int p0 = half * 64;                        // first position of this wave's half
   const int ptile = tile * 2 + half;
-  const bool pstore = act && lane < 16 && int64_t(ptile) * PART_TILE < s.N;
+  const bool pstore = act && lane < 16 && row < R && int64_t(ptile) * PART_TILE < s.N;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
@@ -457,11 +465,12 @@ k_score_ring(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int H
 #pragma unroll
     for (int k = 0; k < 4; ++k) issue_k_piece(u, k);
   };
-  // memory rows of unit u: R rows of 512 B, 32 chunks of 16 B per row, chunk slot
-  // s of row r holds chunk s ^ (r & 15); wave w issues R/16 of the R/2 1-KB pieces
-  const int nm = R >> 4;
+  // memory rows of unit u: R16 rows of 512 B (the pad rows zero), 32 chunks of 16 B per
+  // row, chunk slot s of row r holds chunk s ^ (r & 15); wave w issues R16/16 of the
+  // R16/2 1-KB pieces
+  const int nm = R16 >> 4;
   auto issue_m_piece = [&](int u, int k) {
-    const uint16_t *m0 = msplit + int64_t(u) * R * 256;
+    const uint16_t *m0 = msplit + int64_t(u) * R16 * 256;
     const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
     const int piece = w * nm + k;
     const int r = piece * 2 + (lane >> 5);
@@ -624,7 +633,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int g = lane >> 4, r16 = lane & 15;
-  const int R = s.R;
+  const int R = s.R, R16 = pad16(R);
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const int32_t *S = slot_maps + s.slot_off;
@@ -655,15 +664,15 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 #pragma unroll
       for (int k = 0; k < 8; ++k) issue_k_piece(u, k);
     };
-    // memory rows of unit u (half hf): up to 64 rows of 512 B, chunk slot c of row r
-    // holds chunk c ^ (r & 15); producer pw issues a quarter of the half's 1-KB pieces
-    // (two rows each), npc(hf) of them
+    // memory rows of unit u (half hf): up to 64 rows of 512 B (R16 per unit, the pad rows
+    // zero), chunk slot c of row r holds chunk c ^ (r & 15); producer pw issues a quarter
+    // of the half's 1-KB pieces (two rows each), npc(hf) of them
     const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
     const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
-    auto npc_of = [&](int hf) __attribute__((always_inline)) { return min(64, max(0, R - 64 * hf)) >> 3; };
+    auto npc_of = [&](int hf) __attribute__((always_inline)) { return min(64, max(0, R16 - 64 * hf)) >> 3; };
     auto issue_m_piece = [&](int u, int hf, int k) __attribute__((always_inline)) {
       const int npc = npc_of(hf);
-      const uint16_t *m0 = msplit + (int64_t(u) * R + 64 * hf) * 256;
+      const uint16_t *m0 = msplit + (int64_t(u) * R16 + 64 * hf) * 256;
       const uint32_t st = mlds0 + uint32_t((RH == 1 ? (u & 1) : hf) * MSTAGE * 2);
       const int piece = pw * npc + k;
       const int r = piece * 2 + (lane >> 5);
@@ -775,7 +784,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 
   // ---------------- consumers: logits on the matrix cores, exp2 folded into the rule score
   const int rh = w & 1, p0 = (w >> 1) * 64;         // memory-row half, first position of the half
-  const int nsl = R >> 4;
+  const int nsl = R16 >> 4;
   const float *nl2 = base + z.off_nl2();
   float racc[4][4];
 #pragma unroll
@@ -1006,17 +1015,19 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
           ml[rb][ks][e] = __bf16(v - float(mh[rb][ks][e]));
         }
       }
-    // chunk 0 keeps the split rows for the second pass, in the layout of k_msplit
+    // chunk 0 keeps the split rows for the second pass, in the layout of k_msplit (rows
+    // padded to whole slices, the pad rows zero)
     if (chunk == 0)
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
         const int row = r0 + 16 * rb + r16;
-        if (row < R) {
-          uint16_t *dp = msplit + (int64_t(u) * R + row) * 256;
+        if (row < pad16(R)) {
+          uint16_t *dp = msplit + (int64_t(u) * pad16(R) + row) * 256;
+          const bool real = row < R;
 #pragma unroll
           for (int ks = 0; ks < 4; ++ks) {
-            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16) = mh[rb][ks];
-            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16 + 8) = ml[rb][ks];
+            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16) = real ? mh[rb][ks] : bf16x8{};
+            *reinterpret_cast<bf16x8 *>(dp + (g * 4 + ks) * 16 + 8) = real ? ml[rb][ks] : bf16x8{};
           }
         }
       }

@@ -10,7 +10,11 @@
 
 #include <stdlib.h>
 
+#include <unistd.h>
+
 #include <atomic>
+#include <chrono>
+#include <random>
 
 #include "ikv_internal.hpp"
 
@@ -572,7 +576,11 @@ __global__ void __launch_bounds__(SEL_THREADS) k_select_small(const ikv_session 
 // at the threshold are ranked by the same passes over positions. Nothing in the
 // workspace needs to be cleared beforehand: each workgroup clears its share of the
 // histograms before the first barrier, and the barrier flags carry a stamp that the
-// host draws afresh for every call.
+// host draws afresh for every call (above every earlier call's, with a random tag per
+// process in the top bits, so that no structured leftover in the workspace matches).
+// The barrier polls a bounded number of times; a workgroup whose poll runs out sets a
+// fault word in pinned host memory, which the library's next call turns into IKV_EHIP:
+// the kept set of the call that timed out is not valid.
 constexpr int SC_THREADS = 256;
 constexpr int SC_WAVES = SC_THREADS / WAVE;
 constexpr int SC_PER = 4;                              // positions per thread
@@ -602,19 +610,24 @@ __device__ __forceinline__ void aadd(uint32_t *p, uint32_t v) {
 // the stamp and waits until every flag of the session lies in [stamp, last], the
 // stamps of this barrier and of the call's later ones (a workgroup may already have
 // moved on). The host draws the call's stamps above every earlier call's, so a flag
-// left by an earlier call never passes; one left by other data passes with odds of
-// about 2^-61. Everything the workgroups exchange is a device-scope atomic, so the
-// barrier needs no cache write-back or invalidation: each thread's atomics are
-// complete once its vector-memory count drains, then one thread sets the flag and one
-// wave polls the flags with coherent loads. Every workgroup of the grid is resident
-// (cooperative launch), so every flag is set; the poll is bounded all the same.
-__device__ __forceinline__ void sc_barrier(uint64_t *flags, int G, int wg, uint64_t stamp, uint64_t last) {
+// left by an earlier call never passes, and puts a random per-process tag in the top
+// 24 bits, so that leftovers of other calls (counts, bitsets, floats) pass only by
+// matching both the tag and an 8-stamp window. Everything the workgroups exchange is a
+// device-scope atomic, so the barrier needs no cache write-back or invalidation: each
+// thread's atomics are complete once its vector-memory count drains, then one thread
+// sets the flag and one wave polls the flags with coherent loads. Every workgroup of
+// the grid is resident (cooperative launch), so every flag is set; the poll is bounded
+// all the same (`spins` polls), and a poll that runs out sets `timed_out` and lets the
+// workgroup go on.
+__device__ __forceinline__ void sc_barrier(uint64_t *flags, int G, int wg, uint64_t stamp, uint64_t last,
+                                           uint32_t spins, int *sh_ok, bool &timed_out) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   const int t = threadIdx.x;
   if (t < WAVE) {
     if (t == 0) __hip_atomic_store(flags + wg, stamp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (uint32_t spin = 0; spin < (1u << 24); ++spin) {
+    bool done = false;
+    for (uint32_t spin = 0; spin < spins; ++spin) {
       bool ok = true;
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
@@ -624,11 +637,16 @@ __device__ __forceinline__ void sc_barrier(uint64_t *flags, int G, int wg, uint6
           ok = ok && f >= stamp && f <= last;
         }
       }
-      if (__all(ok)) break;
+      if (__all(ok)) {
+        done = true;
+        break;
+      }
       __builtin_amdgcn_s_sleep(1);
     }
+    if (t == 0) *sh_ok = done;
   }
   __syncthreads();
+  timed_out = timed_out || !*sh_ok;
 }
 
 // Sum and maximum over the workgroup of SC_THREADS threads.
@@ -663,6 +681,10 @@ __device__ __forceinline__ int sc_sum(int v, int *red) {
 // to sh[0], sh[1]. Every thread must call it.
 __device__ __forceinline__ void sc_find_bin(const uint32_t *gh, uint32_t *lh, int kk, int *red, int *sh) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if (t == 0) {          // no bin holds rank kk only if the histograms are not whole (a timed-out barrier)
+    sh[0] = 0;
+    sh[1] = 1;
+  }
   constexpr int per = SEL_BINS / SC_THREADS;
   const int hi_bin = SEL_BINS - 1 - t * per;
   uint32_t v[per];
@@ -708,7 +730,8 @@ __device__ __forceinline__ void sc_find_bin(const uint32_t *gh, uint32_t *lh, in
 // value; *cnt is the number of counted values equal to it.
 template <class Get>
 __device__ uint32_t sc_kth(Get get, uint32_t lo, uint32_t hi, int kk, uint32_t *cw, int hist0, uint32_t *lh,
-                           int *red, int *sh, uint64_t &stamp, uint64_t last, int G, int wg, int &cnt) {
+                           int *red, int *sh, uint64_t &stamp, uint64_t last, int G, int wg, int &cnt,
+                           uint32_t spins, bool &timed_out) {
   const int t = threadIdx.x;
   int pass = 0;
   cnt = -1;
@@ -729,13 +752,13 @@ __device__ uint32_t sc_kth(Get get, uint32_t lo, uint32_t hi, int kk, uint32_t *
     uint32_t *gh = cw + SC_HIST0 + (hist0 + pass) * SEL_BINS;
     for (int i = t; i < SEL_BINS; i += SC_THREADS)
       if (lh[i]) aadd(gh + i, lh[i]);
-    sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last);
+    sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last, spins, sh + 2, timed_out);
     sc_find_bin(gh, lh, kk, red, sh);
     const uint32_t nlo = lo + (uint32_t(sh[0]) << shift);
     hi = shift == 0 ? nlo : min(hi, nlo + ((1u << shift) - 1u));
     lo = nlo;
     kk = sh[1];
-    cnt = int(lh[sh[0]]);
+    cnt = int(lh[min(sh[0], SEL_BINS - 1)]);
     ++pass;
     __syncthreads();
   }
@@ -747,11 +770,12 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
                                                             const float *__restrict__ scores,
                                                             uint8_t *__restrict__ keep, int32_t *__restrict__ n_keep,
                                                             float *__restrict__ tau, uint32_t *__restrict__ coop,
-                                                            uint64_t epoch) {
+                                                            uint64_t stamp0, uint32_t spins,
+                                                            uint32_t *__restrict__ host_fault) {
   __shared__ uint32_t ck[SC_CHUNK];                  // keys of this chunk (0: not a candidate)
   __shared__ uint32_t lh[SEL_BINS];
   __shared__ int red[SC_WAVES];
-  __shared__ int sh[2];
+  __shared__ int sh[3];                              // bin, rank within it; barrier outcome
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   const int N = s.N;
@@ -801,9 +825,10 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
   if (t < 4) ast(part + 4 * wg + t, t == 0 ? uint32_t(nl) : t == 1 ? uint32_t(nf) : t == 2 ? nmin : kmax);
   // this workgroup's share of the session's histograms starts at zero
   for (int i = wg * SC_THREADS + t; i < SC_HIST * SEL_BINS; i += G * SC_THREADS) ast(cw + SC_HIST0 + i, 0u);
-  uint64_t stamp = epoch * SC_BARS;
+  uint64_t stamp = stamp0;
   const uint64_t last = stamp + SC_BARS - 1;
-  sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last);
+  bool timed_out = false;
+  sc_barrier(reinterpret_cast<uint64_t *>(cw), G, wg, ++stamp, last, spins, sh + 2, timed_out);
   // the session's totals from every workgroup's partials (the same in every workgroup)
   uint32_t p0 = 0u, p1 = 0u, p2 = 0u, p3 = 0u;
   if (t < G) {
@@ -819,7 +844,7 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
   if (take > 0) {
     int cnt;
     thr = sc_kth([&](int i, uint32_t &v, bool &c) { v = ck[i]; c = v != 0u; }, lo_key, hi_key,
-                 take, cw, 0, lh, red, sh, stamp, last, G, wg, cnt);
+                 take, cw, 0, lh, red, sh, stamp, last, G, wg, cnt, spins, timed_out);
     // rank of the threshold among the keys equal to it, and how many there are
     const int eq = cnt < 0 ? tl - tf : cnt;           // no pass: every candidate has the same key
     const int kt = cnt < 0 ? take : sh[1];
@@ -829,7 +854,8 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
     } else {
       int c2;
       tpos = ~sc_kth([&](int i, uint32_t &v, bool &c) { v = ~uint32_t(j0 + i); c = ck[i] == thr; },
-                     ~uint32_t(N - 1), 0xffffffffu, kt, cw, 3, lh, red, sh, stamp, last, G, wg, c2);
+                     ~uint32_t(N - 1), 0xffffffffu, kt, cw, 3, lh, red, sh, stamp, last, G, wg, c2, spins,
+                     timed_out);
     }
   }
 #pragma unroll
@@ -845,6 +871,9 @@ __global__ void __launch_bounds__(SC_THREADS) k_select_coop(const ikv_session *_
     n_keep[b] = skip ? tl : tf + take;
     tau[b] = skip ? -INFINITY : (take > 0 ? key_score(thr) : INFINITY);
   }
+  // a timed-out barrier: the host's fault word, which the library's next call reports
+  if (t == 0 && timed_out && host_fault)
+    __hip_atomic_store(host_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // Words before the cooperative path's block (which starts 256-byte aligned).
@@ -856,7 +885,14 @@ size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_posi
   return size_t(select_coop_off(sess, B, total_positions) + int64_t(B) * SC_WORDS) * sizeof(uint32_t);
 }
 
-// Workgroups of k_select_coop that the current device holds at once (0: no cooperative launch).
+// Polls of a grid barrier before it gives up: IKV_SELECT_SPINS in the environment
+// (read on every call; a host-side way to force the give-up path in tests), else 2^24.
+static uint32_t select_spin_limit() {
+  const char *e = getenv("IKV_SELECT_SPINS");
+  if (e == nullptr || e[0] == '\0') return 1u << 24;
+  return uint32_t(strtoul(e, nullptr, 10));
+}
+
 // Workgroups a cooperative launch of k_select_coop may have on the current device
 // (0: not available). IKV_NO_COOP=1 in the environment turns the cooperative path off,
 // for tools that cannot follow a cooperative launch; the selection is the same.
@@ -887,12 +923,22 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
   const int64_t gmax = cdiv(maxN, SC_CHUNK);
   if (maxN > 0 && maxN <= SC_MAXN && gmax * B <= coop_capacity()) {
     uint32_t *coop = ws + select_coop_off(sess_host, B, total_positions);
-    // the barrier stamps of this call, above every earlier call's
+    // the barrier stamps of this call: a random per-process tag in bits 40-63, above it
+    // a counter of calls (2^37 calls before it wraps), SC_BARS stamps per call
+    static const uint64_t tag = [] {
+      std::random_device rd;
+      uint64_t x = (uint64_t(rd()) << 32) ^ rd() ^ uint64_t(getpid()) ^
+                   uint64_t(std::chrono::steady_clock::now().time_since_epoch().count());
+      x &= 0xffffffull;
+      return (x == 0 || x == 0xffffffull ? 0x5a5a5aull : x) << 40;
+    }();
     static std::atomic<uint64_t> calls{1};
-    uint64_t epoch = calls.fetch_add(1);
+    uint64_t stamp0 = tag | ((calls.fetch_add(1) * SC_BARS) & ((1ull << 40) - 1));
+    uint32_t spins = select_spin_limit();
+    uint32_t *fault = host_fault_word();
     KTimer kt_("k_select_coop", st);
     void *args[] = {(void *)&sess_dev, (void *)&slot_maps, (void *)&dead, (void *)&scores, (void *)&keep,
-                    (void *)&n_keep, (void *)&tau, (void *)&coop, (void *)&epoch};
+                    (void *)&n_keep, (void *)&tau, (void *)&coop, (void *)&stamp0, (void *)&spins, (void *)&fault};
     hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_select_coop), dim3(unsigned(gmax), B),
                                               dim3(SC_THREADS), args, 0, st);
     if (e != hipSuccess) return e;

@@ -303,15 +303,28 @@ def residual_sizes(D: int, h_c: int = 128, hidden: int = 256):
 
 
 def residual_blob(D: int, seed: int, variant: str = "random", alpha: float = 1.0,
-                  std: float = 0.02) -> np.ndarray:
+                  std: float = 0.02, units: int = 1, out_std: float = 0.01) -> np.ndarray:
     """Residual-head parameters as one float32 blob.
 
     ``random``: every weight and bias ~ N(0, std^2), alpha as given.
     ``zero``: as ``random`` but the output projection (w_2, b_2) is zero, which is
     the head's initial state.
+    ``scaled``: weights under which every term of the head moves the scores of a
+    full-size workload. The mean key row averages ``units`` = L * Hkv rows, so its
+    entries are about sqrt(units) times smaller than a key's; random weights of a
+    fixed scale then leave the cross-attention logits near zero and its output near
+    constant across candidates. Here every matrix entry is N(0, 1/fan_in), the
+    columns that read the mean key row (and its product with the memory mean), and
+    W_K, W_V, are multiplied by sqrt(units); W_Q by 2 (attention over the query
+    keys well away from uniform) and W_1's cross-attention columns by 4; biases are
+    N(0, 0.1^2); w_2 and b_2 are N(0, (out_std / 4)^2) and N(0, out_std^2), so the
+    head's output varies across candidates by about ``out_std`` (pick it near the
+    spread of the rule scores).
     """
     sizes = residual_sizes(D)
     total = sum(n for _, n in sizes)
+    if variant == "scaled":
+        return _residual_blob_scaled(D, seed, alpha, units, out_std)
     blob = stream(seed, T_RESID).standard_normal(total, dtype=np.float32) * np.float32(std)
     o = 0
     for name, n in sizes:
@@ -321,6 +334,27 @@ def residual_blob(D: int, seed: int, variant: str = "random", alpha: float = 1.0
             blob[o] = alpha
         o += n
     return blob
+
+
+def _residual_blob_scaled(D: int, seed: int, alpha: float, units: int, out_std: float) -> np.ndarray:
+    f, hc, hid = 3 * D + 1, 128, 256
+    g = stream(seed, T_RESID, 1)
+    ku = np.sqrt(float(units))
+    WQ = g.standard_normal((hc, f)) / np.sqrt(f)
+    WQ[:, :D] *= ku
+    WQ[:, 2 * D:3 * D] *= ku
+    WQ *= 2.0
+    WK = g.standard_normal((hc, D)) / np.sqrt(D) * ku
+    WV = g.standard_normal((hc, D)) / np.sqrt(D) * ku
+    W1 = g.standard_normal((hid, f + hc)) / np.sqrt(f + hc)
+    W1[:, :D] *= ku
+    W1[:, 2 * D:3 * D] *= ku
+    W1[:, f:] *= 4.0
+    parts = {"W_Q": WQ, "b_Q": 0.1 * g.standard_normal(hc), "W_K": WK, "b_K": 0.1 * g.standard_normal(hc),
+             "W_V": WV, "b_V": 0.1 * g.standard_normal(hc), "W_1": W1, "b_1": 0.1 * g.standard_normal(hid),
+             "w_2": out_std / 4.0 * g.standard_normal(hid), "b_2": out_std * g.standard_normal(1),
+             "alpha": np.array([alpha])}
+    return np.concatenate([np.asarray(parts[n], np.float64).ravel() for n, _ in residual_sizes(D)]).astype(np.float32)
 
 
 # ----------------------------------------------------------------------------- named workloads
@@ -561,13 +595,13 @@ def build_native(verbose: bool = False) -> str:
 def batched_share_full(seed: int = 5, B: int = 64) -> Batch:
     """The batched one-GPU share at full size: B sessions in the shape of one GPU's half of
     a Qwen2.5-14B tensor-parallel pair (48 layers, 20 query / 4 KV heads, D = 128), N ~
-    U{4096..65536}, R ~ 16 U{2..8}, budget 8192, the last 64 positions the query span and
+    U{4096..65536}, R ~ U{32..128}, budget 8192, the last 64 positions the query span and
     the cross-attention queries, one shared paged pool. Keys and values are not drawn
     here (k_pool = v_pool = None): fill_share_pools() writes them on the GPU, and
     share_rows() regenerates any rows on the host. No span rows (no memory update)."""
     g = stream(seed, T_TURNS, 2)
     Ns = [int(n) for n in g.integers(4096, 65537, B)]
-    Rs = [int(r) for r in 16 * g.integers(2, 9, B)]
+    Rs = [int(r) for r in g.integers(32, 129, B)]
     shape = Shape(L=48, Hq=20, Hkv=4, D=128)
     alloc, num_slots = paged_slots(Ns, seed, 16, spare_pages=64)
     sessions = [SessionSpec(N=n, C=8192, pi=0, qs=n - 64, qe=n, R=r) for n, r in zip(Ns, Rs)]

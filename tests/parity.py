@@ -59,3 +59,49 @@ def check_attention(o_gpu, o_o, bf16: bool):
     err = np.abs(o_gpu - o_o)
     assert np.all(err <= tol), f"attention error {err.max():.3e} above tolerance"
     return float(err.max())
+
+
+def oracle_scores_pair(k_pool, S, st, M, Hkv, R, blob, qpos, dead):
+    """Oracle scores with the residual head, with and without its cross-attention (the
+    '- x-attn' ablation of Sec. 3.3), from one rule-score pass: the oracle's own steps
+    (rule, key means, memory mean, residual) composed as oracle.scores composes them."""
+    import oracle
+    S = np.asarray(S)
+    N = len(S)
+    full = np.full(N, -np.inf)
+    nox = full.copy()
+    idx = np.nonzero(st["cand"])[0]
+    if st["skip"] or len(idx) == 0:
+        return full, nox
+    D = k_pool.shape[-1]
+    rule = oracle.rule_scores(k_pool, S, st["cand"], M, Hkv, R)
+    qpos = np.asarray(qpos, np.int64)
+    qlive = qpos[S[qpos] != dead] if len(qpos) else qpos
+    kb, kq, mb = oracle.kbar(k_pool, S, idx), oracle.kbar(k_pool, S, qlive), oracle.mbar(M)
+    full[idx] = oracle.residual_scores(rule[idx], kb, mb, kq, blob, D, xattn=True)
+    nox[idx] = oracle.residual_scores(rule[idx], kb, mb, kq, blob, D, xattn=False)
+    return full, nox
+
+
+def check_xattn_visible(full, nox, st, factor=10.0):
+    """The cross-attention term of Eq. 6 must matter at this size: dropping it moves some
+    score by more than `factor` times the score tolerance and changes the kept set. A
+    kernel that dropped or garbled the term would then fail the score comparison."""
+    import oracle
+    c = st["cand"]
+    a, b = full[c], nox[c]
+    tol = SCORE_RTOL * np.abs(a) + SCORE_FLOOR * np.abs(a).max()
+    ratio = float((np.abs(a - b) / tol).max())
+    assert ratio > factor, f"cross-attention moves scores by only {ratio:.1f}x the tolerance"
+    k1 = oracle.select_budget(full, st)[0]
+    k2 = oracle.select_budget(nox, st)[0]
+    nd = int((k1 != k2).sum())
+    assert nd >= 1, "cross-attention changes no kept position"
+    return ratio, nd
+
+
+def check_decode_on(o_gpu, q, k_pool, v_pool, live, bf16: bool):
+    """Decode output against the oracle's attention over the given live slot list (the
+    GPU's own, which is a valid answer whenever the kept set is)."""
+    import oracle
+    return check_attention(o_gpu, oracle.decode(q, k_pool, v_pool, live), bf16)

@@ -8,7 +8,9 @@ starting from zero), and when N > C scores (residual head on), selects and redir
 with the system prefix of 64 positions radix-protected; then it decodes over the live
 slots. After every turn the GPU's kept set must match the oracle's outside the
 selection band; both sides then continue from the GPU's decision, so the slot maps,
-freed and live lists are compared exactly turn after turn."""
+freed and live lists are compared exactly turn after turn. The residual head's weights
+make its cross-attention move every turn's scores and kept set visibly (checked on the
+oracle), so a kernel that dropped or garbled it would fail the comparison."""
 from collections import deque
 
 import numpy as np
@@ -17,7 +19,7 @@ import pytest
 import oracle
 import synth
 from paper_2606_09916_amd import ikv
-from parity import band_positions, check_attention, check_keep, check_scores
+from parity import check_attention, check_keep, check_scores, check_xattn_visible, oracle_scores_pair
 
 pytestmark = pytest.mark.gpu
 DEAD = synth.DEAD_SLOT
@@ -45,7 +47,7 @@ def test_multi_turn_session(dev):
     v_dev = torch.zeros_like(k_dev)
     pool = ikv.make_pool(k_dev, v_dev, L, Hq, Hkv, D, num_slots, DEAD)
     ikv.init_dead_slot(pool)
-    blob = synth.residual_blob(D, seed=24)
+    blob = synth.residual_blob(D, seed=24, variant="scaled", units=L * Hkv, out_std=5e-3)
     blob_dev = torch.from_numpy(blob).to(dev)
     ws = ikv.Workspace(dev)
     M_dev = torch.zeros(L * Hkv * R * D, dtype=torch.float32, device=dev)
@@ -92,12 +94,14 @@ def test_multi_turn_session(dev):
             ikv.score_history(pool, sess, S_dev, M_dev, scores, ws, qpos=torch.from_numpy(qpos).to(dev),
                               residual=blob_dev, flags=ikv.IKV_RESIDUAL)
             ikv.select_budget(sess, S_dev, DEAD, scores, keep, n_keep, tau, ws)
-            want = oracle.scores(k_host, S, sets, M_o, Hkv, R, blob, oracle.FLAG_RESIDUAL, qpos, DEAD)
+            want, nox = oracle_scores_pair(k_host, S, sets, M_o, Hkv, R, blob, qpos, DEAD)
+            ratio, nd = check_xattn_visible(want, nox, sets)
             check_scores(scores.cpu().numpy(), want, sets["cand"])
             keep_o, n_o, tau_o = oracle.select_budget(want, sets)
             keep_g = keep.cpu().numpy().astype(bool)
             ndiff = check_keep(keep_g, int(n_keep.item()), keep_o, n_o, want, tau_o, sets["cand"])
-            print(f"turn {t}: N = {N}, live = {int(sets['live'].sum())}, kept = {n_o}, band differences = {ndiff}")
+            print(f"turn {t}: N = {N}, live = {int(sets['live'].sum())}, kept = {n_o}, band differences = {ndiff}, "
+                  f"cross-attention {ratio:.0f}x tolerance / {nd} kept positions")
 
             # redirect from the GPU's kept set, on both sides
             freed = torch.empty(N, dtype=torch.int32, device=dev)

@@ -131,3 +131,33 @@ def test_redirect_large_pools_exact(dev, num_slots):
         assert int(n_freed[b]) == len(freed_o) and int(n_live[b]) == len(live_o)
         assert np.array_equal(freed[o:o + len(freed_o)], freed_o)
         assert np.array_equal(live[o:o + len(live_o)], live_o)
+
+
+def test_select_barrier_give_up_is_reported(dev, monkeypatch):
+    """The cooperative selection's grid barriers wait a bounded number of polls. Forced
+    from the host to give up at once (IKV_SELECT_SPINS=0, so every kernel still runs to
+    its end), the call's outputs are not valid and the library's next call returns
+    IKV_EHIP; the call after that selects exactly again."""
+    torch = _torch()
+    monkeypatch.delenv("IKV_NO_COOP", raising=False)
+    n = 40000
+    rows = _rows((n,))
+    S = synth.slot_map(n, 2 * n + 1, seed=101)
+    sc = synth.score_vector(n, seed=201, ties=False)
+    ikv.timing(True)
+    try:
+        monkeypatch.setenv("IKV_SELECT_SPINS", "0")
+        _select(dev, rows, S, sc)
+        names = [name for name, _ in ikv.timing_read()]
+    finally:
+        ikv.timing(False)
+    if "k_select_coop" not in names:
+        pytest.skip(f"the cooperative selection did not run here ({names})")
+    monkeypatch.delenv("IKV_SELECT_SPINS")
+    with pytest.raises(ikv.IkvError) as e:
+        _select(dev, rows, S, sc)
+    assert e.value.status == -5 and "gave up" in str(e.value)
+    keep, n_keep, tau = _select(dev, rows, S, sc)
+    k_o, n_o, t_o = oracle.select_budget(sc.astype(np.float64), _sets(S, rows[0]))
+    assert np.array_equal(keep.astype(bool), k_o) and int(n_keep[0]) == n_o
+    torch.cuda.synchronize()
