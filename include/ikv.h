@@ -202,6 +202,28 @@ ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_de
                              void *stream);
 
 /*
+ * ikv_select_budget without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation). Same arguments, semantics and results as ikv_select_budget; the
+ * scratch is a static device array of IKV_SELECT_STATIC_MAX_BYTES per GPU, resolved
+ * on the first call on each device and held until the process ends. The call
+ * allocates nothing: no hipMalloc, hipFree or allocating library routine (it reports
+ * a timed-out grid barrier only if an earlier ikv_select_budget call has created the
+ * host fault word).
+ *   Sessions whose selection scratch (ikv_workspace_bytes with IKV_CALL_SELECT)
+ *   exceeds IKV_SELECT_STATIC_MAX_BYTES are rejected with IKV_EWORKSPACE before
+ *   anything is enqueued; that is about 6 bytes per position plus 44 KB per session.
+ *   Every call on one GPU shares that GPU's scratch, whatever its stream: calls that
+ *   overlap on one GPU race and give undefined results. Consecutive calls need
+ *   nothing cleared in between.
+ */
+#define IKV_SELECT_STATIC_MAX_BYTES (32u << 20)
+ikv_status ikv_select_budget_static(const ikv_session *sess, const ikv_session *sess_dev,
+                                    int32_t B, const int32_t *slot_maps, int32_t dead_slot,
+                                    const float *scores, uint8_t *keep, int32_t *n_keep,
+                                    float *tau, void *stream);
+
+/*
  * Slot-map eviction, Eq. 7, and the prefix-safe free of Sec. 3.4 / Appendix H.
  *   For every live position j with keep[j] == 0: slot_maps[j] <- dead_slot. Kept
  *   positions keep their slot; K/V rows are never touched.

@@ -182,6 +182,11 @@ uint32_t *host_fault_word() {
   return g_fault_dev;
 }
 
+uint32_t *host_fault_word_if_any() {
+  std::lock_guard<std::mutex> lk(g_fault_mu);
+  return g_fault_host.load(std::memory_order_acquire) ? g_fault_dev : nullptr;
+}
+
 bool take_host_fault() {
   uint32_t *h = g_fault_host.load(std::memory_order_acquire);
   return h != nullptr && __atomic_exchange_n(h, 0u, __ATOMIC_ACQ_REL) != 0u;
@@ -373,8 +378,29 @@ ikv_status ikv_select_budget(const ikv_session *sess, const ikv_session *sess_de
   if ((r = check_ws(workspace, workspace_bytes, select_bytes(sess, B)))) return r;
   return hip_status(ikv::launch_select(sess, sess_dev, B, max_n(sess, B), slot_maps, dead_slot, scores, keep, n_keep,
                                        tau, static_cast<uint32_t *>(workspace), total_positions(sess, B),
-                                       (hipStream_t)stream),
+                                       (hipStream_t)stream, true),
                     "ikv_select_budget");
+}
+
+ikv_status ikv_select_budget_static(const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                                    const int32_t *slot_maps, int32_t dead_slot, const float *scores,
+                                    uint8_t *keep, int32_t *n_keep, float *tau, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
+  ikv_status r = check_sessions(sess, sess_dev, B);
+  if (r) return r;
+  if (B == 0) return ok();
+  if (!slot_maps || !scores || !keep || !n_keep || !tau)
+    return fail(IKV_EINVAL, "slot_maps / scores / keep / n_keep / tau is NULL");
+  if (dead_slot < 0) return fail(IKV_ESHAPE, "dead_slot < 0");
+  const size_t need = select_bytes(sess, B);
+  if (need > size_t(IKV_SELECT_STATIC_MAX_BYTES))
+    return fail(IKV_EWORKSPACE, "these sessions need %zu bytes of selection scratch; the static scratch holds %zu",
+                need, size_t(IKV_SELECT_STATIC_MAX_BYTES));
+  uint32_t *scr = nullptr;
+  if ((r = hip_status(ikv::select_static_scratch(&scr), "ikv_select_budget_static: scratch address"))) return r;
+  return hip_status(ikv::launch_select(sess, sess_dev, B, max_n(sess, B), slot_maps, dead_slot, scores, keep, n_keep,
+                                       tau, scr, total_positions(sess, B), (hipStream_t)stream, false),
+                    "ikv_select_budget_static");
 }
 
 ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_dev, int32_t B, int64_t num_slots,

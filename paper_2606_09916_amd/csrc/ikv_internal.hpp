@@ -235,9 +235,15 @@ hipError_t launch_init_dead_slot(const ikv_pool &pool, hipStream_t st);
 hipError_t launch_qm_update(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_rows,
                             float *M, const void *q_span, float decay, hipStream_t st);
 hipError_t launch_score(const ScoreArgs &a, hipStream_t st);
+// may_alloc: the call may allocate the pinned host fault word on first use (false on
+// the allocation-free entry point, which reports through the word only if it exists).
 hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_dev, int B, int maxN,
                          const int32_t *slot_maps, int32_t dead, const float *scores, uint8_t *keep,
-                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st);
+                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st,
+                         bool may_alloc);
+// Device address of the allocation-free selection's static scratch on the current
+// device (IKV_SELECT_STATIC_MAX_BYTES), resolved on the first call per device.
+hipError_t select_static_scratch(uint32_t **ptr);
 size_t select_workspace_bytes(const ikv_session *sess, int B, int64_t total_positions);
 hipError_t launch_redirect(const ikv_session *sess_dev, int B, int64_t num_slots, int32_t *slot_maps,
                            int32_t dead, const uint8_t *keep, int32_t *freed, int32_t *n_freed,
@@ -253,6 +259,7 @@ int decode_splits(int maxN);
 // kept for the life of the process; nullptr if the allocation failed. take_host_fault()
 // returns whether it was set and clears it.
 uint32_t *host_fault_word();
+uint32_t *host_fault_word_if_any();   // the word if it exists, never allocating
 bool take_host_fault();
 
 }  // namespace ikv

@@ -13,6 +13,7 @@
 #include <unistd.h>
 
 #include <atomic>
+#include <mutex>
 #include <chrono>
 #include <random>
 
@@ -915,9 +916,36 @@ static int coop_capacity() {
   return cap[dev];
 }
 
+// ---- scratch of the allocation-free selection (ikv_select_budget_static): one array
+// per device, held until the process ends, shared by every call on that device. Host
+// code reaches it only through the address hipGetSymbolAddress returns.
+static __device__ __align__(256) uint32_t scratch[IKV_SELECT_STATIC_MAX_BYTES / 4];
+
+namespace {
+std::mutex g_scratch_mu;
+uint32_t *g_scratch[64];                           // per device, resolved once with that device current
+}  // namespace
+
+hipError_t select_static_scratch(uint32_t **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = static_cast<uint32_t *>(p);
+  }
+  *ptr = g_scratch[dev];
+  return hipSuccess;
+}
+
 hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_dev, int B, int maxN,
                          const int32_t *slot_maps, int32_t dead, const float *scores, uint8_t *keep,
-                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st) {
+                         int32_t *n_keep, float *tau, uint32_t *ws, int64_t total_positions, hipStream_t st,
+                         bool may_alloc) {
   const int64_t keys_off = sel_chunks_before(sess_host, B) * SEL_PART;
   const int64_t res_off = keys_off + total_positions;
   const int64_t gmax = cdiv(maxN, SC_CHUNK);
@@ -935,7 +963,7 @@ hipError_t launch_select(const ikv_session *sess_host, const ikv_session *sess_d
     static std::atomic<uint64_t> calls{1};
     uint64_t stamp0 = tag | ((calls.fetch_add(1) * SC_BARS) & ((1ull << 40) - 1));
     uint32_t spins = select_spin_limit();
-    uint32_t *fault = host_fault_word();
+    uint32_t *fault = may_alloc ? host_fault_word() : host_fault_word_if_any();
     KTimer kt_("k_select_coop", st);
     void *args[] = {(void *)&sess_dev, (void *)&slot_maps, (void *)&dead, (void *)&scores, (void *)&keep,
                     (void *)&n_keep, (void *)&tau, (void *)&coop, (void *)&stamp0, (void *)&spins, (void *)&fault};

@@ -20,7 +20,7 @@ STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE",
           -5: "IKV_EHIP"}
 
 # Every symbol include/ikv.h declares.
-SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget",
+SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget", "ikv_select_budget_static",
            "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error",
            "ikv_timing", "ikv_timing_read")
 
@@ -61,6 +61,8 @@ def lib() -> ctypes.CDLL:
                                   c_void_p, c_void_p, c_size_t, c_void_p],
             "ikv_select_budget": [S, c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                   c_void_p, c_size_t, c_void_p],
+            "ikv_select_budget_static": [S, c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p, c_void_p,
+                                         c_void_p, c_void_p],
             "ikv_redirect_slots": [S, c_void_p, c_int32, c_int64, c_void_p, c_int32, c_void_p, c_void_p, c_void_p,
                                    c_void_p, c_void_p, c_void_p, c_size_t, c_void_p],
             "ikv_decode_attend_slotmap": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
@@ -179,6 +181,13 @@ def select_budget(sess: Sessions, slot_maps, dead_slot: int, scores, keep, n_kee
     _check(lib().ikv_select_budget(sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps), dead_slot, _ptr(scores),
                                    _ptr(keep), _ptr(n_keep), _ptr(tau), wp, wn, _stream(stream)),
            "ikv_select_budget")
+
+
+def select_budget_static(sess: Sessions, slot_maps, dead_slot: int, scores, keep, n_keep, tau, stream=None) -> None:
+    """ikv_select_budget on the library's static scratch: no workspace, nothing allocated."""
+    _check(lib().ikv_select_budget_static(sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps), dead_slot,
+                                          _ptr(scores), _ptr(keep), _ptr(n_keep), _ptr(tau), _stream(stream)),
+           "ikv_select_budget_static")
 
 
 def redirect_slots(sess: Sessions, num_slots: int, slot_maps, dead_slot: int, keep, freed, n_freed, live, n_live,
