@@ -262,6 +262,77 @@ ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *se
                                      size_t workspace_bytes, void *stream);
 
 /*
+ * Session management on the host (no device work; every call below is synchronous,
+ * thread-safe per store, and touches host memory only).
+ *
+ * Session key (Appendix A, session identification; Appendix H, session id
+ * derivation), from the first source available, in this order:
+ *   IKV_KEY_EXPLICIT  an explicit session id (session_id, session_id_len > 0 bytes);
+ *   IKV_KEY_SPAN      the token tuple of a designated session span
+ *                     tokens[span_start, span_end) (span_end > span_start);
+ *   IKV_KEY_PREFIX    the first min(n_tokens, IKV_PREFIX_TOKENS = 256) input tokens;
+ *   IKV_KEY_LOCAL     a key local to the request (no token ids), never equal to any
+ *                     other key, so unrelated requests never share a memory.
+ * Keys of different kinds never match, and keys match only when their bytes are
+ * equal (a hash only speeds the lookup).
+ */
+#define IKV_KEY_EXPLICIT 1
+#define IKV_KEY_SPAN     2
+#define IKV_KEY_PREFIX   3
+#define IKV_KEY_LOCAL    4
+#define IKV_PREFIX_TOKENS 256
+
+typedef struct ikv_key_source {
+  const char *session_id;     /* host bytes of an explicit id, or NULL */
+  int32_t session_id_len;     /* bytes of session_id; 0: none */
+  int32_t n_tokens;           /* input token ids of the request (0: none) */
+  const int32_t *tokens;      /* host, n_tokens entries, or NULL */
+  int32_t span_start, span_end; /* designated session span within tokens; equal: none */
+} ikv_key_source;
+
+/*
+ * The QueryMemory store of one compressor (Appendix A: an LRU of 1,024 memories per
+ * compressor; concurrent requests update disjoint keys). The store maps session keys
+ * to rows of a caller-owned device arena of `capacity` memories, each
+ * [L][Hkv*R][D] float32; a session's memory is at arena + slot * L * Hkv * R * D
+ * (its ikv_session.mem_off). The store holds no device memory.
+ *   ikv_memstore_create: a store of `capacity` >= 1 memories (host allocation).
+ *   ikv_memstore_acquire: the memory of src's session. A known key becomes the most
+ *     recently used and *fresh = 0. A new key takes an unused row, or else the row of
+ *     the least recently used memory that is not acquired (IKV_EUNSUPPORTED if every
+ *     memory is acquired), and *fresh = 1: the caller zeroes that row before its
+ *     first ikv_qm_update (a new session starts from M = 0). *kind (may be NULL)
+ *     gets the IKV_KEY_* that was used. Every acquire pins the memory against
+ *     eviction until the matching ikv_memstore_release.
+ *   ikv_memstore_trigger: whether a compression event runs now for the memory at
+ *     `slot` of a request of N positions and budget C: N > C (Appendix H), and at
+ *     least `trigger` positions (512 in the paper, Appendix A) since the last event
+ *     that fired for this memory (none yet counts as position 0). *fire = 1 records N.
+ *   ikv_memstore_size: memories held.
+ */
+typedef struct ikv_memstore ikv_memstore;
+ikv_status ikv_memstore_create(int32_t capacity, ikv_memstore **out);
+void ikv_memstore_destroy(ikv_memstore *store);
+ikv_status ikv_memstore_acquire(ikv_memstore *store, const ikv_key_source *src, int32_t *slot,
+                                int32_t *fresh, int32_t *kind);
+ikv_status ikv_memstore_release(ikv_memstore *store, int32_t slot);
+ikv_status ikv_memstore_trigger(ikv_memstore *store, int32_t slot, int32_t N, int32_t C,
+                                int32_t trigger, int32_t *fire);
+ikv_status ikv_memstore_size(ikv_memstore *store, int32_t *n);
+
+/*
+ * The actionable query span [qs, qe) (Sec. 3.1: the latest user, tool or function
+ * message that can affect the next decision, after template rendering). The caller
+ * passes the rendered request's messages as position ranges [msg_start, msg_end)
+ * in order, with actionable[m] != 0 for user, tool and function messages. The span
+ * is the latest non-empty actionable message; with none, the bounded query-tail
+ * fallback [max(0, N - tail_w), N) (W = 32 in the paper, Appendix A). Host arrays.
+ */
+ikv_status ikv_resolve_span(int32_t N, const int32_t *msg_start, const int32_t *msg_end,
+                            const uint8_t *actionable, int32_t n_msgs, int32_t tail_w,
+                            int32_t *qs, int32_t *qe);
+
+/*
  * Workspace size of one call (IKV_CALL_*) for these sessions, in bytes (0 when
  * the call needs none). `pool` may be NULL for SELECT; REDIRECT reads only
  * pool->num_slots. `flags` matter for SCORE only and are the score call's flags.

@@ -162,6 +162,16 @@ ikv_status pending_fault() {
 
 namespace ikv {
 
+ikv_status set_error(ikv_status code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
 namespace {
 std::mutex g_fault_mu;
 std::atomic<uint32_t *> g_fault_host{nullptr};   // pinned, mapped; never freed

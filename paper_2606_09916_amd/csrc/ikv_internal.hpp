@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "ikv.h"
+#include "ikv_error.hpp"
 
 namespace ikv {
 

@@ -22,7 +22,9 @@ STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE",
 # Every symbol include/ikv.h declares.
 SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget", "ikv_select_budget_static",
            "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error",
-           "ikv_timing", "ikv_timing_read")
+           "ikv_timing", "ikv_timing_read", "ikv_memstore_create", "ikv_memstore_destroy", "ikv_memstore_acquire",
+           "ikv_memstore_release", "ikv_memstore_trigger", "ikv_memstore_size", "ikv_resolve_span")
+IKV_KEY_EXPLICIT, IKV_KEY_SPAN, IKV_KEY_PREFIX, IKV_KEY_LOCAL = 1, 2, 3, 4
 
 
 class IkvError(RuntimeError):
@@ -41,6 +43,11 @@ class Session(ctypes.Structure):
     _fields_ = [("slot_off", c_int64), ("mem_off", c_int64), ("qspan_off", c_int64), ("qpos_off", c_int64),
                 ("N", c_int32), ("pi", c_int32), ("qs", c_int32), ("qe", c_int32), ("C", c_int32),
                 ("radix_prefix", c_int32), ("R", c_int32), ("nq", c_int32)]
+
+
+class KeySource(ctypes.Structure):
+    _fields_ = [("session_id", ctypes.c_char_p), ("session_id_len", c_int32), ("n_tokens", c_int32),
+                ("tokens", c_void_p), ("span_start", c_int32), ("span_end", c_int32)]
 
 
 _lib = None
@@ -69,12 +76,22 @@ def lib() -> ctypes.CDLL:
                                           c_void_p, c_size_t, c_void_p],
             "ikv_workspace_bytes": [P, S, c_int32, c_int32, c_uint32, ctypes.POINTER(c_size_t)],
             "ikv_timing": [c_int32],
+            "ikv_memstore_create": [c_int32, ctypes.POINTER(c_void_p)],
+            "ikv_memstore_acquire": [c_void_p, ctypes.POINTER(KeySource), ctypes.POINTER(c_int32),
+                                     ctypes.POINTER(c_int32), ctypes.POINTER(c_int32)],
+            "ikv_memstore_release": [c_void_p, c_int32],
+            "ikv_memstore_trigger": [c_void_p, c_int32, c_int32, c_int32, c_int32, ctypes.POINTER(c_int32)],
+            "ikv_memstore_size": [c_void_p, ctypes.POINTER(c_int32)],
+            "ikv_resolve_span": [c_int32, c_void_p, c_void_p, c_void_p, c_int32, c_int32, ctypes.POINTER(c_int32),
+                                 ctypes.POINTER(c_int32)],
             "ikv_timing_read": [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(c_float), c_int32],
         }
         for name, args in sig.items():
             f = getattr(L, name)
             f.argtypes = args
             f.restype = c_int32
+        L.ikv_memstore_destroy.argtypes = [c_void_p]
+        L.ikv_memstore_destroy.restype = None
         L.ikv_last_error.argtypes = []
         L.ikv_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -222,3 +239,73 @@ def timing_read(cap: int = 65536) -> list[tuple[str, float]]:
     if n < 0:
         _check(n, "ikv_timing_read")
     return [(names[i].decode(), float(ms[i])) for i in range(min(n, cap))]
+
+
+# ----------------------------------------------------------------------------- session management (host)
+
+class MemStore:
+    """The QueryMemory store of one compressor (ikv_memstore_*): session keys to rows of a
+    caller-owned device arena, least recently used rows reused first."""
+
+    def __init__(self, capacity: int = 1024):
+        h = c_void_p()
+        _check(lib().ikv_memstore_create(capacity, ctypes.byref(h)), "ikv_memstore_create")
+        self._h = h
+        self.capacity = capacity
+
+    def close(self) -> None:
+        if self._h:
+            lib().ikv_memstore_destroy(self._h)
+            self._h = c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def acquire(self, session_id: bytes | None = None, tokens=None, span: tuple[int, int] | None = None):
+        """(slot, fresh, kind) of the session the sources identify."""
+        import numpy as np
+        src = KeySource()
+        keep = []
+        if session_id:
+            src.session_id = session_id
+            src.session_id_len = len(session_id)
+        if tokens is not None and len(tokens):
+            t = np.ascontiguousarray(tokens, dtype=np.int32)
+            keep.append(t)
+            src.tokens = t.ctypes.data
+            src.n_tokens = len(t)
+            if span is not None:
+                src.span_start, src.span_end = int(span[0]), int(span[1])
+        slot, fresh, kind = c_int32(), c_int32(), c_int32()
+        _check(lib().ikv_memstore_acquire(self._h, ctypes.byref(src), ctypes.byref(slot), ctypes.byref(fresh),
+                                          ctypes.byref(kind)), "ikv_memstore_acquire")
+        return slot.value, bool(fresh.value), kind.value
+
+    def release(self, slot: int) -> None:
+        _check(lib().ikv_memstore_release(self._h, slot), "ikv_memstore_release")
+
+    def trigger(self, slot: int, N: int, C: int, trigger: int = 512) -> bool:
+        fire = c_int32()
+        _check(lib().ikv_memstore_trigger(self._h, slot, N, C, trigger, ctypes.byref(fire)), "ikv_memstore_trigger")
+        return bool(fire.value)
+
+    def __len__(self) -> int:
+        n = c_int32()
+        _check(lib().ikv_memstore_size(self._h, ctypes.byref(n)), "ikv_memstore_size")
+        return n.value
+
+
+def resolve_span(N: int, messages, tail_w: int = 32) -> tuple[int, int]:
+    """[qs, qe) from the rendered messages [(start, end, actionable)], or the tail fallback."""
+    import numpy as np
+    m = list(messages)
+    st = np.ascontiguousarray([a for a, _, _ in m] or [0], dtype=np.int32)
+    en = np.ascontiguousarray([b for _, b, _ in m] or [0], dtype=np.int32)
+    ac = np.ascontiguousarray([1 if c else 0 for _, _, c in m] or [0], dtype=np.uint8)
+    qs, qe = c_int32(), c_int32()
+    _check(lib().ikv_resolve_span(N, st.ctypes.data, en.ctypes.data, ac.ctypes.data, len(m), tail_w,
+                                  ctypes.byref(qs), ctypes.byref(qe)), "ikv_resolve_span")
+    return qs.value, qe.value
