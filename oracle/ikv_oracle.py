@@ -357,3 +357,84 @@ def step(k_pool, v_pool, S, M, q_dec, Hkv, R, pi, qs, qe, C, radix_prefix, dead=
     o = decode(q_dec, k_pool, v_pool, live)
     return {"sets": st, "scores": s, "keep": keep, "n_keep": n_keep, "tau": tau,
             "S": S_new, "freed": freed, "live": live, "out": o}
+
+
+# ----------------------------------------------------------------------------- baseline scorers on the substrate
+# Sec. 4.1 (baselines) and Appendix A (compression settings): SnapKV with an observation
+# window of W = 32 tail query rows, kernel-7 max-pool smoothing; H2O in ratio mode with
+# a recent-window floor. Appendix "substrate integration": every scorer feeds the same
+# selection, dead-slot redirect and decode. Query head h reads KV head h // G.
+
+def attention_mass(k_pool, S, cand, q_rows, Hkv):
+    """Attention each candidate receives from a set of query rows, per (layer, KV head).
+
+    ``q_rows`` [L][Hq][n][D]: n post-RoPE query rows of every query head. For layer l
+    and KV head g, every row of the G query heads h with h // G = g takes a softmax
+    over the candidate set A of q . K[l, S[i], g] / sqrt(D); v[l, g, j] is the sum of
+    those softmax weights at j. Returns float64 [L][Hkv][N], zero off A.
+    """
+    S = np.asarray(S)
+    q = widen(q_rows)
+    L, Hq, n, D = q.shape
+    G = Hq // Hkv
+    N = len(S)
+    v = np.zeros((L, Hkv, N))
+    idx = np.nonzero(cand)[0]
+    if len(idx) == 0 or n == 0:
+        return v
+    for l in range(L):
+        Kl = widen(k_pool[l][S[idx]])              # [|A|][Hkv][D]
+        for h in range(Hq):
+            g = h // G
+            X = q[l, h] @ Kl[:, g, :].T / math.sqrt(D)   # [n][|A|]
+            X = X - X.max(axis=1, keepdims=True)
+            P = np.exp(X)
+            P = P / P.sum(axis=1, keepdims=True)
+            v[l, g, idx] += P.sum(axis=0)
+    return v
+
+
+def h2o_scores(k_pool, S, st, q_obs, Hkv):
+    """H2O-style heavy-hitter score: the attention a candidate has received from the
+    observed query rows, summed over layers and query heads. -inf off A; all -inf when
+    the compression gate skips the session."""
+    N = len(S)
+    if st["skip"]:
+        return np.full(N, -np.inf)
+    v = attention_mass(k_pool, S, st["cand"], q_obs, Hkv)
+    out = v.sum(axis=(0, 1))
+    out[~st["cand"]] = -np.inf
+    return out
+
+
+def max_pool(v, kernel):
+    """1-D max pooling of v along its last axis, stride 1, window of `kernel` (odd)
+    positions centred on each position, positions past either end left out."""
+    r = kernel // 2
+    N = v.shape[-1]
+    out = np.empty_like(v)
+    for j in range(N):
+        out[..., j] = v[..., max(0, j - r):min(N, j + r + 1)].max(axis=-1)
+    return out
+
+
+def snapkv_scores(k_pool, S, st, q_win, Hkv, kernel=7):
+    """SnapKV-style score: per (layer, KV head) the attention mass from the observation
+    window's query rows (attention_mass), smoothed by a max pool of `kernel` positions
+    along the position axis (non-candidates hold zero mass), then summed over layers
+    and KV heads. -inf off A; all -inf when the compression gate skips the session."""
+    N = len(S)
+    if st["skip"]:
+        return np.full(N, -np.inf)
+    v = attention_mass(k_pool, S, st["cand"], q_win, Hkv)
+    out = max_pool(v, kernel).sum(axis=(0, 1))
+    out[~st["cand"]] = -np.inf
+    return out
+
+
+def recent_window(N, C, recent_ratio):
+    """H2O's ratio mode with a recent-window floor: the last ceil(recent_ratio * C)
+    positions form the forced recent window [qs, N); the rest of the budget goes to the
+    heavy hitters."""
+    w = min(N, int(math.ceil(recent_ratio * C)))
+    return N - w, N

@@ -66,8 +66,16 @@ PLANTS = [
      "if j > radix_prefix and u != dead and u not in kept_slots:"),
     ("live list in slot order", "live_list = S_new[S_new != dead]", "live_list = np.sort(S_new[S_new != dead])"),
     # ---- decode
-    ("decode GQA head mapping", "            g = h // G\n", "            g = h % Hkv\n"),
+    ("decode GQA head mapping", "            g = h // G\n            x = Kl", "            g = h % Hkv\n            x = Kl"),
     ("decode without 1/sqrt(D)", "x = Kl[:, g, :] @ q[l, h] / math.sqrt(D)", "x = Kl[:, g, :] @ q[l, h]"),
+    # ---- baseline scorers on the substrate (Sec. 4.1)
+    ("attention mass GQA head mapping", "            g = h // G\n            X = q[l, h]",
+     "            g = h % Hkv\n            X = q[l, h]"),
+    ("attention mass without 1/sqrt(D)", "X = q[l, h] @ Kl[:, g, :].T / math.sqrt(D)", "X = q[l, h] @ Kl[:, g, :].T"),
+    ("SnapKV pooling after the unit sum", "out = max_pool(v, kernel).sum(axis=(0, 1))",
+     "out = max_pool(v.sum(axis=(0, 1)), kernel)"),
+    ("pool window one too wide", "    r = kernel // 2\n", "    r = kernel // 2 + 1\n"),
+    ("recent window rounded down", "w = min(N, int(math.ceil(recent_ratio * C)))", "w = min(N, int(recent_ratio * C))"),
 ]
 
 

@@ -656,3 +656,95 @@ def test_gate_counts_dead_positions():
     assert np.array_equal(keep, st["live"]) and n_keep == 9 and tau == s[st["cand"]].min()
     st12 = oracle.sets(S, 0, 10, 12, C=12, dead=0)
     assert st12["skip"] and np.all(np.isneginf(oracle.scores(pool, S, st12, M, Hkv, R)))
+
+
+# ============================================================================ baseline scorers (Sec. 4.1)
+
+def test_max_pool_hand():
+    v = np.array([0, 3, 1, 0, 0, 0, 0, 0, 5, 2], dtype=np.float64)
+    np.testing.assert_array_equal(oracle.ikv_oracle.max_pool(v, 7), [3, 3, 3, 3, 3, 5, 5, 5, 5, 5])
+    np.testing.assert_array_equal(oracle.ikv_oracle.max_pool(v, 3), [3, 3, 3, 1, 0, 0, 0, 5, 5, 5])
+    np.testing.assert_array_equal(oracle.ikv_oracle.max_pool(v, 1), v)
+
+
+def _one_row_pool(x):
+    """One layer, one KV head, one query head, one query row q = e0, D = 4: the logit of
+    position i is x_i by construction (K_i = 2 x_i e0, scale 1/sqrt(4))."""
+    N = len(x)
+    K = np.zeros((1, N, 1, 4), np.float32)
+    K[0, :, 0, 0] = 2 * np.asarray(x)
+    S = np.arange(1, N + 1, dtype=np.int32)
+    pool = pool_from_logical(K, S, N + 1)
+    q = np.zeros((1, 1, 1, 4), np.float32)
+    q[0, 0, 0, 0] = 1.0
+    return pool, S, q
+
+
+def test_snapkv_hand_worked():
+    """Logits (ln 4, 0, 0, 0, 0, ln 2, 0, 0, 0, 0): softmax weights (4,1,1,1,1,2,1,1,1,1)/14,
+    max-pooled over 7 positions: (4,4,4,4,2,2,2,2,2,1)/14. The keys are float32, so the
+    logits carry the float32 rounding of ln 2 (relative 1e-8 in the weights)."""
+    ln2 = math.log(2.0)
+    x = [2 * ln2, 0, 0, 0, 0, ln2, 0, 0, 0, 0]
+    pool, S, q = _one_row_pool(x)
+    st = oracle.sets(S, 0, 10, 10, 0, 0)                  # no forced positions, C = 0: every position scored
+    np.testing.assert_allclose(oracle.ikv_oracle.snapkv_scores(pool, S, st, q, 1),
+                               np.array([4, 4, 4, 4, 2, 2, 2, 2, 2, 1]) / 14.0, rtol=1e-7)
+    np.testing.assert_allclose(oracle.ikv_oracle.h2o_scores(pool, S, st, q, 1),
+                               np.array([4, 1, 1, 1, 1, 2, 1, 1, 1, 1]) / 14.0, rtol=1e-7)
+    # position 0 forced: out of the softmax, zero mass in the pool windows; weights
+    # (1,1,1,1,2,1,1,1,1)/10 on positions 1..9, position 5's 2/10 reaching positions 2..8
+    st_f = oracle.sets(S, 1, 10, 10, 0, 0)
+    s = oracle.ikv_oracle.snapkv_scores(pool, S, st_f, q, 1)
+    assert s[0] == -math.inf
+    np.testing.assert_allclose(s[1:], np.array([1, 2, 2, 2, 2, 2, 2, 2, 1]) / 10.0, rtol=1e-7)
+
+
+def _baseline_case(seed, L=2, N=40, Hkv=2, G=3, D=8, n=5):
+    rng = np.random.default_rng(seed)
+    pool, S = rand_pool(rng, L, N, Hkv, D)
+    S[rng.choice(N, 6, replace=False)] = 0
+    q = rng.standard_normal((L, Hkv * G, n, D)).astype(np.float32)
+    st = oracle.sets(S, 2, N - 4, N, 10, 0)
+    return pool, S, q, st
+
+
+def test_attention_mass_closed_form_and_brute_force():
+    pool, S, q, st = _baseline_case(21)
+    L, Hq, n, D = q.shape
+    Hkv = 2
+    v = oracle.ikv_oracle.attention_mass(pool, S, st["cand"], q, Hkv)
+    # every query row's softmax sums to one: each KV head collects G * n, the total L * Hq * n
+    np.testing.assert_allclose(v.sum(axis=2), (Hq // Hkv) * n, rtol=1e-13)
+    assert np.all(v[:, :, ~st["cand"]] == 0)
+    cand = np.nonzero(st["cand"])[0]
+    for l in range(L):
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            for t in range(n):
+                logit = {i: float(q[l, h, t].astype(np.float64) @ pool[l, S[i], g].astype(np.float64)) / math.sqrt(D)
+                         for i in cand}
+                den = sum(math.exp(x) for x in logit.values())
+                for i in cand[:3]:
+                    v[l, g, i] -= math.exp(logit[i]) / den
+    assert np.abs(v[:, :, cand[:3]]).max() < 1e-12
+
+
+def test_snapkv_pool_bounds_and_kernel_one():
+    pool, S, q, st = _baseline_case(22)
+    h2o = oracle.ikv_oracle.h2o_scores(pool, S, st, q, 2)
+    np.testing.assert_array_equal(oracle.ikv_oracle.snapkv_scores(pool, S, st, q, 2, kernel=1), h2o)
+    snap = oracle.ikv_oracle.snapkv_scores(pool, S, st, q, 2)
+    c = st["cand"]
+    assert np.all(snap[c] >= h2o[c]) and np.all(np.isneginf(snap[~c]))
+    # the pooled sum is at most the sum of the per-unit maxima over each window
+    v = oracle.ikv_oracle.attention_mass(pool, S, c, q, 2)
+    j = int(np.nonzero(c)[0][5])
+    lo, hi = max(0, j - 3), j + 4
+    assert math.isclose(snap[j], v[:, :, lo:hi].max(axis=2).sum(), rel_tol=1e-13)
+
+
+def test_recent_window_hand():
+    assert oracle.ikv_oracle.recent_window(32768, 8192, 0.5) == (32768 - 4096, 32768)
+    assert oracle.ikv_oracle.recent_window(100, 8192, 0.5) == (0, 100)
+    assert oracle.ikv_oracle.recent_window(1000, 301, 0.5) == (849, 1000)
