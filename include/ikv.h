@@ -65,6 +65,7 @@ typedef int32_t ikv_status;
 /* ikv_score_history flags. */
 #define IKV_RESIDUAL  1u   /* add alpha * MLP(phi ++ c), Eq. 4 (needs `residual`)           */
 #define IKV_NO_XATTN  2u   /* the "- x-attn" ablation: c_j = 0 in Eq. 4 (Sec. 3.3)          */
+#define IKV_POOL7     4u   /* SnapKV-style score (Sec. 4.1 baselines): see ikv_score_history  */
 
 /* ikv_workspace_bytes call ids. */
 #define IKV_CALL_SCORE    1
@@ -160,6 +161,21 @@ ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess,
  *   Sessions with N <= C are skipped (Appendix H): all their scores are -INFINITY.
  *   slot_maps, M, qpos: read only. M + mem_off must be 16-byte aligned for every
  *   session (IKV_EINVAL otherwise).
+ */
+/*
+ * The same call scores for the baseline compressors of Sec. 4.1 on the same substrate
+ * (Appendix: every scorer feeds the same selection, redirect and decode), with M
+ * holding query rows instead of memory rows: a KV head's R rows are the n query rows
+ * of each of its G query heads, so q[L][Hq][n][D] is M as it stands, with R = G * n.
+ *   H2O-style (heavy hitters): flags 0, M the observed query rows: s_j is the
+ *     attention j receives from them, summed over layers and query heads. The recent
+ *     window of ratio mode is the forced span [qs, qe) the caller sets.
+ *   SnapKV-style: flags IKV_POOL7, M the W = 32 window query rows: per (layer, KV
+ *     head) the attention mass of the window's rows at each position (zero off A),
+ *     max-pooled over the 7 positions j-3 .. j+3 (within [0, N)), then summed.
+ *     IKV_POOL7 runs on the matrix-core path only (D = 128, bf16 pool, even Hkv,
+ *     R <= 128; IKV_EUNSUPPORTED otherwise) and excludes IKV_RESIDUAL (IKV_EINVAL).
+ *     Its workspace adds L * Hkv floats per position of the batch.
  */
 ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
                              const ikv_session *sess_dev, int32_t B,

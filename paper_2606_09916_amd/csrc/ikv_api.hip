@@ -111,18 +111,19 @@ bool use_mfma(const ikv_pool *p, const ikv_session *, int) {
   return p->D == 128 && p->kv_dtype == IKV_BF16;
 }
 
+int64_t total_positions(const ikv_session *sess, int B) {
+  int64_t total = 0;
+  for (int b = 0; b < B; ++b) total = std::max<int64_t>(total, sess[b].slot_off + sess[b].N);
+  return total;
+}
+
 size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flags) {
   const bool resid = (flags & IKV_RESIDUAL) != 0;
   const int units = p->L * p->Hkv;
   int64_t f = ikv::score_offset(s, B, p->L, units, p->D, resid, use_mfma(p, s, B));
   if (resid) f += ikv::score_shared_floats(p->D);
+  if (flags & IKV_POOL7) f += int64_t(units) * total_positions(s, B);    // per-unit attention masses
   return size_t(f) * sizeof(float);
-}
-
-int64_t total_positions(const ikv_session *sess, int B) {
-  int64_t total = 0;
-  for (int b = 0; b < B; ++b) total = std::max<int64_t>(total, sess[b].slot_off + sess[b].N);
-  return total;
 }
 
 size_t select_bytes(const ikv_session *sess, int B) {
@@ -333,7 +334,8 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   ikv_status r = check_pool(pool);
   if (r) return r;
   if ((r = check_sessions(sess, sess_dev, B))) return r;
-  if (flags & ~(IKV_RESIDUAL | IKV_NO_XATTN)) return fail(IKV_EINVAL, "unknown flag bits 0x%x", flags);
+  if (flags & ~(IKV_RESIDUAL | IKV_NO_XATTN | IKV_POOL7)) return fail(IKV_EINVAL, "unknown flag bits 0x%x", flags);
+  if ((flags & IKV_POOL7) && (flags & IKV_RESIDUAL)) return fail(IKV_EINVAL, "IKV_POOL7 excludes IKV_RESIDUAL");
   if (B == 0) return ok();
   if (!slot_maps || !M || !scores) return fail(IKV_EINVAL, "slot_maps / M / scores is NULL");
   const bool resid = (flags & IKV_RESIDUAL) != 0;
@@ -368,6 +370,9 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
             int64_t(pool->num_slots) * pool->Hkv * pool->D * 2 <= int64_t(UINT32_MAX);
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
+  a.total_positions = total_positions(sess, B);
+  if ((flags & IKV_POOL7) && !a.stats)
+    return fail(IKV_EUNSUPPORTED, "IKV_POOL7 needs D = 128, a bf16 pool, an even Hkv and R <= 128");
   a.maxR = maxR;
   a.minR = minR;
   a.maxNq = maxNq;

@@ -218,6 +218,7 @@ struct ScoreArgs {
   float *ws;           // session blocks, then the shared block
   float *ws_shared;
   int maxN, maxR, minR, maxNq;
+  int64_t total_positions;   // max over sessions of slot_off + N: the row stride of the per-unit masses
   bool mfma;           // MFMA score passes (D = 128, bf16 pool)
   bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)

@@ -940,17 +940,28 @@ __device__ __forceinline__ void dma16s(const void *sbase, uint32_t voff, uint32_
 // SIMD); either way two workgroups share a CU. A batch that holds both kinds of
 // session runs one launch of each, and each launch skips the other's sessions
 // (`big`: 0 every session, 1 only R <= 64, 2 only R > 64).
-template <int NW>
+//
+// MASS: the same pass after the row normalisers are known (the SnapKV-style scorer):
+// the accumulators start from the rows' seeds -(max + log2 Z), so exp2 of a logit is
+// its softmax weight, and each position keeps its attention mass in this unit (the
+// sum over the unit's rows) instead of the rows' statistics. The masses of a tile are
+// summed over the waves of a head through a small LDS buffer at the top of the next
+// tile and parked in the tile's bias / key-offset entries, which no later step reads;
+// the chunk's masses leave once, at the end: umass[u][slot_off + j] (row stride
+// ustride), zero off the candidates.
+template <int NW, bool MASS = false>
 __global__ void __launch_bounds__(128 * NW) __attribute__((amdgpu_waves_per_eu(NW, NW)))
 k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
               const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-              const float *__restrict__ M, float *__restrict__ scores, bool resid, int CH, int big) {
+              const float *__restrict__ M, float *__restrict__ scores, bool resid, int CH, int big,
+              float *__restrict__ umass = nullptr, int64_t ustride = 0) {
   constexpr int ST_THREADS = 128 * NW;
   constexpr int ST_STAGES = 4;
   constexpr int KI = 8 / NW;                     // key loads (1 KB each) per wave per stage
   __shared__ __align__(1024) uint16_t ring[ST_STAGES * ST_STAGE];
   __shared__ uint32_t koff[ST_CHMAX];            // byte offset of each position's key rows in the layer
   __shared__ __align__(16) float bias[ST_CHMAX];  // 0 for a candidate, -inf otherwise
+  __shared__ float mred[MASS ? 2 * 2 * NW * ST_TILE : 1];   // per tile parity, head, wave: 32 masses
 
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
@@ -960,7 +971,7 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   const int c0 = chunk * CH;
   if (c0 >= s.N) return;
   if (s.N <= s.C) {                              // the gate: nothing is scored
-    if (hp == 0)
+    if (hp == 0 && !MASS)
       for (int j = c0 + int(threadIdx.x); j < min(s.N, c0 + CH); j += ST_THREADS) scores[s.slot_off + j] = -INFINITY;
     return;
   }
@@ -1017,7 +1028,7 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
       }
     // chunk 0 keeps the split rows for the second pass, in the layout of k_msplit (rows
     // padded to whole slices, the pad rows zero)
-    if (chunk == 0)
+    if (chunk == 0 && !MASS)
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
         const int row = r0 + 16 * rb + r16;
@@ -1040,6 +1051,16 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
     const bool cand = in && slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
     koff[p] = uint32_t(slot) * slot_bytes;
     bias[p] = cand ? 0.f : -INFINITY;
+  }
+  // the mass pass: seeds of the lane's two rows (-inf past R, so those rows add nothing)
+  float sd[2] = {0.f, 0.f};
+  if constexpr (MASS) {
+    const float *nl2 = base + z.off_nl2();
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const int row = r0 + 16 * rb + r16;
+      sd[rb] = row < R ? nl2[int64_t(u) * R + row] : -INFINITY;
+    }
   }
   // every compiler-issued load of the set-up is complete before the first key load
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1079,7 +1100,8 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       const float4 bv = *reinterpret_cast<const float4 *>(bias + tt * ST_TILE + 16 * pb + 4 * g);
-      acc[pb][0] = acc[pb][1] = f32x4{bv.x, bv.y, bv.z, bv.w};
+      acc[pb][0] = f32x4{bv.x + sd[0], bv.y + sd[0], bv.z + sd[0], bv.w + sd[0]};
+      acc[pb][1] = f32x4{bv.x + sd[1], bv.y + sd[1], bv.z + sd[1], bv.w + sd[1]};
     }
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
@@ -1090,6 +1112,30 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
           acc[pb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[pb][ks], mh[rb][ks], acc[pb][rb], 0, 0, 0);
           acc[pb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[pb][ks], ml[rb][ks], acc[pb][rb], 0, 0, 0);
         }
+    if constexpr (MASS) {
+      // position 16 pb + 4 g + i: its softmax weights under the wave's 32 rows, summed
+      // over the 16 lanes of the lane group
+      float pm[2][4];
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = ex2(acc[pb][0][i]) + ex2(acc[pb][1][i]);
+          v += __shfl_xor(v, 1, WAVE);
+          v += __shfl_xor(v, 2, WAVE);
+          v += __shfl_xor(v, 4, WAVE);
+          v += __shfl_xor(v, 8, WAVE);
+          pm[pb][i] = v;
+        }
+      if (r16 == 0) {
+        float *mr = mred + (((tt & 1) * 2 + hh) * NW + (w % NW)) * ST_TILE;
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mr[16 * pb + 4 * g + i] = pm[pb][i];
+      }
+      return;
+    }
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       float m = Mr[rb];
@@ -1109,6 +1155,17 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   };
 
   const bool act = __builtin_amdgcn_readfirstlane(r0) < R;   // a wave past the last row only loads
+  // the mass pass: tile k's masses of head hh, summed over the head's active waves (in
+  // wave order), into bias (head 0) or koff (head 1) at the tile's positions
+  auto mass_fold = [&](int k) {
+    if (!MASS || w % NW != 0 || lane >= ST_TILE) return;
+    const int nwa = min(NW, (R + 31) / 32);
+    const float *mr = mred + ((k & 1) * 2 + hh) * NW * ST_TILE + lane;
+    float v = 0.f;
+    for (int q = 0; q < nwa; ++q) v += mr[q * ST_TILE];
+    if (hh == 0) bias[k * ST_TILE + lane] = v;
+    else koff[k * ST_TILE + lane] = __float_as_uint(v);
+  };
   for (int k = 0; k < ST_STAGES - 1 && k < T; ++k) issue(k);
   for (int tt = 0; tt < T; ++tt) {
     // tile tt's KI loads per wave are done once at most those of the later tiles
@@ -1116,7 +1173,20 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
     vm_wait(KI * min(ST_STAGES - 2, T - 1 - tt));
     __syncthreads();
     if (tt + ST_STAGES - 1 < T) issue(tt + ST_STAGES - 1);
+    if (tt > 0) mass_fold(tt - 1);
     if (act) compute(tt);
+  }
+  if constexpr (MASS) {
+    __syncthreads();
+    mass_fold(T - 1);
+    __syncthreads();
+    const int u0 = l * Hkv + h0;
+    float *o0 = umass + int64_t(u0) * ustride + s.slot_off + c0, *o1 = o0 + ustride;
+    for (int p = t; p < npos; p += ST_THREADS) {
+      o0[p] = bias[p];
+      o1[p] = __uint_as_float(koff[p]);
+    }
+    return;
   }
 
   // chunk 0 with the residual head: column sums of the head pair's 2 R memory rows
@@ -1247,6 +1317,47 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   }
 }
 
+// The SnapKV-style score: for each candidate j, the sum over units u of the largest
+// attention mass among positions j - 3 .. j + 3 of unit u (a max pool of 7 positions,
+// positions outside [0, N) left out; non-candidates hold zero mass). A workgroup owns 64
+// positions; its four waves take every fourth unit, each lane one position, and their
+// sums are added in wave order.
+constexpr int PL_POS = 64;
+
+__global__ void __launch_bounds__(256) k_pool7(const ikv_session *__restrict__ sess,
+                                               const int32_t *__restrict__ slot_maps, int dead,
+                                               const float *__restrict__ umass, int64_t ustride, int units,
+                                               float *__restrict__ scores) {
+  __shared__ float part[4][PL_POS];
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;                          // the gate: the first pass wrote -inf
+  const int j0 = blockIdx.x * PL_POS;
+  if (j0 >= s.N) return;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int j = j0 + lane;
+  const int jj = min(j, s.N - 1);
+  int nb[7];
+#pragma unroll
+  for (int d = 0; d < 7; ++d) nb[d] = min(max(jj + d - 3, 0), s.N - 1);   // clamped: repeats leave the max alone
+  const float *base = umass + s.slot_off;
+  float acc = 0.f;
+  for (int u = w; u < units; u += 4) {
+    const float *v = base + int64_t(u) * ustride;
+    float m = v[nb[0]];
+#pragma unroll
+    for (int d = 1; d < 7; ++d) m = fmaxf(m, v[nb[d]]);
+    acc += m;
+  }
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && j < s.N) {
+    const int32_t slot = slot_maps[s.slot_off + j];
+    const bool c = slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+    scores[s.slot_off + j] = c ? ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane] : -INFINITY;
+  }
+}
+
 hipError_t launch_residual(const ScoreArgs &a, hipStream_t st);
 
 hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
@@ -1287,6 +1398,35 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
       k_score_mfma<false, false><<<dim3(tiles, a.B), 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
                                                                    a.slot_maps, a.ws, a.scores, resid);
     }
+  if (a.flags & IKV_POOL7) {
+    // the SnapKV-style score: row normalisers, the per-unit attention masses, the pool
+    {
+      KTimer kt_("k_lse_mfma", st);
+      k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(
+          a.sess_dev, a.ws, p.L, p.Hkv, false, chunk, a.slot_maps, a.qpos, p.dead_slot, true, false, 0, kp,
+          p.num_slots, a.residual, a.ws_shared);
+    }
+    float *umass = a.ws_shared;                     // after the sessions' blocks
+    {
+      KTimer kt_("k_score_mass", st);
+      const dim3 grid(unsigned(units / 2 * cdiv(a.maxN, chunk)), a.B);
+      const bool small = a.minR <= 64, large = a.maxR > 64;
+      if (small)
+        k_score_stats<2, true><<<grid, 256, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                     a.slot_maps, a.ws, a.M, a.scores, false, chunk, large ? 1 : 0,
+                                                     umass, a.total_positions);
+      if (large)
+        k_score_stats<4, true><<<grid, 512, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev,
+                                                     a.slot_maps, a.ws, a.M, a.scores, false, chunk, small ? 2 : 0,
+                                                     umass, a.total_positions);
+    }
+    {
+      KTimer kt_("k_pool7", st);
+      k_pool7<<<dim3(unsigned(cdiv(a.maxN, PL_POS)), a.B), 256, 0, st>>>(a.sess_dev, a.slot_maps, p.dead_slot,
+                                                                         umass, a.total_positions, units, a.scores);
+    }
+    return hipGetLastError();
+  }
   {
     // with the matrix-core residual head, this launch also folds its first layer (one
     // item of fold_items() per thread) and builds K', V'

@@ -189,8 +189,11 @@ def paged_slots(Ns, seed: int, page: int = 16, spare_pages: int = 0):
 
 
 def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
-               layout: str = "paged", page: int = 16, spare_pages: int = 0) -> Batch:
+               layout: str = "paged", page: int = 16, spare_pages: int = 0, span_rows: bool = True) -> Batch:
     """Draw a batch of sessions sharing one paged pool.
+
+    ``span_rows``: draw the query-span rows of the memory update ([L][Hkv*R][qe-qs][D]
+    per session); False leaves them empty (a step without a memory update).
 
     ``layout``: ``"identity"`` (single session, S[j] = j + 1), ``"shuffled"``
     (single session, S a seeded permutation of 1..N) or ``"paged"`` (pages of
@@ -269,9 +272,9 @@ def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
         m = stream(seed, T_M, b).standard_normal((L, Hkv * s.R, D), dtype=np.float32)
         Ms.append(m.ravel())
         om += m.size
-        n = s.qe - s.qs
+        n = s.qe - s.qs if span_rows else 0
         q = stream(seed, T_QSPAN, b).standard_normal((n, L, Hkv * s.R, D), dtype=np.float32)
-        cs = rope_cos_sin(np.arange(s.qs, s.qe), D)
+        cs = rope_cos_sin(np.arange(s.qs, s.qs + n), D)
         q = rope_neox(q.astype(np.float64), *cs).transpose(1, 2, 0, 3)
         spans.append(to_dtype(np.ascontiguousarray(q), kv_dtype).ravel())
         osp += spans[-1].size
@@ -392,6 +395,19 @@ def qwen25_14b_92k_heavy(R: int = 64, seed: int = 3) -> Batch:
     return make_batch(qwen25_14b_shape(), [s], seed=seed, kv_dtype=BF16, layout="paged")
 
 
+# ----------------------------------------------------------------------------- query rows of the baseline scorers
+
+def window_queries(shape: Shape, N: int, W: int, seed: int, session: int = 0) -> np.ndarray:
+    """Post-RoPE query rows of the last W positions N-W .. N-1 of every query head, as a
+    model in bf16 would emit them: N(0,1), rotated at their positions, rounded to bf16,
+    returned widened to float32 [L][Hq][W][D]. Viewed as [L][Hkv*G*W][D] this is the
+    memory-row argument of the scorer with R = G * W (query head h pairs with KV head
+    h // G, its rows contiguous)."""
+    q = stream(seed, T_QWIN, session).standard_normal((W, shape.L, shape.Hq, shape.D), dtype=np.float32)
+    q = rope_neox(q.astype(np.float64), *rope_cos_sin(np.arange(N - W, N), shape.D)).transpose(1, 2, 0, 3)
+    return bf16_to_f32(f64_to_bf16(np.ascontiguousarray(q)))
+
+
 # ----------------------------------------------------------------------------- isolated-call inputs
 
 def score_vector(n: int, seed: int, ties: bool = True) -> np.ndarray:
@@ -440,6 +456,7 @@ def slot_map(n: int, num_slots: int, seed: int, dead_frac: float = 0.1, dead: in
 T_MISC_SCORES, T_MISC_KEEP, T_MISC_ALIAS, T_MISC_SLOTS = 20, 21, 22, 23
 T_TURNS = 24
 T_TABLE_K, T_TABLE_V = 25, 26
+T_QWIN = 27
 
 
 # ----------------------------------------------------------------------------- multi-turn session
