@@ -438,3 +438,36 @@ def recent_window(N, C, recent_ratio):
     heavy hitters."""
     w = min(N, int(math.ceil(recent_ratio * C)))
     return N - w, N
+
+
+# ----------------------------------------------------------------------------- compact apply path
+# Sec. 3.4 (standard compactors left-pack the kept rows and re-index RoPE) and the
+# Appendix layout ablation (Table 7: compact vs dead-slot apply path).
+
+def rope_rotate(x, delta, base, D):
+    """Neox (rotate-half) RoPE rotation of rows x[..., D] by `delta` positions: channel
+    pair (i, i + D/2) turns by delta * base^(-2i/D). Rotating a key made at position j by
+    t - j gives the key the same projection would have made at position t."""
+    x = np.asarray(x, dtype=np.float64)
+    h = D // 2
+    ang = float(delta) * base ** (-2.0 * np.arange(h) / D)
+    c, s = np.cos(ang), np.sin(ang)
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def compact_apply(k_pool, v_pool, S, keep, dst, base):
+    """Left-pack the kept positions of one session. The t-th kept position j (in position
+    order) moves to position t and slot dst[t]: on every layer and KV head its key is
+    re-rotated by t - j and its value copied. Returns float64 (K', V') [L][n_keep][Hkv][D],
+    the rows written at dst[0 .. n_keep), and the new slot map dst[0 .. n_keep)."""
+    S = np.asarray(S)
+    kept = np.nonzero(np.asarray(keep, dtype=bool))[0]
+    D = k_pool.shape[-1]
+    L, Hkv = k_pool.shape[0], k_pool.shape[2]
+    Kn = np.zeros((L, len(kept), Hkv, D))
+    Vn = np.zeros((L, len(kept), Hkv, D))
+    for t, j in enumerate(kept):
+        Kn[:, t] = rope_rotate(widen(k_pool[:, S[j]]), t - int(j), base, D)
+        Vn[:, t] = widen(v_pool[:, S[j]])
+    return Kn, Vn, np.asarray(dst[:len(kept)], dtype=np.int32)

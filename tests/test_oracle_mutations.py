@@ -76,6 +76,13 @@ PLANTS = [
      "out = max_pool(v.sum(axis=(0, 1)), kernel)"),
     ("pool window one too wide", "    r = kernel // 2\n", "    r = kernel // 2 + 1\n"),
     ("recent window rounded down", "w = min(N, int(math.ceil(recent_ratio * C)))", "w = min(N, int(recent_ratio * C))"),
+    # ---- compact apply path (Sec. 3.4, Table 7)
+    ("re-rotation sign", "Kn[:, t] = rope_rotate(widen(k_pool[:, S[j]]), t - int(j), base, D)",
+     "Kn[:, t] = rope_rotate(widen(k_pool[:, S[j]]), int(j) - t, base, D)"),
+    ("rotation frequencies over D/2", "ang = float(delta) * base ** (-2.0 * np.arange(h) / D)",
+     "ang = float(delta) * base ** (-2.0 * np.arange(h) / h)"),
+    ("rotate-half pairing", "return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)\n\n\ndef compact",
+     "return np.concatenate([x1 * c + x2 * s, x2 * c - x1 * s], axis=-1)\n\n\ndef compact"),
 ]
 
 

@@ -748,3 +748,51 @@ def test_recent_window_hand():
     assert oracle.ikv_oracle.recent_window(32768, 8192, 0.5) == (32768 - 4096, 32768)
     assert oracle.ikv_oracle.recent_window(100, 8192, 0.5) == (0, 100)
     assert oracle.ikv_oracle.recent_window(1000, 301, 0.5) == (849, 1000)
+
+
+# ============================================================================ compact apply path (Sec. 3.4, Table 7)
+
+def test_rope_rotate_hand():
+    """D = 4, base 1e4: the pairs (0, 2) and (1, 3) turn by delta and delta / 100."""
+    x = np.array([1.0, 0.0, 0.0, 2.0])
+    y = oracle.ikv_oracle.rope_rotate(x, -2, 1.0e4, 4)
+    np.testing.assert_allclose(y, [math.cos(2.0), -2 * math.sin(-0.02), -math.sin(2.0), 2 * math.cos(0.02)],
+                               rtol=0, atol=1e-15)
+    np.testing.assert_array_equal(oracle.ikv_oracle.rope_rotate(x, 0, 1.0e4, 4), x)
+
+
+def test_rope_rotate_composes_with_the_generator_rope():
+    """A key rotated at position j (the input generator's own RoPE) and re-rotated by
+    t - j equals the key rotated at t."""
+    rng = np.random.default_rng(30)
+    D = 128
+    x = rng.standard_normal((5, D))
+    j, t = np.array([700, 91000, 33, 5000, 12]), np.array([3, 8191, 33, 77, 0])
+    a = synth.rope_neox(x, *synth.rope_cos_sin(j, D))
+    b = synth.rope_neox(x, *synth.rope_cos_sin(t, D))
+    for k in range(5):
+        np.testing.assert_allclose(oracle.ikv_oracle.rope_rotate(a[k], t[k] - j[k], synth.ROPE_BASE, D), b[k],
+                                   rtol=0, atol=1e-9)
+
+
+def test_compact_apply_order_values_and_norms():
+    rng = np.random.default_rng(31)
+    L, N, Hkv, D = 2, 30, 2, 8
+    kp, S = rand_pool(rng, L, N, Hkv, D)
+    vp, _ = rand_pool(rng, L, N, Hkv, D)
+    vp = vp[:, :]                                            # values by the same slots
+    keep = rng.random(N) < 0.4
+    keep[3] = True
+    dst = np.arange(100, 100 + N, dtype=np.int32)
+    Kn, Vn, Sn = oracle.ikv_oracle.compact_apply(kp, vp, S, keep, dst, 1.0e4)
+    kept = np.nonzero(keep)[0]
+    assert len(Sn) == len(kept) and np.array_equal(Sn, dst[:len(kept)])
+    np.testing.assert_array_equal(Vn, vp[:, S[kept]].astype(np.float64))          # values move unchanged
+    np.testing.assert_allclose(np.linalg.norm(Kn, axis=-1),                       # rotations keep norms
+                               np.linalg.norm(kp[:, S[kept]].astype(np.float64), axis=-1), rtol=1e-13)
+    t0 = int(np.nonzero(kept == 3)[0][0])
+    np.testing.assert_allclose(Kn[:, t0], oracle.ikv_oracle.rope_rotate(kp[:, S[3]], t0 - 3, 1.0e4, D), rtol=0,
+                               atol=1e-15)
+    # everything kept: no position moves, every key stays as it was
+    Kall, _, _ = oracle.ikv_oracle.compact_apply(kp, vp, S, np.ones(N, bool), dst, 1.0e4)
+    np.testing.assert_array_equal(Kall, kp[:, S].astype(np.float64))
