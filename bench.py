@@ -57,6 +57,23 @@ def log(msg: str) -> None:
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
+def baseline_workload(scorer: str):
+    """The Qwen3-8B 32k workload scored by a baseline compressor of Sec. 4.1 on the same
+    substrate: the W = 32 window query rows as M (R = G * W). SnapKV-style: the window is
+    the forced span, IKV_POOL7. H2O-style: the same rows as the observed queries, ratio
+    mode with half of the budget as the forced recent window."""
+    import numpy as np
+    import oracle
+    import synth
+    shape = synth.qwen3_8b_shape()
+    N, C, W = 32768, 8192, 32
+    qs = N - W if scorer == "snapkv" else oracle.ikv_oracle.recent_window(N, C, 0.5)[0]
+    spec = synth.SessionSpec(N=N, C=C, pi=0, qs=qs, qe=N, R=shape.G * W, qpos=np.zeros(0, np.int32))
+    batch = synth.make_batch(shape, [spec], seed=2, kv_dtype=synth.BF16, layout="paged", span_rows=False)
+    batch.M = synth.window_queries(shape, N, W, seed=2).reshape(-1).copy()
+    return batch, f"qwen3_8b_shape_hist32768_budget8192_{scorer}_style_W32"
+
+
 def workload(name: str, R: int):
     import synth
     if name == "qwen3_8b_32k":
@@ -74,7 +91,7 @@ def scored(s) -> bool:
     return s.N > s.C                                 # at or under the budget the event is skipped
 
 
-def cpu_baseline(batch, blob, flags, layers: int):
+def cpu_baseline(batch, blob, flags, layers: int, scorer: str = "intentkv"):
     """The float64 oracle on a bounded sample: the per-layer work (rule score and key
     mean) on `layers` of the L layers for every candidate, scaled by L / layers, plus
     the residual MLP and the selection over every candidate, done once. On one session
@@ -102,6 +119,20 @@ def cpu_baseline(batch, blob, flags, layers: int):
     else:
         kp, vp = batch.k_pool[:Ls], batch.v_pool[:Ls]
     M = batch.M_of(b)[:Ls]
+    if scorer != "intentkv":                         # a baseline scorer: the oracle's own, on the sample
+        q = M.reshape(Ls, sh.Hq, s.R // sh.G, sh.D)
+        fn = oracle.ikv_oracle.snapkv_scores if scorer == "snapkv" else oracle.ikv_oracle.h2o_scores
+        t0 = time.perf_counter()
+        sc = fn(kp, S, sets, q, sh.Hkv)
+        t_layers = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.select_budget(sc, sets)
+        t_once = time.perf_counter() - t0
+        return {"value": len(idx) / (t_layers * sh.L / Ls + t_once), "unit": "history tokens/s",
+                "cores": int(threads), "kind": "oracle",
+                "sample": f"float64 oracle {scorer}-style score on {Ls} of {sh.L} layers for all {len(idx)} "
+                          f"candidates (scaled x{sh.L / Ls:g}), selection once; {t_layers + t_once:.1f} s measured",
+                "host_cpus": os.cpu_count()}
     t0 = time.perf_counter()
     rule = oracle.rule_scores(kp, S, sets["cand"], M, sh.Hkv, s.R)
     kb = oracle.kbar(kp, S, idx)
@@ -126,6 +157,128 @@ def cpu_baseline(batch, blob, flags, layers: int):
             "decode_ms_estimate": 1e3 * t_dec, "host_cpus": os.cpu_count()}
 
 
+def multiturn_bench(args, dev) -> dict:
+    """The multi-turn agent session (Qwen3-8B shape, 8 turns from 4096 to 49,152
+    positions, R = G = 4 memory rows per KV head from a zero memory, the 64-position
+    system prefix forced and radix-protected, budget 8192, residual head on). Every
+    turn's key, value, span and decode-query rows are staged in HBM before timing.
+    Per turn, untimed: the new rows are written at their slots (freed slots first,
+    oldest first, then unused ones) and the descriptors uploaded; timed with events:
+    memory update, scoring, selection, redirect, decode; untimed: the freed list comes
+    back for the next turn's slots. The session runs `warmup` times, then `steps` times
+    timed; each turn reports its median."""
+    from collections import deque
+
+    import torch
+
+    import synth
+    from paper_2606_09916_amd import ikv
+    shape = synth.qwen3_8b_shape()
+    L, Hq, Hkv, D = shape.L, shape.Hq, shape.Hkv, shape.D
+    R, C, pi, seed = Hq // Hkv, 8192, 64, 4
+    plan = synth.multi_turn_plan(seed)
+    total = sum(a + q for a, q in plan)
+    num_slots = 1 + total
+    log(f"multi-turn: staging {len(plan)} turns, {total} positions")
+    k_pool = torch.zeros((L, num_slots, Hkv, D), dtype=torch.bfloat16, device=dev)
+    v_pool = torch.zeros_like(k_pool)
+    pool = ikv.make_pool(k_pool, v_pool, L, Hq, Hkv, D, num_slots, 0)
+    ikv.init_dead_slot(pool)
+
+    def bf(a):
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    turns, N0 = [], 0
+    for t, (n_tool, n_q) in enumerate(plan):
+        N = N0 + n_tool + n_q
+        k_rows, v_rows = synth.turn_kv_rows(seed, t, N0, N - N0, shape)
+        qpos = np.arange(N - n_q, N, dtype=np.int32)
+        turns.append(dict(N0=N0, N=N, n_q=n_q, k=bf(k_rows), v=bf(v_rows),
+                          span=bf(synth.turn_span_rows(seed, t, qpos, shape, R)),
+                          q=bf(synth.turn_decode_query(seed, t, N, shape)[None]),
+                          qpos=torch.from_numpy(qpos).to(dev)))
+        N0 = N
+    blob = torch.from_numpy(synth.residual_blob(D, seed=24, variant="scaled", units=L * Hkv, out_std=5e-3)).to(dev)
+    ws = ikv.Workspace(dev)
+    M = torch.zeros(L * Hkv * R * D, dtype=torch.float32, device=dev)
+    scores = torch.empty(total, dtype=torch.float32, device=dev)
+    keep = torch.empty(total, dtype=torch.uint8, device=dev)
+    freed = torch.empty(total, dtype=torch.int32, device=dev)
+    live = torch.empty(total, dtype=torch.int32, device=dev)
+    n_keep, n_freed, n_live = (torch.empty(1, dtype=torch.int32, device=dev) for _ in range(3))
+    tau = torch.empty(1, dtype=torch.float32, device=dev)
+    out = torch.empty((1, L, Hq, D), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+
+    def session(record):
+        M.zero_()
+        S = torch.zeros(0, dtype=torch.int32, device=dev)
+        free, fresh = deque(), 1
+        per = []
+        for tr in turns:
+            N0, N = tr["N0"], tr["N"]
+            new = []
+            for _ in range(N - N0):
+                if free:
+                    new.append(free.popleft())
+                else:
+                    new.append(fresh)
+                    fresh += 1
+            idx = torch.tensor(new, dtype=torch.int64, device=dev)
+            k_pool[:, idx] = tr["k"]
+            v_pool[:, idx] = tr["v"]
+            S = torch.cat([S, idx.to(torch.int32)])
+            sess = ikv.Sessions([dict(slot_off=0, mem_off=0, qspan_off=0, qpos_off=0, N=N, pi=pi, qs=N - tr["n_q"],
+                                      qe=N, C=C, radix_prefix=pi, R=R, nq=tr["n_q"])], dev)
+            cand = int((S[pi:N - tr["n_q"]] != 0).sum().item()) if N > C else 0
+            torch.cuda.synchronize()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+            ev[0].record()
+            ikv.qm_update(pool, sess, M, tr["span"], 0.5)
+            ev[1].record()
+            if N > C:
+                ikv.score_history(pool, sess, S, M, scores, ws, qpos=tr["qpos"], residual=blob,
+                                  flags=ikv.IKV_RESIDUAL)
+                ev[2].record()
+                ikv.select_budget(sess, S, 0, scores, keep, n_keep, tau, ws)
+                ev[3].record()
+                ikv.redirect_slots(sess, num_slots, S, 0, keep, freed, n_freed, live, n_live, ws)
+                ev[4].record()
+                lv, nl = live, n_live
+            else:
+                ev[2].record()
+                ev[3].record()
+                ev[4].record()
+                lv = S[S != 0].contiguous()
+                nl = torch.tensor([lv.numel()], dtype=torch.int32, device=dev)
+            ikv.decode_attend_slotmap(pool, sess, tr["q"], lv, nl, out, ws)
+            ev[5].record()
+            torch.cuda.synchronize()
+            if N > C:
+                nf = int(n_freed.item())
+                free.extend(freed[:nf].cpu().tolist())
+            if record:
+                per.append([ev[i].elapsed_time(ev[i + 1]) for i in range(5)] + [cand])
+        return per
+
+    for _ in range(args.warmup):
+        session(False)
+    runs = [session(True) for _ in range(args.steps)]
+    arr = np.median(np.array(runs), axis=0)             # [turn][qm, score, select, redirect, decode, cand]
+    cand = arr[:, 5]
+    t_ss = (arr[:, 1] + arr[:, 2]) / 1e3
+    scored = cand > 0
+    tps = float(cand[scored].sum() / t_ss[scored].sum())
+    per_turn = [{"turn": i, "N": tr["N"], "candidates": int(cand[i]), "qm_update_ms": round(float(arr[i, 0]), 4),
+                 "score_ms": round(float(arr[i, 1]), 4), "select_ms": round(float(arr[i, 2]), 4),
+                 "redirect_ms": round(float(arr[i, 3]), 4), "decode_ms": round(float(arr[i, 4]), 4),
+                 "step_ms": round(float(arr[i, :5].sum()), 4),
+                 "score_gbs_keys_once": round(float(cand[i] * L * Hkv * D * 2 / (arr[i, 1] / 1e3) / 1e9), 1)
+                 if cand[i] else None} for i, tr in enumerate(turns)]
+    return {"value": round(tps, 1), "per_turn": per_turn,
+            "ms_per_step": round(float(arr[:, :5].sum()), 4), "workload": "qwen3_8b_shape_multi_turn_8_turns_4096_to_49152_budget8192_R4"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -139,6 +292,8 @@ def main() -> int:
     ap.add_argument("--no-residual", action="store_true", help="the rule score alone (the '- residual' ablation)")
     ap.add_argument("--no-xattn", action="store_true", help="residual head without its cross-attention")
     ap.add_argument("--query-mode", action="store_true", help="memory update with lambda = inf (no history)")
+    ap.add_argument("--scorer", default="intentkv", choices=("intentkv", "snapkv", "h2o"),
+                    help="the scorer feeding selection, redirect and decode (Qwen3-8B 32k workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=None,
                     help="layers of the CPU baseline sample (default 36; 8 for a pool drawn on the GPU)")
@@ -158,11 +313,26 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
-    log(f"generating workload {args.workload} R={args.R}")
-    batch, wname = workload(args.workload, args.R)
+    if args.workload == "multiturn":
+        r = multiturn_bench(args, dev)
+        print(json.dumps({
+            "metric": "history tokens scored+selected/s and slot-map decode attn HBM GB/s, 32k hist/8k budget",
+            "value": r["value"], "unit": "history tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": r["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16 MFMA (memory rows split hi+lo), f32 accumulate", "data": "synthetic",
+            "config": {"workload": r["workload"], "turns": len(r["per_turn"])}, "per_turn": r["per_turn"]}),
+            flush=True)
+        return 0
+    log(f"generating workload {args.workload} R={args.R} scorer={args.scorer}")
+    if args.scorer != "intentkv":
+        batch, wname = baseline_workload(args.scorer)
+    else:
+        batch, wname = workload(args.workload, args.R)
     sh = batch.shape
     s = batch.sessions[0]
     flags = 0 if args.no_residual else ikv.IKV_RESIDUAL | (ikv.IKV_NO_XATTN if args.no_xattn else 0)
+    if args.scorer != "intentkv":
+        flags = ikv.IKV_POOL7 if args.scorer == "snapkv" else 0
     blob = synth.residual_blob(sh.D, seed=22)
     mem_update = len(batch.q_span) > 0              # a workload without span rows has no memory update
     log("uploading")
@@ -236,6 +406,27 @@ def main() -> int:
     for name, ms in recs:
         per_kernel.setdefault(name, []).append(ms)
 
+    # Layout ablation (Table 7): the compact apply path of the standard compactors on the
+    # same kept set, left-packing the kept rows (keys re-rotated) into the slots the
+    # redirect freed, against the redirect itself. One session only.
+    layout = None
+    if len(batch.sessions) == 1 and int(st.host("n_freed")[0]) >= int(st.host("n_keep")[0]) > 0:
+        nk_t = torch.zeros(1, dtype=torch.int32, device=dev)
+        dst = st.freed.clone()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+        torch.cuda.synchronize()
+        for k in range(10):
+            evs[k].record()
+            ikv.compact_apply(st.pool, st.sess, st.S0, st.keep, dst, nk_t, st.ws, rope_base=synth.ROPE_BASE)
+        evs[10].record()
+        torch.cuda.synchronize()
+        c_ms = float(np.median([evs[k].elapsed_time(evs[k + 1]) for k in range(10)]))
+        nk = int(nk_t.item())
+        c_bytes = nk * 2 * (2 * sh.L * sh.Hkv * sh.D * 2) + nk * 12
+        r_bytes = s.N * (4 + 1 + 4 + 4)
+        layout = {"compact_apply_ms": round(c_ms, 4), "compact_bytes": c_bytes,
+                  "compact_gbs": round(c_bytes / (c_ms / 1e3) / 1e9, 1), "redirect_ms": round(float(phase_ms[4]), 4),
+                  "redirect_bytes": r_bytes, "kept_rows_moved": nk}
     n_live_all = st.host("n_live").astype(np.int64)
     n_keep_all = st.host("n_keep").astype(np.int64)
     n_live, n_keep = int(n_live_all.sum()), int(n_keep_all.sum())
@@ -285,6 +476,9 @@ def main() -> int:
         "k_select_small": sum(Ns) * (4 + 4 + 1),
         "k_residual_mfma": nA * (sh.D * 4 + 4 + 4),
         "k_redirect<bytes>": sum(Ns) * (4 + 1 + 4 + 4),
+        # the SnapKV-style passes: the per-unit attention masses (float32 per unit and position)
+        "k_score_mass": key_bytes + mem_bytes + n_scored * units * 4,
+        "k_pool7": n_scored * units * 4 + n_scored * (4 + 4),
     }
     kernels = {}
     for name, v in per_kernel.items():
@@ -316,7 +510,9 @@ def main() -> int:
                    "sessions": len(batch.sessions), "N": s.N if len(Ns) == 1 else [min(Ns), max(Ns)],
                    "positions": sum(Ns), "C": s.C, "R": s.R if len(set(Rs)) == 1 else [min(Rs), max(Rs)],
                    "kv_storage": "bf16" if batch.kv_dtype == synth.BF16 else "f32",
-                   "residual": bool(flags), "cross_attention": bool(flags) and not args.no_xattn,
+                   "scorer": args.scorer,
+                   "residual": bool(flags & ikv.IKV_RESIDUAL),
+                   "cross_attention": bool(flags & ikv.IKV_RESIDUAL) and not args.no_xattn,
                    "memory_update": "query mode" if (mem_update and args.query_mode) else mem_update,
                    "candidates": nA, "n_keep": n_keep,
                    "n_live": n_live},
@@ -325,11 +521,12 @@ def main() -> int:
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
         "kernels": kernels,
+        "layout_ablation": layout,
     }
     if not args.no_cpu_baseline:
         layers = args.cpu_layers if args.cpu_layers is not None else (36 if batch.k_pool is not None else 8)
         log(f"cpu baseline (oracle, {layers} layers)")
-        out["cpu_baseline"] = cpu_baseline(batch, blob, flags, layers)
+        out["cpu_baseline"] = cpu_baseline(batch, blob, flags, layers, args.scorer)
     print(json.dumps(out), flush=True)
     return 0
 

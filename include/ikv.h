@@ -72,6 +72,7 @@ typedef int32_t ikv_status;
 #define IKV_CALL_SELECT   2
 #define IKV_CALL_REDIRECT 3
 #define IKV_CALL_DECODE   4
+#define IKV_CALL_COMPACT  5
 
 /*
  * The paged KV pool (Sec. 3.1: post-RoPE K, V in R^{L x Hkv x N x D}, stored by
@@ -347,6 +348,28 @@ ikv_status ikv_memstore_size(ikv_memstore *store, int32_t *n);
 ikv_status ikv_resolve_span(int32_t N, const int32_t *msg_start, const int32_t *msg_end,
                             const uint8_t *actionable, int32_t n_msgs, int32_t tail_w,
                             int32_t *qs, int32_t *qe);
+
+/*
+ * The compact apply path that the standard compactors use (Sec. 3.4; the Appendix
+ * layout ablation, Table 7, compares it with ikv_redirect_slots): the kept positions
+ * of each session are left-packed. The t-th kept live position j (position order)
+ * moves to position t and slot dst_slots[slot_off + t]: on every layer and KV head
+ *   K[l][dst][h] = RoPE_{t - j}(K[l][S[j]][h])   (Neox rotate-half: channel pair
+ *                  (i, i + D/2) turns by (t - j) * rope_base^(-2i/D); angles in float64,
+ *                  rotation in float32, one rounding to the pool's type),
+ *   V[l][dst][h] = V[l][S[j]][h].
+ * The session's new slot map is dst_slots[slot_off .. slot_off + n_keep[b]) and its new
+ * length n_keep[b]; every old slot can go back to the allocator, and the radix prefix
+ * cache no longer matches (the compact layout forces it off). No source slot may be a
+ * destination slot (results undefined otherwise).
+ *   keep: device uint8 per session [N] (ikv_select_budget's mask); dead positions are
+ *   never kept. dst_slots: device int32 per session [N] (first n_keep used).
+ *   n_keep: device int32 [B]. workspace: ikv_workspace_bytes(IKV_CALL_COMPACT).
+ */
+ikv_status ikv_compact_apply(const ikv_pool *pool, const ikv_session *sess,
+                             const ikv_session *sess_dev, int32_t B, const int32_t *slot_maps,
+                             const uint8_t *keep, const int32_t *dst_slots, double rope_base,
+                             int32_t *n_keep, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Workspace size of one call (IKV_CALL_*) for these sessions, in bytes (0 when

@@ -291,6 +291,10 @@ ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, in
       if ((r = check_sessions(sess, sess, B))) return r;
       *bytes = decode_bytes(pool, sess, B);
       return ok();
+    case IKV_CALL_COMPACT:
+      if ((r = check_sessions(sess, sess, B))) return r;
+      *bytes = size_t(total_positions(sess, B)) * sizeof(int32_t);
+      return ok();
     default:
       return fail(IKV_EINVAL, "unknown call id %d", call);
   }
@@ -434,6 +438,23 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
   return hip_status(ikv::launch_redirect(sess_dev, B, num_slots, slot_maps, dead_slot, keep, freed, n_freed, live,
                                          n_live, static_cast<uint32_t *>(workspace), (hipStream_t)stream),
                     "ikv_redirect_slots");
+}
+
+ikv_status ikv_compact_apply(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                             const int32_t *slot_maps, const uint8_t *keep, const int32_t *dst_slots, double rope_base,
+                             int32_t *n_keep, void *workspace, size_t workspace_bytes, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  if ((r = check_sessions(sess, sess_dev, B))) return r;
+  if (B == 0) return ok();
+  if (!slot_maps || !keep || !dst_slots || !n_keep) return fail(IKV_EINVAL, "slot_maps / keep / dst_slots / n_keep is NULL");
+  if (!(rope_base > 1.0)) return fail(IKV_EINVAL, "rope_base must be > 1");
+  const size_t need = size_t(total_positions(sess, B)) * sizeof(int32_t);
+  if ((r = check_ws(workspace, workspace_bytes, need))) return r;
+  return hip_status(ikv::launch_compact(*pool, sess_dev, B, max_n(sess, B), slot_maps, keep, dst_slots, rope_base,
+                                        n_keep, static_cast<int32_t *>(workspace), (hipStream_t)stream),
+                    "ikv_compact_apply");
 }
 
 ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev,

@@ -254,6 +254,10 @@ hipError_t launch_decode(const ikv_pool &pool, const ikv_session *sess_dev, int 
                          const void *q, const int32_t *live, const int32_t *n_live, void *out,
                          float *ws, hipStream_t st);
 
+hipError_t launch_compact(const ikv_pool &pool, const ikv_session *sess_dev, int B, int maxN,
+                          const int32_t *slot_maps, const uint8_t *keep, const int32_t *dst, double base,
+                          int32_t *n_keep, int32_t *pos_list, hipStream_t st);
+
 int decode_splits(int maxN);
 
 // A word of pinned host memory that kernels set (system scope) to report a fault the

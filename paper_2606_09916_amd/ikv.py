@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(PKG, "libikv.so")
 
 IKV_BF16, IKV_F32 = 0, 1
 IKV_RESIDUAL, IKV_NO_XATTN, IKV_POOL7 = 1, 2, 4
-CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE = 1, 2, 3, 4
+CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE, CALL_COMPACT = 1, 2, 3, 4, 5
 STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE", -4: "IKV_EUNSUPPORTED",
           -5: "IKV_EHIP"}
 
@@ -23,7 +23,8 @@ STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE",
 SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_select_budget", "ikv_select_budget_static",
            "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error",
            "ikv_timing", "ikv_timing_read", "ikv_memstore_create", "ikv_memstore_destroy", "ikv_memstore_acquire",
-           "ikv_memstore_release", "ikv_memstore_trigger", "ikv_memstore_size", "ikv_resolve_span")
+           "ikv_memstore_release", "ikv_memstore_trigger", "ikv_memstore_size", "ikv_resolve_span",
+           "ikv_compact_apply")
 IKV_KEY_EXPLICIT, IKV_KEY_SPAN, IKV_KEY_PREFIX, IKV_KEY_LOCAL = 1, 2, 3, 4
 
 
@@ -75,6 +76,8 @@ def lib() -> ctypes.CDLL:
             "ikv_decode_attend_slotmap": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p],
             "ikv_workspace_bytes": [P, S, c_int32, c_int32, c_uint32, ctypes.POINTER(c_size_t)],
+            "ikv_compact_apply": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, ctypes.c_double, c_void_p,
+                                  c_void_p, c_size_t, c_void_p],
             "ikv_timing": [c_int32],
             "ikv_memstore_create": [c_int32, ctypes.POINTER(c_void_p)],
             "ikv_memstore_acquire": [c_void_p, ctypes.POINTER(KeySource), ctypes.POINTER(c_int32),
@@ -222,6 +225,15 @@ def decode_attend_slotmap(pool: Pool, sess: Sessions, q, live, n_live, out, ws: 
     _check(lib().ikv_decode_attend_slotmap(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(q),
                                            _ptr(live), _ptr(n_live), _ptr(out), wp, wn, _stream(stream)),
            "ikv_decode_attend_slotmap")
+
+
+def compact_apply(pool: Pool, sess: Sessions, slot_maps, keep, dst_slots, n_keep, ws: Workspace,
+                  rope_base: float = 1.0e6, stream=None) -> None:
+    """Left-pack the kept rows into dst_slots with RoPE re-rotation (the compact layout)."""
+    wp, wn = ws.get(workspace_bytes(pool, sess, CALL_COMPACT))
+    _check(lib().ikv_compact_apply(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps),
+                                   _ptr(keep), _ptr(dst_slots), float(rope_base), _ptr(n_keep), wp, wn,
+                                   _stream(stream)), "ikv_compact_apply")
 
 
 # ----------------------------------------------------------------------------- timing
