@@ -471,3 +471,36 @@ def compact_apply(k_pool, v_pool, S, keep, dst, base):
         Kn[:, t] = rope_rotate(widen(k_pool[:, S[j]]), t - int(j), base, D)
         Vn[:, t] = widen(v_pool[:, S[j]])
     return Kn, Vn, np.asarray(dst[:len(kept)], dtype=np.int32)
+
+
+# ----------------------------------------------------------------------------- prefill of the query span
+# Sec. 3.5 (post-RoPE Q and K captured from the model's attention: the RoPE hook) with
+# Sec. 3.2 (Enc(q_t) is the mean of the span's post-RoPE Q rows) and Eq. 6 (the
+# cross-attention keys are the mean key rows at the query positions): the span's
+# prefill attention produces everything the retention step needs from the span.
+
+def prefill_attention(q, k_pool, v_pool, hist_slots, span_slots):
+    """Causal attention of the span's query rows. ``q`` [L][Hq][n][D] post-RoPE query
+    rows of span tokens 0 .. n-1. Query row t of head h (KV head h // G) attends over
+    the history slots (every one) and the span's own slots span_slots[u] for u <= t:
+    o = softmax(q . K / sqrt(D)) V. float64 [L][Hq][n][D]."""
+    q = widen(q)
+    L, Hq, n, D = q.shape
+    Hkv = k_pool.shape[2]
+    G = Hq // Hkv
+    hist = np.asarray(hist_slots, dtype=np.int64)
+    span = np.asarray(span_slots, dtype=np.int64)
+    out = np.zeros((L, Hq, n, D))
+    for l in range(L):
+        for t in range(n):
+            slots = np.concatenate([hist, span[:t + 1]])
+            Kl = widen(k_pool[l][slots])
+            Vl = widen(v_pool[l][slots])
+            for h in range(Hq):
+                g = h // G
+                x = Kl[:, g, :] @ q[l, h, t] / math.sqrt(D)
+                x = x - x.max()
+                p = np.exp(x)
+                p = p / p.sum()
+                out[l, h, t] = p @ Vl[:, g, :]
+    return out

@@ -81,6 +81,9 @@ PLANTS = [
      "Kn[:, t] = rope_rotate(widen(k_pool[:, S[j]]), int(j) - t, base, D)"),
     ("rotation frequencies over D/2", "ang = float(delta) * base ** (-2.0 * np.arange(h) / D)",
      "ang = float(delta) * base ** (-2.0 * np.arange(h) / h)"),
+    ("prefill not causal", "slots = np.concatenate([hist, span[:t + 1]])", "slots = np.concatenate([hist, span])"),
+    ("prefill excludes its own key", "slots = np.concatenate([hist, span[:t + 1]])",
+     "slots = np.concatenate([hist, span[:t]])"),
     ("rotate-half pairing", "return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)\n\n\ndef compact",
      "return np.concatenate([x1 * c + x2 * s, x2 * c - x1 * s], axis=-1)\n\n\ndef compact"),
 ]

@@ -796,3 +796,41 @@ def test_compact_apply_order_values_and_norms():
     # everything kept: no position moves, every key stays as it was
     Kall, _, _ = oracle.ikv_oracle.compact_apply(kp, vp, S, np.ones(N, bool), dst, 1.0e4)
     np.testing.assert_array_equal(Kall, kp[:, S].astype(np.float64))
+
+
+# ============================================================================ span prefill (Sec. 3.5)
+
+def test_prefill_attention_causal_brute_force():
+    rng = np.random.default_rng(40)
+    L, Hq, Hkv, D, n = 2, 4, 2, 4, 3
+    kp = rng.standard_normal((L, 12, Hkv, D)).astype(np.float32)
+    vp = rng.standard_normal((L, 12, Hkv, D)).astype(np.float32)
+    q = rng.standard_normal((L, Hq, n, D)).astype(np.float32)
+    hist, span = [5, 1, 9], [2, 7, 11]
+    o = oracle.ikv_oracle.prefill_attention(q, kp, vp, hist, span)
+    for l in range(L):
+        for h in range(Hq):
+            g = h // 2
+            for t in range(n):
+                slots = hist + span[:t + 1]
+                xs = [sum(float(q[l, h, t, d]) * float(kp[l, u, g, d]) for d in range(D)) / 2.0 for u in slots]
+                ws = [math.exp(x) for x in xs]
+                for d in range(D):
+                    ref = sum(w * float(vp[l, u, g, d]) for w, u in zip(ws, slots)) / sum(ws)
+                    assert math.isclose(o[l, h, t, d], ref, rel_tol=1e-12, abs_tol=1e-14)
+
+
+def test_prefill_attention_reduces_to_decode():
+    """One span token attends over the history and itself: the decode of that query over
+    the history slots followed by its own slot."""
+    rng = np.random.default_rng(41)
+    L, Hq, Hkv, D = 2, 8, 2, 16
+    kp = rng.standard_normal((L, 40, Hkv, D)).astype(np.float32)
+    vp = rng.standard_normal((L, 40, Hkv, D)).astype(np.float32)
+    q = rng.standard_normal((L, Hq, 1, D)).astype(np.float32)
+    hist = [3, 17, 8, 30, 22]
+    o = oracle.ikv_oracle.prefill_attention(q, kp, vp, hist, [39])
+    np.testing.assert_allclose(o[:, :, 0], oracle.decode(q[:, :, 0], kp, vp, hist + [39]), rtol=1e-13, atol=1e-15)
+    # the first span token of a longer span sees only its own span key
+    o2 = oracle.ikv_oracle.prefill_attention(np.repeat(q, 3, axis=2), kp, vp, hist, [39, 4, 5])
+    np.testing.assert_allclose(o2[:, :, 0], o[:, :, 0], rtol=1e-13, atol=1e-15)
