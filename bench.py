@@ -427,6 +427,45 @@ def main() -> int:
         layout = {"compact_apply_ms": round(c_ms, 4), "compact_bytes": c_bytes,
                   "compact_gbs": round(c_bytes / (c_ms / 1e3) / 1e9, 1), "redirect_ms": round(float(phase_ms[4]), 4),
                   "redirect_bytes": r_bytes, "kept_rows_moved": nk}
+    # The span's prefill (RoPE hook, pool write, causal attention over the history, Enc and
+    # the memory update with one row per query head, the span's key means): the last 64
+    # positions as the span over the first N - 64 as history. One session only.
+    prefill = None
+    if len(batch.sessions) == 1 and sh.D == 128 and batch.kv_dtype == synth.BF16 and s.qe - s.qs <= 256 // sh.G:
+        n = s.qe - s.qs
+        hist_h = np.asarray(batch.S(0))[:s.qs]
+        hist_h = hist_h[hist_h != st.dead].astype(np.int32)
+        hist = torch.zeros(s.N, dtype=torch.int32, device=dev)
+        hist[:len(hist_h)] = torch.from_numpy(hist_h).to(dev)
+        n_hist = torch.tensor([len(hist_h)], dtype=torch.int32, device=dev)
+        sp = ikv.Sessions([dict(slot_off=0, mem_off=0, qspan_off=0, qpos_off=0, N=s.N, pi=0, qs=s.qs, qe=s.qe, C=s.C,
+                                radix_prefix=0, R=sh.G, nq=0)], dev)
+        gen = torch.Generator(device=dev).manual_seed(5)
+        q_raw = torch.randn((sh.L, sh.Hq, n, sh.D), device=dev, generator=gen).to(torch.bfloat16)
+        k_raw = torch.randn((sh.L, sh.Hkv, n, sh.D), device=dev, generator=gen).to(torch.bfloat16)
+        v_raw = torch.randn((sh.L, sh.Hkv, n, sh.D), device=dev, generator=gen).to(torch.bfloat16)
+        q_out, p_out = torch.empty_like(q_raw), torch.empty_like(q_raw)
+        kq = torch.empty((n, sh.D), dtype=torch.float32, device=dev)
+        Mp = torch.nn.functional.normalize(torch.randn((sh.L * sh.Hq, sh.D), device=dev, generator=gen), dim=1)
+        Mp = Mp.reshape(-1).contiguous()
+        S_span = st.S0.clone()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+        ikv.prefill_span(st.pool, sp, S_span, q_raw, k_raw, v_raw, hist, n_hist, q_out, p_out, kq, st.ws, M=Mp,
+                         rope_base=synth.ROPE_BASE)
+        torch.cuda.synchronize()
+        for k in range(10):
+            evs[k].record()
+            ikv.prefill_span(st.pool, sp, S_span, q_raw, k_raw, v_raw, hist, n_hist, q_out, p_out, kq, st.ws, M=Mp,
+                             rope_base=synth.ROPE_BASE)
+        evs[10].record()
+        torch.cuda.synchronize()
+        p_ms = float(np.median([evs[k].elapsed_time(evs[k + 1]) for k in range(10)]))
+        nh = len(hist_h)
+        kv_hist = nh * sh.L * sh.Hkv * sh.D * 2 * 2          # history keys and values, read once
+        flops = 2 * 2.0 * sh.L * sh.Hq * n * (nh + (n + 1) / 2) * sh.D
+        prefill = {"span_tokens": n, "history": nh, "ms": round(p_ms, 4), "history_kv_bytes": kv_hist,
+                   "gbs_history_kv": round(kv_hist / (p_ms / 1e3) / 1e9, 1),
+                   "attention_tflops": round(flops / (p_ms / 1e3) / 1e12, 1)}
     n_live_all = st.host("n_live").astype(np.int64)
     n_keep_all = st.host("n_keep").astype(np.int64)
     n_live, n_keep = int(n_live_all.sum()), int(n_keep_all.sum())
@@ -522,6 +561,7 @@ def main() -> int:
         "roofline": roofline,
         "kernels": kernels,
         "layout_ablation": layout,
+        "prefill_span": prefill,
     }
     if not args.no_cpu_baseline:
         layers = args.cpu_layers if args.cpu_layers is not None else (36 if batch.k_pool is not None else 8)

@@ -73,6 +73,7 @@ typedef int32_t ikv_status;
 #define IKV_CALL_REDIRECT 3
 #define IKV_CALL_DECODE   4
 #define IKV_CALL_COMPACT  5
+#define IKV_CALL_PREFILL  6
 
 /*
  * The paged KV pool (Sec. 3.1: post-RoPE K, V in R^{L x Hkv x N x D}, stored by
@@ -370,6 +371,36 @@ ikv_status ikv_compact_apply(const ikv_pool *pool, const ikv_session *sess,
                              const ikv_session *sess_dev, int32_t B, const int32_t *slot_maps,
                              const uint8_t *keep, const int32_t *dst_slots, double rope_base,
                              int32_t *n_keep, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Prefill of each session's actionable query span [qs, qe), n = qe - qs tokens, with the
+ * retention step's inputs produced on the way (Sec. 3.5: the post-RoPE Q and K that the
+ * step uses are the ones the model's attention computes; Sec. 3.2: Enc(q_t); Eq. 2;
+ * Eq. 6's keys). For every layer, token t of the span (position qs + t) and head:
+ *   q' = RoPE_{qs+t}(q_raw), k' = RoPE_{qs+t}(k_raw) (Neox rotate-half, base rope_base;
+ *        float64 angles, float32 rotation, one rounding to the pool's type);
+ *   k', v_raw are written into the pool at slot_maps[slot_off + qs + t] (the caller has
+ *        assigned the span's slots);
+ *   q_out = q'; out = causal attention of q' over the history slots
+ *        hist[slot_off .. slot_off + n_hist[b]) (positions before qs; every span query
+ *        sees all of them) and the span's slots of tokens 0 .. t;
+ *   with M (not NULL): Eq. 2 with Enc = the mean of the n rows q' of each query head,
+ *        in place (the memory's R must equal Hq / Hkv: one row per query head, the
+ *        paper's M_t in R^{L x Hq x D});
+ *   kq[t] = the mean of k' over layers and KV heads (Eq. 5's key mean at the span's
+ *        positions, the cross-attention keys of Eq. 6), float32.
+ * Packing: sessions in order; session b's rows start after those of the sessions before
+ * it: q_raw, q_out, out [L][Hq][n][D] and k_raw, v_raw [L][Hkv][n][D] (pool's type), kq
+ * [n][D]. Supported: D = 128, a bf16 pool, n * (Hq / Hkv) <= 256, Hq * D <= 8192 and
+ * Hkv * D <= 2048 (IKV_EUNSUPPORTED otherwise). lambda as in ikv_qm_update.
+ * workspace: ikv_workspace_bytes(IKV_CALL_PREFILL).
+ */
+ikv_status ikv_prefill_span(const ikv_pool *pool, const ikv_session *sess,
+                            const ikv_session *sess_dev, int32_t B, const int32_t *slot_maps,
+                            const void *q_raw, const void *k_raw, const void *v_raw,
+                            const int32_t *hist, const int32_t *n_hist, double rope_base,
+                            float lambda, float *M, void *q_out, void *out, float *kq,
+                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Workspace size of one call (IKV_CALL_*) for these sessions, in bytes (0 when

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libikv.so")
 ARCH = "gfx950"
 
 SOURCES = ["ikv_api.hip", "k_memory.hip", "k_score.hip", "k_score_mfma.hip", "k_residual.hip",
-           "k_residual_mfma.hip", "k_select.hip", "k_decode.hip", "k_compact.hip", "ikv_session.cpp"]
+           "k_residual_mfma.hip", "k_select.hip", "k_decode.hip", "k_compact.hip", "k_prefill.hip", "ikv_session.cpp"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",

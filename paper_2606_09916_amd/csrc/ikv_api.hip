@@ -152,6 +152,12 @@ size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
   return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
 }
 
+size_t prefill_bytes(const ikv_pool *p, const ikv_session *s, int B) {
+  int64_t n = 0;
+  for (int b = 0; b < B; ++b) n += std::max(0, s[b].qe - s[b].qs);
+  return size_t(n) * p->L * p->D * sizeof(float);
+}
+
 ikv_status pending_fault() {
   if (ikv::take_host_fault())
     return fail(IKV_EHIP, "a grid barrier of an earlier ikv_select_budget call gave up waiting; "
@@ -290,6 +296,11 @@ ikv_status ikv_workspace_bytes(const ikv_pool *pool, const ikv_session *sess, in
       if ((r = check_pool(pool))) return r;
       if ((r = check_sessions(sess, sess, B))) return r;
       *bytes = decode_bytes(pool, sess, B);
+      return ok();
+    case IKV_CALL_PREFILL:
+      if ((r = check_pool(pool))) return r;
+      if ((r = check_sessions(sess, sess, B))) return r;
+      *bytes = prefill_bytes(pool, sess, B);
       return ok();
     case IKV_CALL_COMPACT:
       if ((r = check_sessions(sess, sess, B))) return r;
@@ -455,6 +466,40 @@ ikv_status ikv_compact_apply(const ikv_pool *pool, const ikv_session *sess, cons
   return hip_status(ikv::launch_compact(*pool, sess_dev, B, max_n(sess, B), slot_maps, keep, dst_slots, rope_base,
                                         n_keep, static_cast<int32_t *>(workspace), (hipStream_t)stream),
                     "ikv_compact_apply");
+}
+
+ikv_status ikv_prefill_span(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev, int32_t B,
+                            const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
+                            const int32_t *hist, const int32_t *n_hist, double rope_base, float lambda, float *M,
+                            void *q_out, void *out, float *kq, void *workspace, size_t workspace_bytes, void *stream) {
+  if (ikv_status f = pending_fault()) return f;
+  ikv_status r = check_pool(pool);
+  if (r) return r;
+  if ((r = check_sessions(sess, sess_dev, B))) return r;
+  if (B == 0) return ok();
+  if (!slot_maps || !q_raw || !k_raw || !v_raw || !hist || !n_hist || !q_out || !out || !kq)
+    return fail(IKV_EINVAL, "an input or output pointer is NULL");
+  if (pool->D != 128 || pool->kv_dtype != IKV_BF16)
+    return fail(IKV_EUNSUPPORTED, "ikv_prefill_span needs D = 128 and a bf16 pool");
+  if (pool->Hq * pool->D > 8192 || pool->Hkv * pool->D > 2048)
+    return fail(IKV_EUNSUPPORTED, "ikv_prefill_span: Hq * D must be <= 8192 and Hkv * D <= 2048");
+  if (!(rope_base > 1.0)) return fail(IKV_EINVAL, "rope_base must be > 1");
+  if (M && !(lambda >= 0.0f)) return fail(IKV_EINVAL, "lambda must be >= 0 (got %g)", double(lambda));
+  const int G = pool->Hq / pool->Hkv;
+  int max_n = 0;
+  for (int b = 0; b < B; ++b) {
+    const int n = sess[b].qe - sess[b].qs;
+    if (n * G > 256) return fail(IKV_EUNSUPPORTED, "session %d: span of %d tokens x %d heads per KV head > 256", b, n, G);
+    if (M && sess[b].R != G) return fail(IKV_ESHAPE, "session %d: the memory update needs R = Hq / Hkv = %d", b, G);
+    max_n = std::max(max_n, n);
+  }
+  if ((r = check_ws(workspace, workspace_bytes, prefill_bytes(pool, sess, B)))) return r;
+  if (max_n == 0) return ok();
+  const float decay = isinf(lambda) ? 0.0f : float(exp(-double(lambda)));
+  return hip_status(ikv::launch_prefill(*pool, sess_dev, B, max_n, slot_maps, q_raw, k_raw, v_raw, hist, n_hist,
+                                        rope_base, decay, M, q_out, out, kq, static_cast<float *>(workspace),
+                                        (hipStream_t)stream),
+                    "ikv_prefill_span");
 }
 
 ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess, const ikv_session *sess_dev,

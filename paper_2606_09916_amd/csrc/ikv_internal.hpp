@@ -258,6 +258,11 @@ hipError_t launch_compact(const ikv_pool &pool, const ikv_session *sess_dev, int
                           const int32_t *slot_maps, const uint8_t *keep, const int32_t *dst, double base,
                           int32_t *n_keep, int32_t *pos_list, hipStream_t st);
 
+hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n,
+                          const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
+                          const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
+                          void *q_out, void *out, float *kq, float *ws, hipStream_t st);
+
 int decode_splits(int maxN);
 
 // A word of pinned host memory that kernels set (system scope) to report a fault the

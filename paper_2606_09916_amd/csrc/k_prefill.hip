@@ -1,0 +1,352 @@
+// Prefill of the actionable query span (Sec. 3.5: the post-RoPE Q and K the retention
+// step needs are the ones the model's own attention computes; Sec. 3.2: Enc(q_t) is
+// the mean of the span's post-RoPE Q rows; Eq. 6: the cross-attention keys are the
+// mean key rows at the query positions). One call per turn, before the retention step:
+//
+//   k_prefill_rope  one workgroup per (layer, session), over the span's tokens in
+//                   order: Neox RoPE at each token's position (pair angles in float64,
+//                   cos / sin in LDS, rotation in float32, one rounding to the pool's
+//                   type) of the query rows (written out) and key rows (written into
+//                   the pool at the span's slots, with the value rows); the sum of the
+//                   rotated query rows per head (Enc) and, with a memory, the update of
+//                   Eq. 2 in place; per token, the sum of its rotated key rows over the
+//                   KV heads (this layer's part of the mean key row);
+//   k_prefill_attn  one workgroup per (layer, KV head, session): causal attention of
+//                   the span's query rows of the KV head's G query heads over the
+//                   history slots and the span's own slots (matrix cores, below);
+//   k_prefill_kq    the mean key rows of the span tokens: the layers' parts summed in
+//                   layer order.
+#include <math.h>
+
+#include "ikv_internal.hpp"
+
+namespace ikv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int PD = 128;                          // head dimension of the attention kernel
+constexpr int PR_THREADS = 256;
+constexpr int PR_QMAX = 8192;                    // Hq * D: query channels of a layer (Enc in LDS)
+constexpr int PR_KMAX = 2048;                    // Hkv * D: key channels of a layer
+constexpr int PR_QE = PR_QMAX / PR_THREADS;      // query channels per thread
+
+// Per session b: n = qe - qs span tokens; the packed inputs and outputs of the sessions
+// before b: rows of q (Hq per layer) and of k / v (Hkv per layer), and the mean key rows.
+__device__ __forceinline__ void prefill_offsets(const ikv_session *sess, int b, int L, int Hq, int Hkv, int D,
+                                                int64_t *q_off, int64_t *kv_off, int64_t *kq_off) {
+  int64_t nq = 0;
+  for (int i = 0; i < b; ++i) nq += sess[i].qe - sess[i].qs;
+  *q_off = nq * L * Hq * D;
+  *kv_off = nq * L * Hkv * D;
+  *kq_off = nq * D;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(PR_THREADS) k_prefill_rope(const ikv_session *__restrict__ sess, int L, int Hq,
+                                                             int Hkv, int D, T *__restrict__ kpool,
+                                                             T *__restrict__ vpool, int64_t num_slots,
+                                                             const int32_t *__restrict__ slot_maps,
+                                                             const T *__restrict__ q_raw, const T *__restrict__ k_raw,
+                                                             const T *__restrict__ v_raw, T *__restrict__ q_out,
+                                                             float *__restrict__ M, float decay, double base,
+                                                             float *__restrict__ kq_part) {
+  __shared__ float cs[64], sn[64];
+  __shared__ float red[PR_THREADS];
+  __shared__ float ksum[PR_KMAX];                // this token's rotated key rows [Hkv][D]
+  __shared__ float encs[PR_QMAX];                // the layer's summed query rows [Hq][D]
+  const int l = blockIdx.x, b = blockIdx.y;
+  const ikv_session s = sess[b];
+  const int n = s.qe - s.qs;
+  if (n <= 0) return;
+  int64_t q_off, kv_off, kq_off;
+  prefill_offsets(sess, b, L, Hq, Hkv, D, &q_off, &kv_off, &kq_off);
+  const int t0 = threadIdx.x, h2 = D / 2;
+  // the query channels (head, channel) = t0, t0 + 256, ... that this thread sums over the tokens
+  float enc[PR_QE];
+#pragma unroll
+  for (int k = 0; k < PR_QE; ++k) enc[k] = 0.f;
+  const int nq_el = Hq * D, nk_el = Hkv * D;
+  for (int t = 0; t < n; ++t) {
+    const int pos = s.qs + t;
+    if (t0 < h2) {
+      const double ang = double(pos) * pow(base, -2.0 * double(t0) / double(D));
+      cs[t0] = float(cos(ang));
+      sn[t0] = float(sin(ang));
+    }
+    __syncthreads();
+    // query rows: element e = (head, channel); channel c < D/2 pairs with c + D/2
+    for (int e = t0, k = 0; e < nq_el; e += PR_THREADS, ++k) {
+      const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
+      const int64_t base_row = q_off + ((int64_t(l) * Hq + h) * n + t) * D;
+      const float x = Store<T>::ld(q_raw + base_row + c);
+      const float y = Store<T>::ld(q_raw + base_row + (c < h2 ? c + h2 : c - h2));
+      const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
+      const T rv = Store<T>::from(r);
+      q_out[base_row + c] = rv;
+      enc[k] += Store<T>::ld(&rv);
+    }
+    // key rows into the pool at the token's slot, value rows copied
+    const int64_t slot = slot_maps[s.slot_off + pos];
+    for (int e = t0; e < nk_el; e += PR_THREADS) {
+      const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
+      const int64_t src = kv_off + ((int64_t(l) * Hkv + h) * n + t) * D;
+      const float x = Store<T>::ld(k_raw + src + c);
+      const float y = Store<T>::ld(k_raw + src + (c < h2 ? c + h2 : c - h2));
+      const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
+      const T rv = Store<T>::from(r);
+      const int64_t dst = ((int64_t(l) * num_slots + slot) * Hkv + h) * D + c;
+      kpool[dst] = rv;
+      vpool[dst] = v_raw[src + c];
+      ksum[e] = Store<T>::ld(&rv);
+    }
+    __syncthreads();
+    // this layer's part of the token's mean key row: the rotated rows summed over KV heads in order
+    for (int c = t0; c < D; c += PR_THREADS) {
+      float a = 0.f;
+      for (int h = 0; h < Hkv; ++h) a += ksum[h * D + c];
+      kq_part[(kq_off * L) + (int64_t(l) * n + t) * D + c] = a;
+    }
+    __syncthreads();
+  }
+  if (!M) return;
+  // Eq. 2 for the layer's Hq memory rows (one per query head): M <- decay M + Enc, then
+  // each row divided by max(||row||, 1e-12) (the norm summed in a fixed tree order)
+  for (int e = t0, k = 0; e < nq_el; e += PR_THREADS, ++k) encs[e] = enc[k];
+  __syncthreads();
+  float *Ml = M + s.mem_off + int64_t(l) * Hq * D;
+  const float inv_n = 1.0f / float(n);
+  for (int h = 0; h < Hq; ++h) {
+    const float v = t0 < D ? decay * Ml[int64_t(h) * D + t0] + encs[h * D + t0] * inv_n : 0.f;
+    red[t0] = v * v;
+    __syncthreads();
+    for (int off = PR_THREADS / 2; off > 0; off >>= 1) {
+      if (t0 < off) red[t0] += red[t0 + off];
+      __syncthreads();
+    }
+    const float norm = fmaxf(sqrtf(red[0]), 1e-12f);
+    __syncthreads();
+    if (t0 < D) Ml[int64_t(h) * D + t0] = v / norm;
+  }
+}
+
+// ------------------------------------------------------------------ causal attention
+// Workgroup (layer l, KV head g, session b), sixteen waves: query row r = h' n + t (h'
+// the query head within the group, t the span token) belongs to wave r / 16. Keys
+// stream in tiles of 64: the history slots, then the span's slots. Per tile a wave
+// computes S^T = K Q^T (16 keys x 16 rows per MFMA block, bf16 inputs exact, float32
+// accumulation), keeps an online (max, sum) per row, and adds O^T += V^T P^T, the
+// weights P split into bf16 hi + lo (two MFMAs; 2^-17 relative). The weights of keys
+// 16 kb + 4 g + i that a lane holds are already the B operand of the second product, up
+// to the order of the contraction index (perm32): the transposed value tile in LDS is
+// read in that order. Key rows stay as loaded (rows of 136 bf16); value rows are
+// written transposed (rows of 72 bf16 per channel).
+constexpr int PA_WAVES = 16;
+constexpr int PA_THREADS = PA_WAVES * WAVE;
+constexpr int PA_TILE = 64;
+constexpr int PA_KROW = PD + 8;
+constexpr int PA_VROW = PA_TILE + 8;
+
+__global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *__restrict__ sess, int L, int Hq,
+                                                             int Hkv, const uint16_t *__restrict__ kpool,
+                                                             const uint16_t *__restrict__ vpool, int64_t num_slots,
+                                                             const int32_t *__restrict__ slot_maps,
+                                                             const int32_t *__restrict__ hist,
+                                                             const int32_t *__restrict__ n_hist,
+                                                             const uint16_t *__restrict__ q_rot,
+                                                             uint16_t *__restrict__ out) {
+  __shared__ __align__(16) uint16_t ks[2][PA_TILE * PA_KROW];
+  __shared__ __align__(16) uint16_t vt[2][PD * PA_VROW];
+  const int lg = blockIdx.x, b = blockIdx.y;
+  const int l = lg / Hkv, g_kv = lg - l * Hkv;
+  const ikv_session s = sess[b];
+  const int n = s.qe - s.qs;
+  if (n <= 0) return;
+  const int G = Hq / Hkv, nrows = n * G;
+  int64_t q_off, kv_off, kq_off;
+  prefill_offsets(sess, b, L, Hq, Hkv, PD, &q_off, &kv_off, &kq_off);
+  const int nh = n_hist[b];
+  const int T = nh + n;                           // keys: history, then the span
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int g = lane >> 4, c = lane & 15;
+  const int row = min(16 * w + c, nrows - 1);     // this lane's query row (clamped; the extra rows are never written)
+  const int hq = row / n, tr = row - hq * n;
+  const bool wave_on = 16 * w < nrows;
+  const float scale = 1.4426950408889634f / sqrtf(float(PD));
+
+  // query fragments (B operand of S^T): row `row`, channels 32 ks + 8 g .. + 8
+  bf16x8 qf[4];
+  {
+    const uint16_t *qr = q_rot + q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD;
+#pragma unroll
+    for (int ks4 = 0; ks4 < 4; ++ks4) qf[ks4] = *reinterpret_cast<const bf16x8 *>(qr + 32 * ks4 + 8 * g);
+  }
+  const int32_t *S = slot_maps + s.slot_off;
+  const int32_t *H = hist + s.slot_off;
+  auto key_slot = [&](int kk) -> int64_t {
+    if (kk >= T) return s.qs < s.N ? S[s.qs] : 0;  // past the end: a valid row, masked out
+    return kk < nh ? H[kk] : S[s.qs + (kk - nh)];
+  };
+  // tile loads: thread t takes key t / 16 of the tile, 16-byte chunk t % 16 of its K and V rows
+  const int lk = t >> 4, lc = t & 15;
+  uint4 kreg, vreg;
+  auto load_tile = [&](int tile) {
+    const int64_t slot = key_slot(tile * PA_TILE + lk);
+    const int64_t o = ((int64_t(l) * num_slots + slot) * Hkv + g_kv) * PD + lc * 8;
+    kreg = *reinterpret_cast<const uint4 *>(kpool + o);
+    vreg = *reinterpret_cast<const uint4 *>(vpool + o);
+  };
+  auto store_tile = [&](int stg) {
+    *reinterpret_cast<uint4 *>(&ks[stg][lk * PA_KROW + lc * 8]) = kreg;
+    const uint32_t wv[4] = {vreg.x, vreg.y, vreg.z, vreg.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vt[stg][(lc * 8 + 2 * e) * PA_VROW + lk] = uint16_t(wv[e] & 0xffffu);
+      vt[stg][(lc * 8 + 2 * e + 1) * PA_VROW + lk] = uint16_t(wv[e] >> 16);
+    }
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;          // this lane's row (rows are the lane index c)
+  f32x4 o[8];                                     // O^T blocks: channel 16 db + 4 g + i, row c
+#pragma unroll
+  for (int db = 0; db < 8; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ntile = (T + PA_TILE - 1) / PA_TILE;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int tile = 0; tile < ntile; ++tile) {
+    const int stg = tile & 1;
+    if (tile + 1 < ntile) load_tile(tile + 1);
+    if (wave_on) {
+      // S^T: key blocks kb (keys 16 kb .. + 15), lane (g, c): keys 16 kb + 4 g + i, row c
+      f32x4 sacc[4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const uint16_t *kr = &ks[stg][(16 * kb + c) * PA_KROW];
+#pragma unroll
+        for (int ks4 = 0; ks4 < 4; ++ks4)
+          sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8 *>(kr + 32 * ks4 + 8 * g),
+                                                             qf[ks4], sacc[kb], 0, 0, 0);
+      }
+      // mask (keys past the end; span keys after this row's token) and the online softmax
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kk = tile * PA_TILE + 16 * kb + 4 * g + i;
+          const bool ok = kk < T && (kk < nh || kk - nh <= tr);
+          const float x = ok ? sacc[kb][i] * scale : -INFINITY;
+          sacc[kb][i] = x;
+          tmax = fmaxf(tmax, x);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, WAVE));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, WAVE));
+      const float m_new = fmaxf(m_run, tmax);
+      const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      float psum = 0.f;
+      float p[4][4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          p[kb][i] = sacc[kb][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sacc[kb][i] - m_new);
+          psum += p[kb][i];
+        }
+      psum += __shfl_xor(psum, 16, WAVE);
+      psum += __shfl_xor(psum, 32, WAVE);
+      l_run = l_run * corr + psum;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[db][i] *= corr;
+      // O^T += V^T P^T over two 32-key steps; k index 8 g + e stands for key perm32(g, e)
+#pragma unroll
+      for (int st2 = 0; st2 < 2; ++st2) {
+        bf16x8 ph, pl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = e < 4 ? p[2 * st2][e] : p[2 * st2 + 1][e - 4];
+          ph[e] = __bf16(v);
+          pl[e] = __bf16(v - float(ph[e]));
+        }
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+          const uint16_t *vr = &vt[stg][(16 * db + c) * PA_VROW + 32 * st2];
+          const uint2 a = *reinterpret_cast<const uint2 *>(vr + 4 * g);
+          const uint2 bq = *reinterpret_cast<const uint2 *>(vr + 16 + 4 * g);
+          const uint4 av = make_uint4(a.x, a.y, bq.x, bq.y);
+          const bf16x8 va = __builtin_bit_cast(bf16x8, av);
+          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, o[db], 0, 0, 0);
+          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, o[db], 0, 0, 0);
+        }
+      }
+    }
+    if (tile + 1 < ntile) store_tile(stg ^ 1);
+    __syncthreads();
+  }
+  // out[l][g_kv G + h'][t][:] = O / l
+  if (wave_on) {
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ch = 16 * db + 4 * g + i;
+        if (16 * w + c < nrows)
+          out[q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD + ch] = float_to_bf16_bits(o[db][i] * inv);
+      }
+  }
+}
+
+__global__ void __launch_bounds__(128) k_prefill_kq(const ikv_session *__restrict__ sess, int L, int Hq, int Hkv,
+                                                    int D, const float *__restrict__ kq_part, float *__restrict__ kq) {
+  const int t = blockIdx.x, b = blockIdx.y;
+  const ikv_session s = sess[b];
+  const int n = s.qe - s.qs;
+  if (t >= n || int(threadIdx.x) >= D) return;
+  int64_t q_off, kv_off, kq_off;
+  prefill_offsets(sess, b, L, Hq, Hkv, D, &q_off, &kv_off, &kq_off);
+  float a = 0.f;
+  for (int l = 0; l < L; ++l) a += kq_part[kq_off * L + (int64_t(l) * n + t) * D + threadIdx.x];
+  kq[kq_off + int64_t(t) * D + threadIdx.x] = a / float(L * Hkv);
+}
+
+hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n,
+                          const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
+                          const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
+                          void *q_out, void *out, float *kq, float *ws, hipStream_t st) {
+  const dim3 g1(unsigned(pool.L), B);
+  {
+    KTimer kt_("k_prefill_rope", st);
+    if (pool.kv_dtype == IKV_BF16)
+      k_prefill_rope<uint16_t><<<g1, PR_THREADS, 0, st>>>(
+          sess_dev, pool.L, pool.Hq, pool.Hkv, pool.D, static_cast<uint16_t *>(pool.k_pool),
+          static_cast<uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, static_cast<const uint16_t *>(q_raw),
+          static_cast<const uint16_t *>(k_raw), static_cast<const uint16_t *>(v_raw), static_cast<uint16_t *>(q_out),
+          M, decay, base, ws);
+    else
+      k_prefill_rope<float><<<g1, PR_THREADS, 0, st>>>(
+          sess_dev, pool.L, pool.Hq, pool.Hkv, pool.D, static_cast<float *>(pool.k_pool),
+          static_cast<float *>(pool.v_pool), pool.num_slots, slot_maps, static_cast<const float *>(q_raw),
+          static_cast<const float *>(k_raw), static_cast<const float *>(v_raw), static_cast<float *>(q_out), M, decay,
+          base, ws);
+  }
+  {
+    KTimer kt_("k_prefill_attn", st);
+    k_prefill_attn<<<dim3(unsigned(pool.L * pool.Hkv), B), PA_THREADS, 0, st>>>(
+        sess_dev, pool.L, pool.Hq, pool.Hkv, static_cast<const uint16_t *>(pool.k_pool),
+        static_cast<const uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, hist, n_hist,
+        static_cast<const uint16_t *>(q_out), static_cast<uint16_t *>(out));
+  }
+  {
+    KTimer kt_("k_prefill_kq", st);
+    k_prefill_kq<<<dim3(unsigned(max_n), B), 128, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv, pool.D, ws, kq);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ikv

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(PKG, "libikv.so")
 
 IKV_BF16, IKV_F32 = 0, 1
 IKV_RESIDUAL, IKV_NO_XATTN, IKV_POOL7 = 1, 2, 4
-CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE, CALL_COMPACT = 1, 2, 3, 4, 5
+CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE, CALL_COMPACT, CALL_PREFILL = 1, 2, 3, 4, 5, 6
 STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE", -4: "IKV_EUNSUPPORTED",
           -5: "IKV_EHIP"}
 
@@ -24,7 +24,7 @@ SYMBOLS = ("ikv_init_dead_slot", "ikv_qm_update", "ikv_score_history", "ikv_sele
            "ikv_redirect_slots", "ikv_decode_attend_slotmap", "ikv_workspace_bytes", "ikv_last_error",
            "ikv_timing", "ikv_timing_read", "ikv_memstore_create", "ikv_memstore_destroy", "ikv_memstore_acquire",
            "ikv_memstore_release", "ikv_memstore_trigger", "ikv_memstore_size", "ikv_resolve_span",
-           "ikv_compact_apply")
+           "ikv_compact_apply", "ikv_prefill_span")
 IKV_KEY_EXPLICIT, IKV_KEY_SPAN, IKV_KEY_PREFIX, IKV_KEY_LOCAL = 1, 2, 3, 4
 
 
@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
             "ikv_workspace_bytes": [P, S, c_int32, c_int32, c_uint32, ctypes.POINTER(c_size_t)],
             "ikv_compact_apply": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, ctypes.c_double, c_void_p,
                                   c_void_p, c_size_t, c_void_p],
+            "ikv_prefill_span": [P, S, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 ctypes.c_double, c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                 c_void_p],
             "ikv_timing": [c_int32],
             "ikv_memstore_create": [c_int32, ctypes.POINTER(c_void_p)],
             "ikv_memstore_acquire": [c_void_p, ctypes.POINTER(KeySource), ctypes.POINTER(c_int32),
@@ -234,6 +237,16 @@ def compact_apply(pool: Pool, sess: Sessions, slot_maps, keep, dst_slots, n_keep
     _check(lib().ikv_compact_apply(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps),
                                    _ptr(keep), _ptr(dst_slots), float(rope_base), _ptr(n_keep), wp, wn,
                                    _stream(stream)), "ikv_compact_apply")
+
+
+def prefill_span(pool: Pool, sess: Sessions, slot_maps, q_raw, k_raw, v_raw, hist, n_hist, q_out, out, kq,
+                 ws: Workspace, M=None, lam: float = 0.5, rope_base: float = 1.0e6, stream=None) -> None:
+    """RoPE, pool write, causal span attention, Enc and memory update, and key means of the span."""
+    wp, wn = ws.get(workspace_bytes(pool, sess, CALL_PREFILL))
+    _check(lib().ikv_prefill_span(ctypes.byref(pool), sess.host_ptr, sess.dev_ptr, sess.B, _ptr(slot_maps),
+                                  _ptr(q_raw), _ptr(k_raw), _ptr(v_raw), _ptr(hist), _ptr(n_hist), float(rope_base),
+                                  float(lam), _ptr(M), _ptr(q_out), _ptr(out), _ptr(kq), wp, wn, _stream(stream)),
+           "ikv_prefill_span")
 
 
 # ----------------------------------------------------------------------------- timing

@@ -1,0 +1,146 @@
+"""Prefill of the query span with the retention step's inputs produced on the way
+(Sec. 3.5, Sec. 3.2, Eq. 2, Eq. 6), against the float64 oracle.
+
+The rotated rows are stored rounded (bf16): the query rows written out and the key rows
+written into the pool must lie within one bf16 unit in the last place of the oracle's
+exact rotation, the value rows must be copied exactly. Everything computed from the
+rounded rows (attention, the memory update, the key means) is compared with the oracle
+run on the GPU's own rounded rows: attention within 2e-3 plus half a bf16 ulp, the
+memory within 4e-6, the key means within 1e-6 relative."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2606_09916_amd import ikv
+from parity import check_attention
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _bf(a, dev):
+    torch = _torch()
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+def _host16(t):
+    torch = _torch()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def _ulp_check(got, want):
+    ax = np.abs(want)
+    ulp = np.exp2(np.floor(np.log2(np.where(ax > 0, ax, 1.0))) - 7)
+    err = np.abs(synth.widen(got) - want)
+    assert np.all(err <= np.maximum(ulp, 1e-6)), f"rotated rows off by {err.max():.3e}"
+
+
+def _setup(shape, N0, n, seed, dead=0.0, memory=True):
+    """A session of N0 history positions and an n-token span at the end; the span's slots
+    assigned. Pre-RoPE span rows N(0,1) in bf16."""
+    torch = _torch()
+    G = shape.G
+    spec = synth.SessionSpec(N=N0 + n, C=max(1, (N0 + n) // 4), pi=0, qs=N0, qe=N0 + n, R=G, dead_frac=dead,
+                             qpos=np.zeros(0, np.int32))
+    batch = synth.make_batch(shape, [spec], seed=seed, kv_dtype=synth.BF16, layout="paged", span_rows=False)
+    g = synth.stream(seed, synth.T_QWIN, 7)
+    L, Hq, Hkv, D = shape.L, shape.Hq, shape.Hkv, shape.D
+    q_raw = synth.f32_to_bf16(g.standard_normal((L, Hq, n, D), dtype=np.float32))
+    k_raw = synth.f32_to_bf16(g.standard_normal((L, Hkv, n, D), dtype=np.float32))
+    v_raw = synth.f32_to_bf16(g.standard_normal((L, Hkv, n, D), dtype=np.float32))
+    M0 = g.standard_normal((L, Hq, D)).astype(np.float32)
+    M0 /= np.linalg.norm(M0, axis=-1, keepdims=True)
+    dev = torch.device("cuda:0")
+    k_dev, v_dev = _bf(batch.k_pool, dev), _bf(batch.v_pool, dev)
+    pool = ikv.make_pool(k_dev, v_dev, L, Hq, Hkv, D, batch.num_slots, synth.DEAD_SLOT)
+    S = batch.S(0)
+    hist = S[:N0][S[:N0] != synth.DEAD_SLOT].astype(np.int32)
+    hist_full = np.zeros(N0 + n, np.int32)
+    hist_full[:len(hist)] = hist
+    sess = ikv.Sessions([dict(slot_off=0, mem_off=0, qspan_off=0, qpos_off=0, N=N0 + n, pi=0, qs=N0, qe=N0 + n,
+                              C=spec.C, radix_prefix=0, R=G, nq=0)], dev)
+    d = dict(batch=batch, pool=pool, k=k_dev, v=v_dev, sess=sess, S=torch.from_numpy(S.copy()).to(dev),
+             hist=torch.from_numpy(hist_full).to(dev), n_hist=torch.tensor([len(hist)], dtype=torch.int32, device=dev),
+             q_raw=_bf(q_raw, dev), k_raw=_bf(k_raw, dev), v_raw=_bf(v_raw, dev),
+             q_out=torch.empty((L, Hq, n, D), dtype=torch.bfloat16, device=dev),
+             out=torch.empty((L, Hq, n, D), dtype=torch.bfloat16, device=dev),
+             kq=torch.empty((n, D), dtype=torch.float32, device=dev),
+             M=torch.from_numpy(M0.reshape(-1).copy()).to(dev) if memory else None,
+             host=dict(q_raw=q_raw, k_raw=k_raw, v_raw=v_raw, M0=M0, hist=hist, S=S))
+    return d
+
+
+def _run(d, lam=0.5):
+    ws = ikv.Workspace(d["k"].device)
+    ikv.prefill_span(d["pool"], d["sess"], d["S"], d["q_raw"], d["k_raw"], d["v_raw"], d["hist"], d["n_hist"],
+                     d["q_out"], d["out"], d["kq"], ws, M=d["M"], lam=lam, rope_base=synth.ROPE_BASE)
+    _torch().cuda.synchronize()
+
+
+def _check(d, layers=None, tokens=None):
+    h = d["host"]
+    batch = d["batch"]
+    sh = batch.shape
+    L, Hq, Hkv, D = sh.L, sh.Hq, sh.Hkv, sh.D
+    s = batch.sessions[0]
+    n = s.qe - s.qs
+    layers = range(L) if layers is None else layers
+    q_out = _host16(d["q_out"])
+    kp, vp = _host16(d["k"]), _host16(d["v"])
+    span_slots = h["S"][s.qs:s.qe]
+    pos = np.arange(s.qs, s.qe)
+    # the rotations, one rounding each, on every layer
+    for l in range(L):
+        for t in range(n):
+            _ulp_check(q_out[l, :, t], oracle.ikv_oracle.rope_rotate(synth.widen(h["q_raw"][l, :, t]), pos[t],
+                                                                     synth.ROPE_BASE, D))
+            _ulp_check(kp[l, span_slots[t]], oracle.ikv_oracle.rope_rotate(synth.widen(h["k_raw"][l, :, t]), pos[t],
+                                                                           synth.ROPE_BASE, D))
+            assert np.array_equal(vp[l, span_slots[t]], h["v_raw"][l, :, t])
+    # attention on the GPU's rounded rows
+    out = synth.widen(_host16(d["out"]))
+    for l in layers:
+        toks = range(n) if tokens is None else tokens
+        for t in toks:
+            # token t alone: its keys are the history and span tokens 0 .. t-1 (every one
+            # visible to it) followed by its own
+            hist_t = np.concatenate([h["hist"], span_slots[:t]])
+            want = oracle.ikv_oracle.prefill_attention(q_out[l:l + 1, :, t:t + 1], kp[l:l + 1], vp[l:l + 1], hist_t,
+                                                       span_slots[t:t + 1])
+            check_attention(out[l:l + 1, :, t], want[:, :, 0], bf16=True)
+    # the memory update (Enc = mean of the rounded rows) and the key means, over every layer
+    if d["M"] is not None:
+        M_o = oracle.qm_update(h["M0"].reshape(L * Hq, D), q_out.reshape(L * Hq, n, D))
+        np.testing.assert_allclose(d["M"].cpu().numpy().reshape(L * Hq, D), M_o, atol=4e-6, rtol=0)
+    kq_o = oracle.kbar(kp, h["S"], pos)
+    np.testing.assert_allclose(d["kq"].cpu().numpy(), kq_o, rtol=1e-6, atol=1e-7)
+
+
+@pytest.mark.parametrize("N0,n,Hkv,G,dead", [(500, 32, 2, 4, 0.0), (1300, 64, 2, 4, 0.2), (700, 1, 2, 4, 0.0),
+                                             (0, 16, 2, 4, 0.0), (900, 32, 2, 8, 0.1), (333, 48, 4, 1, 0.0)])
+def test_prefill_span_small(dev, N0, n, Hkv, G, dead):
+    shape = synth.Shape(L=2, Hq=Hkv * G, Hkv=Hkv, D=128)
+    d = _setup(shape, N0, n, seed=N0 + n + G, dead=dead)
+    _run(d)
+    _check(d)
+
+
+def test_prefill_span_without_memory(dev):
+    shape = synth.Shape(L=2, Hq=8, Hkv=2, D=128)
+    d = _setup(shape, 400, 20, seed=3, memory=False)
+    _run(d)
+    _check(d)
+
+
+def test_prefill_span_qwen3_8b_32k(dev):
+    """Qwen3-8B shape: a 64-token span over a 32,704-position history (the default
+    workload's span), checked on three layers and three tokens per layer for the
+    attention, every layer for the rotations, the memory and the key means."""
+    d = _setup(synth.qwen3_8b_shape(), 32704, 64, seed=2)
+    _run(d)
+    _check(d, layers=[0, 17, 35], tokens=[0, 31, 63])
