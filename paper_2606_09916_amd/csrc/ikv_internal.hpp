@@ -51,6 +51,9 @@ __host__ __device__ inline int pad16(int R) { return (R + 15) & ~15; }
 //          zero past the live ones (residual on the MFMA path only)
 //   mbp    [units / 2][D] column sums of the memory rows per head pair, the partials
 //          of mbar when the unit-major first pass runs (residual on the MFMA path only)
+//   clist  the candidate list (MFMA path): chunk c of the launch's chunk size CH keeps its
+//          candidate positions in position order at [c CH ...], then the counts per
+//          chunk (int32)
 // followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN], and on the
 // MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC], columns
 // ordered within each 32-wide head as perm32 below.
@@ -59,10 +62,10 @@ constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score
 constexpr int PART_TILE = 64;       // positions per partial of the position-major first pass
 
 struct ScoreSizes {
-  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp;
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp, clist;
   int64_t lse_pairs;   // units * R * 2: the (max, 1/Z) pairs at the start of lse
   __host__ __device__ int64_t total() const {
-    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf + mbp;
+    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf + mbp + clist;
   }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
@@ -78,6 +81,8 @@ struct ScoreSizes {
   __host__ __device__ int64_t off_qlist() const { return off_fold() + fold; }
   __host__ __device__ int64_t off_kvf() const { return off_qlist() + qlist; }
   __host__ __device__ int64_t off_mbp() const { return off_kvf() + kvf; }
+  __host__ __device__ int64_t off_clist() const { return off_mbp() + mbp; }
+  __host__ __device__ int64_t off_ccount(int N) const { return off_clist() + align64f(int64_t(N) + 1024); }
 };
 
 // Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0,
@@ -113,6 +118,7 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   z.qlist = resid ? align64f(s.nq) : 0;
   z.kvf = resid && mfma ? align64f(KVF_BF16 / 2) : 0;
   z.mbp = resid && mfma ? align64f(int64_t(units / 2) * D) : 0;
+  z.clist = mfma ? align64f(int64_t(s.N) + 1024) + align64f(cdiv(s.N, 128) + 1) : 0;
   return z;
 }
 
@@ -127,6 +133,16 @@ __host__ __device__ inline int64_t score_offset(const ikv_session *sess, int b, 
 __host__ __device__ inline int64_t score_shared_floats(int D) {
   return align64f(int64_t(3 * D + 1) * HC) + align64f(int64_t(3 * D + 1 + HC) * HIDDEN) +
          align64f(int64_t(HIDDEN) * HC);
+}
+
+// Positions per chunk of the unit-major first pass and of the candidate list of the
+// matrix-core path: about nine rounds of two workgroups per CU at the largest sizes,
+// whole 128-position multiples (the second pass and the residual head take the list in
+// tiles of 128).
+inline int stats_chunk(int maxN, int head_pairs) {
+  int64_t c = cdiv(cdiv(int64_t(maxN) * head_pairs, 4608), 128) * 128;
+  c = c < 128 ? 128 : (c > 1024 ? 1024 : c);
+  return int(c);
 }
 
 // Redirect workspace: two slot bitsets (kept slots, freed slots) per session.

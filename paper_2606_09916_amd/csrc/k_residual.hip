@@ -79,8 +79,38 @@ __global__ void __launch_bounds__(256) k_res_setup(const ikv_session *__restrict
   res_setup_body<D>(sess, int(blockIdx.x), slot_maps, qpos, dead, ws, L, Hkv, mfma, pairs);
 }
 
+// kq on the matrix-core path, where the second pass keeps kbar at the candidates only
+// (a live query position in the query span is never one): row i of the kq block is the
+// mean over the L Hkv units of the bf16 key row of the i-th live query position, summed
+// layer-major in float32 and scaled by 1 / (L Hkv) as the second pass does. One
+// workgroup per live row, thread = channel.
+template <int D>
+__global__ void __launch_bounds__(D) k_res_kq(const ikv_session *__restrict__ sess, const uint16_t *__restrict__ kpool,
+                                              int64_t num_slots, int L, int Hkv,
+                                              const int32_t *__restrict__ slot_maps, float *__restrict__ ws) {
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int units = L * Hkv;
+  const ScoreSizes z = score_sizes(s, L, units, D, true, true);
+  float *base = ws + score_offset(sess, b, L, units, D, true, true);
+  const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
+  const int i = blockIdx.x;
+  if (i >= n) return;
+  const int q = reinterpret_cast<const int *>(base + z.off_qlist())[i];
+  const int64_t slot = slot_maps[s.slot_off + q];
+  const int d = threadIdx.x;
+  float a = 0.f;
+  for (int u = 0; u < units; ++u) {
+    const int l = u / Hkv, h = u - l * Hkv;
+    a += bf16_bits_to_float(kpool[((int64_t(l) * num_slots + slot) * Hkv + h) * D + d]);
+  }
+  base[z.off_kq() + int64_t(i) * D + d] = a * (1.0f / float(units));
+}
+
 // K' = W_K kq + b_K and V' = W_V kq + b_V for four live query rows per workgroup,
-// kq = kbar at the live query positions (from the second pass).
+// kq = kbar at the live query positions (from the second pass; on the matrix-core path
+// the kq block of k_res_kq, row i for the i-th live row).
 template <int D>
 __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restrict__ sess, const float *__restrict__ blob,
                                             float *__restrict__ ws, int L, int Hkv, bool mfma) {
@@ -91,7 +121,7 @@ __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restric
   const ResLayout lay(D);
   const ScoreSizes z = score_sizes(s, L, units, D, true, mfma);
   float *base = ws + score_offset(sess, b, L, units, D, true, mfma);
-  const float *kbar = base + z.off_kbar();
+  const float *kbar = base + (mfma ? z.off_kq() : z.off_kbar());
   float *kp = base + z.off_kp();
   float *vp = base + z.off_vp();
   const int n = reinterpret_cast<const int *>(base + z.off_misc() + int64_t(MBAR_PARTS) * D)[D];
@@ -102,8 +132,8 @@ __device__ __forceinline__ void res_kv_body(int bx, const ikv_session *__restric
   const int t = threadIdx.x;
   for (int e = t; e < 4 * D; e += 256) {
     const int r = e / D, d = e - r * D;
-    const int q = qlist[min(i0 + r, n - 1)];          // a live row stands in past n
-    const float v = kbar[int64_t(q) * D + d];
+    const int i = min(i0 + r, n - 1);                  // a live row stands in past n
+    const float v = kbar[int64_t(mfma ? i : qlist[i]) * D + d];
     kq[r][d] = (i0 + r < n) ? v : 0.f;
   }
   __syncthreads();
@@ -326,6 +356,12 @@ static hipError_t launch_residual_t(const ScoreArgs &a, hipStream_t st) {
       KTimer kt_("k_res_setup<D>", st);
       k_res_setup<D><<<a.B, 256, 0, st>>>(a.sess_dev, a.slot_maps, a.qpos, p.dead_slot, a.ws, p.L, p.Hkv, a.mfma,
                                           a.stats);
+    }
+  if (a.maxNq > 0 && !a.mfma_resid && a.mfma)
+    {
+      KTimer kt_("k_res_kq<D>", st);
+      k_res_kq<D><<<dim3(unsigned(a.maxNq), a.B), D, 0, st>>>(a.sess_dev, static_cast<const uint16_t *>(p.k_pool),
+                                                              p.num_slots, p.L, p.Hkv, a.slot_maps, a.ws);
     }
   if (a.maxNq > 0 && !a.mfma_resid)
     {

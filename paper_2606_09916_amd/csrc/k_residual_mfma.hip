@@ -99,7 +99,7 @@ __device__ __forceinline__ void rs_wait(int n) {
 __global__ void __launch_bounds__(64 * RWAVES) __attribute__((amdgpu_waves_per_eu(2)))
 k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, int dead,
                 float *__restrict__ scores, const float *__restrict__ ws, const float *__restrict__ shared,
-                const float *__restrict__ blob, int L, int Hkv, bool xattn) {
+                const float *__restrict__ blob, int L, int Hkv, bool xattn, int CH) {
   __shared__ __align__(1024) uint16_t ring[RS_STAGES * RS_STAGE];
   __shared__ __align__(16) float cst[2 * (HC + HIDDEN) + HIDDEN];   // q0 | h0, rule column, w_2
   const int b = blockIdx.y;
@@ -108,8 +108,9 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int g = lane >> 4, i = lane & 15;
-  const int j0 = blockIdx.x * RT;
-  if (j0 >= s.N) return;
+  // list tile: tiles k of chunk c take entries [c CH + 128 k, + 128) of the candidate list
+  const int per = CH / RT, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  if (int64_t(lc) * CH >= s.N) return;
   const int units = L * Hkv;
   constexpr int64_t F = 3 * RD + 1;
   const ScoreSizes z = score_sizes(s, L, units, RD, true, true);
@@ -131,10 +132,16 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
   const float alpha = fminf(fmaxf(blob[oW2 + HIDDEN + 1], -5.0f), 5.0f);
   float *out = scores + s.slot_off;
 
-  // lane (g, i) of wave w works for candidate j0 + 16 w + i
-  const int j = j0 + RW * w + i, jc = min(j, s.N - 1);
-  const int slot = slot_maps[s.slot_off + jc];
-  const bool cand = j < s.N && slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+  // lane (g, i) of wave w works for list entry 16 w + i of the tile (a candidate)
+  const int32_t *lst = reinterpret_cast<const int32_t *>(base + z.off_clist()) + lc * CH + lk * RT;
+  const int cnt = reinterpret_cast<const int32_t *>(base + z.off_ccount(s.N))[lc];
+  const int ne = min(RT, cnt - lk * RT);
+  if (ne <= 0) return;
+  const bool ident = cnt == min(CH, s.N - lc * CH);   // every position a candidate: its own list
+  const int e = RW * w + i;
+  const bool cand = e < ne;
+  const int ec = cand ? e : ne - 1;
+  const int j = ident ? lc * CH + lk * RT + ec : lst[ec], jc = j;
   if (!__syncthreads_or(cand)) return;
   const float rule = out[jc];
   for (int k = t; k < 2 * (HC + HIDDEN); k += 64 * RWAVES) cst[k] = c0[k];
@@ -319,9 +326,10 @@ hipError_t launch_residual_mfma(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   {
     KTimer kt_("k_residual_mfma", st);
-    k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, RT)), a.B), 64 * RWAVES, 0, st>>>(
+    const int lch = stats_chunk(a.maxN, std::max(1, p.L * p.Hkv / 2));   // the candidate lists' chunk
+    k_residual_mfma<<<dim3(unsigned(cdiv(a.maxN, lch) * (lch / RT)), a.B), 64 * RWAVES, 0, st>>>(
         a.sess_dev, a.slot_maps, p.dead_slot, a.scores, a.ws, a.ws_shared, a.residual, p.L, p.Hkv,
-        (a.flags & IKV_NO_XATTN) == 0);
+        (a.flags & IKV_NO_XATTN) == 0, lch);
   }
   return hipGetLastError();
 }

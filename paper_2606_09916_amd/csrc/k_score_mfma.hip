@@ -619,16 +619,16 @@ template <bool KBAR, int RH>
 __global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
            const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
-           float *__restrict__ scores, bool resid, int big) {
+           float *__restrict__ scores, bool resid, int big, int CH) {
   __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
 
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   if ((big == 1 && s.R > 64) || (big == 2 && s.R <= 64)) return;   // the other launch's session
-  const int tile = blockIdx.x;
-  const int j0 = tile * MFMA_TILE;
-  if (j0 >= s.N) return;
+  // list tile: tiles k of chunk c cover entries [c CH + 128 k, + 128) of the candidate list
+  const int per = CH / MFMA_TILE, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  if (int64_t(lc) * CH >= s.N) return;
   const int units = L * Hkv;
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -638,6 +638,14 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const int32_t *S = slot_maps + s.slot_off;
   const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  const int32_t *lst = reinterpret_cast<const int32_t *>(base + z.off_clist()) + lc * CH + lk * MFMA_TILE;
+  const int cnt = reinterpret_cast<const int32_t *>(base + z.off_ccount(s.N))[lc];
+  const int ne = min(MFMA_TILE, cnt - lk * MFMA_TILE);
+  if (ne <= 0) return;
+  // a chunk whose every position is a candidate is its own list: entry e is position e0 + e
+  const bool ident = cnt == min(CH, s.N - lc * CH);
+  const int e0 = lc * CH + lk * MFMA_TILE;
+  auto pos_of = [&](int e) __attribute__((always_inline)) { return ident ? e0 + e : lst[e]; };
 
   if (w >= 4) {
     // ---------------- producers: the ring's loads, and the mean key row
@@ -649,8 +657,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int tok = (8 * pw + k) * 4 + (lane >> 4);
-      const int j = j0 + tok;
-      const int slot = j < s.N ? S[j] : dead;      // past the end: any valid row
+      const int slot = tok < ne ? S[pos_of(tok)] : dead;   // past the list: any valid row
       src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
     }
     asm volatile("" ::"v"(src[0]), "v"(src[7]));   // the slot loads are complete before the first DMA
@@ -774,9 +781,9 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       // producer pw stores positions 32 pw .. + 31: two rows (32 lanes x 16 B each) per instruction
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const int pr = 32 * pw + 2 * q + (lane >> 5), j = j0 + pr;
+        const int pr = 32 * pw + 2 * q + (lane >> 5);
         const float4 v = *reinterpret_cast<const float4 *>(kt + pr * KT_ROW + 4 * (lane & 31));
-        if (j < s.N) reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(j) * MD)[lane & 31] = v;
+        if (pr < ne) reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(pos_of(pr)) * MD)[lane & 31] = v;
       }
     }
     return;
@@ -898,13 +905,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       if (r16 == 0) red[rh * MFMA_TILE + p0 + blk * 16 + 4 * g + i] = v;
     }
   __syncthreads();
-  if (t < MFMA_TILE) {
-    const int j = j0 + t;
-    if (j < s.N) {
-      const bool c = S[j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
-      scores[s.slot_off + j] = c ? red[t] + red[MFMA_TILE + t] : -INFINITY;
-    }
-  }
+  if (t < ne) scores[s.slot_off + pos_of(t)] = red[t] + red[MFMA_TILE + t];   // every list entry is a candidate
 }
 
 // ------------------------------------------------------------------ first pass, unit-major (R <= 64, even Hkv)
@@ -975,7 +976,12 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
       for (int j = c0 + int(threadIdx.x); j < min(s.N, c0 + CH); j += ST_THREADS) scores[s.slot_off + j] = -INFINITY;
     return;
   }
-  const int npos = min(CH, s.N - c0);
+  // the chunk's entries: its candidates from the list (MASS: every position of the chunk)
+  const ScoreSizes z0 = score_sizes(s, L, L * Hkv, MD, resid, true);
+  const float *wsb = ws + score_offset(sess, b, L, L * Hkv, MD, resid, true);
+  const int32_t *lst = reinterpret_cast<const int32_t *>(wsb + z0.off_clist());
+  const int npos = MASS ? min(CH, s.N - c0) : reinterpret_cast<const int32_t *>(wsb + z0.off_ccount(s.N))[chunk];
+  const bool ident = MASS || npos == min(CH, s.N - c0);   // every position a candidate: its own list
   const int T = int(cdiv(npos, ST_TILE));
   const int l = hp / (Hkv / 2), h0 = 2 * (hp - l * (Hkv / 2));
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -994,7 +1000,10 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   // the chunk's key offsets (dead slot past the end) and candidate biases
   int32_t sv[ST_CHMAX / ST_THREADS];
 #pragma unroll
-  for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) sv[k] = S[c0 + min(t + k * ST_THREADS, npos - 1)];
+  for (int k = 0; k < ST_CHMAX / ST_THREADS; ++k) {
+    const int p = t + k * ST_THREADS;
+    sv[k] = p < npos ? S[ident ? c0 + p : lst[c0 + p]] : dead;
+  }
   // memory rows of this wave as B-operand fragments: lane (g, r16) holds row r0 + 16 rb + r16
   // (the last row stands in for rows past R, whose results are never stored), channels
   // (4 ks + g) * 8 .. + 8 of M * log2(e) / sqrt(D), split into bf16 hi + lo (both rounded
@@ -1048,7 +1057,8 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
     const int p = t + k * ST_THREADS, j = c0 + p;
     const bool in = p < npos;
     const int slot = in ? sv[k] : dead;
-    const bool cand = in && slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+    // list entries are candidates; the mass pass walks positions and tests them
+    const bool cand = in && (!MASS || (slot != dead && !(j < s.pi || (j >= s.qs && j < s.qe))));
     koff[p] = uint32_t(slot) * slot_bytes;
     bias[p] = cand ? 0.f : -INFINITY;
   }
@@ -1227,13 +1237,6 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
   }
 }
 
-// Positions per chunk of the unit-major first pass: about nine rounds of two
-// workgroups per CU at the largest sizes, whole 64-position multiples.
-inline int stats_chunk(int maxN, int head_pairs) {
-  const int64_t c = cdiv(cdiv(int64_t(maxN) * head_pairs, 4608), 64) * 64;
-  return int(std::min<int64_t>(std::max<int64_t>(c, 64), 1024));
-}
-
 // Per (unit, row): combine the per-tile statistics into (max, 1/Z), log2 domain.
 // A workgroup takes 64 consecutive rows; its eight waves split the tiles (lane =
 // row, so each load instruction reads 512 contiguous bytes), fold them online into
@@ -1317,6 +1320,46 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   }
 }
 
+// The candidate list of each session for the MFMA passes: chunk c (CH positions)
+// keeps its candidates in position order at clist[c CH ...] and their count at
+// ccount[c]; every other position's score is -inf (all of them for a session at or
+// under its budget, whose counts are zero). One workgroup per (chunk, session); the
+// order within a chunk comes from wave ballots and a prefix over the waves.
+constexpr int CLIST_THREADS = 1024;              // a whole chunk (at most 1024 positions) per round
+
+__global__ void __launch_bounds__(CLIST_THREADS) k_cand_list(const ikv_session *__restrict__ sess,
+                                                             const int32_t *__restrict__ slot_maps, int dead,
+                                                             float *__restrict__ ws, float *__restrict__ scores,
+                                                             int L, int Hkv, bool resid, int CH) {
+  __shared__ int wsum[CLIST_THREADS / WAVE];
+  const int b = blockIdx.y, c = blockIdx.x;
+  const ikv_session s = sess[b];
+  const int c0 = c * CH;
+  if (c0 >= s.N) return;
+  const int units = L * Hkv;
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  int32_t *lst = reinterpret_cast<int32_t *>(base + z.off_clist()) + c0;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const bool gated = s.N <= s.C;
+  int count = 0;
+  for (int r = 0; r < CH; r += CLIST_THREADS) {
+    const int j = c0 + r + t;
+    const bool in = r + t < CH && j < s.N;         // a round may reach past a 128-position chunk
+    const bool cand = in && !gated && slot_maps[s.slot_off + j] != dead && !(j < s.pi || (j >= s.qs && j < s.qe));
+    if (in && !cand) scores[s.slot_off + j] = -INFINITY;
+    const uint64_t m = __ballot(cand);
+    if (lane == 0) wsum[w] = __popcll(m);
+    __syncthreads();
+    int off = count;
+    for (int q = 0; q < w; ++q) off += wsum[q];
+    if (cand) lst[off + __popcll(m & ((uint64_t(1) << lane) - 1))] = j;
+    for (int q = 0; q < CLIST_THREADS / WAVE; ++q) count += wsum[q];
+    __syncthreads();
+  }
+  if (t == 0) reinterpret_cast<int32_t *>(base + z.off_ccount(s.N))[c] = count;
+}
+
 // The SnapKV-style score: for each candidate j, the sum over units u of the largest
 // attention mass among positions j - 3 .. j + 3 of unit u (a max pool of 7 positions,
 // positions outside [0, N) left out; non-candidates hold zero mass). A workgroup owns 64
@@ -1368,12 +1411,21 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   const uint16_t *kp = static_cast<const uint16_t *>(p.k_pool);
   const bool ring = a.maxR <= 64;
   const bool stats = a.stats;                      // the unit-major pass splits the memory rows itself
+  // the candidate lists (and -inf for every other position)
+  const int lch = stats_chunk(a.maxN, std::max(1, units / 2));
+  {
+    KTimer kt_("k_cand_list", st);
+    k_cand_list<<<dim3(unsigned(cdiv(a.maxN, lch)), a.B), CLIST_THREADS, 0, st>>>(a.sess_dev, a.slot_maps,
+                                                                                  p.dead_slot, a.ws, a.scores, p.L,
+                                                                                  p.Hkv, resid, lch);
+  }
+  const unsigned ltiles = unsigned(cdiv(a.maxN, lch) * (lch / MFMA_TILE));
   if (!stats)
     {
       KTimer kt_("k_msplit", st);
       k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, a.scores, p.L, p.Hkv, resid);
     }
-  const int chunk = stats ? stats_chunk(a.maxN, units / 2) : 0;
+  const int chunk = stats ? lch : 0;
   if (stats)
     {
       KTimer kt_("k_score_stats", st);
@@ -1446,25 +1498,25 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     {
       KTimer kt_("k_score_ws<true>", st);
       if (ws_small)
-        k_score_ws<true, 1><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+        k_score_ws<true, 1><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
                                                                     a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
-                                                                    ws_large ? 1 : 0);
+                                                                    ws_large ? 1 : 0, lch);
       if (ws_large)
-        k_score_ws<true, 2><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+        k_score_ws<true, 2><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
                                                                     a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
-                                                                    ws_small ? 2 : 0);
+                                                                    ws_small ? 2 : 0, lch);
     }
   else if (a.maxR <= 128)
     {
       KTimer kt_("k_score_ws<false>", st);
       if (ws_small)
-        k_score_ws<false, 1><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+        k_score_ws<false, 1><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
                                                                      a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
-                                                                     ws_large ? 1 : 0);
+                                                                     ws_large ? 1 : 0, lch);
       if (ws_large)
-        k_score_ws<false, 2><<<dim3(tiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
+        k_score_ws<false, 2><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot,
                                                                      a.sess_dev, a.slot_maps, a.ws, a.scores, resid,
-                                                                     ws_small ? 2 : 0);
+                                                                     ws_small ? 2 : 0, lch);
     }
   else if (resid)
     {
