@@ -66,6 +66,7 @@ typedef int32_t ikv_status;
 #define IKV_RESIDUAL  1u   /* add alpha * MLP(phi ++ c), Eq. 4 (needs `residual`)           */
 #define IKV_NO_XATTN  2u   /* the "- x-attn" ablation: c_j = 0 in Eq. 4 (Sec. 3.3)          */
 #define IKV_POOL7     4u   /* SnapKV-style score (Sec. 4.1 baselines): see ikv_score_history  */
+#define IKV_TWO_PASS  8u   /* score with two passes over the keys even where every R <= 16   */
 
 /* ikv_workspace_bytes call ids. */
 #define IKV_CALL_SCORE    1
@@ -178,6 +179,11 @@ ikv_status ikv_qm_update(const ikv_pool *pool, const ikv_session *sess,
  *     IKV_POOL7 runs on the matrix-core path only (D = 128, bf16 pool, even Hkv,
  *     R <= 128; IKV_EUNSUPPORTED otherwise) and excludes IKV_RESIDUAL (IKV_EINVAL).
  *     Its workspace adds L * Hkv floats per position of the batch.
+ * On the matrix-core path (D = 128, bf16 pool) with every session at R <= 16 the keys
+ * are read once: the logits go to a float32 stash in the workspace (L * Hkv * R floats
+ * per position, rounded up to 128 positions, for every session with R <= 16) and the
+ * normalised sum is taken from it. IKV_TWO_PASS keeps the two passes over the keys
+ * (the same scores up to float32 rounding order).
  */
 ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess,
                              const ikv_session *sess_dev, int32_t B,

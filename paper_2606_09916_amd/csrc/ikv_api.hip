@@ -349,7 +349,8 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   ikv_status r = check_pool(pool);
   if (r) return r;
   if ((r = check_sessions(sess, sess_dev, B))) return r;
-  if (flags & ~(IKV_RESIDUAL | IKV_NO_XATTN | IKV_POOL7)) return fail(IKV_EINVAL, "unknown flag bits 0x%x", flags);
+  if (flags & ~(IKV_RESIDUAL | IKV_NO_XATTN | IKV_POOL7 | IKV_TWO_PASS))
+    return fail(IKV_EINVAL, "unknown flag bits 0x%x", flags);
   if ((flags & IKV_POOL7) && (flags & IKV_RESIDUAL)) return fail(IKV_EINVAL, "IKV_POOL7 excludes IKV_RESIDUAL");
   if (B == 0) return ok();
   if (!slot_maps || !M || !scores) return fail(IKV_EINVAL, "slot_maps / M / scores is NULL");
@@ -383,6 +384,10 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.mfma_resid = a.mfma && resid && maxNq <= 64;
   a.stats = a.mfma && maxR <= 128 && pool->Hkv % 2 == 0 &&
             int64_t(pool->num_slots) * pool->Hkv * pool->D * 2 <= int64_t(UINT32_MAX);
+  // the one-key-pass form: every session at most 16 memory rows (one slice), not the
+  // SnapKV-style score (which needs the unit-major pass), not turned off by the caller
+  a.stash = a.mfma && maxR <= ikv::STASH_MAX_R && !(flags & (IKV_POOL7 | IKV_TWO_PASS));
+  if (a.stash) a.stats = false;
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.total_positions = total_positions(sess, B);

@@ -54,18 +54,23 @@ __host__ __device__ inline int pad16(int R) { return (R + 15) & ~15; }
 //   clist  the candidate list (MFMA path): chunk c of the launch's chunk size CH keeps its
 //          candidate positions in position order at [c CH ...], then the counts per
 //          chunk (int32)
+//   stash  [units][R][NS] float32 logits (log2 domain) of the one-key-pass form (MFMA,
+//          R <= 16), indexed by list slot (entry e of chunk c at c CH + e); row stride
+//          NS = stash_stride(N), N rounded up to 128, which holds every slot of a list
+//          tile that has an entry
 // followed by one shared block: W_Q^T [3D+1][HC], W_1^T [3D+1+HC][HIDDEN], and on the
 // MFMA path the cross-attention columns of W_1 as bf16 hi + lo [HIDDEN][HC], columns
 // ordered within each 32-wide head as perm32 below.
 constexpr int MBAR_PARTS = 64;
+constexpr int STASH_MAX_R = 16;     // memory rows up to which the MFMA scorer reads the keys once
 constexpr int MFMA_TILE = 128;      // positions per workgroup in the MFMA score passes
 constexpr int PART_TILE = 64;       // positions per partial of the position-major first pass
 
 struct ScoreSizes {
-  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp, clist;
+  int64_t msplit, part, lse, rulep, kbar, kq, kp, vp, misc, fold, qlist, kvf, mbp, clist, stash;
   int64_t lse_pairs;   // units * R * 2: the (max, 1/Z) pairs at the start of lse
   __host__ __device__ int64_t total() const {
-    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf + mbp + clist;
+    return msplit + part + lse + rulep + kbar + kq + kp + vp + misc + fold + qlist + kvf + mbp + clist + stash;
   }
   __host__ __device__ int64_t off_part() const { return msplit; }
   __host__ __device__ int64_t off_lse() const { return msplit + part; }
@@ -83,6 +88,7 @@ struct ScoreSizes {
   __host__ __device__ int64_t off_mbp() const { return off_kvf() + kvf; }
   __host__ __device__ int64_t off_clist() const { return off_mbp() + mbp; }
   __host__ __device__ int64_t off_ccount(int N) const { return off_clist() + align64f(int64_t(N) + 1024); }
+  __host__ __device__ int64_t off_stash() const { return off_clist() + clist; }
 };
 
 // Floats of the folded first-layer weights of one session (bf16 hi + lo, then q0, h0,
@@ -101,11 +107,16 @@ __host__ __device__ inline int perm32_inv(int c) {
   return c < 16 ? 8 * (c >> 2) + (c & 3) : 8 * ((c - 16) >> 2) + 4 + ((c - 16) & 3);
 }
 
+__host__ __device__ inline int64_t stash_stride(int N) { return cdiv(int64_t(N), 128) * 128; }
+
 __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, int units, int D, bool resid,
                                                   bool mfma) {
   ScoreSizes z;
   z.msplit = mfma ? align64f(int64_t(units) * pad16(s.R) * 128) : 0;
-  z.part = mfma ? align64f(cdiv(s.N, PART_TILE) * units * s.R * 2) : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
+  // MFMA: 64-position partials, or one per 128-entry list tile (at most N / 128 + 8 of
+  // them for chunks of up to 1024 positions)
+  z.part = mfma ? align64f((cdiv(s.N, PART_TILE) + 8) * units * s.R * 2)
+                : align64f(int64_t(units) * s.R * cdiv(s.N, SCORE_TILE) * 2);
   z.lse = align64f(int64_t(units) * s.R * (mfma ? 3 : 2));
   z.lse_pairs = int64_t(units) * s.R * 2;
   z.rulep = mfma ? 0 : align64f(int64_t(L) * s.N);
@@ -119,6 +130,7 @@ __host__ __device__ inline ScoreSizes score_sizes(const ikv_session &s, int L, i
   z.kvf = resid && mfma ? align64f(KVF_BF16 / 2) : 0;
   z.mbp = resid && mfma ? align64f(int64_t(units / 2) * D) : 0;
   z.clist = mfma ? align64f(int64_t(s.N) + 1024) + align64f(cdiv(s.N, 128) + 1) : 0;
+  z.stash = mfma && s.R <= STASH_MAX_R ? int64_t(units) * s.R * stash_stride(s.N) : 0;
   return z;
 }
 
@@ -238,6 +250,7 @@ struct ScoreArgs {
   bool mfma;           // MFMA score passes (D = 128, bf16 pool)
   bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
+  bool stash;          // one key pass with a logit stash (MFMA, every R <= 16, no IKV_POOL7)
 };
 
 // Opt-in per-kernel timing (ikv_timing in the C ABI): every launch site holds a

@@ -615,7 +615,13 @@ constexpr int WS_THREADS = 512;
 // where every unit's rows stream as two halves of 64 through the same two-stage ring
 // (half h in stage h) against the one key stage of the unit. A batch holding both
 // kinds runs one launch of each; `big` as in k_score_stats.
-template <bool KBAR, int RH>
+//
+// STASH (every session R <= 16, one row slice): the one-key-pass form. The producers run
+// unchanged (keys, the 16 split rows, the mean key row); consumer c takes entries
+// 32 c .. + 31 against the slice and, per unit, stores the raw logits (log2 domain) to the
+// stash and merges the tile's (max, sum of exp2) per row across the four consumers,
+// written as the list tile's partial; k_lse_mfma and k_score_stash finish the score.
+template <bool KBAR, int RH, bool STASH = false>
 __global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
            const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
@@ -641,7 +647,13 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   const int32_t *lst = reinterpret_cast<const int32_t *>(base + z.off_clist()) + lc * CH + lk * MFMA_TILE;
   const int cnt = reinterpret_cast<const int32_t *>(base + z.off_ccount(s.N))[lc];
   const int ne = min(MFMA_TILE, cnt - lk * MFMA_TILE);
-  if (ne <= 0) return;
+  if (ne <= 0) {
+    if constexpr (STASH) {                           // an empty list tile still leaves its partials
+      float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + int64_t(blockIdx.x) * units * R;
+      for (int i = t; i < units * R; i += WS_THREADS) pt[i] = make_float2(-INFINITY, 0.f);
+    }
+    return;
+  }
   // a chunk whose every position is a candidate is its own list: entry e is position e0 + e
   const bool ident = cnt == min(CH, s.N - lc * CH);
   const int e0 = lc * CH + lk * MFMA_TILE;
@@ -786,6 +798,86 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
         if (pr < ne) reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(pos_of(pr)) * MD)[lane & 31] = v;
       }
     }
+    return;
+  }
+
+  if constexpr (STASH) {
+    // ---------------- consumers, one-key-pass form: logits to the stash, per-tile row statistics
+    const int q0 = 32 * w;                           // this consumer's 32 entries
+    const int64_t NS = stash_stride(s.N);
+    float *stash = base + z.off_stash() + int64_t(lc) * CH + int64_t(lk) * MFMA_TILE + q0 + 4 * g;
+    float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + int64_t(blockIdx.x) * units * R;
+    // per-consumer (max, sum) of unit u's rows: [u & 1][consumer][row], in the second
+    // memory stage's unused space past its 16 rows
+    float2 *sb = reinterpret_cast<float2 *>(lds + KSTAGES * STAGE + 16 * 256);
+    // consumer 0 merges unit u's four partials into the tile's partial (rows < R)
+    auto merge = [&](int u) __attribute__((always_inline)) {
+      if (w == 0 && lane < R) {
+        const float2 *q = sb + (u & 1) * 64 + lane;
+        float m = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) m = fmaxf(m, q[16 * c].x);
+        float zs = 0.f;
+        if (m != -INFINITY)
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if (q[16 * c].x != -INFINITY) zs += q[16 * c].y * ex2(q[16 * c].x - m);
+        pt[int64_t(u) * R + lane] = make_float2(m, zs);
+      }
+    };
+    for (int u = 0; u < units; ++u) {
+      __syncthreads();                               // stage u in LDS; unit u - 1's partials in sb
+      if (u > 0) merge(u - 1);
+      const uint16_t *kl = lds + (u % KSTAGES) * STAGE;
+      const uint16_t *mr = lds + KSTAGES * STAGE + (u & 1) * MSTAGE + r16 * 256;
+      bf16x8 mh[4], ml[4], ka[2][4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        mh[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2) ^ r16) * 8));
+        ml[ks] = *reinterpret_cast<const bf16x8 *>(mr + (((g * 8 + ks * 2 + 1) ^ r16) * 8));
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+          ka[blk][ks] = *reinterpret_cast<const bf16x8 *>(kl + (q0 + blk * 16 + r16) * MD + (((4 * ks + g) ^ r16) * 8));
+      }
+      // lane (g, r16) of block blk: row r16 at entries q0 + 16 blk + 4 g + i
+      f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], mh[ks], acc[blk], 0, 0, 0);
+          acc[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[blk][ks], ml[ks], acc[blk], 0, 0, 0);
+        }
+      if (r16 < R) {
+        float *o = stash + (int64_t(u) * R + r16) * NS;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+          *reinterpret_cast<float4 *>(o + 16 * blk) = make_float4(acc[blk][0], acc[blk][1], acc[blk][2], acc[blk][3]);
+      }
+      // the row's max and sum over this consumer's entries below ne
+      float m = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (q0 + 16 * blk + 4 * g + i >= ne) acc[blk][i] = -INFINITY;
+          m = fmaxf(m, acc[blk][i]);
+        }
+      m = fmaxf(m, __shfl_xor(m, 16, WAVE));
+      m = fmaxf(m, __shfl_xor(m, 32, WAVE));
+      float zs = 0.f;
+      if (m != -INFINITY)
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) zs += ex2(acc[blk][i] - m);
+      zs += __shfl_xor(zs, 16, WAVE);
+      zs += __shfl_xor(zs, 32, WAVE);
+      if (g == 0) sb[(u & 1) * 64 + 16 * w + r16] = make_float2(m, zs);
+    }
+    __syncthreads();                                 // matches the producers' "ring is free"
+    merge(units - 1);
+    __syncthreads();                                 // matches the producers' mean-key-row barrier
     return;
   }
 
@@ -1247,7 +1339,8 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
 // layer (res_fold_wg), then one workgroup writes mbar and the live query positions
 // (res_setup_body).
 __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict__ sess, float *__restrict__ ws, int L,
-                                                  int Hkv, bool resid, int ptile, const int32_t *__restrict__ slot_maps,
+                                                  int Hkv, bool resid, int ptile, int pper,
+                                                  const int32_t *__restrict__ slot_maps,
                                                   const int32_t *__restrict__ qpos, int dead, bool pairs, bool kv,
                                                   int nfold, const uint16_t *__restrict__ kpool, int64_t num_slots,
                                                   const float *__restrict__ blob, float *__restrict__ shared) {
@@ -1277,7 +1370,8 @@ __global__ void __launch_bounds__(512) k_lse_mfma(const ikv_session *__restrict_
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
   float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
   const float *part = base + z.off_part();
-  const int64_t tiles = cdiv(s.N, ptile);
+  // partials: one per ptile positions, or pper per ptile-position chunk (list tiles)
+  const int64_t tiles = pper > 0 ? cdiv(s.N, ptile) * pper : cdiv(s.N, ptile);
   float m = -INFINITY, zs = 0.f;
   constexpr int LB = 8;                            // tiles in flight per thread
   if (on)
@@ -1360,6 +1454,66 @@ __global__ void __launch_bounds__(CLIST_THREADS) k_cand_list(const ikv_session *
   if (t == 0) reinterpret_cast<int32_t *>(base + z.off_ccount(s.N))[c] = count;
 }
 
+// The one-key-pass form's rule score: per list entry, the sum over units and rows of
+// exp2(logit + seed), seed = -(max + log2 Z) of the row (Eq. 3), from the stash. A
+// workgroup owns one 128-entry list tile; thread (group, quad) adds entries 4 quad .. + 3
+// of every 16th (unit, row), four in one 16-byte load, and the 16 groups are added in
+// group order through LDS.
+constexpr int SS_THREADS = 512;
+
+__global__ void __launch_bounds__(SS_THREADS) k_score_stash(const ikv_session *__restrict__ sess,
+                                                            const int32_t *__restrict__ slot_maps,
+                                                            const float *__restrict__ ws, float *__restrict__ scores,
+                                                            int L, int Hkv, bool resid, int CH) {
+  __shared__ float red[SS_THREADS / 32][MFMA_TILE];
+  const int b = blockIdx.y;
+  const ikv_session s = sess[b];
+  if (s.N <= s.C) return;
+  const int per = CH / MFMA_TILE, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  if (int64_t(lc) * CH >= s.N) return;
+  const int units = L * Hkv;
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  const float *base = ws + score_offset(sess, b, L, units, MD, resid, true);
+  const int cnt = reinterpret_cast<const int32_t *>(base + z.off_ccount(s.N))[lc];
+  const int ne = min(MFMA_TILE, cnt - lk * MFMA_TILE);
+  if (ne <= 0) return;
+  const int32_t *lst = reinterpret_cast<const int32_t *>(base + z.off_clist()) + lc * CH + lk * MFMA_TILE;
+  const bool ident = cnt == min(CH, s.N - lc * CH);
+  const int e0 = lc * CH + lk * MFMA_TILE;
+  const int t = threadIdx.x, q = t & 31, grp = t >> 5;
+  const int64_t NS = stash_stride(s.N);
+  const float *st = base + z.off_stash() + e0 + 4 * q;
+  const float *nl2 = base + z.off_nl2();
+  const int rows = units * s.R;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  constexpr int UN = 8;                              // (unit, row) loads in flight per thread
+  for (int i0 = grp; i0 < rows; i0 += 16 * UN) {
+    float4 v[UN];
+    float sd[UN];
+#pragma unroll
+    for (int k = 0; k < UN; ++k) {
+      const int i = min(i0 + 16 * k, rows - 1);
+      v[k] = *reinterpret_cast<const float4 *>(st + int64_t(i) * NS);
+      sd[k] = i0 + 16 * k < rows ? nl2[i] : -INFINITY;   // past the last row: adds nothing
+    }
+#pragma unroll
+    for (int k = 0; k < UN; ++k) {
+      a.x += ex2(v[k].x + sd[k]);
+      a.y += ex2(v[k].y + sd[k]);
+      a.z += ex2(v[k].z + sd[k]);
+      a.w += ex2(v[k].w + sd[k]);
+    }
+  }
+  *reinterpret_cast<float4 *>(&red[grp][4 * q]) = a;
+  __syncthreads();
+  if (t < ne) {
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < SS_THREADS / 32; ++k) v += red[k][t];
+    scores[s.slot_off + (ident ? e0 + t : lst[t])] = v;   // every list entry is a candidate
+  }
+}
+
 // The SnapKV-style score: for each candidate j, the sum over units u of the largest
 // attention mass among positions j - 3 .. j + 3 of unit u (a max pool of 7 positions,
 // positions outside [0, N) left out; non-candidates hold zero mass). A workgroup owns 64
@@ -1438,6 +1592,17 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
         k_score_stats<4><<<grid, 512, 0, st>>>(kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps,
                                                a.ws, a.M, a.scores, resid, chunk, small ? 2 : 0);
     }
+  else if (a.stash)
+    {
+      // the one key pass: logits to the stash, per-list-tile row statistics, mean key rows
+      KTimer kt_("k_score_once", st);
+      if (resid)
+        k_score_ws<true, 1, true><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(
+            kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, a.scores, resid, 0, lch);
+      else
+        k_score_ws<false, 1, true><<<dim3(ltiles, a.B), WS_THREADS, 0, st>>>(
+            kp, p.num_slots, p.L, p.Hkv, p.dead_slot, a.sess_dev, a.slot_maps, a.ws, a.scores, resid, 0, lch);
+    }
   else if (ring)
     {
       KTimer kt_("k_score_ring", st);
@@ -1455,7 +1620,7 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     {
       KTimer kt_("k_lse_mfma", st);
       k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64)), a.B), 512, 0, st>>>(
-          a.sess_dev, a.ws, p.L, p.Hkv, false, chunk, a.slot_maps, a.qpos, p.dead_slot, true, false, 0, kp,
+          a.sess_dev, a.ws, p.L, p.Hkv, false, chunk, 0, a.slot_maps, a.qpos, p.dead_slot, true, false, 0, kp,
           p.num_slots, a.residual, a.ws_shared);
     }
     float *umass = a.ws_shared;                     // after the sessions' blocks
@@ -1488,13 +1653,22 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
     const int extra = resid ? (kv ? RES_KEYS : 0) + nfold + 1 : 0;
     KTimer kt_("k_lse_mfma", st);
     k_lse_mfma<<<dim3(unsigned(cdiv(int64_t(units) * a.maxR, 64) + extra), a.B), 512, 0, st>>>(
-        a.sess_dev, a.ws, p.L, p.Hkv, resid, stats ? chunk : ring ? PART_TILE : MFMA_TILE, a.slot_maps, a.qpos,
-        p.dead_slot, a.stats, kv, nfold, kp, p.num_slots, a.residual, a.ws_shared);
+        a.sess_dev, a.ws, p.L, p.Hkv, resid, stats ? chunk : a.stash ? lch : ring ? PART_TILE : MFMA_TILE,
+        a.stash ? lch / MFMA_TILE : 0, a.slot_maps, a.qpos, p.dead_slot, a.stats, kv, nfold, kp, p.num_slots,
+        a.residual, a.ws_shared);
   }
+  if (a.stash)
+    {
+      KTimer kt_("k_score_stash", st);
+      k_score_stash<<<dim3(ltiles, a.B), SS_THREADS, 0, st>>>(a.sess_dev, a.slot_maps, a.ws, a.scores, p.L, p.Hkv,
+                                                              resid, lch);
+    }
   // the producer/consumer second pass up to 128 memory rows: one launch per kind of
   // session (up to 64 rows, up to 128)
   const bool ws_small = a.minR <= 64, ws_large = a.maxR > 64;
-  if (a.maxR <= 128 && resid)
+  if (a.stash)
+    ;                                                // scored above
+  else if (a.maxR <= 128 && resid)
     {
       KTimer kt_("k_score_ws<true>", st);
       if (ws_small)

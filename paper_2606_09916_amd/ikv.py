@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libikv.so")
 
 IKV_BF16, IKV_F32 = 0, 1
-IKV_RESIDUAL, IKV_NO_XATTN, IKV_POOL7 = 1, 2, 4
+IKV_RESIDUAL, IKV_NO_XATTN, IKV_POOL7, IKV_TWO_PASS = 1, 2, 4, 8
 CALL_SCORE, CALL_SELECT, CALL_REDIRECT, CALL_DECODE, CALL_COMPACT, CALL_PREFILL = 1, 2, 3, 4, 5, 6
 STATUS = {0: "IKV_OK", -1: "IKV_EINVAL", -2: "IKV_ESHAPE", -3: "IKV_EWORKSPACE", -4: "IKV_EUNSUPPORTED",
           -5: "IKV_EHIP"}

@@ -1,6 +1,12 @@
 """Comparison rules between the HIP path and the float64 oracle.
 
-* scores: |s_gpu - s_o| <= 1e-3 |s_o| + 1e-6 max|s_o| on candidates, -inf elsewhere;
+* scores: |s_gpu - s_o| <= 1e-3 |s_o| + f max|s_o| on candidates, -inf elsewhere, with
+  the floor f = 1e-6 for float32 arithmetic (the rule path, and the residual head on the
+  vector units); with the residual head on the matrix cores f = 1e-5: its products take
+  each float32 operand as a bf16 hi + lo pair, about 2^-18 relative, so a score carries
+  an absolute error set by the size of the head's terms rather than by the score, which
+  the residual can bring near zero (measured up to 3.5e-6 max|s_o| with one layer pair
+  and one KV head, where the mean key rows are largest);
 * kept sets: identical except at positions whose oracle score lies within
   1e-5 |tau_o| of the oracle threshold tau_o; the kept counts are identical;
 * attention outputs: |o_gpu - o_o| <= 2e-3 plus half a bf16 ulp of o_o for bf16
@@ -12,17 +18,18 @@ import numpy as np
 
 SCORE_RTOL = 1e-3
 SCORE_FLOOR = 1e-6
+RESID_MFMA_FLOOR = 1e-5
 BAND = 1e-5
 ATTN_ATOL = 2e-3
 
 
-def check_scores(s_gpu, s_o, cand):
+def check_scores(s_gpu, s_o, cand, floor=SCORE_FLOOR):
     s_gpu = np.asarray(s_gpu, np.float64)
     assert np.all(np.isneginf(s_gpu[~cand])), "non-candidates must score -inf"
     if not cand.any():
         return 0.0
     a, o = s_gpu[cand], s_o[cand]
-    tol = SCORE_RTOL * np.abs(o) + SCORE_FLOOR * np.abs(o).max()
+    tol = SCORE_RTOL * np.abs(o) + floor * np.abs(o).max()
     err = np.abs(a - o)
     bad = np.nonzero(err > tol)[0]
     assert len(bad) == 0, f"{len(bad)} scores out of tolerance, worst {err.max():.3e}"
@@ -83,14 +90,15 @@ def oracle_scores_pair(k_pool, S, st, M, Hkv, R, blob, qpos, dead):
     return full, nox
 
 
-def check_xattn_visible(full, nox, st, factor=10.0):
+def check_xattn_visible(full, nox, st, factor=10.0, floor=RESID_MFMA_FLOOR):
     """The cross-attention term of Eq. 6 must matter at this size: dropping it moves some
-    score by more than `factor` times the score tolerance and changes the kept set. A
-    kernel that dropped or garbled the term would then fail the score comparison."""
+    score by more than `factor` times the score tolerance (the one the scores are checked
+    with) and changes the kept set. A kernel that dropped or garbled the term would then
+    fail the score comparison."""
     import oracle
     c = st["cand"]
     a, b = full[c], nox[c]
-    tol = SCORE_RTOL * np.abs(a) + SCORE_FLOOR * np.abs(a).max()
+    tol = SCORE_RTOL * np.abs(a) + floor * np.abs(a).max()
     ratio = float((np.abs(a - b) / tol).max())
     assert ratio > factor, f"cross-attention moves scores by only {ratio:.1f}x the tolerance"
     k1 = oracle.select_budget(full, st)[0]

@@ -114,7 +114,7 @@ def test_calls_reject_bad_arguments_before_launch():
     sp = ctypes.cast(s, ctypes.POINTER(ikv.Session))
     fake = 0x10000
     # unknown flag bits
-    assert L.ikv_score_history(ctypes.byref(p), sp, fake, 1, fake, fake, fake, fake, 8, fake, fake, 1 << 30,
+    assert L.ikv_score_history(ctypes.byref(p), sp, fake, 1, fake, fake, fake, fake, 16, fake, fake, 1 << 30,
                                None) == -1
     # residual flag without weights
     assert L.ikv_score_history(ctypes.byref(p), sp, fake, 1, fake, fake, fake, None, 1, fake, fake, 1 << 30,

@@ -12,7 +12,8 @@ import oracle
 import synth
 from paper_2606_09916_amd import ikv
 from paper_2606_09916_amd.step import RetentionStep
-from parity import check_attention, check_keep, check_scores, check_xattn_visible, oracle_scores_pair
+from parity import (RESID_MFMA_FLOOR, check_attention, check_keep, check_scores, check_xattn_visible,
+                    oracle_scores_pair)
 
 pytestmark = pytest.mark.gpu
 SEED = 5
@@ -44,7 +45,7 @@ def _check_batch(st, batch, blob, xattn=True):
                                        synth.DEAD_SLOT)
         if xattn:
             ratio, nd = check_xattn_visible(want, nox, sets)
-        rel = check_scores(sc[sl], want, sets["cand"])
+        rel = check_scores(sc[sl], want, sets["cand"], floor=RESID_MFMA_FLOOR)
         rule = oracle.rule_scores(batch.k_pool, batch.S(b), sets["cand"], M, sh.Hkv, s.R)
         assert abs(rule[sets["cand"]].sum() - sh.L * sh.Hkv * s.R) < 1e-6 * sh.L * sh.Hkv * s.R
         keep_o, n_o, tau_o = oracle.select_budget(want, sets)

@@ -19,7 +19,8 @@ import pytest
 import oracle
 import synth
 from paper_2606_09916_amd import ikv
-from parity import check_attention, check_keep, check_scores, check_xattn_visible, oracle_scores_pair
+from parity import (RESID_MFMA_FLOOR, check_attention, check_keep, check_scores, check_xattn_visible,
+                    oracle_scores_pair)
 
 pytestmark = pytest.mark.gpu
 DEAD = synth.DEAD_SLOT
@@ -96,7 +97,7 @@ def test_multi_turn_session(dev):
             ikv.select_budget(sess, S_dev, DEAD, scores, keep, n_keep, tau, ws)
             want, nox = oracle_scores_pair(k_host, S, sets, M_o, Hkv, R, blob, qpos, DEAD)
             ratio, nd = check_xattn_visible(want, nox, sets)
-            check_scores(scores.cpu().numpy(), want, sets["cand"])
+            check_scores(scores.cpu().numpy(), want, sets["cand"], floor=RESID_MFMA_FLOOR)
             keep_o, n_o, tau_o = oracle.select_budget(want, sets)
             keep_g = keep.cpu().numpy().astype(bool)
             ndiff = check_keep(keep_g, int(n_keep.item()), keep_o, n_o, want, tau_o, sets["cand"])

@@ -14,8 +14,8 @@ import oracle
 import synth
 from paper_2606_09916_amd import ikv
 from paper_2606_09916_amd.step import RetentionStep
-from parity import (band_positions, check_attention, check_decode_on, check_keep, check_scores, check_xattn_visible,
-                    oracle_scores_pair)
+from parity import (RESID_MFMA_FLOOR, SCORE_FLOOR, band_positions, check_attention, check_decode_on, check_keep,
+                    check_scores, check_xattn_visible, oracle_scores_pair)
 
 pytestmark = pytest.mark.gpu
 
@@ -139,7 +139,7 @@ def test_scores_d128_odd_kv_heads(dev, R, N, Hkv, flags):
     st.init_dead_slot()
     st.score(flags=flags)
     want, sets = oracle_scores(batch, 0, blob, flags)
-    rel = check_scores(st.host("scores"), want, sets["cand"])
+    rel = check_scores(st.host("scores"), want, sets["cand"], floor=RESID_MFMA_FLOOR if flags else SCORE_FLOOR)
     assert rel < 1e-5, rel
     st.select()
     keep_o, n_o, tau_o = oracle.select_budget(want, sets)
@@ -161,7 +161,8 @@ def test_residual_scores_d128_matrix_cores(dev, R, flags, nq):
     st = RetentionStep(batch, dev, residual=blob, flags=flags)
     st.score()
     want, sets = oracle_scores(batch, 0, blob, flags)
-    rel = check_scores(st.host("scores"), want, sets["cand"])
+    # up to 64 live query rows the head runs on the matrix cores, beyond on the vector units
+    rel = check_scores(st.host("scores"), want, sets["cand"], floor=RESID_MFMA_FLOOR if nq <= 64 else SCORE_FLOOR)
     print(f"max scale-aware relative score error {rel:.2e}")
     keep_o, n_o, tau_o = oracle.select_budget(want, sets)
     st.select()
@@ -417,7 +418,9 @@ def _compare_step(st, batch, b, blob, flags, update_memory, xattn_check=False):
     if sets["skip"]:
         assert np.all(np.isneginf(seg(st.host("scores"), batch, b)))
     else:
-        check_scores(seg(st.host("scores"), batch, b), want, sets["cand"])
+        mfma_head = (flags & ikv.IKV_RESIDUAL) and batch.shape.D == 128 and batch.kv_dtype == synth.BF16
+        check_scores(seg(st.host("scores"), batch, b), want, sets["cand"],
+                     floor=RESID_MFMA_FLOOR if mfma_head else SCORE_FLOOR)
     keep_o, n_o, tau_o = oracle.select_budget(want, sets)
     nk = int(st.host("n_keep")[b])
     keep_g = seg(st.host("keep"), batch, b).astype(bool)
