@@ -35,11 +35,14 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 CALIB_BYTES = 256 << 20        # the calibration copy (bytes read = bytes written)
 
 # HBM bytes per launch read from hardware counters (FETCH_SIZE and WRITE_SIZE, each
-# scaled by what it reads for the calibration copy) on one workload, for the kernel
-# as built from the hashed sources; reported only while those sources are unchanged.
+# scaled by what it reads for the calibration copy) on one workload and memory-row count,
+# for the kernel as built from the hashed sources; reported only while those sources are
+# unchanged.
 MEASURED_TRAFFIC = {
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_ws<true>"): (2509128196, "57b7749d6575b808"),
-    ("qwen3_8b_shape_hist32768_budget8192", "k_score_stats"): (2445701783, "57b7749d6575b808"),
+    ("qwen3_8b_shape_hist32768_budget8192", 64, "k_score_ws<true>"): (2504369844, "6b877f54ee252e59"),
+    ("qwen3_8b_shape_hist32768_budget8192", 64, "k_score_stats"): (2439997658, "6b877f54ee252e59"),
+    ("qwen3_8b_shape_hist32768_budget8192", 4, "k_score_once"): (2601121881, "6b877f54ee252e59"),
+    ("qwen3_8b_shape_hist32768_budget8192", 4, "k_score_stash"): (151217452, "6b877f54ee252e59"),
 }
 TRAFFIC_SOURCES = ("paper_2606_09916_amd/csrc/k_score_mfma.hip", "paper_2606_09916_amd/csrc/ikv_internal.hpp")
 
@@ -406,6 +409,38 @@ def main() -> int:
     for name, ms in recs:
         per_kernel.setdefault(name, []).append(ms)
 
+    # The paper's own QueryMemory shape, one row per query head (R = G; Sec. 3.2), on the
+    # same pool and kept budget: the same timed step with every phase, and the one key pass
+    # the scorer takes at R <= 16. Only when the main line runs another R.
+    rows_per_head = None
+    if (args.workload == "qwen3_8b_32k" and args.scorer == "intentkv" and s.R != sh.G and len(batch.sessions) == 1
+            and mem_update):
+        bg = synth.with_memory_rows(batch, sh.G, seed=7)
+        sg = RetentionStep(bg, dev, residual=blob, flags=flags, k_dev=st.k_pool, v_dev=st.v_pool)
+        evg = [[torch.cuda.Event(enable_timing=True) for _ in range(n_phase + 1)] for _ in range(args.steps)]
+        st_main = st
+        st = sg                                        # one_step drives `st`
+        for _ in range(args.warmup):
+            one_step([torch.cuda.Event(enable_timing=True) for _ in range(n_phase + 1)])
+        for k in range(args.steps):
+            one_step(evg[k])
+        torch.cuda.synchronize()
+        st = st_main
+        ph = np.zeros(n_phase)
+        for evs in evg:
+            for i in range(n_phase):
+                ph[i] += evs[i].elapsed_time(evs[i + 1])
+        ph /= args.steps
+        g_ms = float(sum(e[0].elapsed_time(e[-1]) for e in evg) / args.steps)
+        Sg = np.asarray(bg.S(0))
+        jg = np.arange(len(Sg))
+        nAg = int(((Sg != sg.dead) & ~((jg < s.pi) | ((jg >= s.qs) & (jg < s.qe)))).sum())
+        rows_per_head = {"R": sh.G, "value": round(nAg / ((ph[2] + ph[3]) / 1e3), 1), "ms_per_step": round(g_ms, 4),
+                         "phase_ms": {n: round(float(v), 4) for n, v in zip(names, ph)},
+                         "score_gbs_keys_once": round(nAg * sh.L * sh.Hkv * sh.D * 2 / (ph[2] / 1e3) / 1e9, 1)}
+        del sg
+        log(f"R = G = {sh.G}: {rows_per_head['value']:.0f} tokens/s, {g_ms:.3f} ms per step")
+
     # Layout ablation (Table 7): the compact apply path of the standard compactors on the
     # same kept set, left-packing the kept rows (keys re-rotated) into the slots the
     # redirect freed, against the redirect itself. One session only.
@@ -518,6 +553,11 @@ def main() -> int:
         # the SnapKV-style passes: the per-unit attention masses (float32 per unit and position)
         "k_score_mass": key_bytes + mem_bytes + n_scored * units * 4,
         "k_pool7": n_scored * units * 4 + n_scored * (4 + 4),
+        # the one key pass (R <= 16): keys once, the logits written (float32 per candidate,
+        # unit and row), the mean key rows; then the logits read back for the rule score
+        "k_score_once": key_bytes + mem_bytes + sum(a * units * R * 4 for R, a in zip(Rs, nA_b))
+        + (n_scored * sh.D * 4 if flags & ikv.IKV_RESIDUAL else 0),
+        "k_score_stash": sum(a * units * R * 4 for R, a in zip(Rs, nA_b)) + nA * 4,
     }
     kernels = {}
     for name, v in per_kernel.items():
@@ -533,7 +573,7 @@ def main() -> int:
     dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     d = kernels[dom]
     ach = d.get("gbs")
-    meas = MEASURED_TRAFFIC.get((wname, dom))
+    meas = MEASURED_TRAFFIC.get((wname, s.R, dom)) if len(set(Rs)) == 1 else None
     traffic = meas[0] if meas is not None and meas[1] == sources_sha() else None
     roofline = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4) if ach is not None else None, "traffic": traffic,
@@ -560,6 +600,7 @@ def main() -> int:
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
         "kernels": kernels,
+        "rows_per_query_head": rows_per_head,
         "layout_ablation": layout,
         "prefill_span": prefill,
     }

@@ -108,8 +108,11 @@ k_residual_mfma(const ikv_session *__restrict__ sess, const int32_t *__restrict_
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int g = lane >> 4, i = lane & 15;
-  // list tile: tiles k of chunk c take entries [c CH + 128 k, + 128) of the candidate list
-  const int per = CH / RT, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  // list tile k of chunk c takes entries [c CH + 128 k, + 128) of the candidate list; the
+  // grid runs tile-index-major (block x = k * chunks + c), which spreads the tiles of
+  // sparse chunks over the XCDs
+  const int per = CH / RT, nch = int(gridDim.x) / per;
+  const int lc = int(blockIdx.x) % nch, lk = int(blockIdx.x) / nch;
   if (int64_t(lc) * CH >= s.N) return;
   const int units = L * Hkv;
   constexpr int64_t F = 3 * RD + 1;

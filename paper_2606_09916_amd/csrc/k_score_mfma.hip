@@ -122,6 +122,22 @@ __global__ void __launch_bounds__(256) k_msplit(const ikv_session *__restrict__ 
 
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Sum over the 16 lanes of a row (lanes 16 q .. 16 q + 15), left in every lane of the row,
+// by DPP lane moves instead of LDS permutes: quad_perm [1,0,3,2] and [2,3,0,1] add within
+// each quad, row_half_mirror adds the other quad of the half row, row_mirror the other
+// half. Each step adds a commutative pair, so every lane holds the same bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);                            // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);                            // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);                           // row_half_mirror
+  v += dpp_mov<0x140>(v);                           // row_mirror
+  return v;
+}
+
 constexpr int RING = 4;                          // LDS stages of key rows
 constexpr int STAGE = MFMA_TILE * MD;            // bf16 per stage (32 KB)
 
@@ -620,7 +636,8 @@ constexpr int WS_THREADS = 512;
 // unchanged (keys, the 16 split rows, the mean key row); consumer c takes entries
 // 32 c .. + 31 against the slice and, per unit, stores the raw logits (log2 domain) to the
 // stash and merges the tile's (max, sum of exp2) per row across the four consumers,
-// written as the list tile's partial; k_lse_mfma and k_score_stash finish the score.
+// written as the list tile's partial (chunk-major, c per + k, whatever the grid order);
+// k_lse_mfma and k_score_stash finish the score.
 template <bool KBAR, int RH, bool STASH = false>
 __global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
@@ -632,8 +649,12 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
   if ((big == 1 && s.R > 64) || (big == 2 && s.R <= 64)) return;   // the other launch's session
-  // list tile: tiles k of chunk c cover entries [c CH + 128 k, + 128) of the candidate list
-  const int per = CH / MFMA_TILE, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  // list tile k of chunk c covers entries [c CH + 128 k, + 128) of the candidate list. The
+  // grid runs tile-index-major (block x = k * chunks + c): chunk-major, tile k of every
+  // chunk would land on XCD k, and a session whose chunks hold few candidates would pile
+  // its work onto the first XCDs while the empty tiles of the others finish at once.
+  const int per = CH / MFMA_TILE, nch = int(gridDim.x) / per;
+  const int lc = int(blockIdx.x) % nch, lk = int(blockIdx.x) / nch;
   if (int64_t(lc) * CH >= s.N) return;
   const int units = L * Hkv;
   const int t = threadIdx.x, lane = t & 63;
@@ -649,7 +670,7 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   const int ne = min(MFMA_TILE, cnt - lk * MFMA_TILE);
   if (ne <= 0) {
     if constexpr (STASH) {                           // an empty list tile still leaves its partials
-      float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + int64_t(blockIdx.x) * units * R;
+      float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + (int64_t(lc) * per + lk) * units * R;
       for (int i = t; i < units * R; i += WS_THREADS) pt[i] = make_float2(-INFINITY, 0.f);
     }
     return;
@@ -806,11 +827,11 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
     const int q0 = 32 * w;                           // this consumer's 32 entries
     const int64_t NS = stash_stride(s.N);
     float *stash = base + z.off_stash() + int64_t(lc) * CH + int64_t(lk) * MFMA_TILE + q0 + 4 * g;
-    float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + int64_t(blockIdx.x) * units * R;
-    // per-consumer (max, sum) of unit u's rows: [u & 1][consumer][row], in the second
+    float2 *pt = reinterpret_cast<float2 *>(base + z.off_part()) + (int64_t(lc) * per + lk) * units * R;
+    // per-consumer (max, sum) of unit u's rows: [u & 1][consumer][row], in the first
     // memory stage's unused space past its 16 rows
     float2 *sb = reinterpret_cast<float2 *>(lds + KSTAGES * STAGE + 16 * 256);
-    // consumer 0 merges unit u's four partials into the tile's partial (rows < R)
+    // consumer 0 merges unit u's four partials of each row < R into the tile's partial
     auto merge = [&](int u) __attribute__((always_inline)) {
       if (w == 0 && lane < R) {
         const float2 *q = sb + (u & 1) * 64 + lane;
@@ -854,7 +875,9 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
         for (int blk = 0; blk < 2; ++blk)
           *reinterpret_cast<float4 *>(o + 16 * blk) = make_float4(acc[blk][0], acc[blk][1], acc[blk][2], acc[blk][3]);
       }
-      // the row's max and sum over this consumer's entries below ne
+      // the row's max and sum over this consumer's entries below ne (the four lane groups
+      // of a row combined by shuffles: a merge of per-lane partials by consumer 0 made it
+      // the straggler at every unit's barrier, 0.49 against 0.37 ms per multi-turn call)
       float m = -INFINITY;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
@@ -1222,12 +1245,7 @@ k_score_stats(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int 
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float v = ex2(acc[pb][0][i]) + ex2(acc[pb][1][i]);
-          v += __shfl_xor(v, 1, WAVE);
-          v += __shfl_xor(v, 2, WAVE);
-          v += __shfl_xor(v, 4, WAVE);
-          v += __shfl_xor(v, 8, WAVE);
-          pm[pb][i] = v;
+          pm[pb][i] = row16_sum(ex2(acc[pb][0][i]) + ex2(acc[pb][1][i]));
         }
       if (r16 == 0) {
         float *mr = mred + (((tt & 1) * 2 + hh) * NW + (w % NW)) * ST_TILE;
@@ -1469,7 +1487,9 @@ __global__ void __launch_bounds__(SS_THREADS) k_score_stash(const ikv_session *_
   const int b = blockIdx.y;
   const ikv_session s = sess[b];
   if (s.N <= s.C) return;
-  const int per = CH / MFMA_TILE, lc = int(blockIdx.x) / per, lk = int(blockIdx.x) - lc * per;
+  // list tiles in the grid order of k_score_ws (tile-index-major)
+  const int per = CH / MFMA_TILE, nch = int(gridDim.x) / per;
+  const int lc = int(blockIdx.x) % nch, lk = int(blockIdx.x) / nch;
   if (int64_t(lc) * CH >= s.N) return;
   const int units = L * Hkv;
   const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);

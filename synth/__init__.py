@@ -22,6 +22,7 @@ from __future__ import annotations
 
 import os
 from concurrent.futures import ThreadPoolExecutor
+import dataclasses
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -261,7 +262,16 @@ def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
     with ThreadPoolExecutor(_workers()) as ex:
         list(ex.map(fill, jobs))
 
-    # --- QueryMemory, span rows, query positions, decode queries ----------------------
+    return Batch(shape=shape, kv_dtype=kv_dtype, sessions=sessions, num_slots=num_slots,
+                 k_pool=k_pool, v_pool=v_pool, slot_maps=slot_maps, slot_off=slot_off, heavy=heavy,
+                 **_queries(shape, sessions, seed, kv_dtype, span_rows))
+
+
+def _queries(shape: Shape, sessions: list, seed: int, kv_dtype: int, span_rows: bool) -> dict:
+    """QueryMemory, span rows, query positions and decode queries of a batch (the fields
+    of Batch that depend on the memory rows R, not on the pool)."""
+    L, Hkv, D = shape.L, shape.Hkv, shape.D
+    B = len(sessions)
     mem_off = np.zeros(B, dtype=np.int64)
     qspan_off = np.zeros(B, dtype=np.int64)
     qpos_off = np.zeros(B, dtype=np.int64)
@@ -281,18 +291,23 @@ def make_batch(shape: Shape, sessions: list, seed: int, kv_dtype: int = BF16,
         qp = s.query_positions()
         qps.append(qp)
         oq += len(qp)
-    q_dec = np.zeros((B, L, shape.Hq, D), dtype=st)
+    q_dec = np.zeros((B, L, shape.Hq, D), dtype=np.uint16 if kv_dtype == BF16 else np.float32)
     for b, s in enumerate(sessions):
         q = stream(seed, T_QDEC, b).standard_normal((1, L, shape.Hq, D), dtype=np.float32)
         q = rope_neox(q.astype(np.float64), *rope_cos_sin(np.array([s.N]), D))
         q_dec[b] = to_dtype(q[0], kv_dtype)
+    return dict(M=np.concatenate(Ms) if Ms else np.zeros(0, np.float32), mem_off=mem_off,
+                q_span=np.concatenate(spans), qspan_off=qspan_off,
+                qpos=np.concatenate(qps).astype(np.int32), qpos_off=qpos_off, q_dec=q_dec)
 
-    return Batch(shape=shape, kv_dtype=kv_dtype, sessions=sessions, num_slots=num_slots,
-                 k_pool=k_pool, v_pool=v_pool, slot_maps=slot_maps, slot_off=slot_off,
-                 M=np.concatenate(Ms) if Ms else np.zeros(0, np.float32), mem_off=mem_off,
-                 q_span=np.concatenate(spans), qspan_off=qspan_off,
-                 qpos=np.concatenate(qps).astype(np.int32), qpos_off=qpos_off,
-                 q_dec=q_dec, heavy=heavy)
+
+def with_memory_rows(batch: Batch, R: int, seed: int, span_rows: bool = True) -> Batch:
+    """The same sessions over the same pool (keys, values and slot maps shared, not
+    copied) with R memory rows per KV head: QueryMemory, span rows and queries drawn
+    afresh from `seed`."""
+    sessions = [dataclasses.replace(s, R=R) for s in batch.sessions]
+    return dataclasses.replace(batch, sessions=sessions,
+                               **_queries(batch.shape, sessions, seed, batch.kv_dtype, span_rows))
 
 
 # ----------------------------------------------------------------------------- residual weights
