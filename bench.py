@@ -409,6 +409,33 @@ def main() -> int:
     for name, ms in recs:
         per_kernel.setdefault(name, []).append(ms)
 
+    # Reference rate for decode: a plain read of the same live key and value rows of every
+    # layer (synth/read_ceiling.hip, nothing computed), in pieces of 4 and of 8 adjacent
+    # KV heads, the median of ten launches each. Outside the timed region.
+    read_ceiling = None
+    if batch.kv_dtype == synth.BF16 and sh.D == 128:
+        nl_b = st.host("n_live").astype(np.int64)
+        parts = [st.live[int(st.sess[b].slot_off):int(st.sess[b].slot_off) + int(n)] for b, n in enumerate(nl_b) if n > 0]
+        if parts:
+            lv_all = torch.cat(parts).contiguous()
+            n_all = int(lv_all.numel())
+            bytes_all = n_all * sh.L * sh.Hkv * sh.D * 2 * 2
+            read_ceiling = {"bytes": bytes_all}
+            for hpw in (4, 8):
+                if sh.Hkv % hpw:
+                    continue
+                splits = max(1, min(4096, n_all // 256))
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+                synth.read_ceiling(st.k_pool, st.v_pool, lv_all, n_all, hpw, splits)
+                for k in range(10):
+                    ev[k].record()
+                    synth.read_ceiling(st.k_pool, st.v_pool, lv_all, n_all, hpw, splits)
+                ev[10].record()
+                torch.cuda.synchronize()
+                c_ms = float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(10)]))
+                read_ceiling[f"heads{hpw}_gbs"] = round(bytes_all / (c_ms / 1e3) / 1e9, 1)
+            del lv_all
+
     # The paper's own QueryMemory shape, one row per query head (R = G; Sec. 3.2), on the
     # same pool and kept budget: the same timed step with every phase, and the one key pass
     # the scorer takes at R <= 16. Only when the main line runs another R.
@@ -596,6 +623,7 @@ def main() -> int:
                    "candidates": nA, "n_keep": n_keep,
                    "n_live": n_live},
         "decode_attn_gbs": round(decode_gbs, 1), "decode_hbm_frac": round(decode_gbs / HBM_PEAK_GBS, 4),
+        "decode_read_ceiling": read_ceiling,
         "phase_ms": {n: round(float(v), 4) for n, v in zip(names, phase_ms)},
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,

@@ -37,8 +37,15 @@
  *    On an error return nothing has been enqueued, except for IKV_EHIP, which
  *    reports a failed launch, or a fault that a kernel of an earlier call reported
  *    (see ikv_select_budget); a call that returns such a fault enqueues nothing.
- *  - Slot ids in slot maps and live lists must lie in [0, num_slots); the
- *    kernels do not check them.
+ *  - Slot ids in slot maps, live lists, history and destination slot lists must
+ *    lie in [0, num_slots), and cross-attention query positions in [0, N); the
+ *    kernels do not check them (an id outside the pool reads or writes outside
+ *    it). With IKV_DEBUG=1 in the environment (read on every call), the calls
+ *    that read such ids (score_history, redirect_slots, decode_attend_slotmap,
+ *    compact_apply, prefill_span) first copy them to the host, after the
+ *    stream's earlier work, and return IKV_EINVAL naming the session, the array
+ *    and the index of the first bad entry, with no kernel launched. This
+ *    synchronises the stream on every call; it is meant for debugging.
  */
 #ifndef IKV_H
 #define IKV_H

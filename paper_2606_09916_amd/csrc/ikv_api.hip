@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include <algorithm>
 #include <atomic>
@@ -162,6 +163,52 @@ ikv_status pending_fault() {
   if (ikv::take_host_fault())
     return fail(IKV_EHIP, "a grid barrier of an earlier ikv_select_budget call gave up waiting; "
                           "that call's kept set is not valid");
+  return IKV_OK;
+}
+
+// ---- IKV_DEBUG=1 in the environment (read on every call): before anything is
+// enqueued, the slot ids a call reads are copied to the host, after the stream's
+// earlier work, and checked. The kernels never check them; an id outside the pool
+// would read or write outside it. Synchronises the stream; for debugging only.
+bool debug_mode() {
+  const char *e = getenv("IKV_DEBUG");
+  return e != nullptr && e[0] != '\0' && e[0] != '0';
+}
+
+template <typename T>
+ikv_status debug_fetch(std::vector<T> &h, const T *dev, int64_t n, hipStream_t st, const char *what, int b) {
+  h.resize(size_t(n > 0 ? n : 0));
+  if (n <= 0) return IKV_OK;
+  hipError_t e = hipMemcpyAsync(h.data(), dev, size_t(n) * sizeof(T), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(IKV_EHIP, "IKV_DEBUG: reading %s of session %d: %s", what, b, hipGetErrorString(e));
+  return IKV_OK;
+}
+
+// Entries [off, off + n) of the device array `ids` must lie in [lo, hi).
+ikv_status debug_ids(const int32_t *ids, int64_t off, int64_t n, int64_t lo, int64_t hi, hipStream_t st,
+                     const char *what, int b) {
+  std::vector<int32_t> h;
+  if (ikv_status r = debug_fetch(h, ids + off, n, st, what, b)) return r;
+  for (int64_t i = 0; i < n; ++i)
+    if (h[size_t(i)] < lo || h[size_t(i)] >= hi)
+      return fail(IKV_EINVAL, "IKV_DEBUG: session %d: %s[%lld] = %d outside [%lld, %lld)", b, what, (long long)i,
+                  h[size_t(i)], (long long)lo, (long long)hi);
+  return IKV_OK;
+}
+
+// The count a device array holds for session b, clamped to [0, cap].
+ikv_status debug_count(const int32_t *counts, int b, int64_t cap, hipStream_t st, const char *what, int64_t *n) {
+  std::vector<int32_t> h;
+  if (ikv_status r = debug_fetch(h, counts + b, 1, st, what, b)) return r;
+  *n = std::min<int64_t>(std::max<int64_t>(h[0], 0), cap);
+  return IKV_OK;
+}
+
+ikv_status debug_slot_maps(const ikv_session *sess, int B, const int32_t *slot_maps, int64_t num_slots,
+                           hipStream_t st) {
+  for (int b = 0; b < B; ++b)
+    if (ikv_status r = debug_ids(slot_maps, sess[b].slot_off, sess[b].N, 0, num_slots, st, "slot map", b)) return r;
   return IKV_OK;
 }
 
@@ -397,6 +444,12 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   a.minR = minR;
   a.maxNq = maxNq;
   if (a.maxN == 0) return ok();
+  if (debug_mode()) {
+    if ((r = debug_slot_maps(sess, B, slot_maps, pool->num_slots, (hipStream_t)stream))) return r;
+    if (resid)
+      for (int b = 0; b < B; ++b)
+        if ((r = debug_ids(qpos, sess[b].qpos_off, sess[b].nq, 0, sess[b].N, (hipStream_t)stream, "qpos", b))) return r;
+  }
   return hip_status(ikv::launch_score(a, (hipStream_t)stream), "ikv_score_history");
 }
 
@@ -451,6 +504,7 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
   if (!slot_maps || !keep || !freed || !n_freed || !live || !n_live)
     return fail(IKV_EINVAL, "slot_maps / keep / freed / n_freed / live / n_live is NULL");
   if ((r = check_ws(workspace, workspace_bytes, redirect_bytes(num_slots, B)))) return r;
+  if (debug_mode() && (r = debug_slot_maps(sess, B, slot_maps, num_slots, (hipStream_t)stream))) return r;
   return hip_status(ikv::launch_redirect(sess_dev, B, num_slots, slot_maps, dead_slot, keep, freed, n_freed, live,
                                          n_live, static_cast<uint32_t *>(workspace), (hipStream_t)stream),
                     "ikv_redirect_slots");
@@ -468,6 +522,19 @@ ikv_status ikv_compact_apply(const ikv_pool *pool, const ikv_session *sess, cons
   if (!(rope_base > 1.0)) return fail(IKV_EINVAL, "rope_base must be > 1");
   const size_t need = size_t(total_positions(sess, B)) * sizeof(int32_t);
   if ((r = check_ws(workspace, workspace_bytes, need))) return r;
+  if (debug_mode()) {
+    const hipStream_t st = (hipStream_t)stream;
+    if ((r = debug_slot_maps(sess, B, slot_maps, pool->num_slots, st))) return r;
+    for (int b = 0; b < B; ++b) {           // one destination slot per kept live position
+      std::vector<int32_t> S;
+      std::vector<uint8_t> kp;
+      if ((r = debug_fetch(S, slot_maps + sess[b].slot_off, sess[b].N, st, "slot map", b))) return r;
+      if ((r = debug_fetch(kp, keep + sess[b].slot_off, sess[b].N, st, "keep", b))) return r;
+      int64_t nk = 0;
+      for (int j = 0; j < sess[b].N; ++j) nk += kp[size_t(j)] && S[size_t(j)] != pool->dead_slot;
+      if ((r = debug_ids(dst_slots, sess[b].slot_off, nk, 0, pool->num_slots, st, "dst_slots", b))) return r;
+    }
+  }
   return hip_status(ikv::launch_compact(*pool, sess_dev, B, max_n(sess, B), slot_maps, keep, dst_slots, rope_base,
                                         n_keep, static_cast<int32_t *>(workspace), (hipStream_t)stream),
                     "ikv_compact_apply");
@@ -500,6 +567,15 @@ ikv_status ikv_prefill_span(const ikv_pool *pool, const ikv_session *sess, const
   }
   if ((r = check_ws(workspace, workspace_bytes, prefill_bytes(pool, sess, B)))) return r;
   if (max_n == 0) return ok();
+  if (debug_mode()) {
+    const hipStream_t st = (hipStream_t)stream;
+    if ((r = debug_slot_maps(sess, B, slot_maps, pool->num_slots, st))) return r;
+    for (int b = 0; b < B; ++b) {
+      int64_t nh = 0;
+      if ((r = debug_count(n_hist, b, sess[b].N, st, "n_hist", &nh))) return r;
+      if ((r = debug_ids(hist, sess[b].slot_off, nh, 0, pool->num_slots, st, "hist", b))) return r;
+    }
+  }
   const float decay = isinf(lambda) ? 0.0f : float(exp(-double(lambda)));
   return hip_status(ikv::launch_prefill(*pool, sess_dev, B, max_n, slot_maps, q_raw, k_raw, v_raw, hist, n_hist,
                                         rope_base, decay, M, q_out, out, kq, static_cast<float *>(workspace),
@@ -518,6 +594,12 @@ ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *se
   if (!q || !live || !n_live || !out) return fail(IKV_EINVAL, "q / live / n_live / out is NULL");
   if ((r = check_ws(workspace, workspace_bytes, decode_bytes(pool, sess, B)))) return r;
   const int splits = ikv::decode_splits(live_bound(sess, B));
+  if (debug_mode())
+    for (int b = 0; b < B; ++b) {
+      int64_t nl = 0;
+      if ((r = debug_count(n_live, b, sess[b].N, (hipStream_t)stream, "n_live", &nl))) return r;
+      if ((r = debug_ids(live, sess[b].slot_off, nl, 0, pool->num_slots, (hipStream_t)stream, "live", b))) return r;
+    }
   return hip_status(ikv::launch_decode(*pool, sess_dev, B, splits, q, live, n_live, out,
                                        static_cast<float *>(workspace), (hipStream_t)stream),
                     "ikv_decode_attend_slotmap");

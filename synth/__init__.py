@@ -606,17 +606,42 @@ def device_table_rows(pool, L: int, num_slots: int, Hkv: int, D: int, slots, tab
         raise RuntimeError(f"synth_table_rows failed with HIP error {err}")
 
 
+def read_ceiling(k_pool, v_pool, live, n: int, hpw: int, splits: int, stream_=None):
+    """Plain read of the key and value rows of the first n slots of the device int32
+    tensor `live`, every layer, in pieces of hpw adjacent heads (read_ceiling.hip): the
+    bench's reference rate for decode attention. Returns the device tensor of per-
+    workgroup words (asynchronous)."""
+    import ctypes
+    import torch
+    if not os.path.exists(_SYNTH_LIB):
+        raise RuntimeError(f"{_SYNTH_LIB} is missing: run __graft_entry__.build()")
+    lib = ctypes.CDLL(_SYNTH_LIB)
+    fn = lib.synth_read_ceiling
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    L, num_slots, Hkv, D = k_pool.shape
+    out = torch.empty(splits * L * (Hkv // hpw), dtype=torch.int32, device=k_pool.device)
+    st = (stream_ or torch.cuda.current_stream()).cuda_stream
+    err = fn(k_pool.data_ptr(), v_pool.data_ptr(), L, num_slots, Hkv, D, hpw, live.data_ptr(), int(n), splits,
+             out.data_ptr(), st)
+    if err != 0:
+        raise RuntimeError(f"synth_read_ceiling failed with HIP error {err}")
+    return out
+
+
 def build_native(verbose: bool = False) -> str:
-    """Compile table_rows.hip into synth/libsynth.so (gfx950)."""
+    """Compile table_rows.hip and read_ceiling.hip into synth/libsynth.so (gfx950)."""
     import shutil
     import subprocess
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-    src = os.path.join(os.path.dirname(_SYNTH_LIB), "table_rows.hip")
+    here = os.path.dirname(_SYNTH_LIB)
+    srcs = [os.path.join(here, f) for f in ("table_rows.hip", "read_ceiling.hip")]
     cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Xclang", "-target-feature",
-           "-Xclang", "-packed-fp32-ops", src, "-o", _SYNTH_LIB + ".tmp"]
+           "-Xclang", "-packed-fp32-ops", *srcs, "-o", _SYNTH_LIB + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed on table_rows.hip:\n{r.stdout}\n{r.stderr}")
+        raise RuntimeError(f"hipcc failed on synth's sources:\n{r.stdout}\n{r.stderr}")
     os.replace(_SYNTH_LIB + ".tmp", _SYNTH_LIB)
     if verbose:
         print(f"built {_SYNTH_LIB}")
