@@ -37,7 +37,26 @@ hipError_t launch_init_dead_slot(const ikv_pool &p, hipStream_t st) {
 // One wavefront per memory row: Enc = mean of the span rows, M = decay * M + Enc,
 // then the row is divided by max(||row||, 1e-12). Lane (g, c) reads channels
 // 8c .. 8c+7 of span rows g, g + G, ... (G = 512 / D rows per wave step) with
-// 16-byte loads; the G row groups fold with shuffles.
+// 16-byte loads; the G row groups fold with shuffles. The span rows are read once, with
+// the non-temporal hint (each load instruction covers G whole rows).
+typedef unsigned int qm_u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void load8_once(const uint16_t *p, float *o) {
+  const qm_u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const qm_u32x4 *>(p));
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = __uint_as_float(w[i] << 16);
+    o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8_once(const float *p, float *o) {
+  const qm_u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const qm_u32x4 *>(p));
+  const qm_u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const qm_u32x4 *>(p + 4));
+  const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = __uint_as_float(w[i]);
+}
+
 template <typename T, int D>
 __global__ void __launch_bounds__(256) k_qm_update(const ikv_session *__restrict__ sess, int L, int Hkv,
                                                    float *__restrict__ M, const T *__restrict__ q_span,
@@ -60,7 +79,7 @@ __global__ void __launch_bounds__(256) k_qm_update(const ikv_session *__restrict
   for (; tq + 3 * G < n; tq += 4 * G) {          // four loads in flight per lane
     float a[4][8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) load8(q + int64_t(tq + u * G) * D, a[u]);
+    for (int u = 0; u < 4; ++u) load8_once(q + int64_t(tq + u * G) * D, a[u]);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
@@ -68,7 +87,7 @@ __global__ void __launch_bounds__(256) k_qm_update(const ikv_session *__restrict
   }
   for (; tq < n; tq += G) {
     float a[8];
-    load8(q + int64_t(tq) * D, a);
+    load8_once(q + int64_t(tq) * D, a);
 #pragma unroll
     for (int k = 0; k < 8; ++k) e[k] += a[k];
   }
