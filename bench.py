@@ -298,6 +298,9 @@ def main() -> int:
     ap.add_argument("--scorer", default="intentkv", choices=("intentkv", "snapkv", "h2o"),
                     help="the scorer feeding selection, redirect and decode (Qwen3-8B 32k workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--probe-exchange", action="store_true",
+                    help="time the per-unit normaliser exchange a one-key-pass score at 64 memory rows would "
+                         "need (synth/exchange_probe.hip) and print its table instead of the bench line")
     ap.add_argument("--cpu-layers", type=int, default=None,
                     help="layers of the CPU baseline sample (default 36; 8 for a pool drawn on the GPU)")
     args = ap.parse_args()
@@ -316,6 +319,22 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     dev = torch.device("cuda:0")
+    if args.probe_exchange:
+        # One step stands for one unit (layer, KV head) of a score pass whose workgroups
+        # each own a tile of positions: a Qwen3-8B 32k pass over 288 units takes about
+        # 1.45 us per unit. Mode 0: the spin and a barrier per step; mode 1: with the
+        # exchange, each unit's normalisers awaited `lag` steps after its partials.
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        G = 256 if cus >= 256 else 128
+        rows = []
+        for work in (0, 1450):
+            rows.append({"work_ns": work, "mode": "no exchange", **synth.exchange_probe(G, 288, 3, 0, work, dev)})
+            for lag in (3, 4, 6, 8, 12):
+                rows.append({"work_ns": work, "mode": "exchange", "lag": lag,
+                             **synth.exchange_probe(G, 288, lag, 1, work, dev)})
+        print(json.dumps({"probe": "per-unit normaliser exchange", "workgroups": G, "units": 288, "rows": rows}),
+              flush=True)
+        return 0
     if args.workload == "multiturn":
         r = multiturn_bench(args, dev)
         print(json.dumps({
@@ -570,6 +589,9 @@ def main() -> int:
         "k_score_ring": key_bytes + mem_bytes,
         "k_score_ws<true>": key_bytes + mem_bytes + n_scored * 4 + n_scored * sh.D * 4,
         "k_score_ws<false>": key_bytes + mem_bytes + n_scored * 4,
+        # the one key pass at 16 < R <= 64 (opt-in): what the second pass alone reads and writes
+        "k_score_fused": key_bytes + mem_bytes + n_scored * 4
+        + (n_scored * sh.D * 4 if flags & ikv.IKV_RESIDUAL else 0),
         "k_decode_split<T, D, G>": kv_live + q_rows,
         "k_decode_heads<G>": kv_live + q_rows,
         "k_qm_update<T, 128>": span_bytes,

@@ -124,6 +124,7 @@ size_t score_bytes(const ikv_pool *p, const ikv_session *s, int B, uint32_t flag
   int64_t f = ikv::score_offset(s, B, p->L, units, p->D, resid, use_mfma(p, s, B));
   if (resid) f += ikv::score_shared_floats(p->D);
   if (flags & IKV_POOL7) f += int64_t(units) * total_positions(s, B);    // per-unit attention masses
+  f = ikv::align64f(f) + ikv::fused_exchange_floats(*p, s, B, flags);   // the one-key-pass form's exchange
   return size_t(f) * sizeof(float);
 }
 
@@ -161,8 +162,8 @@ size_t prefill_bytes(const ikv_pool *p, const ikv_session *s, int B) {
 
 ikv_status pending_fault() {
   if (ikv::take_host_fault())
-    return fail(IKV_EHIP, "a grid barrier of an earlier ikv_select_budget call gave up waiting; "
-                          "that call's kept set is not valid");
+    return fail(IKV_EHIP, "a wait between workgroups of an earlier call (ikv_select_budget's grid barrier or "
+                          "ikv_score_history's normaliser exchange) gave up; that call's results are not valid");
   return IKV_OK;
 }
 
@@ -435,6 +436,14 @@ ikv_status ikv_score_history(const ikv_pool *pool, const ikv_session *sess, cons
   // SnapKV-style score (which needs the unit-major pass), not turned off by the caller
   a.stash = a.mfma && maxR <= ikv::STASH_MAX_R && !(flags & (IKV_POOL7 | IKV_TWO_PASS));
   if (a.stash) a.stats = false;
+  a.fused_tiles = a.mfma && !a.stash ? ikv::fused_tiles(*pool, sess, B, flags) : 0;
+  if (a.fused_tiles > 0) a.stats = false;
+  {
+    int64_t xo = ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
+    if (resid) xo += ikv::score_shared_floats(pool->D);
+    if (flags & IKV_POOL7) xo += int64_t(pool->L) * pool->Hkv * total_positions(sess, B);
+    a.xch = reinterpret_cast<uint64_t *>(a.ws + ikv::align64f(xo));
+  }
   a.ws_shared = a.ws + ikv::score_offset(sess, B, pool->L, pool->L * pool->Hkv, pool->D, resid, a.mfma);
   a.maxN = max_n(sess, B);
   a.total_positions = total_positions(sess, B);

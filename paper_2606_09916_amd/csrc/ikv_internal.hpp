@@ -251,7 +251,16 @@ struct ScoreArgs {
   bool stats;          // the unit-major first pass (MFMA, R <= 64, even Hkv, a layer under 4 GB)
   bool mfma_resid;     // MFMA residual head (MFMA passes and every nq <= 64)
   bool stash;          // one key pass with a logit stash (MFMA, every R <= 16, no IKV_POOL7)
+  int fused_tiles;     // > 0: one key pass with the normaliser exchange (k_score_fused), on this many tiles
+  uint64_t *xch;       // its exchange area (after the shared block)
 };
+
+// The one-key-pass form at 16 < R <= 64 (one session whose list tiles fit on the device
+// at once): its workgroup count, 0 where it does not apply; and the floats of its
+// exchange area, which follows the score workspace's shared block (0 where it does not
+// apply). It is opt-in: IKV_FUSED=1 in the environment (read on every call) turns it on.
+int fused_tiles(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags);
+int64_t fused_exchange_floats(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags);
 
 // Opt-in per-kernel timing (ikv_timing in the C ABI): every launch site holds a
 // KTimer, which, while timing is on, records a HIP event pair around its launch.

@@ -20,6 +20,13 @@
 //           registers; with the residual head on, the mean key row accumulates from
 //           the same LDS tiles.
 #include <math.h>
+#include <stdlib.h>
+#include <unistd.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <random>
 
 #include "ikv_internal.hpp"
 #include "res_setup.hpp"
@@ -1023,6 +1030,479 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
   if (t < ne) scores[s.slot_off + pos_of(t)] = red[t] + red[MFMA_TILE + t];   // every list entry is a candidate
 }
 
+// ------------------------------------------------------------------ one key pass at R <= 64
+// k_score_fused: the rule score of Eq. 3 with one read of the keys, for a session whose
+// list tiles all fit on the device at once (one workgroup per tile, cooperative launch).
+// Eq. 3 needs each memory row's normaliser over every candidate before any score, and a
+// tile's workgroup sees only its own 128 positions. So for every unit the workgroups
+// exchange per-row partials while they go on: a tile computes unit v's logits, keeps
+// e = exp2(x - m) of its 64 positions per row (m its own row maximum) and publishes
+// (m, sum e); FU_LAG units later the row normaliser c = max + log2 Z of that unit is in,
+// and the tile adds exp2(m - c) * e over the rows to each position's score.
+//
+// Producers (waves 4-7) are the second pass's: the key and memory-row rings and the mean
+// key row. Producer 3 also combines the rows it owns: row r of unit x belongs to
+// workgroup (x * R16 + r) mod G, one row every G / R16 units. At the top of a unit it
+// checks the partials its loads of the previous top returned, stores the row's stamped
+// normaliser when every partial is in and reissues the loads when not; it waits only
+// when the row is due (FU_LAG units after the partials).
+// Consumers (waves 0-3): wave c takes memory rows 32 (c & 1) .. + 31 against entries
+// 64 (c >> 1) .. + 63, as two 32 x 32 blocks of v_mfma_f32_32x32x16_bf16 (keys as A,
+// split memory rows as B, hi then lo): lane l holds row 32 (c & 1) + l % 32 and 32
+// entries. Unit v's step: finish unit v - 1 - FU_LAG (its normaliser loaded at the
+// previous step; the weighted rows reduce-scatter over the 32 lanes of a half, so each
+// lane keeps one entry's running score), then unit v's MFMAs with unit v - 1's row
+// statistics and exp2 folded in between. Five 32-register slots rotate over the units.
+//
+// Exchange words (device scope, 64 bits, never cached non-coherently): partial
+// (unit u, row r, half q) = {m | lo(S_u)}, {sum | hi(S_u)} and normaliser (u, r) =
+// {c | lo(S_u)}, {c | hi(S_u)}, S_u = stamp + u, a 64-bit stamp the host draws per call
+// (a random per-process tag above a call counter), so leftovers of other calls and of
+// other data never pass. Every wait is bounded (`spins` polls); one that runs out sets
+// the host fault word, which the library's next call reports as IKV_EHIP.
+constexpr int FU_LAG = 4;
+constexpr int FU_SLOTS = FU_LAG + 1;
+constexpr int FU_MIN_TILES = 64;                 // >= 64 rows per unit: one owned row per unit at most
+constexpr int FU_MAX_TILES = 256;                // partials per owner lane: at most 8
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void fu_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ __forceinline__ u32x4 ld_coherent16(const void *p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void st_word(uint64_t *p, float v, uint32_t tag) {
+  __hip_atomic_store(p, (uint64_t(__float_as_uint(v)) << 32) | tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_word(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <bool KBAR>
+__global__ void __launch_bounds__(WS_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_score_fused(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv, int dead,
+              const ikv_session *__restrict__ sess, const int32_t *__restrict__ slot_maps, float *__restrict__ ws,
+              float *__restrict__ scores, bool resid, int CH, uint64_t *__restrict__ xch, uint64_t stamp,
+              uint32_t spins, uint32_t *__restrict__ host_fault) {
+  __shared__ __align__(1024) uint16_t lds[KSTAGES * STAGE + 2 * MSTAGE];
+
+  const ikv_session s = sess[0];
+  if (s.N <= s.C) return;                          // every workgroup alike: no event
+  const int G = int(gridDim.x), wgi = int(blockIdx.x);
+  const int per = CH / MFMA_TILE, nch = G / per;
+  const int lc = wgi % nch, lk = wgi / nch;
+  const int units = L * Hkv;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int R = s.R, R16 = pad16(R);
+  const int P = 2 * G;                             // partials per (unit, row)
+  const ScoreSizes z = score_sizes(s, L, units, MD, resid, true);
+  float *base = ws + score_offset(sess, 0, L, units, MD, resid, true);
+  const int32_t *S = slot_maps + s.slot_off;
+  const uint32_t lds0 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  const int32_t *lst = reinterpret_cast<const int32_t *>(base + z.off_clist()) + lc * CH + lk * MFMA_TILE;
+  const int cnt = reinterpret_cast<const int32_t *>(base + z.off_ccount(s.N))[lc];
+  const int ne = max(0, min(MFMA_TILE, cnt - lk * MFMA_TILE));   // an empty tile still takes part
+  const bool ident = cnt == min(CH, s.N - lc * CH);
+  const int e0 = lc * CH + lk * MFMA_TILE;
+  auto pos_of = [&](int e) __attribute__((always_inline)) { return ident ? e0 + e : lst[e]; };
+  uint64_t *xpart = xch;
+  uint64_t *xnrm = xch + int64_t(units) * R16 * P * 2;
+  bool timed_out = false;
+
+  if (w >= 4) {
+    // ---------------- producers: the rings and the mean key row (as the second pass)
+    const int pw = w - 4;
+    const int64_t slot_stride = int64_t(Hkv) * MD;
+    const uint16_t *src[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int tok = (8 * pw + k) * 4 + (lane >> 4);
+      const int slot = tok < ne ? S[pos_of(tok)] : dead;   // past the list: any valid row
+      src[k] = kpool + int64_t(slot) * slot_stride + ((lane & 15) ^ (tok & 15)) * 8;
+    }
+    asm volatile("" ::"v"(src[0]), "v"(src[7]));
+    auto issue_k_piece = [&](int u, int k) __attribute__((always_inline)) {
+      const int l = u / Hkv, h = u - l * Hkv;
+      const int64_t off = int64_t(l) * num_slots * slot_stride + int64_t(h) * MD;
+      const uint32_t st = lds0 + uint32_t((u % KSTAGES) * STAGE * 2);
+      dma16_nt(src[k] + off, __builtin_amdgcn_readfirstlane(st + uint32_t(((8 * pw + k) * 4) * MD * 2)));
+    };
+    auto issue_k = [&](int u) __attribute__((always_inline)) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) issue_k_piece(u, k);
+    };
+    const uint16_t *msplit = reinterpret_cast<const uint16_t *>(base);
+    const uint32_t mlds0 = lds0 + uint32_t(KSTAGES * STAGE * 2);
+    const int npc = min(64, R16) >> 3;
+    auto issue_m_piece = [&](int u, int k) __attribute__((always_inline)) {
+      const uint16_t *m0 = msplit + int64_t(u) * R16 * 256;
+      const uint32_t st = mlds0 + uint32_t((u & 1) * MSTAGE * 2);
+      const int piece = pw * npc + k;
+      const int r = piece * 2 + (lane >> 5);
+      const int sl = lane & 31;
+      dma16(m0 + r * 256 + ((sl ^ (r & 15)) * 8), __builtin_amdgcn_readfirstlane(st + uint32_t(piece * 1024)));
+    };
+    const int pp = 32 * pw + (lane & 31), hc = lane >> 5;
+    float kb[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) kb[i] = 0.f;
+    auto kbar_step = [&](const uint16_t *kr, int c) __attribute__((always_inline)) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(kr + (((8 * hc + c) ^ (pp & 15)) * 8));
+      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        kb[8 * c + 2 * e] += __uint_as_float(q[e] << 16);
+        kb[8 * c + 2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
+      }
+    };
+    // ---- producer 3: the owned rows. Lane l holds partials l + 64 q of the row (16 B each).
+    // The loads into vv are inline assembly, invisible to the compiler's wait insertion:
+    // from an o_issue until the wait that covers it nothing may touch vv's registers, so
+    // every path that issues again (o_force) starts with no such load in flight.
+    const bool owner = pw == 3;
+    int oc = -1, orow = 0, onext = 0;
+    u32x4 vv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) vv[q] = u32x4{0u, 0u, 0u, 0u};
+    auto o_issue = [&](int x, int r) __attribute__((always_inline)) {
+      const uint64_t *p = xpart + (int64_t(x) * R16 + r) * P * 2;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (lane + 64 * q < P) vv[q] = ld_coherent16(p + 2 * (lane + 64 * q));
+    };
+    auto o_landed = [&]() __attribute__((always_inline)) {   // order the reads of vv after a wait
+#pragma unroll
+      for (int q = 0; q < 8; ++q) asm volatile("" : "+v"(vv[q]));
+    };
+    auto o_finish = [&](int x, int r) __attribute__((always_inline)) -> bool {
+      const uint64_t Sx = stamp + uint64_t(x);
+      const uint32_t lo = uint32_t(Sx), hi = uint32_t(Sx >> 32);
+      bool ok = true;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (lane + 64 * q < P) {
+          ok = ok && vv[q].x == lo && vv[q].z == hi;
+          mx = fmaxf(mx, __uint_as_float(vv[q].y));
+        }
+      if (!__all(ok)) return false;
+      mx = wave_max(mx);
+      float zs = 0.f;
+      if (mx != -INFINITY)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (lane + 64 * q < P) {
+            const float mq = __uint_as_float(vv[q].y);
+            if (mq != -INFINITY) zs += __uint_as_float(vv[q].w) * ex2(mq - mx);
+          }
+      zs = wave_sum(zs);
+      const float c = (mx == -INFINITY || !(zs > 0.f)) ? -INFINITY : mx + log2f(zs);
+      if (lane == 0) {
+        uint64_t *o = xnrm + (int64_t(x) * R16 + r) * 2;
+        st_word(o, c, lo);
+        st_word(o + 1, c, hi);
+      }
+      return true;
+    };
+    // a row that must be finished now: retry until every partial is in (bounded)
+    auto o_force = [&](int x, int r) __attribute__((always_inline)) {
+      bool done = false;
+      const uint32_t lim = timed_out ? 1u : spins;   // after one wait ran out, one try only
+      for (uint32_t sp = 0; !done && sp < lim; ++sp) {
+        if (sp) __builtin_amdgcn_s_sleep(2);
+        o_issue(x, r);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        o_landed();
+        done = o_finish(x, r);
+      }
+      if (!done) timed_out = true;
+    };
+    // the owned row of unit x, or -1
+    auto o_row = [&](int x) __attribute__((always_inline)) {
+      const int r = int((int64_t(wgi) - int64_t(x) * R16 % G + G) % G);
+      return r < R ? r : -1;
+    };
+
+    issue_k(0);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (k < npc) issue_m_piece(0, k);
+    if (units > 1) issue_k(1);
+    for (int u = 0; u < units; ++u) {
+      if (u + 1 < units) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      fu_barrier();
+      if (owner) {
+        // the loads issued at the previous top are older than K(u + 1): they have landed
+        o_landed();
+        if (oc >= 0) {
+          const bool done = o_finish(oc, orow);
+          if (!done && oc + FU_LAG <= u) o_force(oc, orow);   // due: unit oc + 1 + FU_LAG needs it
+          if (done || oc + FU_LAG <= u) oc = -1;
+        }
+        while (oc < 0 && onext <= u - 2) {                    // partials of unit u - 2 are out
+          const int x = onext++;
+          const int r = o_row(x);
+          if (r >= 0) {
+            oc = x;
+            orow = r;
+          }
+        }
+        if (oc >= 0) o_issue(oc, orow);
+      }
+      const uint16_t *kr = lds + (u % KSTAGES) * STAGE + pp * MD;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        if (c < 4) {
+#pragma unroll
+          for (int k = 2 * c; k < 2 * c + 2; ++k)
+            if (k < npc && u + 1 < units) issue_m_piece(u + 1, k);
+        } else if (u + 2 < units) {
+          issue_k_piece(u + 2, 2 * (c - 4));
+          issue_k_piece(u + 2, 2 * (c - 4) + 1);
+        }
+        if (KBAR) kbar_step(kr, c);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (owner) {
+      // The loads of the last top may still be in flight, and the compiler's own wait
+      // insertion does not see loads written in inline assembly: o_force would build its
+      // addresses in vv's registers and a late return would overwrite them. Wait first.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      o_landed();
+      // the rows still open, in unit order, each waited for
+      if (oc >= 0 && !o_finish(oc, orow)) o_force(oc, orow);
+      for (int x = onext; x < units; ++x) {
+        const int r = o_row(x);
+        if (r >= 0) o_force(x, r);
+      }
+    }
+    fu_barrier();                                    // the ring is free (matches the consumers)
+    float *kt = reinterpret_cast<float *>(lds) + 2 * MFMA_TILE;
+    constexpr int KT_ROW = MD + 4;
+    if (KBAR) {
+      const float inv = 1.0f / float(units);
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        *reinterpret_cast<float4 *>(kt + pp * KT_ROW + 64 * hc + 4 * q) =
+            make_float4(kb[4 * q] * inv, kb[4 * q + 1] * inv, kb[4 * q + 2] * inv, kb[4 * q + 3] * inv);
+    }
+    fu_barrier();
+    if (KBAR) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int pr = 32 * pw + 2 * q + (lane >> 5);
+        const float4 v = *reinterpret_cast<const float4 *>(kt + pr * KT_ROW + 4 * (lane & 31));
+        if (pr < ne) reinterpret_cast<float4 *>(base + z.off_kbar() + int64_t(pos_of(pr)) * MD)[lane & 31] = v;
+      }
+    }
+    if (timed_out && host_fault) __hip_atomic_store(host_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    return;
+  }
+
+  // ---------------- consumers
+  const int rh = w & 1, ph = w >> 1, p0 = 64 * ph;
+  const int jr = lane & 31, hl = lane >> 5;
+  const int mrow = 32 * rh + jr;                    // this lane's memory row
+  const bool real_row = mrow < R;
+  // LDS: key entry p0 + 32 t + jr (16-byte chunk slots swizzled by jr & 15) and the split
+  // memory row (channel block cb at chunk ((cb % 4) * 4 + cb / 4) * 2, then lo, swizzled)
+  // the entry (within the tile) of slot value v of block t, and of the lane's scattered sum
+  auto entry_of = [&](int tb, int v) __attribute__((always_inline)) { return p0 + 32 * tb + 8 * (v >> 2) + 4 * hl + (v & 3); };
+  const int my_a = lane & 31;
+  const int my_entry = entry_of(my_a >> 4, my_a & 15);
+  // bit a of vmask: slot value a (block a / 16, value a % 16) is an entry of the tile
+  uint32_t vmask = 0u;
+#pragma unroll
+  for (int a = 0; a < 32; ++a) vmask |= uint32_t(entry_of(a >> 4, a & 15) < ne) << a;
+  f32x16 X[FU_SLOTS][2];
+  float mh[FU_SLOTS];
+#pragma unroll
+  for (int i = 0; i < FU_SLOTS; ++i) {
+    X[i][0] = f32x16{};
+    X[i][1] = f32x16{};
+    mh[i] = -INFINITY;
+  }
+  float pos_acc = 0.f;
+  uint64_t pre0 = 0, pre1 = 0;                       // normaliser words of the next unit to finish
+  auto prefetch = [&](int x) __attribute__((always_inline)) {
+    if (real_row) {
+      const uint64_t *p = xnrm + (int64_t(x) * R16 + mrow) * 2;
+      pre0 = ld_word(p);
+      pre1 = ld_word(p + 1);
+    }
+  };
+  // finish unit x: weight its rows by exp2(m - c), sum over the rows (reduce-scatter)
+  auto fin = [&](int x, f32x16 (&E)[2], float m) __attribute__((always_inline)) {
+    const uint64_t Sx = stamp + uint64_t(x);
+    const uint32_t lo = uint32_t(Sx), hi = uint32_t(Sx >> 32);
+    const bool need = real_row && m != -INFINITY;
+    uint64_t a = pre0, b = pre1;
+    auto ready = [&]() __attribute__((always_inline)) { return uint32_t(a) == lo && uint32_t(b) == hi; };
+    uint32_t sp = 0;
+    const uint32_t lim = timed_out ? 0u : spins;     // after one wait ran out, no more waiting
+    while (!__all(!need || ready()) && sp < lim) {
+      __builtin_amdgcn_s_sleep(1);
+      if (need && !ready()) {
+        const uint64_t *p = xnrm + (int64_t(x) * R16 + mrow) * 2;
+        a = ld_word(p);
+        b = ld_word(p + 1);
+      }
+      ++sp;
+    }
+    if (!__all(!need || ready())) timed_out = true;
+    const float c = __uint_as_float(uint32_t(a >> 32));
+    const float f = need && ready() && c != -INFINITY ? ex2(m - c) : 0.f;
+    // a row that takes no part adds an exact zero (a pad row's logits come from stale LDS)
+    const bool add = need && f != 0.f;
+    float r[32];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      r[q] = add ? f * E[0][q] : 0.f;
+      r[16 + q] = add ? f * E[1][q] : 0.f;
+    }
+    // reduce-scatter over the 32 lanes of the half: in the step on bit b the lane keeps the
+    // indices whose bit b equals its own and adds a partner's, a lane with the other bit b
+    // and the same higher bits (lane ^ 16, then within a row its mirror, half-row mirror,
+    // quad mirror and quad neighbour: DPP moves). The lane ends with index lane % 32.
+    int lb = lane;
+    asm volatile("" : "+v"(lb));
+    auto rs_step = [&](auto mov, int sb) __attribute__((always_inline)) {
+      const bool up = (lb & sb) != 0;
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        if (q < sb) {
+          const float keep = up ? r[q + sb] : r[q];
+          const float give = up ? r[q] : r[q + sb];
+          r[q] = keep + mov(give);
+        }
+    };
+    rs_step([&](float x) __attribute__((always_inline)) { return __shfl_xor(x, 16, WAVE); }, 16);
+    rs_step([](float x) __attribute__((always_inline)) { return dpp_mov<0x140>(x); }, 8);   // row_mirror
+    rs_step([](float x) __attribute__((always_inline)) { return dpp_mov<0x141>(x); }, 4);   // row_half_mirror
+    rs_step([](float x) __attribute__((always_inline)) { return dpp_mov<0x1B>(x); }, 2);    // quad_perm [3,2,1,0]
+    rs_step([](float x) __attribute__((always_inline)) { return dpp_mov<0xB1>(x); }, 1);    // quad_perm [1,0,3,2]
+    pos_acc += r[0];
+  };
+  auto stats_store = [&](int x, float m, float zsum) __attribute__((always_inline)) {
+    if (hl == 0 && real_row) {
+      const uint64_t Sx = stamp + uint64_t(x);
+      uint64_t *o = xpart + ((int64_t(x) * R16 + mrow) * P + 2 * wgi + ph) * 2;
+      st_word(o, m, uint32_t(Sx));
+      st_word(o + 1, zsum, uint32_t(Sx >> 32));
+    }
+  };
+  // the last unit's row statistics, without MFMAs to hide them under
+  auto last_stats = [&](f32x16 (&E)[2], float &mo) __attribute__((always_inline)) {
+    float m = -INFINITY, zsum = 0.f;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if (!((vmask >> (16 * tb + q)) & 1u)) E[tb][q] = -INFINITY;
+        m = fmaxf(m, E[tb][q]);
+      }
+    m = fmaxf(m, __shfl_xor(m, 32, WAVE));
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        E[tb][q] = m == -INFINITY ? 0.f : ex2(E[tb][q] - m);
+        zsum += E[tb][q];
+      }
+    zsum += __shfl_xor(zsum, 32, WAVE);
+    mo = m;
+    stats_store(units - 1, m, zsum);
+  };
+  // unit v's MFMAs into C, with unit v - 1's row statistics (slot E, max mo) folded in
+  // Steps past the last unit (v >= units) run no MFMAs: step `units` takes the last unit's
+  // statistics, and the steps up to units + FU_LAG finish the units still open.
+  auto step = [&](int v, f32x16 (&C)[2], float &mc, f32x16 (&E)[2], float &mo) __attribute__((always_inline)) {
+    if (v - 1 - FU_LAG >= 0 && v - 1 - FU_LAG < units) fin(v - 1 - FU_LAG, C, mc);
+    if (v - FU_LAG >= 0 && v - FU_LAG < units) prefetch(v - FU_LAG);
+    if (v >= units) {
+      if (v == units) last_stats(E, mo);
+      return;
+    }
+    fu_barrier();                                    // stage v in LDS
+    const bool epi = v >= 1;
+    // lane constants re-derived in every step: hoisted out of the unit loop they would
+    // stay live across it (address offsets per k-step, the entry mask)
+    int lx = lane;
+    asm volatile("" : "+v"(lx));
+    uint32_t vm = vmask;
+    asm volatile("" : "+v"(vm));
+    const int ljr = lx & 31, lhl = lx >> 5, lsw = lx & 15, lrow = 32 * rh + ljr;
+    const uint16_t *kl = lds + (v % KSTAGES) * STAGE + (p0 + ljr) * MD;
+    const uint16_t *mb = lds + KSTAGES * STAGE + (v & 1) * MSTAGE + lrow * 256;
+    bf16x8 ka0[2], ka1[2], mhi[2], mlo[2];
+    auto read_ks = [&](int ks, int bsel) __attribute__((always_inline)) {
+      const int cb = 2 * ks + lhl;
+      const int ko = (cb ^ lsw) * 8;
+      const int mc = (((cb & 3) * 4 + (cb >> 2)) * 2) ^ lsw;
+      ka0[bsel] = *reinterpret_cast<const bf16x8 *>(kl + ko);
+      ka1[bsel] = *reinterpret_cast<const bf16x8 *>(kl + 32 * MD + ko);
+      mhi[bsel] = *reinterpret_cast<const bf16x8 *>(mb + mc * 8);
+      mlo[bsel] = *reinterpret_cast<const bf16x8 *>(mb + (mc ^ 1) * 8);
+    };
+    C[0] = f32x16{};
+    C[1] = f32x16{};
+    read_ks(0, 0);
+    float m = -INFINITY, zsum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const int bs = ks & 1;
+      if (ks + 1 < 8) read_ks(ks + 1, bs ^ 1);
+      C[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0[bs], mhi[bs], C[0], 0, 0, 0);
+      C[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka1[bs], mhi[bs], C[1], 0, 0, 0);
+      C[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka0[bs], mlo[bs], C[0], 0, 0, 0);
+      C[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka1[bs], mlo[bs], C[1], 0, 0, 0);
+      if (epi) {
+        if (ks < 2) {                                 // block ks: mask past the tile, row maximum
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            if (!((vm >> (16 * ks + q)) & 1u)) E[ks][q] = -INFINITY;
+            m = fmaxf(m, E[ks][q]);
+          }
+          if (ks == 1) m = fmaxf(m, __shfl_xor(m, 32, WAVE));
+        } else if (ks < 6) {                          // exp2 of eight values
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const int a = 8 * (ks - 2) + q, tb = a >> 4, qq = a & 15;
+            E[tb][qq] = m == -INFINITY ? 0.f : ex2(E[tb][qq] - m);
+          }
+        } else if (ks == 6) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) zsum += E[0][q] + E[1][q];
+          zsum += __shfl_xor(zsum, 32, WAVE);
+        } else {
+          mo = m;
+          stats_store(v - 1, m, zsum);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  for (int v0 = 0; v0 <= units + FU_LAG; v0 += FU_SLOTS) {
+    step(v0, X[0], mh[0], X[4], mh[4]);
+    step(v0 + 1, X[1], mh[1], X[0], mh[0]);
+    step(v0 + 2, X[2], mh[2], X[1], mh[1]);
+    step(v0 + 3, X[3], mh[3], X[2], mh[2]);
+    step(v0 + 4, X[4], mh[4], X[3], mh[3]);
+  }
+  fu_barrier();                                      // the ring is free: reuse it for the reduction
+  float *red = reinterpret_cast<float *>(lds);       // [2][MFMA_TILE]
+  red[rh * MFMA_TILE + my_entry] = pos_acc;
+  fu_barrier();
+  if (t < ne) scores[s.slot_off + pos_of(t)] = red[t] + red[MFMA_TILE + t];
+  if (timed_out && host_fault) __hip_atomic_store(host_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // ------------------------------------------------------------------ first pass, unit-major (R <= 64, even Hkv)
 // The first pass needs no sum over units per position, so it runs unit by unit: a
 // workgroup owns one head pair of one layer and a chunk of CH positions. The memory
@@ -1577,6 +2057,58 @@ __global__ void __launch_bounds__(256) k_pool7(const ikv_session *__restrict__ s
 
 hipError_t launch_residual(const ScoreArgs &a, hipStream_t st);
 
+// ---- the one-key-pass form at R <= 64 (k_score_fused): when it applies, and its exchange area
+namespace {
+
+// Workgroups a cooperative launch of k_score_fused may hold on the current device (0: none).
+int fused_capacity() {
+  static int cap[64];
+  static bool known[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!known[dev]) {
+    int a = 0, b = 0, cus = 0, coop = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, k_score_fused<true>, WS_THREADS, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k_score_fused<false>, WS_THREADS, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess)
+      a = b = cus = coop = 0;
+    cap[dev] = coop ? std::min(a, b) * cus : 0;
+    known[dev] = true;
+  }
+  return cap[dev];
+}
+
+// Polls of an exchange wait before it gives up: IKV_EXCHANGE_SPINS (read on every call), else 2^20.
+uint32_t fused_spin_limit() {
+  const char *e = getenv("IKV_EXCHANGE_SPINS");
+  if (e == nullptr || e[0] == '\0') return 1u << 20;
+  return uint32_t(strtoul(e, nullptr, 10));
+}
+
+}  // namespace
+
+int fused_tiles(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags) {
+  if (p.D != MD || p.kv_dtype != IKV_BF16 || B != 1) return 0;
+  if (s[0].R <= STASH_MAX_R || s[0].R > 64 || s[0].N <= s[0].C) return 0;
+  if (flags & (IKV_POOL7 | IKV_TWO_PASS)) return 0;
+  const char *e = getenv("IKV_FUSED");               // read on every call; else the two-pass path
+  if (e == nullptr || e[0] == '\0' || e[0] == '0') return 0;
+  const int units = p.L * p.Hkv;
+  if (units >= (1 << 16)) return 0;
+  const int lch = stats_chunk(s[0].N, std::max(1, units / 2));
+  const int64_t tiles = cdiv(s[0].N, lch) * (lch / MFMA_TILE);
+  if (tiles < FU_MIN_TILES || tiles > FU_MAX_TILES || tiles > fused_capacity()) return 0;
+  return int(tiles);
+}
+
+int64_t fused_exchange_floats(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags) {
+  const int tiles = fused_tiles(p, s, B, flags);
+  if (tiles == 0) return 0;
+  const int64_t rows = int64_t(p.L) * p.Hkv * pad16(s[0].R);
+  return align64f(rows * 2 * tiles * 4 + rows * 4);  // two 64-bit words per partial and per normaliser
+}
+
 hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
   const ikv_pool &p = a.pool;
   const int units = p.L * p.Hkv;
@@ -1600,6 +2132,51 @@ hipError_t launch_score_mfma(const ScoreArgs &a, hipStream_t st) {
       k_msplit<<<dim3(MBAR_PARTS, a.B), 256, 0, st>>>(a.sess_dev, a.M, a.ws, a.scores, p.L, p.Hkv, resid);
     }
   const int chunk = stats ? lch : 0;
+  if (a.fused_tiles > 0) {
+    // one key pass: the residual head's set-up first (it reads only M, the query rows' keys
+    // and the weights), then the scores with the exchange of row normalisers
+    if (resid) {
+      constexpr int FOLD_WGS = int((fold_items<MD>() + 511) / 512);
+      const bool kv = a.mfma_resid;
+      const int nfold = kv ? FOLD_WGS : 0;
+      const int extra = (kv ? RES_KEYS : 0) + nfold + 1;
+      KTimer kt_("k_lse_mfma", st);
+      k_lse_mfma<<<dim3(unsigned(extra), a.B), 512, 0, st>>>(a.sess_dev, a.ws, p.L, p.Hkv, resid, MFMA_TILE, 0,
+                                                             a.slot_maps, a.qpos, p.dead_slot, false, kv, nfold, kp,
+                                                             p.num_slots, a.residual, a.ws_shared);
+    }
+    static const uint64_t tag = [] {
+      std::random_device rd;
+      uint64_t x = (uint64_t(rd()) << 32) ^ rd() ^ uint64_t(getpid()) ^
+                   uint64_t(std::chrono::steady_clock::now().time_since_epoch().count());
+      x &= 0xffffffull;
+      return (x == 0 || x == 0xffffffull ? 0x3c3c3cull : x) << 40;
+    }();
+    static std::atomic<uint64_t> calls{1};
+    uint64_t stamp = tag | ((calls.fetch_add(1) << 16) & ((1ull << 40) - 1));
+    uint32_t spins = fused_spin_limit();
+    uint32_t *fault = host_fault_word();
+    uint64_t *xch = a.xch;
+    const ikv_session *sd = a.sess_dev;
+    const int32_t *sm = a.slot_maps;
+    float *ws = a.ws, *scores = a.scores;
+    int64_t ns = p.num_slots;
+    int L = p.L, Hkv = p.Hkv, dead = p.dead_slot, CH = lch;
+    bool rs = resid;
+    void *args[] = {(void *)&kp, (void *)&ns, (void *)&L, (void *)&Hkv, (void *)&dead, (void *)&sd, (void *)&sm,
+                    (void *)&ws, (void *)&scores, (void *)&rs, (void *)&CH, (void *)&xch, (void *)&stamp,
+                    (void *)&spins, (void *)&fault};
+    {
+      KTimer kt_("k_score_fused", st);
+      const void *fn = resid ? reinterpret_cast<const void *>(k_score_fused<true>)
+                             : reinterpret_cast<const void *>(k_score_fused<false>);
+      hipError_t e = hipLaunchCooperativeKernel(fn, dim3(unsigned(a.fused_tiles)), dim3(WS_THREADS), args, 0, st);
+      if (e != hipSuccess) return e;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !resid) return e;
+    return launch_residual(a, st);
+  }
   if (stats)
     {
       KTimer kt_("k_score_stats", st);

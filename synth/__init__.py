@@ -630,13 +630,52 @@ def read_ceiling(k_pool, v_pool, live, n: int, hpw: int, splits: int, stream_=No
     return out
 
 
+_probe_stamp = [1]
+
+
+def exchange_probe(G: int, U: int, lag: int, mode: int, work_ns: int, device, spins: int = 1 << 16) -> dict:
+    """Time the per-unit normaliser exchange probe (exchange_probe.hip) on a resident grid
+    of G workgroups: U steps of `work_ns` spin each, with (mode 1) or without (mode 0) the
+    exchange, normalisers awaited `lag` steps after their partials. Returns microseconds
+    per step (the median of 5 launches) and the failure bits (1: a reader's wait ran out,
+    2: an owner's)."""
+    import ctypes
+    import torch
+    if not os.path.exists(_SYNTH_LIB):
+        raise RuntimeError(f"{_SYNTH_LIB} is missing: run __graft_entry__.build()")
+    lib = ctypes.CDLL(_SYNTH_LIB)
+    fn = lib.synth_exchange_probe
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    part = torch.zeros(U * 64 * G, dtype=torch.int64, device=device)
+    nrm = torch.zeros(U * 64, dtype=torch.int64, device=device)
+    fail = torch.zeros(1, dtype=torch.int32, device=device)
+    st = torch.cuda.current_stream()
+    times = []
+    for _ in range(6):
+        stamp = _probe_stamp[0]
+        _probe_stamp[0] += U + 1
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        err = fn(part.data_ptr(), nrm.data_ptr(), G, U, lag, mode, work_ns, spins, stamp, fail.data_ptr(),
+                 st.cuda_stream)
+        b.record()
+        if err != 0:
+            raise RuntimeError(f"synth_exchange_probe failed with HIP error {err}")
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e3 / U)
+    return {"us_per_step": round(float(np.median(times[1:])), 3), "fail": int(fail.item())}
+
+
 def build_native(verbose: bool = False) -> str:
-    """Compile table_rows.hip and read_ceiling.hip into synth/libsynth.so (gfx950)."""
+    """Compile table_rows.hip, read_ceiling.hip and exchange_probe.hip into
+    synth/libsynth.so (gfx950)."""
     import shutil
     import subprocess
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     here = os.path.dirname(_SYNTH_LIB)
-    srcs = [os.path.join(here, f) for f in ("table_rows.hip", "read_ceiling.hip")]
+    srcs = [os.path.join(here, f) for f in ("table_rows.hip", "read_ceiling.hip", "exchange_probe.hip")]
     cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", *srcs, "-o", _SYNTH_LIB + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
