@@ -431,37 +431,44 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   }
 }
 
+// Merge the splits of one (session, layer, query head) in one round trip to memory:
+// every thread has its output column of every split in flight while the first
+// nsplit lanes load the splits' (max, sum) and share them through LDS; then, with M
+// the largest split maximum, out = sum_k o_k e^(m_k - M) / sum_k l_k e^(m_k - M).
+// An empty split (m = -inf) weighs zero; a row with no live position gives 0.
 template <typename T, int D>
 __global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ ws, int nsplit, int L, int Hq,
                                                       T *__restrict__ out) {
+  constexpr int SMAX = 64;                         // decode_splits() gives at most 64 splits
+  constexpr int NW = D / 64;
+  __shared__ float sm[SMAX], sl[SMAX], wm[NW];
   const int64_t row = int64_t(blockIdx.y) * L * Hq + blockIdx.x;
   const float *p = ws + row * nsplit * (D + 2);
   const int d = threadIdx.x;
-  constexpr int U = 8;                             // splits in flight per thread
-  float mm = -INFINITY, lsum = 0.f, acc = 0.f;     // online over the splits
-  for (int k0 = 0; k0 < nsplit; k0 += U) {
-    float mk[U], lk[U], ok[U];
+  float ok[SMAX];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = min(k0 + u, nsplit - 1);
-      mk[u] = p[k * (D + 2)];
-      lk[u] = p[k * (D + 2) + 1];
-      ok[u] = p[k * (D + 2) + 2 + d];
-    }
+  for (int k = 0; k < SMAX; ++k) ok[k] = k < nsplit ? p[k * (D + 2) + 2 + d] : 0.f;
+  float mk = -INFINITY;
+  if (d < nsplit) {
+    mk = p[d * (D + 2)];
+    sm[d] = mk;
+    sl[d] = p[d * (D + 2) + 1];
+  }
+  mk = wave_max(mk);
+  if ((d & 63) == 0) wm[d >> 6] = mk;
+  __syncthreads();
+  float M = wm[0];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (k0 + u >= nsplit || mk[u] == -INFINITY) continue;
-      if (mk[u] > mm) {
-        const float f = mm == -INFINITY ? 0.f : expf(mm - mk[u]);
-        lsum = fmaf(lsum, f, lk[u]);
-        acc = fmaf(acc, f, ok[u]);
-        mm = mk[u];
-      } else {
-        const float f = expf(mk[u] - mm);
-        lsum = fmaf(lk[u], f, lsum);
-        acc = fmaf(ok[u], f, acc);
+  for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w]);
+  float acc = 0.f, lsum = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int k = 0; k < SMAX; ++k)
+      if (k < nsplit && sm[k] != -INFINITY) {
+        const float f = expf(sm[k] - M);
+        acc = fmaf(ok[k], f, acc);
+        lsum = fmaf(sl[k], f, lsum);
       }
-    }
   }
   out[row * D + d] = Store<T>::from(lsum > 0.f ? acc / lsum : 0.f);
 }
