@@ -487,6 +487,42 @@ def main() -> int:
         del sg
         log(f"R = G = {sh.G}: {rows_per_head['value']:.0f} tokens/s, {g_ms:.3f} ms per step")
 
+    # The one-key-pass score with the normaliser exchange between resident workgroups
+    # (opt-in, IKV_FUSED=1) on the same inputs as the main step's score call: its time
+    # and its largest relative difference from the main step's scores. Reported beside
+    # the line; the line itself is the default (two-pass) path.
+    one_pass = None
+    if (args.workload == "qwen3_8b_32k" and args.scorer == "intentkv" and 16 < s.R <= 64 and len(batch.sessions) == 1
+            and sh.D == 128 and batch.kv_dtype == synth.BF16):
+        prev = os.environ.get("IKV_FUSED")
+        os.environ["IKV_FUSED"] = "1"
+        try:
+            sf = RetentionStep(batch, dev, residual=blob, flags=flags, k_dev=st.k_pool, v_dev=st.v_pool)
+            evf = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+            for k in range(args.warmup + args.steps):
+                sf.reset()
+                if mem_update:
+                    sf.qm_update(float("inf") if args.query_mode else None)
+                if k >= args.warmup:
+                    evf[2 * (k - args.warmup)].record()
+                sf.score()
+                if k >= args.warmup:
+                    evf[2 * (k - args.warmup) + 1].record()
+            torch.cuda.synchronize()
+            f_ms = float(np.median([evf[2 * k].elapsed_time(evf[2 * k + 1]) for k in range(args.steps)]))
+            a, b = st.host("scores"), sf.host("scores")
+            fin = np.isfinite(a) & (a != 0)
+            rel = float(np.max(np.abs(b[fin] - a[fin]) / np.abs(a[fin]))) if fin.any() else 0.0
+            one_pass = {"score_ms": round(f_ms, 4), "two_pass_score_ms": round(float(phase_ms[2]), 4),
+                        "max_rel_diff_vs_two_pass": rel}
+            del sf
+            log(f"one key pass with the exchange: {f_ms:.3f} ms per score call (two passes {phase_ms[2]:.3f})")
+        finally:
+            if prev is None:
+                del os.environ["IKV_FUSED"]
+            else:
+                os.environ["IKV_FUSED"] = prev
+
     # Layout ablation (Table 7): the compact apply path of the standard compactors on the
     # same kept set, left-packing the kept rows (keys re-rotated) into the slots the
     # redirect freed, against the redirect itself. One session only.
@@ -559,6 +595,8 @@ def main() -> int:
         nA_b.append(int(((Sb != st.dead) & ~forced).sum()) if scored(x) else 0)
         sc_b.append(scored(x))
     nA = sum(nA_b)
+    if one_pass is not None:
+        one_pass["gbs_keys_once"] = round(nA * sh.L * sh.Hkv * sh.D * 2 / (one_pass["score_ms"] / 1e3) / 1e9, 1)
     t_ss = (phase_ms[2] + phase_ms[3]) / 1e3
     tokens_per_s = nA / t_ss
 
@@ -650,7 +688,7 @@ def main() -> int:
         "wall_s_timed": round(wall, 3),
         "roofline": roofline,
         "kernels": kernels,
-        "rows_per_query_head": rows_per_head,
+        "rows_per_query_head": rows_per_head, "one_pass_exchange": one_pass,
         "layout_ablation": layout,
         "prefill_span": prefill,
     }
