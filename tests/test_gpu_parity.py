@@ -543,6 +543,25 @@ def test_qwen3_8b_32k_step_full(qwen3_8b):
     print(f"kept-set differences inside the band: {ndiff}")
 
 
+def test_qwen3_8b_32k_step_full_one_pass_exchange(qwen3_8b, dev, monkeypatch):
+    """The same full step with the score call's one-key-pass form (IKV_FUSED=1: every key
+    read once, the row normalisers of Eq. 3 exchanged between resident workgroups), on
+    the same pool, against the full oracle."""
+    batch, blob, st0 = qwen3_8b
+    monkeypatch.setenv("IKV_FUSED", "1")
+    st = RetentionStep(batch, dev, residual=blob, flags=ikv.IKV_RESIDUAL, k_dev=st0.k_pool, v_dev=st0.v_pool)
+    st.reset()
+    ikv.timing(True)
+    try:
+        st.step(update_memory=False)
+        names = [n for n, _ in ikv.timing_read()]
+    finally:
+        ikv.timing(False)
+    assert "k_score_fused" in names, names
+    ndiff = _compare_step(st, batch, 0, blob, ikv.IKV_RESIDUAL, False, xattn_check=True)
+    print(f"kept-set differences inside the band: {ndiff}")
+
+
 @pytest.fixture(scope="module")
 def qwen25_14b(dev):
     batch = synth.qwen25_14b_92k_heavy(R=64)
