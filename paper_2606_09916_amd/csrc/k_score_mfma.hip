@@ -1045,7 +1045,8 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 // workgroup (x * R16 + r) mod G, one row every G / R16 units. At the top of a unit it
 // checks the partials its loads of the previous top returned, stores the row's stamped
 // normaliser when every partial is in and reissues the loads when not; it waits only
-// when the row is due (FU_LAG units after the partials).
+// when the row is due (at the top of unit x + FU_LAG, the last top before a tile
+// finishes unit x).
 // Consumers (waves 0-3): wave c takes memory rows 32 (c & 1) .. + 31 against entries
 // 64 (c >> 1) .. + 63, as two 32 x 32 blocks of v_mfma_f32_32x32x16_bf16 (keys as A,
 // split memory rows as B, hi then lo): lane l holds row 32 (c & 1) + l % 32 and 32
@@ -1060,6 +1061,10 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
 // (a random per-process tag above a call counter), so leftovers of other calls and of
 // other data never pass. Every wait is bounded (`spins` polls); one that runs out sets
 // the host fault word, which the library's next call reports as IKV_EHIP.
+//
+// The form is opt-in (IKV_FUSED=1): at the Qwen3-8B 32k shape a normaliser lands 7-12 us
+// after its unit's last partial, while FU_LAG units of work take about 6 us, so the
+// tiles wait at almost every unit and the call is slower than the two key passes.
 constexpr int FU_LAG = 4;
 constexpr int FU_SLOTS = FU_LAG + 1;
 constexpr int FU_MIN_TILES = 64;                 // >= 64 rows per unit: one owned row per unit at most
