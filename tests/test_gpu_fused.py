@@ -82,6 +82,27 @@ def test_fused_scores_against_oracle_and_two_pass(dev, monkeypatch, N, R, dead, 
     print(f"N={N} R={R}: worst relative score error {rel:.2e}")
 
 
+@pytest.mark.parametrize("L,Hkv,N,R", [(3, 3, 9500, 40), (1, 1, 16000, 64), (5, 1, 8300, 24)])
+def test_fused_unit_counts(dev, monkeypatch, L, Hkv, N, R):
+    """Unit counts that are not a multiple of a head pair (odd KV heads, one layer): the
+    owner of row r of unit x is workgroup (x * R16 + r) mod G whatever the count, and
+    the units past the last one only finish. Rule path against the oracle and its
+    closed form, and against the two-pass form."""
+    batch = _batch(N, R, 0.2, seed=L * 100 + Hkv * 10 + R, L=L, Hkv=Hkv)
+    st, names = _score(dev, batch, 0, None, monkeypatch, fused=True)
+    assert "k_score_fused" in names, names
+    sets = _sets(batch)
+    want = oracle.scores(batch.k_pool, batch.S(0), sets, batch.M_of(0), Hkv, R, None, 0, batch.qpos_of(0),
+                         synth.DEAD_SLOT)
+    cand = sets["cand"]
+    got = st.host("scores")
+    rel = check_scores(got, want, cand, floor=SCORE_FLOOR)
+    assert rel < 1e-5, rel
+    assert math.isclose(float(got[cand].astype(np.float64).sum()), L * Hkv * R, rel_tol=1e-5)
+    st2, _ = _score(dev, batch, 0, None, monkeypatch, fused=False)
+    check_scores(st2.host("scores"), want, cand, floor=SCORE_FLOOR)
+
+
 def test_fused_is_deterministic(dev, monkeypatch):
     batch = _batch(9000, 64, 0.1, seed=77)
     a, _ = _score(dev, batch, 0, None, monkeypatch, fused=True)
