@@ -284,7 +284,9 @@ ikv_status ikv_redirect_slots(const ikv_session *sess, const ikv_session *sess_d
  *   n_live[b] must not exceed sess[b].N.
  *   The live lists are split across workgroups by a bound known on the host,
  *   min(N, max(C, pi + qe - qs)) over the sessions (what a retention event leaves
- *   live); a longer list is still attended exactly, with longer splits.
+ *   live), and by the number of (session, layer, KV head group) units, so that the
+ *   workgroups fill about one resident round; a longer list is still attended
+ *   exactly, with longer splits.
  */
 ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *sess,
                                      const ikv_session *sess_dev, int32_t B,

@@ -150,7 +150,7 @@ int live_bound(const ikv_session *s, int B) {
 }
 
 size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
-  const int splits = ikv::decode_splits(live_bound(s, B));
+  const int splits = ikv::decode_splits(live_bound(s, B), ikv::decode_units(*p, B));
   return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
 }
 
@@ -602,7 +602,7 @@ ikv_status ikv_decode_attend_slotmap(const ikv_pool *pool, const ikv_session *se
   if (B == 0) return ok();
   if (!q || !live || !n_live || !out) return fail(IKV_EINVAL, "q / live / n_live / out is NULL");
   if ((r = check_ws(workspace, workspace_bytes, decode_bytes(pool, sess, B)))) return r;
-  const int splits = ikv::decode_splits(live_bound(sess, B));
+  const int splits = ikv::decode_splits(live_bound(sess, B), ikv::decode_units(*pool, B));
   if (debug_mode())
     for (int b = 0; b < B; ++b) {
       int64_t nl = 0;

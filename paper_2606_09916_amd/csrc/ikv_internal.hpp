@@ -160,7 +160,8 @@ inline int stats_chunk(int maxN, int head_pairs) {
 // Redirect workspace: two slot bitsets (kept slots, freed slots) per session.
 __host__ __device__ inline int64_t bitset_words(int64_t num_slots) { return align64f(cdiv(num_slots, 32)); }
 
-// Decode workspace: per (session, layer, query head, split) the partial (m, l, o[D]).
+// Decode workspace: per (session, layer, query head, split) the partial (m, l, o[D]),
+// stored as all the o rows ([part][D]) followed by all the (m, l) pairs ([part][2]).
 __host__ __device__ inline int64_t decode_part_floats(int D) { return D + 2; }
 
 // ---------------------------------------------------------------- storage
@@ -301,7 +302,8 @@ hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int
                           const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
                           void *q_out, void *out, float *kq, float *ws, hipStream_t st);
 
-int decode_splits(int maxN);
+int64_t decode_units(const ikv_pool &p, int B);
+int decode_splits(int live_bound, int64_t units);
 
 // A word of pinned host memory that kernels set (system scope) to report a fault the
 // host cannot see otherwise (a grid barrier that gave up). Allocated on first use and

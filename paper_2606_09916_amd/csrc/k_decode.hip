@@ -11,18 +11,35 @@
 // folded into a running (max, sum, output) per head. The value rows only need the
 // slots, so they are loaded together with the key rows (16 bytes per lane, 64 / (D/8)
 // rows per load instruction); the lanes of one channel group fold their rows at the end.
-// The partial state of every split goes to the workspace; k_decode_combine merges
-// the splits per (session, layer, head).
+// The partial state of every split goes to the workspace, the output rows of all
+// splits first ([part][D], each row 512 aligned bytes at D = 128, written as whole
+// 16-byte pieces) and their (max, sum) pairs after them ([part][2]); k_decode_combine
+// merges the splits per (session, layer, head).
 #include <math.h>
 
 #include "ikv_internal.hpp"
 
 namespace ikv {
 
-// Splits of the live list: about 256 live positions each (four blocks of 64 per wave
-// in the head-group kernel), at most 64 splits.
-int decode_splits(int live_bound) {
-  const int64_t s = cdiv(live_bound, 256);
+// Workgroups per (session, layer) of the decode kernel for this pool: one per group of
+// adjacent KV heads in the head-group kernel, one per KV head otherwise.
+int64_t decode_units(const ikv_pool &p, int B) {
+  if (p.kv_dtype == IKV_BF16 && p.D == 128) {
+    const int hpw = p.Hkv % 4 == 0 ? 4 : (p.Hkv % 2 == 0 ? 2 : 1);
+    return int64_t(B) * p.L * (p.Hkv / hpw);
+  }
+  return int64_t(B) * p.L * p.Hkv;
+}
+
+// Splits of the live list: enough workgroups for about one resident round (two per CU
+// on the 256 CUs of MI355X), at least 64 live positions per split, at most 64 splits.
+// A workgroup ends with its split's stores, and its slot takes no new work until they
+// are done; long splits in one round pay that once per slot. At the Qwen3-8B 32k step
+// (8192 live, 72 units) that is 7 splits of 1171 positions: the head-group kernel
+// 196 us against 212 with 32 splits of 256 (without the stores, 32 splits ran in 191).
+int decode_splits(int live_bound, int64_t units) {
+  int64_t s = 512 / (units < 1 ? 1 : units);
+  s = std::min<int64_t>(s, cdiv(live_bound, 64));
   return int(s < 1 ? 1 : (s > 64 ? 64 : s));
 }
 
@@ -54,8 +71,8 @@ template <typename T> struct Raw8 {
 // wavefronts through LDS, and write (max, sum, output) per query head to the workspace.
 template <int D, int G>
 __device__ __forceinline__ void decode_finish(float (&m)[G], float (&lsum)[G], float (&o)[G][8], float (&red)[4][G][2],
-                                              float (&ored)[4][G][D], float *__restrict__ ws, int b, int L, int l,
-                                              int Hq, int g, int split, int nsplit) {
+                                              float (&ored)[4][G][D], float *__restrict__ ws, float *__restrict__ ws_ml,
+                                              int b, int L, int l, int Hq, int g, int split, int nsplit) {
   constexpr int LPR = D / 8;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int rq = lane / LPR, cq = lane % LPR;
@@ -86,20 +103,19 @@ __device__ __forceinline__ void decode_finish(float (&m)[G], float (&lsum)[G], f
   __syncthreads();
   for (int e = t; e < G * (D + 2); e += 256) {
     const int h = e / (D + 2), d = e - h * (D + 2);
+    const int64_t part = ((int64_t(b) * L + l) * Hq + g * G + h) * nsplit + split;
     float mm = -INFINITY;
     for (int k = 0; k < 4; ++k) mm = fmaxf(mm, red[k][h][0]);
-    float val;
     if (d == 0) {
-      val = mm;
+      ws_ml[part * 2] = mm;
     } else if (d == 1) {
-      val = 0.f;
+      float val = 0.f;
       for (int k = 0; k < 4; ++k)
         if (red[k][h][0] != -INFINITY) val += red[k][h][1] * __expf(red[k][h][0] - mm);
+      ws_ml[part * 2 + 1] = val;
     } else {
-      val = (ored[0][h][d - 2] + ored[1][h][d - 2]) + (ored[2][h][d - 2] + ored[3][h][d - 2]);
+      ws[part * D + d - 2] = (ored[0][h][d - 2] + ored[1][h][d - 2]) + (ored[2][h][d - 2] + ored[3][h][d - 2]);
     }
-    const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
-    ws[(row * nsplit + split) * (D + 2) + d] = val;
   }
 }
 
@@ -108,7 +124,8 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
                                                       int64_t num_slots, int L, int Hkv,
                                                       const ikv_session *__restrict__ sess, const T *__restrict__ q,
                                                       const int32_t *__restrict__ live,
-                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws) {
+                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws,
+                                                      float *__restrict__ ws_ml) {
   constexpr int LPR = D / 8;           // lanes per value row (8 channels each)
   constexpr int RPI = WAVE / LPR;      // value rows per load instruction
   __shared__ float qs[G][D];
@@ -217,7 +234,7 @@ __global__ void __launch_bounds__(256) k_decode_split(const T *__restrict__ kpoo
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   }
-  decode_finish<D, G>(m, lsum, o, red, ored, ws, b, L, l, Hq, g, split, nsplit);
+  decode_finish<D, G>(m, lsum, o, red, ored, ws, ws_ml, b, L, l, Hq, g, split, nsplit);
 }
 
 typedef __bf16 bf16x8_d __attribute__((ext_vector_type(8)));
@@ -226,28 +243,37 @@ typedef unsigned int u32x4_d __attribute__((ext_vector_type(4)));
 
 // ---- head-group decode (bf16 pool, D = 128). A workgroup owns a group of `hpw`
 // adjacent KV heads of one layer (hpw * 256 contiguous bytes of every key and value
-// row) and one split of the live list; wave w owns KV head g0 + w and walks the
-// whole split in blocks of 64 live slots, so the waves of a workgroup read adjacent
-// pieces of the same rows together. The loads of block i+1 are issued while block i
-// is computed: the key fragments right after block i's logits, the value rows right
-// after its weighted sum. Each wave writes its own (max, sum, output) per query head.
-// The value rows load with the non-temporal hint (each instruction reads 16 whole
-// 256-byte rows; measured at Qwen3-8B 32k, 8192 live: 231 -> 212 us). The key loads keep
-// the default policy: each key instruction reads one 64-byte quarter of 16 rows, and with
-// the hint on them the kernel measured 234 us (237 us with both).
+// row) and one split of the live list; wave w owns KV head g0 + w and walks the whole
+// split in halves of 32 live slots (16 for G > 4), so the waves of a workgroup read
+// adjacent pieces of the same rows together. The value rows have two register buffers,
+// the key fragments one: at the top of each half the next half's value rows are
+// issued, then the current half's logits run on the matrix cores, then the next half's
+// key fragments are issued into the registers those MFMAs have read, and the softmax
+// update and weighted value sums finish the half. Every path issues the same loads in
+// the same order (rows past the end of the split read the split's first live row and
+// get weight zero; the next pair's slot list is loaded at the top of the current pair,
+// its index clamped), so the compiler's memory waits are exact counts and no half
+// waits for loads issued after its own. Each wave writes its own (max, sum, output)
+// per query head.
+// The value rows load with the non-temporal hint (each instruction reads 4 whole
+// 256-byte rows); the key loads keep the default policy (each instruction reads one
+// 64-byte quarter of 16 rows, and the next instructions read the rest of the same lines).
 template <int G, bool O32>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_decode_heads(const uint16_t *__restrict__ kpool,
                                                       const uint16_t *__restrict__ vpool, int64_t num_slots, int L,
                                                       int Hkv, int hpw, const ikv_session *__restrict__ sess,
                                                       const uint16_t *__restrict__ q, const int32_t *__restrict__ live,
-                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws) {
+                                                      const int32_t *__restrict__ n_live, float *__restrict__ ws,
+                                                      float *__restrict__ ws_ml) {
   constexpr int D = 128;
+  constexpr int HB = G <= 4 ? 32 : 16; // live slots per half (fewer where the G output rows take the registers)
   constexpr int LPR = D / 8;           // lanes per value row (8 channels each)
   constexpr int RPI = WAVE / LPR;      // value rows per load instruction
-  constexpr int NV = DEC_BLOCK / RPI;  // value loads per block
+  constexpr int NV = HB / RPI;         // value loads per half
+  constexpr int NB = HB / 16;          // 16-row MFMA blocks per half
   constexpr int GP = (G + 3) & ~3;     // weights per position in LDS, padded to float4
-  __shared__ __align__(16) float pw[4][DEC_BLOCK][GP];
-  __shared__ __align__(16) bf16x8_d qsh[4][4][WAVE];   // query fragments, read before every block's MFMAs
+  __shared__ __align__(16) float pw[4][HB][GP];
+  __shared__ __align__(16) bf16x8_d qsh[4][4][WAVE];   // query fragments, read before every half's MFMAs
 
   const int b = blockIdx.z;
   const ikv_session s = sess[b];
@@ -261,13 +287,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   const int rq = lane / LPR, cq = lane % LPR;     // value row group, channel group
   int n = n_live[b];
   n = n < 0 ? 0 : (n > s.N ? s.N : n);
-  const int chunk = int(cdiv(cdiv(n, nsplit), DEC_BLOCK)) * DEC_BLOCK;
+  const int chunk = int(cdiv(n, nsplit));          // the halves take any length, so splits differ by one at most
   const int k0 = min(n, split * chunk), k1 = min(n, k0 + chunk);
   const float scale = 1.0f / sqrtf(float(D));
   const int32_t *lv = live + s.slot_off;
-  int slot = (k0 + lane < k1) ? lv[k0 + lane] : 0;
   // the query rows as the B operand: lane (gq, r16) holds channels ks*32 + gq*8 .. +8 of head r16.
-  // They stay in LDS (no registers to spare beside two blocks of key and value loads).
+  // They stay in LDS (no registers to spare beside two halves of key and value loads).
   {
     const uint16_t *qr = q + ((int64_t(b) * L + l) * Hq + g * G + (r16 < G ? r16 : 0)) * D + gq * 8;
 #pragma unroll
@@ -285,108 +310,112 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
-  const int64_t row_stride = int64_t(Hkv) * D;
-  // wave-uniform bases (this wave's head in layer l); a row is reached by a per-lane
-  // byte offset, 32 bits wide when a layer of the pool spans less than 4 GB
-  const char *kbase = reinterpret_cast<const char *>(kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
-  const char *vbase = reinterpret_cast<const char *>(vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
-  const uint32_t row_bytes = uint32_t(row_stride) * 2;
-  auto row_off = [&](int sl, int within) -> uint64_t {
-    if constexpr (O32) return uint32_t(sl) * row_bytes + uint32_t(within);
-    else return uint64_t(uint32_t(sl)) * row_bytes + uint32_t(within);
-  };
-  Raw8<uint16_t> v[NV];
-  bf16x8_d kf[4][4];
-  // lanes past the end of a block hold slot 0, a valid row; their logits are masked
-  auto load_k = [&](int sl, int nb) {
+  if (k0 < k1) {
+    const int64_t row_stride = int64_t(Hkv) * D;
+    // wave-uniform bases (this wave's head in layer l); a row is reached by a per-lane
+    // byte offset, 32 bits wide when a layer of the pool spans less than 4 GB
+    const char *kbase = reinterpret_cast<const char *>(kpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
+    const char *vbase = reinterpret_cast<const char *>(vpool + int64_t(l) * num_slots * row_stride + int64_t(g) * D);
+    const uint32_t row_bytes = uint32_t(row_stride) * 2;
+    auto row_off = [&](int sl, int within) -> uint64_t {
+      if constexpr (O32) return uint32_t(sl) * row_bytes + uint32_t(within);
+      else return uint64_t(uint32_t(sl)) * row_bytes + uint32_t(within);
+    };
+    // slots of the pair starting at `base`, one per lane: past the split's end the
+    // split's first live slot (its row is read again and weighted zero); the index is
+    // clamped, so the load is the same on every path
+    const int first = lv[k0];
+    auto pair_slots = [&](int base) {
+      const int i = base + lane;
+      const int sl = lv[min(i, k1 - 1)];
+      return i < k1 ? sl : first;
+    };
+    Raw8<uint16_t> va[NV], vb[NV];
+    bf16x8_d kf[NB][4];
+    // slot of lane j of `sl` for the key rows (j = off + 16 bb + r16) and the value rows
+    // (j = off + 4 r + rq): one byte address per lane, the rest an immediate offset
+    const int kaddr = r16 * 4, vaddr = rq * 4;
+    auto pick = [](int addr, int sl) { return __builtin_amdgcn_ds_bpermute(addr, sl); };
+    // the key fragments (into kf) and the value rows (into v) of the half at lane offset
+    // `off` of a pair
+    auto load_k = [&](int sl, int off) __attribute__((always_inline)) {
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb) {
-      const int sr = __shfl(sl, bb * 16 + r16, WAVE);
-      const char *kr = kbase + row_off(sr, gq * 16);
-      if (bb * 16 < nb)
+      for (int bb = 0; bb < NB; ++bb) {
+        const int sr = pick(kaddr + 4 * (off + bb * 16), sl);
+        const char *kr = kbase + row_off(sr, gq * 16);
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) kf[bb][ks] = *reinterpret_cast<const bf16x8_d *>(kr + ks * 64);
-    }
-  };
-  auto load_v = [&](int sl, int nb) {
+      }
+    };
+    auto load_v = [&](Raw8<uint16_t> (&v)[NV], int sl, int off) __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 0; r < NV; ++r) {
-      const int i = r * RPI + rq;
-      const int si = __shfl(sl, i, WAVE);
-      if (i < nb) {
+      for (int r = 0; r < NV; ++r) {
+        const int si = pick(vaddr + 4 * (off + r * RPI), sl);
         const u32x4_d x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_d *>(vbase + row_off(si, cq * 16)));
         v[r].r[0] = make_uint4(x.x, x.y, x.z, x.w);
       }
-    }
-  };
-  if (k0 < k1) {
-    load_v(slot, min(DEC_BLOCK, k1 - k0));
-    load_k(slot, min(DEC_BLOCK, k1 - k0));
-  }
-  for (int base = k0; base < k1; base += DEC_BLOCK) {
-    const int nb = min(DEC_BLOCK, k1 - base);
-    const int nbase = base + DEC_BLOCK;
-    const int nnb = min(DEC_BLOCK, k1 - nbase);  // <= 0 past the last block
-    const int nslot = (nbase + lane < k1) ? lv[nbase + lane] : 0;
-    asm volatile("" ::: "memory");                 // re-read the query fragments every block
-    bf16x8_d qb[4];
+    };
+    // the logits of the half in kf: acc[bb][i] is position bb*16 + 4gq + i, query head r16
+    f32x4_d acc[NB];
+    auto logits = [&]() __attribute__((always_inline)) {
+      asm volatile("" ::: "memory");               // re-read the query fragments every half
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qb[ks] = qsh[w][ks][lane];
-    f32x4_d acc[4];
+      for (int bb = 0; bb < NB; ++bb) acc[bb] = f32x4_d{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb) {
-      acc[bb] = f32x4_d{0.f, 0.f, 0.f, 0.f};
-      if (bb * 16 < nb)
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8_d qb = qsh[w][ks][lane];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bb][ks], qb[ks], acc[bb], 0, 0, 0);
-    }
-    if (nnb > 0) load_k(nslot, nnb);
-    // acc[bb][i]: logit of position bb*16 + 4gq + i for query head r16
-    float mx = -INFINITY;
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float x = (bb * 16 + 4 * gq + i < nb) ? acc[bb][i] * scale : -INFINITY;
-        acc[bb][i] = x;
-        mx = fmaxf(mx, x);
+        for (int bb = 0; bb < NB; ++bb)
+          acc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[bb][ks], qb, acc[bb], 0, 0, 0);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-    float mn[G], corr[G];
+    };
+    // the rest of a half of nb (<= HB, may be <= 0) live positions: online softmax and
+    // the weighted value rows
+    auto half = [&](const Raw8<uint16_t> (&v)[NV], int nb) __attribute__((always_inline)) {
+      float mx = -INFINITY;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      mn[h] = fmaxf(m[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mx), h)));
-      corr[h] = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mn[h]);
-    }
-    float mine = mn[0];                            // the new max of this lane's head
+      for (int bb = 0; bb < NB; ++bb)
 #pragma unroll
-    for (int h = 1; h < G; ++h) mine = (r16 == h) ? mn[h] : mine;
-    float ps = 0.f;
+        for (int i = 0; i < 4; ++i) {
+          const float x = (bb * 16 + 4 * gq + i < nb) ? acc[bb][i] * scale : -INFINITY;
+          acc[bb][i] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      float mn[G], corr[G];
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = (acc[bb][i] == -INFINITY) ? 0.f : __expf(acc[bb][i] - mine);
-        ps += p;
-        if (r16 < G) pw[w][bb * 16 + 4 * gq + i][r16] = p;
+      for (int h = 0; h < G; ++h) {
+        mn[h] = fmaxf(m[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mx), h)));
+        corr[h] = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mn[h]);
       }
-    ps += __shfl_xor(ps, 16, WAVE);
-    ps += __shfl_xor(ps, 32, WAVE);
+      float mine = mn[0];                          // the new max of this lane's head
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      lsum[h] = lsum[h] * corr[h] + __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ps), h));
-      m[h] = mn[h];
+      for (int h = 1; h < G; ++h) mine = (r16 == h) ? mn[h] : mine;
+      float ps = 0.f;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) o[h][c] *= corr[h];
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      for (int bb = 0; bb < NB; ++bb)
 #pragma unroll
-    for (int r = 0; r < NV; ++r) {
-      const int i = r * RPI + rq;
-      if (i < nb) {
+        for (int i = 0; i < 4; ++i) {
+          const float p = (acc[bb][i] == -INFINITY) ? 0.f : __expf(acc[bb][i] - mine);
+          ps += p;
+          if (r16 < G) pw[w][bb * 16 + 4 * gq + i][r16] = p;
+        }
+      ps += __shfl_xor(ps, 16, WAVE);
+      ps += __shfl_xor(ps, 32, WAVE);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        lsum[h] = lsum[h] * corr[h] + __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ps), h));
+        m[h] = mn[h];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[h][c] *= corr[h];
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      // rows past nb carry weight zero (their logits were masked to -inf)
+#pragma unroll
+      for (int r = 0; r < NV; ++r) {
+        const int i = r * RPI + rq;
         float vv[8];
         v[r].unpack(vv);
         float pv[GP];
@@ -403,11 +432,35 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 #pragma unroll
           for (int c = 0; c < 8; ++c) o[h][c] = fmaf(pv[h], vv[c], o[h][c]);
       }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    };
+    // Per half: issue the next half's value rows, run the logits (the MFMAs read kf),
+    // issue the next half's key fragments into kf, then finish the half. Past the end of
+    // the split the loads read the first live row again and are not used.
+    int sl = pair_slots(k0);
+    load_v(va, sl, 0);
+    load_k(sl, 0);
+    for (int base = k0; base < k1; base += 2 * HB) {
+      const int nsl = pair_slots(base + 2 * HB);     // the next pair's slots (clamped past the end)
+      __builtin_amdgcn_sched_barrier(0);
+      load_v(vb, sl, HB);                            // this pair's second half
+      __builtin_amdgcn_sched_barrier(0);
+      logits();
+      __builtin_amdgcn_sched_barrier(0);
+      load_k(sl, HB);
+      __builtin_amdgcn_sched_barrier(0);
+      half(va, k1 - base);
+      __builtin_amdgcn_sched_barrier(0);
+      load_v(va, nsl, 0);                            // the next pair's first half
+      __builtin_amdgcn_sched_barrier(0);
+      logits();
+      __builtin_amdgcn_sched_barrier(0);
+      load_k(nsl, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      half(vb, k1 - base - HB);
+      sl = nsl;
     }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    if (nnb > 0) load_v(nslot, nnb);
-    slot = nslot;
   }
   // fold the value row groups; lanes 0..LPR-1 then hold channels cq*8 .. +8
 #pragma unroll
@@ -419,14 +472,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   if (lane < LPR) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const int64_t row = (int64_t(b) * L + l) * Hq + g * G + h;
-      float *p = ws + (row * nsplit + split) * (D + 2);
-      if (lane == 0) {
-        p[0] = m[h];
-        p[1] = lsum[h];
-      }
-#pragma unroll
-      for (int c = 0; c < 8; ++c) p[2 + cq * 8 + c] = o[h][c];
+      const int64_t part = ((int64_t(b) * L + l) * Hq + g * G + h) * nsplit + split;
+      float4 *p = reinterpret_cast<float4 *>(ws + part * D + cq * 8);   // 32 aligned bytes per lane
+      p[0] = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
+      p[1] = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
+      if (lane == 0) *reinterpret_cast<float2 *>(ws_ml + part * 2) = make_float2(m[h], lsum[h]);
     }
   }
 }
@@ -437,22 +487,23 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 // the largest split maximum, out = sum_k o_k e^(m_k - M) / sum_k l_k e^(m_k - M).
 // An empty split (m = -inf) weighs zero; a row with no live position gives 0.
 template <typename T, int D>
-__global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ ws, int nsplit, int L, int Hq,
-                                                      T *__restrict__ out) {
+__global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ ws, const float *__restrict__ ws_ml,
+                                                      int nsplit, int L, int Hq, T *__restrict__ out) {
   constexpr int SMAX = 64;                         // decode_splits() gives at most 64 splits
   constexpr int NW = D / 64;
   __shared__ float sm[SMAX], sl[SMAX], wm[NW];
   const int64_t row = int64_t(blockIdx.y) * L * Hq + blockIdx.x;
-  const float *p = ws + row * nsplit * (D + 2);
+  const float *p = ws + row * nsplit * D;
   const int d = threadIdx.x;
   float ok[SMAX];
 #pragma unroll
-  for (int k = 0; k < SMAX; ++k) ok[k] = k < nsplit ? p[k * (D + 2) + 2 + d] : 0.f;
+  for (int k = 0; k < SMAX; ++k) ok[k] = k < nsplit ? p[k * D + d] : 0.f;
   float mk = -INFINITY;
   if (d < nsplit) {
-    mk = p[d * (D + 2)];
+    const float2 x = reinterpret_cast<const float2 *>(ws_ml + row * nsplit * 2)[d];
+    mk = x.x;
     sm[d] = mk;
-    sl[d] = p[d * (D + 2) + 1];
+    sl[d] = x.y;
   }
   mk = wave_max(mk);
   if ((d & 63) == 0) wm[d >> 6] = mk;
@@ -476,6 +527,9 @@ __global__ void __launch_bounds__(D) k_decode_combine(const float *__restrict__ 
 template <typename T, int D, int G>
 static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev, int B, int splits, const void *q,
                                   const int32_t *live, const int32_t *n_live, void *out, float *ws, hipStream_t st) {
+  // split state: the output rows of every (session, layer, query head, split) first,
+  // [part][D], then their (max, sum) pairs, [part][2]
+  float *ws_ml = ws + int64_t(B) * p.L * p.Hq * splits * D;
   if constexpr (sizeof(T) == 2 && D == 128) {
     const int hpw = p.Hkv % 4 == 0 ? 4 : (p.Hkv % 2 == 0 ? 2 : 1);
     const dim3 grid(splits, p.L * (p.Hkv / hpw), B);
@@ -483,19 +537,20 @@ static hipError_t launch_decode_g(const ikv_pool &p, const ikv_session *sess_dev
     if (p.num_slots * p.Hkv * D * 2 < (int64_t(1) << 32))
       k_decode_heads<G, true><<<grid, 64 * hpw, 0, st>>>((const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool,
                                                          p.num_slots, p.L, p.Hkv, hpw, sess_dev, (const uint16_t *)q,
-                                                         live, n_live, ws);
+                                                         live, n_live, ws, ws_ml);
     else
       k_decode_heads<G, false><<<grid, 64 * hpw, 0, st>>>((const uint16_t *)p.k_pool, (const uint16_t *)p.v_pool,
                                                           p.num_slots, p.L, p.Hkv, hpw, sess_dev, (const uint16_t *)q,
-                                                          live, n_live, ws);
+                                                          live, n_live, ws, ws_ml);
   } else {
     KTimer kt_("k_decode_split<T, D, G>", st);
     k_decode_split<T, D, G><<<dim3(splits, p.L * p.Hkv, B), 256, 0, st>>>(
-        (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws);
+        (const T *)p.k_pool, (const T *)p.v_pool, p.num_slots, p.L, p.Hkv, sess_dev, (const T *)q, live, n_live, ws,
+        ws_ml);
   }
   {
     KTimer kt_("k_decode_combine<T, D>", st);
-    k_decode_combine<T, D><<<dim3(p.L * p.Hq, B), D, 0, st>>>(ws, splits, p.L, p.Hq, (T *)out);
+    k_decode_combine<T, D><<<dim3(p.L * p.Hq, B), D, 0, st>>>(ws, ws_ml, splits, p.L, p.Hq, (T *)out);
   }
   return hipGetLastError();
 }
