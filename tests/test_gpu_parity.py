@@ -368,11 +368,15 @@ def test_decode_isolated(dev, kind, frac):
 
 
 @pytest.mark.parametrize("Hkv,G,n_live", [(1, 1, 700), (2, 2, 129), (3, 3, 64), (4, 4, 1000), (8, 5, 300),
-                                          (2, 6, 513), (4, 7, 77), (8, 8, 2100)])
+                                          (2, 6, 513), (4, 7, 77), (8, 8, 2100), (4, 4, 3), (8, 8, 1),
+                                          (4, 4, 640)])
 def test_decode_heads_kernel_variants(dev, Hkv, G, n_live):
     """bf16 pool, D = 128: the head-group decode with one, two or four KV heads per
-    workgroup (Hkv odd, 2 mod 4, 0 mod 4), G from 1 to 8, live lists that end inside
-    a 64-slot block or on its boundary, against the oracle."""
+    workgroup (Hkv odd, 2 mod 4, 0 mod 4), G from 1 to 8 (halves of 32 live slots up to
+    G = 4, of 16 above), against the oracle. The live bound of these sessions is 300, so
+    the lists are split five ways: splits that end inside a half or on a pair boundary
+    (640: two whole pairs each), splits shorter than a half, empty splits (3 and 1 live
+    rows), and lists longer than the bound (513, 1000, 2100)."""
     torch = _torch()
     batch = small_d128(R=16, N=max(2400, n_live + 100), seed=7 * Hkv + G, dead_frac=0.0, L=2, Hkv=Hkv, G=G)
     S = batch.S(0)
