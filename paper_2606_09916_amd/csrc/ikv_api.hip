@@ -154,10 +154,21 @@ size_t decode_bytes(const ikv_pool *p, const ikv_session *s, int B) {
   return size_t(B) * p->L * p->Hq * splits * size_t(ikv::decode_part_floats(p->D)) * sizeof(float);
 }
 
-size_t prefill_bytes(const ikv_pool *p, const ikv_session *s, int B) {
+int prefill_splits(const ikv_pool *p, const ikv_session *s, int B) {
+  int64_t keys = 1;
+  for (int b = 0; b < B; ++b) keys = std::max<int64_t>(keys, int64_t(s[b].N) + std::max(0, s[b].qe - s[b].qs));
+  return ikv::prefill_splits(p->L, p->Hkv, B, keys);
+}
+
+int64_t prefill_kq_floats(const ikv_pool *p, const ikv_session *s, int B) {
   int64_t n = 0;
   for (int b = 0; b < B; ++b) n += std::max(0, s[b].qe - s[b].qs);
-  return size_t(n) * p->L * p->D * sizeof(float);
+  return ikv::align64f(n * p->L * p->D);
+}
+
+size_t prefill_bytes(const ikv_pool *p, const ikv_session *s, int B) {
+  return size_t(prefill_kq_floats(p, s, B) +
+                ikv::prefill_part_floats(p->L, p->Hkv, B, prefill_splits(p, s, B), p->D)) * sizeof(float);
 }
 
 ikv_status pending_fault() {
@@ -586,8 +597,9 @@ ikv_status ikv_prefill_span(const ikv_pool *pool, const ikv_session *sess, const
     }
   }
   const float decay = isinf(lambda) ? 0.0f : float(exp(-double(lambda)));
-  return hip_status(ikv::launch_prefill(*pool, sess_dev, B, max_n, slot_maps, q_raw, k_raw, v_raw, hist, n_hist,
-                                        rope_base, decay, M, q_out, out, kq, static_cast<float *>(workspace),
+  return hip_status(ikv::launch_prefill(*pool, sess_dev, B, max_n, prefill_splits(pool, sess, B), slot_maps, q_raw,
+                                        k_raw, v_raw, hist, n_hist, rope_base, decay, M, q_out, out, kq,
+                                        static_cast<float *>(workspace), prefill_kq_floats(pool, sess, B),
                                         (hipStream_t)stream),
                     "ikv_prefill_span");
 }

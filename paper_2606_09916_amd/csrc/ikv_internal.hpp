@@ -297,10 +297,29 @@ hipError_t launch_compact(const ikv_pool &pool, const ikv_session *sess_dev, int
                           const int32_t *slot_maps, const uint8_t *keep, const int32_t *dst, double base,
                           int32_t *n_keep, int32_t *pos_list, hipStream_t st);
 
-hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n,
+// Key splits of the prefill attention (one workgroup per layer, KV head, session and
+// split of the keys): about nine rounds of workgroups on the 256 CUs (one 16-wave
+// workgroup per CU), at most 16 splits and no more than the 64-key tiles of the
+// longest session (history bound N plus the span).
+inline int prefill_splits(int L, int Hkv, int B, int64_t max_keys) {
+  const int64_t units = int64_t(L) * Hkv * (B < 1 ? 1 : B);
+  int64_t s = (2304 + units / 2) / units;
+  const int64_t tiles = (max_keys + 63) / 64;
+  s = s > tiles ? tiles : s;
+  return int(s < 1 ? 1 : (s > 16 ? 16 : s));
+}
+// Prefill workspace: the per-layer parts of the span's mean key rows (span tokens x L x
+// D floats); with more than one split, then the split state of the attention, 256 query
+// rows per (session, layer, KV head, split): the output rows [part][256][D], then their
+// (max, sum) pairs [part][256][2].
+inline int64_t prefill_part_floats(int L, int Hkv, int B, int splits, int D) {
+  return splits > 1 ? int64_t(B) * L * Hkv * splits * 256 * (D + 2) : 0;
+}
+
+hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n, int splits,
                           const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
                           const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
-                          void *q_out, void *out, float *kq, float *ws, hipStream_t st);
+                          void *q_out, void *out, float *kq, float *ws, int64_t kq_floats, hipStream_t st);
 
 int64_t decode_units(const ikv_pool &p, int B);
 int decode_splits(int live_bound, int64_t units);

@@ -11,9 +11,10 @@
 //                   rotated query rows per head (Enc) and, with a memory, the update of
 //                   Eq. 2 in place; per token, the sum of its rotated key rows over the
 //                   KV heads (this layer's part of the mean key row);
-//   k_prefill_attn  one workgroup per (layer, KV head, session): causal attention of
-//                   the span's query rows of the KV head's G query heads over the
-//                   history slots and the span's own slots (matrix cores, below);
+//   k_prefill_attn  one workgroup per (layer, KV head, session, split of the keys):
+//                   causal attention of the span's query rows of the KV head's G query
+//                   heads over the history slots and the span's own slots (matrix
+//                   cores, below); k_prefill_merge combines the splits;
 //   k_prefill_kq    the mean key rows of the span tokens: the layers' parts summed in
 //                   layer order.
 #include <math.h>
@@ -131,22 +132,33 @@ __global__ void __launch_bounds__(PR_THREADS) k_prefill_rope(const ikv_session *
 }
 
 // ------------------------------------------------------------------ causal attention
-// Workgroup (layer l, KV head g, session b), sixteen waves: query row r = h' n + t (h'
-// the query head within the group, t the span token) belongs to wave r / 16. Keys
-// stream in tiles of 64: the history slots, then the span's slots. Per tile a wave
-// computes S^T = K Q^T (16 keys x 16 rows per MFMA block, bf16 inputs exact, float32
-// accumulation), keeps an online (max, sum) per row, and adds O^T += V^T P^T, the
-// weights P split into bf16 hi + lo (two MFMAs; 2^-17 relative). The weights of keys
-// 16 kb + 4 g + i that a lane holds are already the B operand of the second product, up
-// to the order of the contraction index (perm32): the transposed value tile in LDS is
-// read in that order. Key rows stay as loaded (rows of 136 bf16); value rows are
-// written transposed (rows of 72 bf16 per channel).
+// Workgroup (layer l, KV head g, session b, split z), sixteen waves: query row
+// r = h' n + t (h' the query head within the group, t the span token) belongs to wave
+// r / 16. The keys (the history slots, then the span's slots) are cut into 64-key
+// tiles and the tiles into `nsplit` contiguous runs, one per split, so that a long
+// history fills the chip. Per tile a wave computes S^T = K Q^T (16 keys x 16 rows per
+// MFMA block, bf16 inputs exact, float32 accumulation), keeps an online (max, sum) per
+// row, and adds O^T += V^T P^T, the weights P split into bf16 hi + lo (two MFMAs;
+// 2^-17 relative). The weights of keys 16 kb + 4 g + i that a lane holds are already
+// the B operand of the second product, up to the order of the contraction index
+// (perm32): the transposed value tile in LDS is read in that order. Key rows stay as
+// loaded (rows of 136 bf16); value rows are written transposed (rows of 72 bf16 per
+// channel).
+// Loads: two tiles in registers beyond the one in LDS. While tile i is computed, tile
+// i + 1 is on its way and tile i + 2 is issued, and the slot ids of tile i + 3 load
+// before it. Every iteration issues the same loads whatever the split's length (past
+// the keys' end the first span slot is read and masked), so the compiler's memory
+// waits are exact counts.
+// With one split the rows are written normalised; with more, each split writes its
+// unnormalised rows and (max, sum) and k_prefill_merge combines them.
 constexpr int PA_WAVES = 16;
 constexpr int PA_THREADS = PA_WAVES * WAVE;
 constexpr int PA_TILE = 64;
 constexpr int PA_KROW = PD + 8;
 constexpr int PA_VROW = PA_TILE + 8;
+constexpr int PA_ROWS = 256;                     // query rows of a (layer, KV head) at most: n G <= 256
 
+template <bool PART>
 __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *__restrict__ sess, int L, int Hq,
                                                              int Hkv, const uint16_t *__restrict__ kpool,
                                                              const uint16_t *__restrict__ vpool, int64_t num_slots,
@@ -154,10 +166,11 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
                                                              const int32_t *__restrict__ hist,
                                                              const int32_t *__restrict__ n_hist,
                                                              const uint16_t *__restrict__ q_rot,
-                                                             uint16_t *__restrict__ out) {
+                                                             uint16_t *__restrict__ out, float *__restrict__ part_o,
+                                                             float *__restrict__ part_ml) {
   __shared__ __align__(16) uint16_t ks[2][PA_TILE * PA_KROW];
   __shared__ __align__(16) uint16_t vt[2][PD * PA_VROW];
-  const int lg = blockIdx.x, b = blockIdx.y;
+  const int lg = blockIdx.x, b = blockIdx.y, split = blockIdx.z, nsplit = gridDim.z;
   const int l = lg / Hkv, g_kv = lg - l * Hkv;
   const ikv_session s = sess[b];
   const int n = s.qe - s.qs;
@@ -167,6 +180,9 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
   prefill_offsets(sess, b, L, Hq, Hkv, PD, &q_off, &kv_off, &kq_off);
   const int nh = n_hist[b];
   const int T = nh + n;                           // keys: history, then the span
+  const int ntile_all = (T + PA_TILE - 1) / PA_TILE;
+  const int tps = (ntile_all + nsplit - 1) / nsplit;
+  const int tb = min(ntile_all, split * tps), te = min(ntile_all, tb + tps);
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int g = lane >> 4, c = lane & 15;
   const int row = min(16 * w + c, nrows - 1);     // this lane's query row (clamped; the extra rows are never written)
@@ -174,51 +190,47 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
   const bool wave_on = 16 * w < nrows;
   const float scale = 1.4426950408889634f / sqrtf(float(PD));
 
-  // query fragments (B operand of S^T): row `row`, channels 32 ks + 8 g .. + 8
-  bf16x8 qf[4];
-  {
-    const uint16_t *qr = q_rot + q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD;
-#pragma unroll
-    for (int ks4 = 0; ks4 < 4; ++ks4) qf[ks4] = *reinterpret_cast<const bf16x8 *>(qr + 32 * ks4 + 8 * g);
-  }
-  const int32_t *S = slot_maps + s.slot_off;
-  const int32_t *H = hist + s.slot_off;
-  auto key_slot = [&](int kk) -> int64_t {
-    if (kk >= T) return s.qs < s.N ? S[s.qs] : 0;  // past the end: a valid row, masked out
-    return kk < nh ? H[kk] : S[s.qs + (kk - nh)];
-  };
-  // tile loads: thread t takes key t / 16 of the tile, 16-byte chunk t % 16 of its K and V rows
-  const int lk = t >> 4, lc = t & 15;
-  uint4 kreg, vreg;
-  auto load_tile = [&](int tile) {
-    const int64_t slot = key_slot(tile * PA_TILE + lk);
-    const int64_t o = ((int64_t(l) * num_slots + slot) * Hkv + g_kv) * PD + lc * 8;
-    kreg = *reinterpret_cast<const uint4 *>(kpool + o);
-    vreg = *reinterpret_cast<const uint4 *>(vpool + o);
-  };
-  auto store_tile = [&](int stg) {
-    *reinterpret_cast<uint4 *>(&ks[stg][lk * PA_KROW + lc * 8]) = kreg;
-    const uint32_t wv[4] = {vreg.x, vreg.y, vreg.z, vreg.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      vt[stg][(lc * 8 + 2 * e) * PA_VROW + lk] = uint16_t(wv[e] & 0xffffu);
-      vt[stg][(lc * 8 + 2 * e + 1) * PA_VROW + lk] = uint16_t(wv[e] >> 16);
-    }
-  };
-
   float m_run = -INFINITY, l_run = 0.f;          // this lane's row (rows are the lane index c)
   f32x4 o[8];                                     // O^T blocks: channel 16 db + 4 g + i, row c
 #pragma unroll
   for (int db = 0; db < 8; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int ntile = (T + PA_TILE - 1) / PA_TILE;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int tile = 0; tile < ntile; ++tile) {
-    const int stg = tile & 1;
-    if (tile + 1 < ntile) load_tile(tile + 1);
-    if (wave_on) {
+  if (tb < te) {
+    // query fragments (B operand of S^T): row `row`, channels 32 ks + 8 g .. + 8
+    bf16x8 qf[4];
+    {
+      const uint16_t *qr = q_rot + q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD;
+#pragma unroll
+      for (int ks4 = 0; ks4 < 4; ++ks4) qf[ks4] = *reinterpret_cast<const bf16x8 *>(qr + 32 * ks4 + 8 * g);
+    }
+    const int32_t *S = slot_maps + s.slot_off;
+    const int32_t *H = hist + s.slot_off;
+    // tile loads: thread t takes key t / 16 of the tile, 16-byte chunk t % 16 of its K and V rows
+    const int lk = t >> 4, lc = t & 15;
+    // the slot of this thread's key in tile `tile`: one load from the history list or the
+    // span's slots (past the keys' end, the first span slot: a valid row, masked out)
+    auto tile_slot = [&](int tile) -> int32_t {
+      const int kk = tile * PA_TILE + lk;
+      const int32_t *p = kk < nh ? H + kk : S + s.qs + (kk < T ? kk - nh : 0);
+      return *p;
+    };
+    const int64_t lbase = (int64_t(l) * num_slots * Hkv + g_kv) * PD + lc * 8;
+    auto load_kv = [&](int32_t slot, uint4 &kr, uint4 &vr) {
+      const int64_t o = lbase + int64_t(slot) * Hkv * PD;
+      kr = *reinterpret_cast<const uint4 *>(kpool + o);
+      vr = *reinterpret_cast<const uint4 *>(vpool + o);
+    };
+    auto store_tile = [&](int stg, const uint4 &kr, const uint4 &vr) {
+      *reinterpret_cast<uint4 *>(&ks[stg][lk * PA_KROW + lc * 8]) = kr;
+      const uint32_t wv[4] = {vr.x, vr.y, vr.z, vr.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[stg][(lc * 8 + 2 * e) * PA_VROW + lk] = uint16_t(wv[e] & 0xffffu);
+        vt[stg][(lc * 8 + 2 * e + 1) * PA_VROW + lk] = uint16_t(wv[e] >> 16);
+      }
+    };
+    auto compute = [&](int stg, int tile) __attribute__((always_inline)) {
+      if (!wave_on) return;
       // S^T: key blocks kb (keys 16 kb .. + 15), lane (g, c): keys 16 kb + 4 g + i, row c
       f32x4 sacc[4];
 #pragma unroll
@@ -245,6 +257,7 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, WAVE));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, WAVE));
       const float m_new = fmaxf(m_run, tmax);
+      // a row with no key yet (m_new = -inf) keeps zero weights and sums
       const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
       float psum = 0.f;
       float p[4][4];
@@ -284,12 +297,52 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
           o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, o[db], 0, 0, 0);
         }
       }
-    }
-    if (tile + 1 < ntile) store_tile(stg ^ 1);
+    };
+    // the same order of loads as at the top of every later pair (tile + 2's slot, then
+    // tile + 1's rows), so that the waits the compiler places inside the loop stay exact
+    uint4 kA, vA, kB, vB;
+    load_kv(tile_slot(tb), kA, vA);
+    const int32_t sl1 = tile_slot(tb + 1);
+    int32_t sl2 = tile_slot(tb + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    load_kv(sl1, kB, vB);
+    __builtin_amdgcn_sched_barrier(0);
+    store_tile(0, kA, vA);
     __syncthreads();
+    int tile = tb;
+    for (; tile + 1 < te; tile += 2) {
+      // LDS stage 0 holds `tile`; kB, vB tile + 1; kA, vA take tile + 2
+      const int32_t sl3 = tile_slot(tile + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      load_kv(sl2, kA, vA);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0, tile);
+      store_tile(1, kB, vB);
+      __syncthreads();
+      // LDS stage 1 holds tile + 1; kA, vA tile + 2; kB, vB take tile + 3
+      sl2 = tile_slot(tile + 4);
+      __builtin_amdgcn_sched_barrier(0);
+      load_kv(sl3, kB, vB);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1, tile + 1);
+      store_tile(0, kA, vA);
+      __syncthreads();
+    }
+    if (tile < te) compute(0, tile);              // an odd last tile (its successors' loads go unused)
   }
-  // out[l][g_kv G + h'][t][:] = O / l
-  if (wave_on) {
+  if (!wave_on) return;
+  if constexpr (PART) {
+    // this split's rows, unnormalised, and their (max, sum); rows past nrows are not written
+    if (16 * w + c < nrows) {
+      const int64_t pr = ((int64_t(b) * gridDim.x + lg) * nsplit + split) * PA_ROWS + 16 * w + c;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4 *>(part_o + pr * PD + 16 * db + 4 * g) =
+            make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+      if (g == 0) *reinterpret_cast<float2 *>(part_ml + pr * 2) = make_float2(m_run, l_run);
+    }
+  } else {
+    // out[l][g_kv G + h'][t][:] = O / l
     const float inv = 1.0f / l_run;
 #pragma unroll
     for (int db = 0; db < 8; ++db)
@@ -300,6 +353,50 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
           out[q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD + ch] = float_to_bf16_bits(o[db][i] * inv);
       }
   }
+}
+
+// The splits of each query row of the attention: with M the largest split maximum,
+// out = sum_z o_z 2^(m_z - M) / sum_z l_z 2^(m_z - M) (a split that saw no key of the
+// row has m = -inf and weighs zero). Workgroup (layer and KV head, session, 2 rows);
+// thread (row, channel d) has every split's value and (max, sum) in flight at once.
+constexpr int PM_ROWS = 2;
+constexpr int PM_SMAX = 16;                      // prefill_splits() gives at most 16
+__global__ void __launch_bounds__(PM_ROWS * PD) k_prefill_merge(const ikv_session *__restrict__ sess, int L, int Hq,
+                                                                int Hkv, int nsplit, const float *__restrict__ part_o,
+                                                                const float *__restrict__ part_ml,
+                                                                uint16_t *__restrict__ out) {
+  const int lg = blockIdx.x, b = blockIdx.y;
+  const int l = lg / Hkv, g_kv = lg - l * Hkv;
+  const ikv_session s = sess[b];
+  const int n = s.qe - s.qs;
+  const int G = Hq / Hkv, nrows = n * G;
+  const int r = blockIdx.z * PM_ROWS + threadIdx.x / PD, d = threadIdx.x % PD;
+  if (r >= nrows) return;
+  int64_t q_off, kv_off, kq_off;
+  prefill_offsets(sess, b, L, Hq, Hkv, PD, &q_off, &kv_off, &kq_off);
+  const int64_t p0 = (int64_t(b) * gridDim.x + lg) * nsplit * PA_ROWS + r;
+  float oz[PM_SMAX];
+  float2 mz[PM_SMAX];
+#pragma unroll
+  for (int z = 0; z < PM_SMAX; ++z) {
+    const int64_t pz = p0 + int64_t(z < nsplit ? z : 0) * PA_ROWS;
+    oz[z] = part_o[pz * PD + d];
+    mz[z] = reinterpret_cast<const float2 *>(part_ml)[pz];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int z = 0; z < PM_SMAX; ++z)
+    if (z < nsplit) M = fmaxf(M, mz[z].x);
+  float acc = 0.f, lsum = 0.f;
+#pragma unroll
+  for (int z = 0; z < PM_SMAX; ++z)
+    if (z < nsplit && mz[z].x != -INFINITY) {
+      const float f = __builtin_amdgcn_exp2f(mz[z].x - M);
+      acc = fmaf(oz[z], f, acc);
+      lsum = fmaf(mz[z].y, f, lsum);
+    }
+  const int hq = r / n, tr = r - hq * n;
+  out[q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD + d] = float_to_bf16_bits(acc / lsum);
 }
 
 __global__ void __launch_bounds__(128) k_prefill_kq(const ikv_session *__restrict__ sess, int L, int Hq, int Hkv,
@@ -315,10 +412,10 @@ __global__ void __launch_bounds__(128) k_prefill_kq(const ikv_session *__restric
   kq[kq_off + int64_t(t) * D + threadIdx.x] = a / float(L * Hkv);
 }
 
-hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n,
+hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int B, int max_n, int splits,
                           const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
                           const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
-                          void *q_out, void *out, float *kq, float *ws, hipStream_t st) {
+                          void *q_out, void *out, float *kq, float *ws, int64_t kq_floats, hipStream_t st) {
   const dim3 g1(unsigned(pool.L), B);
   {
     KTimer kt_("k_prefill_rope", st);
@@ -337,10 +434,24 @@ hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int
   }
   {
     KTimer kt_("k_prefill_attn", st);
-    k_prefill_attn<<<dim3(unsigned(pool.L * pool.Hkv), B), PA_THREADS, 0, st>>>(
-        sess_dev, pool.L, pool.Hq, pool.Hkv, static_cast<const uint16_t *>(pool.k_pool),
-        static_cast<const uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, hist, n_hist,
-        static_cast<const uint16_t *>(q_out), static_cast<uint16_t *>(out));
+    const dim3 grid(unsigned(pool.L * pool.Hkv), B, unsigned(splits));
+    float *part_o = ws + kq_floats;
+    float *part_ml = part_o + int64_t(B) * pool.L * pool.Hkv * splits * PA_ROWS * PD;
+    if (splits > 1)
+      k_prefill_attn<true><<<grid, PA_THREADS, 0, st>>>(
+          sess_dev, pool.L, pool.Hq, pool.Hkv, static_cast<const uint16_t *>(pool.k_pool),
+          static_cast<const uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, hist, n_hist,
+          static_cast<const uint16_t *>(q_out), static_cast<uint16_t *>(out), part_o, part_ml);
+    else
+      k_prefill_attn<false><<<grid, PA_THREADS, 0, st>>>(
+          sess_dev, pool.L, pool.Hq, pool.Hkv, static_cast<const uint16_t *>(pool.k_pool),
+          static_cast<const uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, hist, n_hist,
+          static_cast<const uint16_t *>(q_out), static_cast<uint16_t *>(out), nullptr, nullptr);
+    if (splits > 1) {
+      KTimer kt2_("k_prefill_merge", st);
+      k_prefill_merge<<<dim3(unsigned(pool.L * pool.Hkv), B, unsigned(PA_ROWS / PM_ROWS)), PM_ROWS * PD, 0, st>>>(
+          sess_dev, pool.L, pool.Hq, pool.Hkv, splits, part_o, part_ml, static_cast<uint16_t *>(out));
+    }
   }
   {
     KTimer kt_("k_prefill_kq", st);
