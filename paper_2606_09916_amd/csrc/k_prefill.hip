@@ -3,14 +3,14 @@
 // the mean of the span's post-RoPE Q rows; Eq. 6: the cross-attention keys are the
 // mean key rows at the query positions). One call per turn, before the retention step:
 //
-//   k_prefill_rope  one workgroup per (layer, session), over the span's tokens in
-//                   order: Neox RoPE at each token's position (pair angles in float64,
-//                   cos / sin in LDS, rotation in float32, one rounding to the pool's
-//                   type) of the query rows (written out) and key rows (written into
-//                   the pool at the span's slots, with the value rows); the sum of the
-//                   rotated query rows per head (Enc) and, with a memory, the update of
-//                   Eq. 2 in place; per token, the sum of its rotated key rows over the
+//   k_prefill_rope  one workgroup per (layer, span token, session): Neox RoPE at the
+//                   token's position (pair angles in float64, cos / sin in LDS, rotation
+//                   in float32, one rounding to the pool's type) of the query rows
+//                   (written out) and key rows (written into the pool at the token's
+//                   slot, with the value rows); the sum of its rotated key rows over the
 //                   KV heads (this layer's part of the mean key row);
+//   k_prefill_memory with a memory, Eq. 2 per (layer, head): Enc from the rotated query
+//                   rows as written, summed in token order;
 //   k_prefill_attn  one workgroup per (layer, KV head, session, split of the keys):
 //                   causal attention of the span's query rows of the KV head's G query
 //                   heads over the history slots and the span's own slots (matrix
@@ -28,9 +28,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int PD = 128;                          // head dimension of the attention kernel
 constexpr int PR_THREADS = 256;
-constexpr int PR_QMAX = 8192;                    // Hq * D: query channels of a layer (Enc in LDS)
 constexpr int PR_KMAX = 2048;                    // Hkv * D: key channels of a layer
-constexpr int PR_QE = PR_QMAX / PR_THREADS;      // query channels per thread
 
 // Per session b: n = qe - qs span tokens; the packed inputs and outputs of the sessions
 // before b: rows of q (Hq per layer) and of k / v (Hkv per layer), and the mean key rows.
@@ -43,6 +41,10 @@ __device__ __forceinline__ void prefill_offsets(const ikv_session *sess, int b, 
   *kq_off = nq * D;
 }
 
+// One workgroup per (layer, span token, session): the token's angles, its rotated query
+// rows (written out), its rotated key rows (into the pool at the token's slot, with the
+// value rows) and this layer's part of its mean key row (the rotated key rows summed
+// over the KV heads in order).
 template <typename T>
 __global__ void __launch_bounds__(PR_THREADS) k_prefill_rope(const ikv_session *__restrict__ sess, int L, int Hq,
                                                              int Hkv, int D, T *__restrict__ kpool,
@@ -50,85 +52,84 @@ __global__ void __launch_bounds__(PR_THREADS) k_prefill_rope(const ikv_session *
                                                              const int32_t *__restrict__ slot_maps,
                                                              const T *__restrict__ q_raw, const T *__restrict__ k_raw,
                                                              const T *__restrict__ v_raw, T *__restrict__ q_out,
-                                                             float *__restrict__ M, float decay, double base,
-                                                             float *__restrict__ kq_part) {
+                                                             double base, float *__restrict__ kq_part) {
   __shared__ float cs[64], sn[64];
-  __shared__ float red[PR_THREADS];
   __shared__ float ksum[PR_KMAX];                // this token's rotated key rows [Hkv][D]
-  __shared__ float encs[PR_QMAX];                // the layer's summed query rows [Hq][D]
-  const int l = blockIdx.x, b = blockIdx.y;
+  const int l = blockIdx.x, t = blockIdx.y, b = blockIdx.z;
+  const ikv_session s = sess[b];
+  const int n = s.qe - s.qs;
+  if (t >= n) return;
+  int64_t q_off, kv_off, kq_off;
+  prefill_offsets(sess, b, L, Hq, Hkv, D, &q_off, &kv_off, &kq_off);
+  const int t0 = threadIdx.x, h2 = D / 2;
+  const int pos = s.qs + t;
+  if (t0 < h2) {
+    const double ang = double(pos) * pow(base, -2.0 * double(t0) / double(D));
+    cs[t0] = float(cos(ang));
+    sn[t0] = float(sin(ang));
+  }
+  __syncthreads();
+  // query rows: element e = (head, channel); channel c < D/2 pairs with c + D/2
+  const int nq_el = Hq * D, nk_el = Hkv * D;
+  for (int e = t0; e < nq_el; e += PR_THREADS) {
+    const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
+    const int64_t base_row = q_off + ((int64_t(l) * Hq + h) * n + t) * D;
+    const float x = Store<T>::ld(q_raw + base_row + c);
+    const float y = Store<T>::ld(q_raw + base_row + (c < h2 ? c + h2 : c - h2));
+    const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
+    q_out[base_row + c] = Store<T>::from(r);
+  }
+  // key rows into the pool at the token's slot, value rows copied
+  const int64_t slot = slot_maps[s.slot_off + pos];
+  for (int e = t0; e < nk_el; e += PR_THREADS) {
+    const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
+    const int64_t src = kv_off + ((int64_t(l) * Hkv + h) * n + t) * D;
+    const float x = Store<T>::ld(k_raw + src + c);
+    const float y = Store<T>::ld(k_raw + src + (c < h2 ? c + h2 : c - h2));
+    const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
+    const T rv = Store<T>::from(r);
+    const int64_t dst = ((int64_t(l) * num_slots + slot) * Hkv + h) * D + c;
+    kpool[dst] = rv;
+    vpool[dst] = v_raw[src + c];
+    ksum[e] = Store<T>::ld(&rv);
+  }
+  __syncthreads();
+  // this layer's part of the token's mean key row: the rotated rows summed over KV heads in order
+  for (int c = t0; c < D; c += PR_THREADS) {
+    float a = 0.f;
+    for (int h = 0; h < Hkv; ++h) a += ksum[h * D + c];
+    kq_part[(kq_off * L) + (int64_t(l) * n + t) * D + c] = a;
+  }
+}
+
+// Eq. 2 for memory row h of layer l (one per query head): Enc is the mean over the span
+// of the rotated query rows as written (summed in token order), M <- decay M + Enc, then
+// the row divided by max(||row||, 1e-12) (the squares summed in a fixed tree order).
+// Workgroup (layer, head, session); thread c is channel c.
+template <typename T>
+__global__ void __launch_bounds__(PD) k_prefill_memory(const ikv_session *__restrict__ sess, int L, int Hq, int Hkv,
+                                                       const T *__restrict__ q_out, float *__restrict__ M,
+                                                       float decay) {
+  __shared__ float red[PD];
+  const int l = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const ikv_session s = sess[b];
   const int n = s.qe - s.qs;
   if (n <= 0) return;
   int64_t q_off, kv_off, kq_off;
-  prefill_offsets(sess, b, L, Hq, Hkv, D, &q_off, &kv_off, &kq_off);
-  const int t0 = threadIdx.x, h2 = D / 2;
-  // the query channels (head, channel) = t0, t0 + 256, ... that this thread sums over the tokens
-  float enc[PR_QE];
-#pragma unroll
-  for (int k = 0; k < PR_QE; ++k) enc[k] = 0.f;
-  const int nq_el = Hq * D, nk_el = Hkv * D;
-  for (int t = 0; t < n; ++t) {
-    const int pos = s.qs + t;
-    if (t0 < h2) {
-      const double ang = double(pos) * pow(base, -2.0 * double(t0) / double(D));
-      cs[t0] = float(cos(ang));
-      sn[t0] = float(sin(ang));
-    }
-    __syncthreads();
-    // query rows: element e = (head, channel); channel c < D/2 pairs with c + D/2
-    for (int e = t0, k = 0; e < nq_el; e += PR_THREADS, ++k) {
-      const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
-      const int64_t base_row = q_off + ((int64_t(l) * Hq + h) * n + t) * D;
-      const float x = Store<T>::ld(q_raw + base_row + c);
-      const float y = Store<T>::ld(q_raw + base_row + (c < h2 ? c + h2 : c - h2));
-      const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
-      const T rv = Store<T>::from(r);
-      q_out[base_row + c] = rv;
-      enc[k] += Store<T>::ld(&rv);
-    }
-    // key rows into the pool at the token's slot, value rows copied
-    const int64_t slot = slot_maps[s.slot_off + pos];
-    for (int e = t0; e < nk_el; e += PR_THREADS) {
-      const int h = e / D, c = e - h * D, i = c < h2 ? c : c - h2;
-      const int64_t src = kv_off + ((int64_t(l) * Hkv + h) * n + t) * D;
-      const float x = Store<T>::ld(k_raw + src + c);
-      const float y = Store<T>::ld(k_raw + src + (c < h2 ? c + h2 : c - h2));
-      const float r = c < h2 ? x * cs[i] - y * sn[i] : x * cs[i] + y * sn[i];
-      const T rv = Store<T>::from(r);
-      const int64_t dst = ((int64_t(l) * num_slots + slot) * Hkv + h) * D + c;
-      kpool[dst] = rv;
-      vpool[dst] = v_raw[src + c];
-      ksum[e] = Store<T>::ld(&rv);
-    }
-    __syncthreads();
-    // this layer's part of the token's mean key row: the rotated rows summed over KV heads in order
-    for (int c = t0; c < D; c += PR_THREADS) {
-      float a = 0.f;
-      for (int h = 0; h < Hkv; ++h) a += ksum[h * D + c];
-      kq_part[(kq_off * L) + (int64_t(l) * n + t) * D + c] = a;
-    }
-    __syncthreads();
-  }
-  if (!M) return;
-  // Eq. 2 for the layer's Hq memory rows (one per query head): M <- decay M + Enc, then
-  // each row divided by max(||row||, 1e-12) (the norm summed in a fixed tree order)
-  for (int e = t0, k = 0; e < nq_el; e += PR_THREADS, ++k) encs[e] = enc[k];
+  prefill_offsets(sess, b, L, Hq, Hkv, PD, &q_off, &kv_off, &kq_off);
+  const int c = threadIdx.x;
+  const T *qr = q_out + q_off + (int64_t(l) * Hq + h) * n * PD + c;
+  float enc = 0.f;
+  for (int t = 0; t < n; ++t) enc += Store<T>::ld(qr + int64_t(t) * PD);
+  float *Mr = M + s.mem_off + (int64_t(l) * Hq + h) * PD;
+  const float v = decay * Mr[c] + enc * (1.0f / float(n));
+  red[c] = v * v;
   __syncthreads();
-  float *Ml = M + s.mem_off + int64_t(l) * Hq * D;
-  const float inv_n = 1.0f / float(n);
-  for (int h = 0; h < Hq; ++h) {
-    const float v = t0 < D ? decay * Ml[int64_t(h) * D + t0] + encs[h * D + t0] * inv_n : 0.f;
-    red[t0] = v * v;
+  for (int off = PD / 2; off > 0; off >>= 1) {
+    if (c < off) red[c] += red[c + off];
     __syncthreads();
-    for (int off = PR_THREADS / 2; off > 0; off >>= 1) {
-      if (t0 < off) red[t0] += red[t0 + off];
-      __syncthreads();
-    }
-    const float norm = fmaxf(sqrtf(red[0]), 1e-12f);
-    __syncthreads();
-    if (t0 < D) Ml[int64_t(h) * D + t0] = v / norm;
   }
+  Mr[c] = v / fmaxf(sqrtf(red[0]), 1e-12f);
 }
 
 // ------------------------------------------------------------------ causal attention
@@ -416,21 +417,30 @@ hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int
                           const int32_t *slot_maps, const void *q_raw, const void *k_raw, const void *v_raw,
                           const int32_t *hist, const int32_t *n_hist, double base, float decay, float *M,
                           void *q_out, void *out, float *kq, float *ws, int64_t kq_floats, hipStream_t st) {
-  const dim3 g1(unsigned(pool.L), B);
   {
     KTimer kt_("k_prefill_rope", st);
+    const dim3 g1(unsigned(pool.L), unsigned(max_n), B);
     if (pool.kv_dtype == IKV_BF16)
       k_prefill_rope<uint16_t><<<g1, PR_THREADS, 0, st>>>(
           sess_dev, pool.L, pool.Hq, pool.Hkv, pool.D, static_cast<uint16_t *>(pool.k_pool),
           static_cast<uint16_t *>(pool.v_pool), pool.num_slots, slot_maps, static_cast<const uint16_t *>(q_raw),
           static_cast<const uint16_t *>(k_raw), static_cast<const uint16_t *>(v_raw), static_cast<uint16_t *>(q_out),
-          M, decay, base, ws);
+          base, ws);
     else
       k_prefill_rope<float><<<g1, PR_THREADS, 0, st>>>(
           sess_dev, pool.L, pool.Hq, pool.Hkv, pool.D, static_cast<float *>(pool.k_pool),
           static_cast<float *>(pool.v_pool), pool.num_slots, slot_maps, static_cast<const float *>(q_raw),
-          static_cast<const float *>(k_raw), static_cast<const float *>(v_raw), static_cast<float *>(q_out), M, decay,
-          base, ws);
+          static_cast<const float *>(k_raw), static_cast<const float *>(v_raw), static_cast<float *>(q_out), base, ws);
+  }
+  if (M) {
+    KTimer kt_("k_prefill_memory", st);
+    const dim3 gm(unsigned(pool.L), unsigned(pool.Hq), B);
+    if (pool.kv_dtype == IKV_BF16)
+      k_prefill_memory<uint16_t><<<gm, PD, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv,
+                                                     static_cast<const uint16_t *>(q_out), M, decay);
+    else
+      k_prefill_memory<float><<<gm, PD, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv,
+                                                  static_cast<const float *>(q_out), M, decay);
   }
   {
     KTimer kt_("k_prefill_attn", st);
