@@ -133,9 +133,10 @@ __global__ void __launch_bounds__(PD) k_prefill_memory(const ikv_session *__rest
 }
 
 // ------------------------------------------------------------------ causal attention
-// Workgroup (layer l, KV head g, session b, split z), sixteen waves: query row
+// Workgroup (layer l, KV head g, session b, split z), eight waves: query row
 // r = h' n + t (h' the query head within the group, t the span token) belongs to wave
-// r / 16. The keys (the history slots, then the span's slots) are cut into 64-key
+// r / 32, as row r % 16 of its row block (r / 16) % 2; each key and value fragment a
+// wave reads from LDS feeds the MFMAs of both its row blocks. The keys (the history slots, then the span's slots) are cut into 64-key
 // tiles and the tiles into `nsplit` contiguous runs, one per split, so that a long
 // history fills the chip. Per tile a wave computes S^T = K Q^T (16 keys x 16 rows per
 // MFMA block, bf16 inputs exact, float32 accumulation), keeps an online (max, sum) per
@@ -152,12 +153,19 @@ __global__ void __launch_bounds__(PD) k_prefill_memory(const ikv_session *__rest
 // waits are exact counts.
 // With one split the rows are written normalised; with more, each split writes its
 // unnormalised rows and (max, sum) and k_prefill_merge combines them.
-constexpr int PA_WAVES = 16;
+constexpr int PA_WAVES = 8;
 constexpr int PA_THREADS = PA_WAVES * WAVE;
 constexpr int PA_TILE = 64;
 constexpr int PA_KROW = PD + 8;
 constexpr int PA_VROW = PA_TILE + 8;
 constexpr int PA_ROWS = 256;                     // query rows of a (layer, KV head) at most: n G <= 256
+constexpr int PA_RB = 2;                         // 16-row blocks per wave: 32 rows, so each key and
+                                                 // value fragment read from LDS feeds two MFMAs
+// The transposed value tile stores key k of channel ch at k ^ vt_swz(ch): a multiple of
+// 4 that changes with the channel group, so four consecutive keys stay adjacent (one
+// 8-byte read) while the 16-bit stores of a wave's 16 channel groups spread over the
+// LDS banks instead of landing on four of them.
+__device__ __forceinline__ int vt_swz(int ch) { return ((ch >> 3) & 15) << 2; }
 
 template <bool PART>
 __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *__restrict__ sess, int L, int Hq,
@@ -186,173 +194,229 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
   const int tb = min(ntile_all, split * tps), te = min(ntile_all, tb + tps);
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int g = lane >> 4, c = lane & 15;
-  const int row = min(16 * w + c, nrows - 1);     // this lane's query row (clamped; the extra rows are never written)
-  const int hq = row / n, tr = row - hq * n;
-  const bool wave_on = 16 * w < nrows;
+  // this lane's query rows, one per 16-row block (clamped; the extra rows are never written)
+  int hq[PA_RB], tr[PA_RB];
+#pragma unroll
+  for (int rb = 0; rb < PA_RB; ++rb) {
+    const int row = min(32 * w + 16 * rb + c, nrows - 1);
+    hq[rb] = row / n;
+    tr[rb] = row - hq[rb] * n;
+  }
+  const bool wave_on = 32 * w < nrows;
   const float scale = 1.4426950408889634f / sqrtf(float(PD));
 
-  float m_run = -INFINITY, l_run = 0.f;          // this lane's row (rows are the lane index c)
-  f32x4 o[8];                                     // O^T blocks: channel 16 db + 4 g + i, row c
+  float m_run[PA_RB], l_run[PA_RB];              // per row block: this lane's row (rows are the lane index c)
+  f32x4 o[PA_RB][8];                              // O^T blocks: channel 16 db + 4 g + i, row c
 #pragma unroll
-  for (int db = 0; db < 8; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int rb = 0; rb < PA_RB; ++rb) {
+    m_run[rb] = -INFINITY;
+    l_run[rb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) o[rb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
   if (tb < te) {
-    // query fragments (B operand of S^T): row `row`, channels 32 ks + 8 g .. + 8
-    bf16x8 qf[4];
-    {
-      const uint16_t *qr = q_rot + q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD;
+    // query fragments (B operand of S^T): row block rb, channels 32 ks + 8 g .. + 8
+    bf16x8 qf[PA_RB][4];
 #pragma unroll
-      for (int ks4 = 0; ks4 < 4; ++ks4) qf[ks4] = *reinterpret_cast<const bf16x8 *>(qr + 32 * ks4 + 8 * g);
+    for (int rb = 0; rb < PA_RB; ++rb) {
+      const uint16_t *qr = q_rot + q_off + ((int64_t(l) * Hq + g_kv * G + hq[rb]) * n + tr[rb]) * PD;
+#pragma unroll
+      for (int ks4 = 0; ks4 < 4; ++ks4) qf[rb][ks4] = *reinterpret_cast<const bf16x8 *>(qr + 32 * ks4 + 8 * g);
     }
     const int32_t *S = slot_maps + s.slot_off;
     const int32_t *H = hist + s.slot_off;
-    // tile loads: thread t takes key t / 16 of the tile, 16-byte chunk t % 16 of its K and V rows
+    // tile loads: thread t takes keys t / 16 and t / 16 + 32 of the tile, 16-byte chunk
+    // t % 16 of their K and V rows
     const int lk = t >> 4, lc = t & 15;
-    // the slot of this thread's key in tile `tile`: one load from the history list or the
-    // span's slots (past the keys' end, the first span slot: a valid row, masked out)
-    auto tile_slot = [&](int tile) -> int32_t {
-      const int kk = tile * PA_TILE + lk;
+    // the slots of this thread's two keys in tile `tile`: one load each from the history
+    // list or the span's slots (past the keys' end, the first span slot: a valid row,
+    // masked out)
+    auto tile_slot = [&](int tile, int half) __attribute__((always_inline)) -> int32_t {
+      const int kk = tile * PA_TILE + lk + 32 * half;
       const int32_t *p = kk < nh ? H + kk : S + s.qs + (kk < T ? kk - nh : 0);
       return *p;
     };
     const int64_t lbase = (int64_t(l) * num_slots * Hkv + g_kv) * PD + lc * 8;
-    auto load_kv = [&](int32_t slot, uint4 &kr, uint4 &vr) {
-      const int64_t o = lbase + int64_t(slot) * Hkv * PD;
-      kr = *reinterpret_cast<const uint4 *>(kpool + o);
-      vr = *reinterpret_cast<const uint4 *>(vpool + o);
+    struct Regs { uint4 k0, v0, k1, v1; };     // keys lk and lk + 32 (plain members: kept in registers)
+    struct Slots { int32_t s0, s1; };
+    auto slots = [&](int tile) __attribute__((always_inline)) { return Slots{tile_slot(tile, 0), tile_slot(tile, 1)}; };
+    auto load_kv = [&](const Slots &sl, Regs &r) __attribute__((always_inline)) {
+      const int64_t o0 = lbase + int64_t(sl.s0) * Hkv * PD, o1 = lbase + int64_t(sl.s1) * Hkv * PD;
+      r.k0 = *reinterpret_cast<const uint4 *>(kpool + o0);
+      r.v0 = *reinterpret_cast<const uint4 *>(vpool + o0);
+      r.k1 = *reinterpret_cast<const uint4 *>(kpool + o1);
+      r.v1 = *reinterpret_cast<const uint4 *>(vpool + o1);
     };
-    auto store_tile = [&](int stg, const uint4 &kr, const uint4 &vr) {
-      *reinterpret_cast<uint4 *>(&ks[stg][lk * PA_KROW + lc * 8]) = kr;
+    auto store_one = [&](int stg, int key, const uint4 &kr, const uint4 &vr) __attribute__((always_inline)) {
+      *reinterpret_cast<uint4 *>(&ks[stg][key * PA_KROW + lc * 8]) = kr;
       const uint32_t wv[4] = {vr.x, vr.y, vr.z, vr.w};
+      const int kp = key ^ vt_swz(lc * 8);          // channels lc*8 .. +7 share one swizzle
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        vt[stg][(lc * 8 + 2 * e) * PA_VROW + lk] = uint16_t(wv[e] & 0xffffu);
-        vt[stg][(lc * 8 + 2 * e + 1) * PA_VROW + lk] = uint16_t(wv[e] >> 16);
+        vt[stg][(lc * 8 + 2 * e) * PA_VROW + kp] = uint16_t(wv[e] & 0xffffu);
+        vt[stg][(lc * 8 + 2 * e + 1) * PA_VROW + kp] = uint16_t(wv[e] >> 16);
       }
+    };
+    auto store_tile = [&](int stg, const Regs &r) __attribute__((always_inline)) {
+      store_one(stg, lk, r.k0, r.v0);
+      store_one(stg, lk + 32, r.k1, r.v1);
     };
     auto compute = [&](int stg, int tile) __attribute__((always_inline)) {
       if (!wave_on) return;
-      // S^T: key blocks kb (keys 16 kb .. + 15), lane (g, c): keys 16 kb + 4 g + i, row c
-      f32x4 sacc[4];
+      const bool hist_tile = (tile + 1) * PA_TILE <= nh;   // wave-uniform
+      // S^T: key blocks kb (keys 16 kb .. + 15), lane (g, c): keys 16 kb + 4 g + i, row c of block rb
+      f32x4 sacc[PA_RB][4];
+#pragma unroll
+      for (int rb = 0; rb < PA_RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) sacc[rb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
         const uint16_t *kr = &ks[stg][(16 * kb + c) * PA_KROW];
 #pragma unroll
-        for (int ks4 = 0; ks4 < 4; ++ks4)
-          sacc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8 *>(kr + 32 * ks4 + 8 * g),
-                                                             qf[ks4], sacc[kb], 0, 0, 0);
+        for (int ks4 = 0; ks4 < 4; ++ks4) {
+          const bf16x8 kfr = *reinterpret_cast<const bf16x8 *>(kr + 32 * ks4 + 8 * g);
+#pragma unroll
+          for (int rb = 0; rb < PA_RB; ++rb)
+            sacc[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kfr, qf[rb][ks4], sacc[rb][kb], 0, 0, 0);
+        }
       }
-      // mask (keys past the end; span keys after this row's token) and the online softmax
-      float tmax = -INFINITY;
+      // per row block: mask (keys past the end; span keys after the row's token), the
+      // online softmax, and the weights split into bf16 hi + lo for the second product
+      bf16x8 ph[PA_RB][2], pl[PA_RB][2];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+      for (int rb = 0; rb < PA_RB; ++rb) {
+        float tmax = -INFINITY;
+        if (hist_tile) {                            // every key of the tile is history: nothing masked
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kk = tile * PA_TILE + 16 * kb + 4 * g + i;
-          const bool ok = kk < T && (kk < nh || kk - nh <= tr);
-          const float x = ok ? sacc[kb][i] * scale : -INFINITY;
-          sacc[kb][i] = x;
-          tmax = fmaxf(tmax, x);
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float x = sacc[rb][kb][i] * scale;
+              sacc[rb][kb][i] = x;
+              tmax = fmaxf(tmax, x);
+            }
+        } else {
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int kk = tile * PA_TILE + 16 * kb + 4 * g + i;
+              const bool ok = kk < T && (kk < nh || kk - nh <= tr[rb]);
+              const float x = ok ? sacc[rb][kb][i] * scale : -INFINITY;
+              sacc[rb][kb][i] = x;
+              tmax = fmaxf(tmax, x);
+            }
         }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, WAVE));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, WAVE));
-      const float m_new = fmaxf(m_run, tmax);
-      // a row with no key yet (m_new = -inf) keeps zero weights and sums
-      const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      float psum = 0.f;
-      float p[4][4];
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 16, WAVE));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, WAVE));
+        const float m_new = fmaxf(m_run[rb], tmax);
+        // a row with no key yet (m_new = -inf) keeps zero weights and sums
+        const float corr = m_run[rb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[rb] - m_new);
+        float psum = 0.f;
+        float p[4][4];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          p[kb][i] = sacc[kb][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sacc[kb][i] - m_new);
-          psum += p[kb][i];
-        }
-      psum += __shfl_xor(psum, 16, WAVE);
-      psum += __shfl_xor(psum, 32, WAVE);
-      l_run = l_run * corr + psum;
-      m_run = m_new;
+          for (int i = 0; i < 4; ++i) {
+            p[kb][i] = sacc[rb][kb][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sacc[rb][kb][i] - m_new);
+            psum += p[kb][i];
+          }
+        psum += __shfl_xor(psum, 16, WAVE);
+        psum += __shfl_xor(psum, 32, WAVE);
+        l_run[rb] = l_run[rb] * corr + psum;
+        // the outputs are rescaled only when some row's maximum moved (corr = 1 otherwise)
+        if (__builtin_amdgcn_ballot_w64(m_new != m_run[rb]) != 0)
 #pragma unroll
-      for (int db = 0; db < 8; ++db)
+          for (int db = 0; db < 8; ++db)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[db][i] *= corr;
-      // O^T += V^T P^T over two 32-key steps; k index 8 g + e stands for key perm32(g, e)
+            for (int i = 0; i < 4; ++i) o[rb][db][i] *= corr;
+        m_run[rb] = m_new;
+        // k index 8 g + e of 32-key step st2 stands for key perm32(g, e)
+#pragma unroll
+        for (int st2 = 0; st2 < 2; ++st2)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float v = e < 4 ? p[2 * st2][e] : p[2 * st2 + 1][e - 4];
+            ph[rb][st2][e] = __bf16(v);
+            pl[rb][st2][e] = __bf16(v - float(ph[rb][st2][e]));
+          }
+      }
+      // O^T += V^T P^T over two 32-key steps, each value fragment shared by the row blocks
 #pragma unroll
       for (int st2 = 0; st2 < 2; ++st2) {
-        bf16x8 ph, pl;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float v = e < 4 ? p[2 * st2][e] : p[2 * st2 + 1][e - 4];
-          ph[e] = __bf16(v);
-          pl[e] = __bf16(v - float(ph[e]));
-        }
 #pragma unroll
         for (int db = 0; db < 8; ++db) {
-          const uint16_t *vr = &vt[stg][(16 * db + c) * PA_VROW + 32 * st2];
-          const uint2 a = *reinterpret_cast<const uint2 *>(vr + 4 * g);
-          const uint2 bq = *reinterpret_cast<const uint2 *>(vr + 16 + 4 * g);
+          const uint16_t *vr = &vt[stg][(16 * db + c) * PA_VROW];
+          const int sw = vt_swz(16 * db + c);
+          const uint2 a = *reinterpret_cast<const uint2 *>(vr + ((32 * st2 + 4 * g) ^ sw));
+          const uint2 bq = *reinterpret_cast<const uint2 *>(vr + ((32 * st2 + 16 + 4 * g) ^ sw));
           const uint4 av = make_uint4(a.x, a.y, bq.x, bq.y);
           const bf16x8 va = __builtin_bit_cast(bf16x8, av);
-          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph, o[db], 0, 0, 0);
-          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl, o[db], 0, 0, 0);
+#pragma unroll
+          for (int rb = 0; rb < PA_RB; ++rb) {
+            o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, ph[rb][st2], o[rb][db], 0, 0, 0);
+            o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl[rb][st2], o[rb][db], 0, 0, 0);
+          }
         }
       }
     };
-    // the same order of loads as at the top of every later pair (tile + 2's slot, then
+    // the same order of loads as at the top of every later pair (tile + 2's slots, then
     // tile + 1's rows), so that the waits the compiler places inside the loop stay exact
-    uint4 kA, vA, kB, vB;
-    load_kv(tile_slot(tb), kA, vA);
-    const int32_t sl1 = tile_slot(tb + 1);
-    int32_t sl2 = tile_slot(tb + 2);
+    Regs rA, rB;
+    load_kv(slots(tb), rA);
+    const Slots sl1 = slots(tb + 1);
+    Slots sl2 = slots(tb + 2);
     __builtin_amdgcn_sched_barrier(0);
-    load_kv(sl1, kB, vB);
+    load_kv(sl1, rB);
     __builtin_amdgcn_sched_barrier(0);
-    store_tile(0, kA, vA);
+    store_tile(0, rA);
     __syncthreads();
     int tile = tb;
     for (; tile + 1 < te; tile += 2) {
-      // LDS stage 0 holds `tile`; kB, vB tile + 1; kA, vA take tile + 2
-      const int32_t sl3 = tile_slot(tile + 3);
+      // LDS stage 0 holds `tile`; rB tile + 1; rA takes tile + 2
+      const Slots sl3 = slots(tile + 3);
       __builtin_amdgcn_sched_barrier(0);
-      load_kv(sl2, kA, vA);
+      load_kv(sl2, rA);
       __builtin_amdgcn_sched_barrier(0);
       compute(0, tile);
-      store_tile(1, kB, vB);
+      store_tile(1, rB);
       __syncthreads();
-      // LDS stage 1 holds tile + 1; kA, vA tile + 2; kB, vB take tile + 3
-      sl2 = tile_slot(tile + 4);
+      // LDS stage 1 holds tile + 1; rA tile + 2; rB takes tile + 3
+      sl2 = slots(tile + 4);
       __builtin_amdgcn_sched_barrier(0);
-      load_kv(sl3, kB, vB);
+      load_kv(sl3, rB);
       __builtin_amdgcn_sched_barrier(0);
       compute(1, tile + 1);
-      store_tile(0, kA, vA);
+      store_tile(0, rA);
       __syncthreads();
     }
     if (tile < te) compute(0, tile);              // an odd last tile (its successors' loads go unused)
   }
   if (!wave_on) return;
-  if constexpr (PART) {
-    // this split's rows, unnormalised, and their (max, sum); rows past nrows are not written
-    if (16 * w + c < nrows) {
-      const int64_t pr = ((int64_t(b) * gridDim.x + lg) * nsplit + split) * PA_ROWS + 16 * w + c;
+#pragma unroll
+  for (int rb = 0; rb < PA_RB; ++rb) {
+    const int r = 32 * w + 16 * rb + c;
+    if (r >= nrows) continue;
+    if constexpr (PART) {
+      // this split's rows, unnormalised, and their (max, sum)
+      const int64_t pr = ((int64_t(b) * gridDim.x + lg) * nsplit + split) * PA_ROWS + r;
 #pragma unroll
       for (int db = 0; db < 8; ++db)
         *reinterpret_cast<float4 *>(part_o + pr * PD + 16 * db + 4 * g) =
-            make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
-      if (g == 0) *reinterpret_cast<float2 *>(part_ml + pr * 2) = make_float2(m_run, l_run);
+            make_float4(o[rb][db][0], o[rb][db][1], o[rb][db][2], o[rb][db][3]);
+      if (g == 0) *reinterpret_cast<float2 *>(part_ml + pr * 2) = make_float2(m_run[rb], l_run[rb]);
+    } else {
+      // out[l][g_kv G + h'][t][:] = O / l
+      const float inv = 1.0f / l_run[rb];
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          out[q_off + ((int64_t(l) * Hq + g_kv * G + hq[rb]) * n + tr[rb]) * PD + 16 * db + 4 * g + i] =
+              float_to_bf16_bits(o[rb][db][i] * inv);
     }
-  } else {
-    // out[l][g_kv G + h'][t][:] = O / l
-    const float inv = 1.0f / l_run;
-#pragma unroll
-    for (int db = 0; db < 8; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int ch = 16 * db + 4 * g + i;
-        if (16 * w + c < nrows)
-          out[q_off + ((int64_t(l) * Hq + g_kv * G + hq) * n + tr) * PD + ch] = float_to_bf16_bits(o[db][i] * inv);
-      }
   }
 }
 
