@@ -879,8 +879,8 @@ k_score_ws(const uint16_t *__restrict__ kpool, int64_t num_slots, int L, int Hkv
       if (r16 < R) {
         float *o = stash + (int64_t(u) * R + r16) * NS;
 #pragma unroll
-        for (int blk = 0; blk < 2; ++blk)
-          *reinterpret_cast<float4 *>(o + 16 * blk) = make_float4(acc[blk][0], acc[blk][1], acc[blk][2], acc[blk][3]);
+        for (int blk = 0; blk < 2; ++blk)         // read once, by k_score_stash: non-temporal
+          __builtin_nontemporal_store(acc[blk], reinterpret_cast<f32x4 *>(o + 16 * blk));
       }
       // the row's max and sum over this consumer's entries below ne (the four lane groups
       // of a row combined by shuffles: a merge of per-lane partials by consumer 0 made it
@@ -1998,7 +1998,8 @@ __global__ void __launch_bounds__(SS_THREADS) k_score_stash(const ikv_session *_
 #pragma unroll
     for (int k = 0; k < UN; ++k) {
       const int i = min(i0 + 16 * k, rows - 1);
-      v[k] = *reinterpret_cast<const float4 *>(st + int64_t(i) * NS);
+      const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(st + int64_t(i) * NS));
+      v[k] = make_float4(x[0], x[1], x[2], x[3]);
       sd[k] = i0 + 16 * k < rows ? nl2[i] : -INFINITY;   // past the last row: adds nothing
     }
 #pragma unroll
