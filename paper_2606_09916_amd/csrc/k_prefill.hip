@@ -400,12 +400,12 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
     const int r = 32 * w + 16 * rb + c;
     if (r >= nrows) continue;
     if constexpr (PART) {
-      // this split's rows, unnormalised, and their (max, sum)
+      // this split's rows, unnormalised, and their (max, sum); read once, by the merge:
+      // non-temporal
       const int64_t pr = ((int64_t(b) * gridDim.x + lg) * nsplit + split) * PA_ROWS + r;
 #pragma unroll
       for (int db = 0; db < 8; ++db)
-        *reinterpret_cast<float4 *>(part_o + pr * PD + 16 * db + 4 * g) =
-            make_float4(o[rb][db][0], o[rb][db][1], o[rb][db][2], o[rb][db][3]);
+        __builtin_nontemporal_store(o[rb][db], reinterpret_cast<f32x4 *>(part_o + pr * PD + 16 * db + 4 * g));
       if (g == 0) *reinterpret_cast<float2 *>(part_ml + pr * 2) = make_float2(m_run[rb], l_run[rb]);
     } else {
       // out[l][g_kv G + h'][t][:] = O / l
@@ -425,7 +425,7 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
 // row has m = -inf and weighs zero). Workgroup (layer and KV head, session, 2 rows);
 // thread (row, channel d) has every split's value and (max, sum) in flight at once.
 constexpr int PM_ROWS = 2;
-constexpr int PM_SMAX = 16;                      // prefill_splits() gives at most 16
+template <int SMAX>                              // SMAX >= nsplit: loads past nsplit re-read split 0
 __global__ void __launch_bounds__(PM_ROWS * PD) k_prefill_merge(const ikv_session *__restrict__ sess, int L, int Hq,
                                                                 int Hkv, int nsplit, const float *__restrict__ part_o,
                                                                 const float *__restrict__ part_ml,
@@ -440,21 +440,21 @@ __global__ void __launch_bounds__(PM_ROWS * PD) k_prefill_merge(const ikv_sessio
   int64_t q_off, kv_off, kq_off;
   prefill_offsets(sess, b, L, Hq, Hkv, PD, &q_off, &kv_off, &kq_off);
   const int64_t p0 = (int64_t(b) * gridDim.x + lg) * nsplit * PA_ROWS + r;
-  float oz[PM_SMAX];
-  float2 mz[PM_SMAX];
+  float oz[SMAX];
+  float2 mz[SMAX];
 #pragma unroll
-  for (int z = 0; z < PM_SMAX; ++z) {
+  for (int z = 0; z < SMAX; ++z) {
     const int64_t pz = p0 + int64_t(z < nsplit ? z : 0) * PA_ROWS;
-    oz[z] = part_o[pz * PD + d];
+    oz[z] = __builtin_nontemporal_load(part_o + pz * PD + d);
     mz[z] = reinterpret_cast<const float2 *>(part_ml)[pz];
   }
   float M = -INFINITY;
 #pragma unroll
-  for (int z = 0; z < PM_SMAX; ++z)
+  for (int z = 0; z < SMAX; ++z)
     if (z < nsplit) M = fmaxf(M, mz[z].x);
   float acc = 0.f, lsum = 0.f;
 #pragma unroll
-  for (int z = 0; z < PM_SMAX; ++z)
+  for (int z = 0; z < SMAX; ++z)
     if (z < nsplit && mz[z].x != -INFINITY) {
       const float f = __builtin_amdgcn_exp2f(mz[z].x - M);
       acc = fmaf(oz[z], f, acc);
@@ -523,8 +523,15 @@ hipError_t launch_prefill(const ikv_pool &pool, const ikv_session *sess_dev, int
           static_cast<const uint16_t *>(q_out), static_cast<uint16_t *>(out), nullptr, nullptr);
     if (splits > 1) {
       KTimer kt2_("k_prefill_merge", st);
-      k_prefill_merge<<<dim3(unsigned(pool.L * pool.Hkv), B, unsigned(PA_ROWS / PM_ROWS)), PM_ROWS * PD, 0, st>>>(
-          sess_dev, pool.L, pool.Hq, pool.Hkv, splits, part_o, part_ml, static_cast<uint16_t *>(out));
+      const dim3 gm(unsigned(pool.L * pool.Hkv), B, unsigned(PA_ROWS / PM_ROWS));
+      uint16_t *o16 = static_cast<uint16_t *>(out);
+      if (splits <= 4)
+        k_prefill_merge<4><<<gm, PM_ROWS * PD, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv, splits, part_o, part_ml, o16);
+      else if (splits <= 8)
+        k_prefill_merge<8><<<gm, PM_ROWS * PD, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv, splits, part_o, part_ml, o16);
+      else
+        k_prefill_merge<16><<<gm, PM_ROWS * PD, 0, st>>>(sess_dev, pool.L, pool.Hq, pool.Hkv, splits, part_o, part_ml,
+                                                         o16);
     }
   }
   {
