@@ -288,15 +288,11 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
 #pragma unroll
       for (int rb = 0; rb < PA_RB; ++rb) {
         float tmax = -INFINITY;
-        if (hist_tile) {                            // every key of the tile is history: nothing masked
-#pragma unroll
+        if (hist_tile) {                            // every key of the tile is history: nothing masked,
+#pragma unroll                                      // the maximum taken on the raw logits
           for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float x = sacc[rb][kb][i] * scale;
-              sacc[rb][kb][i] = x;
-              tmax = fmaxf(tmax, x);
-            }
+            for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, sacc[rb][kb][i]);
         } else {
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb)
@@ -311,18 +307,29 @@ __global__ void __launch_bounds__(PA_THREADS) k_prefill_attn(const ikv_session *
         }
         tmax = fmaxf(tmax, __shfl_xor(tmax, 16, WAVE));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32, WAVE));
+        if (hist_tile) tmax *= scale;               // scale > 0: the same value as the maximum of the scaled logits
         const float m_new = fmaxf(m_run[rb], tmax);
         // a row with no key yet (m_new = -inf) keeps zero weights and sums
         const float corr = m_run[rb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[rb] - m_new);
         float psum = 0.f;
         float p[4][4];
+        if (hist_tile) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+          for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            p[kb][i] = sacc[rb][kb][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sacc[rb][kb][i] - m_new);
-            psum += p[kb][i];
-          }
+            for (int i = 0; i < 4; ++i) {
+              p[kb][i] = __builtin_amdgcn_exp2f(fmaf(sacc[rb][kb][i], scale, -m_new));
+              psum += p[kb][i];
+            }
+        } else {
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              p[kb][i] = sacc[rb][kb][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sacc[rb][kb][i] - m_new);
+              psum += p[kb][i];
+            }
+        }
         psum += __shfl_xor(psum, 16, WAVE);
         psum += __shfl_xor(psum, 32, WAVE);
         l_run[rb] = l_run[rb] * corr + psum;
