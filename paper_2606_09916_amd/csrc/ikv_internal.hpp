@@ -298,7 +298,7 @@ hipError_t launch_compact(const ikv_pool &pool, const ikv_session *sess_dev, int
                           int32_t *n_keep, int32_t *pos_list, hipStream_t st);
 
 // Key splits of the prefill attention (one workgroup per layer, KV head, session and
-// split of the keys): about nine rounds of workgroups on the 256 CUs (one 16-wave
+// split of the keys): about nine rounds of workgroups on the 256 CUs (one 8-wave
 // workgroup per CU), at most 16 splits and no more than the 64-key tiles of the
 // longest session (history bound N plus the span).
 inline int prefill_splits(int L, int Hkv, int B, int64_t max_keys) {
