@@ -7,6 +7,8 @@ exact rotation, the value rows must be copied exactly. Everything computed from 
 rounded rows (attention, the memory update, the key means) is compared with the oracle
 run on the GPU's own rounded rows: attention within 2e-3 plus half a bf16 ulp, the
 memory within 4e-6, the key means within 1e-6 relative."""
+import types
+
 import numpy as np
 import pytest
 
@@ -144,3 +146,64 @@ def test_prefill_span_qwen3_8b_32k(dev):
     d = _setup(synth.qwen3_8b_shape(), 32704, 64, seed=2)
     _run(d)
     _check(d, layers=[0, 17, 35], tokens=[0, 31, 63])
+
+
+def test_prefill_span_two_sessions(dev):
+    """Two sessions of different history lengths and spans in one call (one pool): the
+    packed span rows, outputs and key means of the second session follow the first's, the
+    rotation grid covers the longer span, and the attention's key splits (16 here, over at
+    most 25 tiles: some splits of the shorter session are empty) are merged per session.
+    Each session is checked as in the single-session cases."""
+    torch = _torch()
+    shape = synth.Shape(L=2, Hq=8, Hkv=2, D=128)
+    L, Hq, Hkv, D, G = shape.L, shape.Hq, shape.Hkv, shape.D, shape.G
+    plan = [(700, 32), (1500, 48)]
+    specs = [synth.SessionSpec(N=N0 + n, C=max(1, (N0 + n) // 4), pi=0, qs=N0, qe=N0 + n, R=G, dead_frac=0.1,
+                               qpos=np.zeros(0, np.int32)) for N0, n in plan]
+    batch = synth.make_batch(shape, specs, seed=41, kv_dtype=synth.BF16, layout="paged", span_rows=False)
+    g = synth.stream(41, synth.T_QWIN, 7)
+    rows = [(synth.f32_to_bf16(g.standard_normal((L, Hq, n, D), dtype=np.float32)),
+             synth.f32_to_bf16(g.standard_normal((L, Hkv, n, D), dtype=np.float32)),
+             synth.f32_to_bf16(g.standard_normal((L, Hkv, n, D), dtype=np.float32))) for _, n in plan]
+    M0 = [g.standard_normal((L, Hq, D)).astype(np.float32) for _ in plan]
+    for m in M0:
+        m /= np.linalg.norm(m, axis=-1, keepdims=True)
+    total = int(batch.slot_off[-1]) + specs[-1].N
+    hist_all = np.zeros(total, np.int32)
+    hists = []
+    for b, (N0, n) in enumerate(plan):
+        S = batch.S(b)
+        h = S[:N0][S[:N0] != synth.DEAD_SLOT].astype(np.int32)
+        hist_all[int(batch.slot_off[b]):int(batch.slot_off[b]) + len(h)] = h
+        hists.append(h)
+    M_all = np.zeros(int(batch.mem_off[-1]) + L * Hq * D, np.float32)
+    for b in range(len(plan)):
+        M_all[int(batch.mem_off[b]):int(batch.mem_off[b]) + L * Hq * D] = M0[b].reshape(-1)
+    k_dev, v_dev = _bf(batch.k_pool, dev), _bf(batch.v_pool, dev)
+    pool = ikv.make_pool(k_dev, v_dev, L, Hq, Hkv, D, batch.num_slots, synth.DEAD_SLOT)
+    sess = ikv.Sessions([dict(slot_off=int(batch.slot_off[b]), mem_off=int(batch.mem_off[b]), qspan_off=0, qpos_off=0,
+                              N=N0 + n, pi=0, qs=N0, qe=N0 + n, C=specs[b].C, radix_prefix=0, R=G, nq=0)
+                         for b, (N0, n) in enumerate(plan)], dev)
+    n_tot = sum(n for _, n in plan)
+    cat = lambda i: np.concatenate([r[i].reshape(-1) for r in rows])   # session blocks one after the other
+    q_out = torch.empty(L * Hq * n_tot * D, dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q_out)
+    kq = torch.empty(n_tot * D, dtype=torch.float32, device=dev)
+    M = torch.from_numpy(M_all).to(dev)
+    ws = ikv.Workspace(dev)
+    ikv.prefill_span(pool, sess, torch.from_numpy(batch.slot_maps.astype(np.int32)).to(dev), _bf(cat(0), dev),
+                     _bf(cat(1), dev), _bf(cat(2), dev), torch.from_numpy(hist_all).to(dev),
+                     torch.tensor([len(h) for h in hists], dtype=torch.int32, device=dev), q_out, out, kq, ws, M=M,
+                     lam=0.5, rope_base=synth.ROPE_BASE)
+    torch.cuda.synchronize()
+    qo = 0
+    for b, (N0, n) in enumerate(plan):
+        one = types.SimpleNamespace(shape=shape, sessions=[specs[b]])    # what the checks read of a batch
+        d = dict(batch=one, k=k_dev, v=v_dev,
+                 q_out=q_out[qo:qo + L * Hq * n * D].view(L, Hq, n, D), out=out[qo:qo + L * Hq * n * D].view(L, Hq, n, D),
+                 kq=kq[sum(m for _, m in plan[:b]) * D:(sum(m for _, m in plan[:b]) + n) * D].view(n, D),
+                 M=M[int(batch.mem_off[b]):int(batch.mem_off[b]) + L * Hq * D],
+                 host=dict(q_raw=rows[b][0], k_raw=rows[b][1], v_raw=rows[b][2], M0=M0[b], hist=hists[b],
+                           S=batch.S(b)))
+        _check(d)
+        qo += L * Hq * n * D
