@@ -259,7 +259,8 @@ struct ScoreArgs {
 // The one-key-pass form at 16 < R <= 64 (one session whose list tiles fit on the device
 // at once): its workgroup count, 0 where it does not apply; and the floats of its
 // exchange area, which follows the score workspace's shared block (0 where it does not
-// apply). It is opt-in: IKV_FUSED=1 in the environment (read on every call) turns it on.
+// apply). It is switched off (fused_tiles returns 0): on some calls one row normaliser
+// came out wrong, and the cause is not found.
 int fused_tiles(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags);
 int64_t fused_exchange_floats(const ikv_pool &p, const ikv_session *s, int B, uint32_t flags);
 

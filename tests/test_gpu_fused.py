@@ -16,7 +16,11 @@ from paper_2606_09916_amd import ikv
 from paper_2606_09916_amd.step import RetentionStep
 from parity import RESID_MFMA_FLOOR, SCORE_FLOOR, check_keep, check_scores
 
-pytestmark = pytest.mark.gpu
+# The form is switched off in the library (fused_tiles returns 0): on some runs one row
+# normaliser came out wrong (test_fused_unit_counts[5-1-8300-24]: relative score errors of
+# 6e-4 to 8e-4 in about one run in three), and the cause is not found.
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skip(reason="one-key-pass form switched off: intermittent wrong row normaliser, cause not found")]
 
 
 def _batch(N, R, dead_frac, seed, L=2, Hkv=2, dead_range=None):
